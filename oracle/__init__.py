@@ -1,0 +1,141 @@
+"""CPU oracle for the sparse 1x1 convolution -- test infrastructure only.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The GPU library never does, and this
+package never imports the GPU library: the two share no code.
+
+``spconv_ref`` evaluates the plain definition
+
+    Y[n, r, p] = act( b[r] + sum_{stored (r, c)} W[r, c] * X[n, c, p] )
+
+(paper Sec. 1 and Sec. 3.2 / Fig. 2: a 1x1 convolution in CHW layout is a
+sparse-weight x dense-activation product; Sec. 3.2: 1xk output-channel blocks
+share one pattern; Sec. 3.3: block-CSR weights) in double precision with the C
+code in ``spconv_ref.c``, then rounds each element once, to nearest-even, to
+the storage type.  It also returns the per-element error scale
+S = sum |W[r, c] * X[n, c, p]| that the parity tolerance is stated in.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spconv_ref.c")
+_LIB = os.path.join(_HERE, "libspconv_ref.so")
+_ACTS = {"none": 0, "relu": 1, "relu6": 2}
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (portable x86-64 code, OpenMP, no FP contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+                               "-o", tmp, _SRC, "-lm"])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def load_library(path: str):
+    """Open an oracle shared library (the default one, or a test's own build)."""
+    lib = ctypes.CDLL(path)
+    lib.spconv_ref_run.restype = ctypes.c_int
+    lib.spconv_ref_run.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_threads.restype = ctypes.c_int
+    lib.spconv_ref_half_to_double.restype = ctypes.c_double
+    lib.spconv_ref_half_to_double.argtypes = [ctypes.c_uint16]
+    return lib
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        _lib = load_library(_LIB)
+    return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle runs with."""
+    return int(_load().spconv_ref_threads())
+
+
+def half_to_double(bits: int) -> float:
+    """The oracle's own binary16 decoder (exposed so tests can pin it)."""
+    return float(_load().spconv_ref_half_to_double(int(bits) & 0xFFFF))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def spconv_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x,
+               storage: str = "f32", with_scale: bool = True, lib=None):
+    """Run the oracle.
+
+    ``x`` is [N, Cin, H, W] (or [N, Cin, HW]) float32 for storage "f32" and
+    float16 for "f16".  Returns ``(y, y64, scale)``: ``y`` rounded to the
+    storage type with the shape [N, Cout, ...] of ``x``, ``y64`` the unrounded
+    double values, ``scale`` the error scale (or None).  ``lib`` selects
+    another build of the oracle (the tests' planted-mistake builds).
+    """
+    lib = _load() if lib is None else lib
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    values = np.ascontiguousarray(values, dtype=np.float32)
+    bias_a = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    if storage == "f16":
+        xa = np.ascontiguousarray(x, dtype=np.float16)
+        xbits = xa.view(np.uint16)
+        f16 = 1
+    else:
+        xa = np.ascontiguousarray(x, dtype=np.float32)
+        xbits = xa
+        f16 = 0
+    n = xa.shape[0]
+    if xa.shape[1] != cin:
+        raise ValueError("x has %d channels, expected %d" % (xa.shape[1], cin))
+    spatial = xa.shape[2:]
+    hw = int(np.prod(spatial)) if len(spatial) else 1
+    y64 = np.empty((n, cout, hw), dtype=np.float64)
+    scale = np.empty((n, cout, hw), dtype=np.float64) if with_scale else None
+    rc = lib.spconv_ref_run(int(cout), int(cin), int(block_rows), _ptr(row_ptr), _ptr(col_idx),
+                            _ptr(values), _ptr(bias_a), _ACTS[act], _ptr(xbits), f16,
+                            int(n), int(hw), _ptr(y64), _ptr(scale))
+    if rc != 0:
+        raise ValueError("oracle rejected the input (code %d)" % rc)
+    y = y64.astype(np.float16 if storage == "f16" else np.float32)
+    shape = (n, cout) + tuple(spatial)
+    return (y.reshape(shape), y64.reshape(shape),
+            None if scale is None else scale.reshape(shape))
+
+
+def spconv_ref_layer(layer, x=None, with_scale: bool = True):
+    """Run the oracle on a ``synth.Layer`` (optionally on another input x)."""
+    return spconv_ref(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx,
+                      layer.values, layer.bias, layer.act, layer.x if x is None else x,
+                      storage=layer.storage, with_scale=with_scale)
+
+
+def tolerance(y_ref, scale, storage: str):
+    """Per-element bound |y_gpu - y_ref| may not exceed.
+
+    fp32: 1e-5 * S + 1e-6.  fp16 storage with fp32 accumulation:
+    2e-3 * |y_ref| + 1e-5 * S + 1e-6 (one fp16 ulp of output rounding, the
+    fp32 accumulation, and fp16 subnormals).
+    """
+    tol = 1e-5 * scale + 1e-6
+    if storage == "f16":
+        tol = tol + 2e-3 * np.abs(y_ref.astype(np.float64))
+    return tol

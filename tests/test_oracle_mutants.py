@@ -1,0 +1,101 @@
+"""The oracle's pins catch plausible mistakes (no GPU).
+
+Each case plants one mistake in a copy of the oracle's C source (a wrong sign,
+a dropped term, a wrong index, a transposed operand, a missing clamp, a wrong
+binary16 decoding step), builds it with gcc into a temporary directory, and
+checks that the pin battery below rejects it.  The unmodified source must pass
+the same battery.
+"""
+
+import json
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import make_layer, densify
+
+SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "spconv_ref.c")
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
+
+MUTANTS = {
+    "sign_of_term": ("acc[p] += prod;", "acc[p] -= prod;"),
+    "block_value_index": ("values[(int64_t)t * k + i]", "values[(int64_t)t * k]"),
+    "bias_index": ("(double)bias[r]", "(double)bias[rb]"),
+    "x_transposed": ("(img * cin + c) * hw", "(c * n + img) * hw"),
+    "dropped_first_term": ("t = row_ptr[rb]; t < row_ptr[rb + 1]", "t = row_ptr[rb] + 1; t < row_ptr[rb + 1]"),
+    "dropped_bias": ("apply_act(acc[p] + b, act)", "apply_act(acc[p], act)"),
+    "relu_unclamped": ("return v > 0.0 ? v : 0.0;", "return v;"),
+    "relu6_unclamped": ("return v < 6.0 ? v : 6.0;", "return v;"),
+    "scale_signed": ("s[p] += fabs(prod);", "s[p] += prod;"),
+    "block_row_order": ("const int32_t r = rb * k + i;", "const int32_t r = rb + i * rows;"),
+    "half_exponent_bias": ("expo - 25", "expo - 24"),
+    "half_implicit_bit": ("(frac | 0x400)", "frac"),
+    "half_subnormal_scale": ("ldexp((double)frac, -24)", "ldexp((double)frac, -25)"),
+}
+
+
+def _act(v, act):
+    if act == "relu":
+        return np.maximum(v, 0.0)
+    if act == "relu6":
+        return np.minimum(np.maximum(v, 0.0), 6.0)
+    return v
+
+
+def _battery(lib):
+    """Return the names of the pins that fail for this build of the oracle."""
+    failed = []
+    for case in json.load(open(GOLDEN))["cases"]:
+        x = np.asarray(case["x"], dtype=np.float32)[None]
+        for act in ("none", "relu", "relu6"):
+            _, y64, s = oracle.spconv_ref(case["cout"], case["cin"], case["block_rows"], case["row_ptr"],
+                                          case["col_idx"], case["values"], case["bias"], act, x, lib=lib)
+            if not np.array_equal(y64[0], np.asarray(case["y_" + act])):
+                failed.append("hand:" + case["name"] + ":" + act)
+            if not np.array_equal(s[0], np.asarray(case["scale"])):
+                failed.append("hand-scale:" + case["name"])
+    for k, storage in ((1, "f32"), (4, "f32"), (4, "f16")):
+        layer = make_layer(12, 16, 3, 5, 2, 0.5, block_rows=k, storage=storage, act="relu6", seed=3)
+        _, y64, s = oracle.spconv_ref(layer.cout, layer.cin, k, layer.row_ptr, layer.col_idx,
+                                      layer.values, layer.bias, "relu6", layer.x, storage=storage, lib=lib)
+        wd = densify(16, 12, k, layer.row_ptr, layer.col_idx, layer.values)
+        x64 = layer.x.astype(np.float64).reshape(2, 12, -1)
+        ref = _act(np.matmul(wd[None], x64) + layer.bias.astype(np.float64)[None, :, None], "relu6")
+        sref = np.matmul(np.abs(wd)[None], np.abs(x64))
+        if not np.all(np.abs(y64.reshape(ref.shape) - ref) <= 1e-12 * (sref + 1.0)):
+            failed.append("brute:k%d:%s" % (k, storage))
+        if not np.allclose(s.reshape(sref.shape), sref, rtol=1e-12, atol=0):
+            failed.append("brute-scale:k%d:%s" % (k, storage))
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    ref = bits.view(np.float16).astype(np.float64)
+    got = np.array([lib.spconv_ref_half_to_double(int(b)) for b in bits])
+    ok = ~np.isnan(ref)
+    if not np.array_equal(got[ok], ref[ok]):
+        failed.append("half-decoder")
+    return failed
+
+
+def _build(tmp_path, name, source):
+    src = tmp_path / (name + ".c")
+    so = tmp_path / ("lib" + name + ".so")
+    src.write_text(source)
+    subprocess.check_call(["gcc", "-O1", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared",
+                           "-o", str(so), str(src), "-lm"])
+    return oracle.load_library(str(so))
+
+
+def test_unmodified_oracle_passes_battery(tmp_path):
+    lib = _build(tmp_path, "pristine", open(SRC).read())
+    assert _battery(lib) == []
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_planted_mistake_is_caught(tmp_path, name):
+    before, after = MUTANTS[name]
+    source = open(SRC).read()
+    assert source.count(before) == 1, "mutation anchor not found exactly once: " + before
+    lib = _build(tmp_path, name, source.replace(before, after))
+    assert _battery(lib), "planted mistake %r passed every pin" % name
