@@ -1,0 +1,173 @@
+/*
+ * spconv.h -- sparse 1x1 convolution (sparse weights x dense CHW activations)
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * The operation (Fast Sparse ConvNets, Sec. 3.2 and Fig. 2: a 1x1
+ * convolution over activations stored channel-major, CHW, is a sparse-matrix
+ * times dense-matrix product; Sec. 3.2: output-channel blocks of k rows share
+ * one nonzero pattern; Sec. 3.3: weights are converted to a block-compressed
+ * sparse row format for inference).  For every image n, output channel r and
+ * spatial position p:
+ *
+ *     Y[n, r, p] = act( b[r] + sum_{stored (r, c)} W[r, c] * X[n, c, p] )
+ *
+ * with act one of identity, max(v, 0) or min(max(v, 0), 6), evaluated in
+ * fp32 and rounded once to the storage type.
+ *
+ * Conventions for every call:
+ *   - Status codes are returned; no C++ exception crosses this interface.
+ *     After a failure, spconv_last_error() returns a message for the calling
+ *     thread.
+ *   - Host arrays passed to a call are only read during that call; the caller
+ *     keeps ownership and may free them on return.
+ *   - Device pointers are plain HIP device addresses (e.g. from hipMalloc or a
+ *     PyTorch tensor's data_ptr()); they stay owned by the caller.
+ */
+#ifndef SPCONV_H
+#define SPCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct spconv_plan_s *spconv_plan; /* opaque, immutable once created */
+
+typedef enum {
+    SPCONV_OK = 0,
+    SPCONV_E_ARG = 1,         /* bad argument: NULL pointer, negative size, x/y overlap, wrong device */
+    SPCONV_E_FORMAT = 2,      /* malformed CSR / block-CSR arrays */
+    SPCONV_E_SHAPE = 3,       /* inconsistent sizes (cout % block_rows, sizes too large) */
+    SPCONV_E_UNSUPPORTED = 4, /* valid request this build does not implement */
+    SPCONV_E_NOMEM = 5,       /* host or device allocation failed */
+    SPCONV_E_HIP = 6          /* a HIP runtime call failed (message names it) */
+} spconv_status;
+
+typedef enum { SPCONV_F32 = 0, SPCONV_F16 = 1 } spconv_dtype;
+
+typedef enum { SPCONV_ACT_NONE = 0, SPCONV_ACT_RELU = 1, SPCONV_ACT_RELU6 = 2 } spconv_act;
+
+/*
+ * Build a plan from CSR (block_rows = 1) or 1 x block_rows block-CSR weights
+ * (Sec. 3.2: k consecutive output channels share one column pattern; k = 4 is
+ * the blocking the paper's models use).  Validates the arrays, orders the
+ * (block) rows by nonzero count for load balance, packs column indices and
+ * values into the layout the kernels stream, and copies the result to the
+ * current HIP device.  Synchronous.
+ *
+ *   out         receives the plan; set to NULL on failure
+ *   cout, cin   output / input channels; cout % block_rows == 0, both >= 1
+ *   block_rows  1 or 4
+ *   row_ptr     host, cout/block_rows + 1 entries: row_ptr[0] = 0, non-decreasing
+ *   col_idx     host, row_ptr[cout/block_rows] entries, each in [0, cin), strictly
+ *               ascending within a (block) row
+ *   values      host, row_ptr[end] * block_rows floats, block-major:
+ *               values[t * k + i] = W[rb * k + i, col_idx[t]] for t in block row rb;
+ *               must be finite.  With storage SPCONV_F16 each value is rounded to
+ *               the nearest fp16 value (ties to even) before use.
+ *   bias        host, cout floats, or NULL for zeros; kept in fp32
+ *   act         epilogue activation
+ *   storage     element type of X and Y (W is used at that precision; the
+ *               accumulation is always fp32)
+ *
+ * Errors: SPCONV_E_ARG (NULL out/row_ptr, NULL col_idx/values with nonzeros,
+ * bad enum), SPCONV_E_SHAPE, SPCONV_E_FORMAT (message names the first bad
+ * entry), SPCONV_E_UNSUPPORTED (block_rows not 1 or 4), SPCONV_E_NOMEM,
+ * SPCONV_E_HIP (no usable device, allocation or copy failure).  Nothing is
+ * leaked on failure.
+ */
+spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                 const int32_t *row_ptr, const int32_t *col_idx,
+                                 const float *values, const float *bias, spconv_act act,
+                                 spconv_dtype storage);
+
+/*
+ * Run the plan:  y = act(W x + b)  on NCHW tensors of the plan's storage type.
+ *
+ *   x       device, n * cin * h * w elements, NCHW contiguous
+ *   y       device, n * cout * h * w elements, NCHW contiguous; must not overlap x
+ *           (every output channel reads every input channel, so in-place is impossible)
+ *   n, h, w batch and spatial sizes, >= 0; n == 0 or h * w == 0 is a no-op
+ *   stream  hipStream_t to launch on, or NULL for the default stream
+ *
+ * Asynchronous: returns once the kernel is queued on `stream`; x and y must
+ * stay alive until that work completes.  Allocates nothing and never
+ * synchronizes.  Pointers need only element alignment (16-byte alignment with
+ * h * w a multiple of the vector width takes the fastest load path).  The plan
+ * must have been created on the current device.  A plan is immutable, so
+ * concurrent runs of one plan on different streams are safe.
+ *
+ * Errors: SPCONV_E_ARG (NULL plan/x/y with work to do, negative sizes, overlap,
+ * other device, host-only plan), SPCONV_E_SHAPE (sizes beyond 2^31 columns or
+ * elements beyond 2^62), SPCONV_E_HIP (launch failure).  Faults during
+ * execution surface at the caller's next synchronization.
+ */
+spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
+                         void *stream);
+
+/* Free the plan and its device buffers.  NULL is a no-op.  The caller must
+ * ensure no queued run still uses the plan. */
+spconv_status spconv_destroy(spconv_plan plan);
+
+/* Message for the calling thread's most recent failure ("" if none).  The
+ * pointer stays valid until the next spconv_* call on the same thread. */
+const char *spconv_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Planner controls and introspection.  These let a caller (and the CPU-only
+ * tests) see what the host-side planner decided without running a kernel.
+ * ------------------------------------------------------------------------- */
+
+typedef struct {
+    int32_t struct_size;   /* sizeof(spconv_options) */
+    int32_t reorder;       /* 1 (default): process rows in descending nonzero order; 0: natural order */
+    int32_t host_only;     /* 1: plan on the host only, no device memory; spconv_run refuses it */
+    int32_t lanes_per_row; /* 0 = choose automatically; else 8, 16, 32 or 64 lanes share one row */
+    int32_t waves;         /* 0 = choose automatically; else 1..16 wavefronts per workgroup */
+} spconv_options;
+
+/* Fill *opts with the defaults used by spconv_plan_create. */
+void spconv_options_init(spconv_options *opts);
+
+/* As spconv_plan_create, with explicit planner options (NULL = defaults). */
+spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                    const int32_t *row_ptr, const int32_t *col_idx,
+                                    const float *values, const float *bias, spconv_act act,
+                                    spconv_dtype storage, const spconv_options *opts);
+
+typedef struct {
+    int32_t cout, cin, block_rows;
+    int32_t storage, act;
+    int32_t kernel;        /* 0: LDS-strip kernel; 1: direct-load kernel for wide inputs */
+    int32_t lanes_per_row; /* lanes sharing one (block) row */
+    int32_t cols_per_lane; /* output columns each lane accumulates */
+    int32_t tile_cols;     /* columns per workgroup tile = lanes_per_row * cols_per_lane */
+    int32_t waves;         /* wavefronts per workgroup */
+    int32_t groups;        /* row groups (rows processed together by one wavefront) */
+    int32_t lds_bytes;     /* LDS per workgroup */
+    int64_t nnzb;          /* stored blocks */
+    int64_t slots;         /* packed (index, value) slots including padding */
+    int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
+    int64_t sum_wave_cost; /* total of the per-wavefront work estimates */
+    int64_t device_bytes;  /* device memory the plan holds */
+} spconv_plan_info;
+
+/* Describe a plan.  Host only; does not touch the device. */
+spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info);
+
+/*
+ * Reconstruct the plan's weights from its packed host image, in the input's
+ * block-CSR form: row_ptr[cout/k + 1], col_idx[nnzb], values[nnzb * k] (each
+ * may be NULL to skip), and perm[cout/k] (may be NULL): perm[i] = the block
+ * row processed i-th.  Host only.  Lets tests check that packing loses nothing.
+ */
+spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
+                                 int32_t *perm);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPCONV_H */

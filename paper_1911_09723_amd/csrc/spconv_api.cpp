@@ -1,0 +1,306 @@
+// C ABI of libspconv (declared in include/spconv.h).
+//
+// spconv_plan_create: validate + plan on the host (planner.cpp), then one
+// device allocation holding every packed array, filled with one synchronous
+// copy.  spconv_run: argument checks, then one asynchronous kernel launch on
+// the caller's stream (spmm_kernels.hip); it allocates nothing and never
+// synchronizes.
+#include "spconv.h"
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "launch.hpp"
+#include "planner.hpp"
+
+struct spconv_plan_s {
+    spconv::PackedPlan host;
+    spconv::DevicePlan dev;
+    int device = -1;
+    void *dmem = nullptr;
+    size_t dbytes = 0;
+    bool host_only = false;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+spconv_status fail(spconv_status st, const std::string &msg) {
+    g_err = msg;
+    return st;
+}
+
+spconv_status hip_fail(const char *what, hipError_t e) {
+    g_err = std::string(what) + " failed: " + hipGetErrorName(e) + " (" + hipGetErrorString(e) + ")";
+    return SPCONV_E_HIP;
+}
+
+// Test hook: SPCONV_FAULT=alloc makes the device allocation in plan creation
+// report failure, to exercise the no-leak error path.
+bool fault_alloc() {
+    const char *f = std::getenv("SPCONV_FAULT");
+    return f && std::strcmp(f, "alloc") == 0;
+}
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+spconv::Input make_input(int32_t cout, int32_t cin, int32_t block_rows, const int32_t *row_ptr,
+                         const int32_t *col_idx, const float *values, const float *bias, spconv_act act,
+                         spconv_dtype storage) {
+    spconv::Input in;
+    in.cout = cout;
+    in.cin = cin;
+    in.block_rows = block_rows;
+    in.row_ptr = row_ptr;
+    in.col_idx = col_idx;
+    in.values = values;
+    in.bias = bias;
+    in.act = static_cast<int32_t>(act);
+    in.storage = static_cast<int32_t>(storage);
+    return in;
+}
+
+spconv_status upload(spconv_plan_s *pl) {
+    const spconv::PackedPlan &h = pl->host;
+    struct Part {
+        const void *src;
+        size_t bytes;
+        size_t off;
+    } parts[6] = {
+        {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
+        {h.val.data(), h.val.size() * sizeof(float), 0},
+        {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
+        {h.rows.data(), h.rows.size() * sizeof(int32_t), 0},
+        {h.wave_ptr.data(), h.wave_ptr.size() * sizeof(int32_t), 0},
+        {h.bias.data(), h.bias.size() * sizeof(float), 0},
+    };
+    size_t total = 0;
+    for (Part &p : parts) {
+        p.off = total;
+        total = align_up(total + p.bytes, 256);
+    }
+    if (fault_alloc())
+        return fail(SPCONV_E_NOMEM, "device allocation failed (SPCONV_FAULT=alloc)");
+    hipError_t e = hipGetDevice(&pl->device);
+    if (e != hipSuccess)
+        return hip_fail("hipGetDevice", e);
+    e = hipMalloc(&pl->dmem, total);
+    if (e == hipErrorOutOfMemory) {
+        pl->dmem = nullptr;
+        return fail(SPCONV_E_NOMEM, "hipMalloc of " + std::to_string(total) + " bytes: out of memory");
+    }
+    if (e != hipSuccess) {
+        pl->dmem = nullptr;
+        return hip_fail("hipMalloc", e);
+    }
+    pl->dbytes = total;
+    std::string image(total, '\0');
+    for (const Part &p : parts)
+        std::memcpy(&image[p.off], p.src, p.bytes);
+    e = hipMemcpy(pl->dmem, image.data(), total, hipMemcpyHostToDevice);
+    if (e != hipSuccess)
+        return hip_fail("hipMemcpy (plan upload)", e);
+    char *base = static_cast<char *>(pl->dmem);
+    spconv::DevicePlan &d = pl->dev;
+    d.idx = reinterpret_cast<const int32_t *>(base + parts[0].off);
+    d.val = reinterpret_cast<const float *>(base + parts[1].off);
+    d.hdr = reinterpret_cast<const int32_t *>(base + parts[2].off);
+    d.rows = reinterpret_cast<const int32_t *>(base + parts[3].off);
+    d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[4].off);
+    d.bias = reinterpret_cast<const float *>(base + parts[5].off);
+    return SPCONV_OK;
+}
+
+void fill_device_geometry(spconv_plan_s *pl) {
+    const spconv::PackedPlan &h = pl->host;
+    spconv::DevicePlan &d = pl->dev;
+    d.kernel = h.kernel;
+    d.lanes_per_row = h.lanes_per_row;
+    d.tile_cols = h.tile_cols;
+    d.waves = h.waves;
+    d.lds_bytes = h.lds_bytes;
+    d.k = h.k;
+    d.storage = h.storage;
+    d.act = h.act;
+    d.cin = h.cin;
+    d.cout = h.cout;
+}
+
+bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + bbytes && b0 < a0 + abytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+void spconv_options_init(spconv_options *opts) {
+    if (!opts)
+        return;
+    std::memset(opts, 0, sizeof(*opts));
+    opts->struct_size = static_cast<int32_t>(sizeof(spconv_options));
+    opts->reorder = 1;
+}
+
+spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                    const int32_t *row_ptr, const int32_t *col_idx, const float *values,
+                                    const float *bias, spconv_act act, spconv_dtype storage,
+                                    const spconv_options *opts) {
+    g_err.clear();
+    if (!out)
+        return fail(SPCONV_E_ARG, "out is NULL");
+    *out = nullptr;
+    spconv_options o;
+    spconv_options_init(&o);
+    if (opts) {
+        if (opts->struct_size != static_cast<int32_t>(sizeof(spconv_options)))
+            return fail(SPCONV_E_ARG, "spconv_options.struct_size does not match this library");
+        o = *opts;
+    }
+    if (o.host_only != 0 && o.host_only != 1)
+        return fail(SPCONV_E_ARG, "host_only must be 0 or 1");
+    spconv::Options po;
+    po.reorder = o.reorder;
+    po.host_only = o.host_only;
+    po.lanes_per_row = o.lanes_per_row;
+    po.waves = o.waves;
+
+    spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
+    if (!pl)
+        return fail(SPCONV_E_NOMEM, "host allocation of the plan failed");
+    std::string err;
+    spconv::Status st;
+    try {
+        st = spconv::build_plan(make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage),
+                                po, pl->host, err);
+    } catch (const std::bad_alloc &) {
+        delete pl;
+        return fail(SPCONV_E_NOMEM, "host allocation failed while packing the plan");
+    }
+    if (st != spconv::OK) {
+        delete pl;
+        return fail(static_cast<spconv_status>(st), err);
+    }
+    fill_device_geometry(pl);
+    pl->host_only = o.host_only == 1;
+    if (!pl->host_only) {
+        spconv_status us = upload(pl);
+        if (us != SPCONV_OK) {
+            if (pl->dmem)
+                (void)hipFree(pl->dmem);
+            delete pl;
+            return us;
+        }
+    }
+    *out = pl;
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                 const int32_t *row_ptr, const int32_t *col_idx, const float *values,
+                                 const float *bias, spconv_act act, spconv_dtype storage) {
+    return spconv_plan_create_ex(out, cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage,
+                                 nullptr);
+}
+
+spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
+                         void *stream) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    if (n < 0 || h < 0 || w < 0)
+        return fail(SPCONV_E_ARG, "n, h and w must be >= 0");
+    if (plan->host_only)
+        return fail(SPCONV_E_ARG, "plan was created with host_only = 1 and has no device data");
+    const int64_t hw = static_cast<int64_t>(h) * w;
+    const int64_t m = static_cast<int64_t>(n) * hw;
+    if (m == 0)
+        return SPCONV_OK;
+    if (!x || !y)
+        return fail(SPCONV_E_ARG, "x or y is NULL");
+    if (hw > INT32_MAX || m > INT32_MAX)
+        return fail(SPCONV_E_SHAPE, "n * h * w must be below 2^31 columns");
+    const spconv::PackedPlan &p = plan->host;
+    const size_t e = p.storage == 1 ? 2 : 4;
+    const int64_t xel = m * p.cin, yel = m * p.cout;
+    if (xel > (int64_t(1) << 62) / 4 || yel > (int64_t(1) << 62) / 4)
+        return fail(SPCONV_E_SHAPE, "tensor too large");
+    if (reinterpret_cast<uintptr_t>(x) % e || reinterpret_cast<uintptr_t>(y) % e)
+        return fail(SPCONV_E_ARG, "x and y must be aligned to the element size");
+    if (ranges_overlap(x, static_cast<size_t>(xel) * e, y, static_cast<size_t>(yel) * e))
+        return fail(SPCONV_E_ARG, "x and y overlap; the operation cannot run in place");
+    int dev = -1;
+    hipError_t he = hipGetDevice(&dev);
+    if (he != hipSuccess)
+        return hip_fail("hipGetDevice", he);
+    if (dev != plan->device)
+        return fail(SPCONV_E_ARG, "plan was created on device " + std::to_string(plan->device) +
+                                      " but the current device is " + std::to_string(dev));
+    const int32_t q = p.cols_per_lane;
+    const int32_t vec = (hw % q == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                        reinterpret_cast<uintptr_t>(y) % 16 == 0;
+    he = spconv::launch_spmm(plan->dev, x, y, m, static_cast<int32_t>(hw), vec,
+                             static_cast<hipStream_t>(stream));
+    if (he != hipSuccess)
+        return hip_fail("kernel launch", he);
+    return SPCONV_OK;
+}
+
+spconv_status spconv_destroy(spconv_plan plan) {
+    g_err.clear();
+    if (!plan)
+        return SPCONV_OK;
+    spconv_status st = SPCONV_OK;
+    if (plan->dmem) {
+        hipError_t e = hipFree(plan->dmem);
+        if (e != hipSuccess)
+            st = hip_fail("hipFree", e);
+    }
+    delete plan;
+    return st;
+}
+
+const char *spconv_last_error(void) { return g_err.c_str(); }
+
+spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
+    g_err.clear();
+    if (!plan || !info)
+        return fail(SPCONV_E_ARG, "plan or info is NULL");
+    const spconv::PackedPlan &p = plan->host;
+    std::memset(info, 0, sizeof(*info));
+    info->cout = p.cout;
+    info->cin = p.cin;
+    info->block_rows = p.k;
+    info->storage = p.storage;
+    info->act = p.act;
+    info->kernel = p.kernel;
+    info->lanes_per_row = p.lanes_per_row;
+    info->cols_per_lane = p.cols_per_lane;
+    info->tile_cols = p.tile_cols;
+    info->waves = p.waves;
+    info->groups = p.groups;
+    info->lds_bytes = p.lds_bytes;
+    info->nnzb = p.nnzb;
+    info->slots = p.slots;
+    info->max_wave_cost = p.max_wave_cost;
+    info->sum_wave_cost = p.sum_wave_cost;
+    info->device_bytes = static_cast<int64_t>(plan->dbytes);
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
+                                 int32_t *perm) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    spconv::unpack_plan(plan->host, row_ptr, col_idx, values, perm);
+    return SPCONV_OK;
+}
+
+}  // extern "C"

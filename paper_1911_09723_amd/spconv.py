@@ -1,0 +1,229 @@
+"""Python binding of libspconv's C ABI (include/spconv.h).
+
+Argument marshalling only: every step of the operation runs inside the
+library (host planner and HIP kernels).  The functions carry the C names;
+``Plan`` is a small convenience wrapper.  PyTorch supplies device memory and
+streams when tensors are passed; raw integer device addresses work too.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIBRARY_PATH = os.path.join(_HERE, "libspconv.so")
+
+OK, E_ARG, E_FORMAT, E_SHAPE, E_UNSUPPORTED, E_NOMEM, E_HIP = range(7)
+STATUS_NAMES = {0: "SPCONV_OK", 1: "SPCONV_E_ARG", 2: "SPCONV_E_FORMAT", 3: "SPCONV_E_SHAPE",
+                4: "SPCONV_E_UNSUPPORTED", 5: "SPCONV_E_NOMEM", 6: "SPCONV_E_HIP"}
+F32, F16 = 0, 1
+ACT_NONE, ACT_RELU, ACT_RELU6 = 0, 1, 2
+_ACTS = {"none": ACT_NONE, "relu": ACT_RELU, "relu6": ACT_RELU6}
+_DTYPES = {"f32": F32, "f16": F16}
+
+# Symbols declared in include/spconv.h.
+EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error",
+            "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack")
+
+
+class SpconvError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), message))
+        self.status = status
+        self.message = message
+
+
+class spconv_options(ctypes.Structure):
+    _fields_ = [("struct_size", ctypes.c_int32), ("reorder", ctypes.c_int32), ("host_only", ctypes.c_int32),
+                ("lanes_per_row", ctypes.c_int32), ("waves", ctypes.c_int32)]
+
+
+class spconv_plan_info(ctypes.Structure):
+    _fields_ = [("cout", ctypes.c_int32), ("cin", ctypes.c_int32), ("block_rows", ctypes.c_int32),
+                ("storage", ctypes.c_int32), ("act", ctypes.c_int32), ("kernel", ctypes.c_int32),
+                ("lanes_per_row", ctypes.c_int32), ("cols_per_lane", ctypes.c_int32),
+                ("tile_cols", ctypes.c_int32), ("waves", ctypes.c_int32), ("groups", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32), ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
+                ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
+                ("device_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+_lib = None
+
+
+def load_library(path: Optional[str] = None):
+    """Load libspconv.so (built in-tree by paper_1911_09723_amd.build).  Fails loudly if missing."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIBRARY_PATH
+    if not os.path.exists(p):
+        raise RuntimeError("libspconv.so is not built (%s); run `python -m paper_1911_09723_amd.build`" % p)
+    lib = ctypes.CDLL(p)
+    vp, i32 = ctypes.c_void_p, ctypes.c_int32
+    lib.spconv_plan_create.restype = i32
+    lib.spconv_plan_create.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, i32]
+    lib.spconv_plan_create_ex.restype = i32
+    lib.spconv_plan_create_ex.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, i32,
+                                          ctypes.POINTER(spconv_options)]
+    lib.spconv_run.restype = i32
+    lib.spconv_run.argtypes = [vp, vp, vp, i32, i32, i32, vp]
+    lib.spconv_destroy.restype = i32
+    lib.spconv_destroy.argtypes = [vp]
+    lib.spconv_last_error.restype = ctypes.c_char_p
+    lib.spconv_last_error.argtypes = []
+    lib.spconv_options_init.restype = None
+    lib.spconv_options_init.argtypes = [ctypes.POINTER(spconv_options)]
+    lib.spconv_plan_get_info.restype = i32
+    lib.spconv_plan_get_info.argtypes = [vp, ctypes.POINTER(spconv_plan_info)]
+    lib.spconv_plan_unpack.restype = i32
+    lib.spconv_plan_unpack.argtypes = [vp, vp, vp, vp, vp]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def _arr(a, dtype):
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(status: int):
+    if status != OK:
+        raise SpconvError(status, spconv_last_error())
+
+
+def spconv_last_error() -> str:
+    return load_library().spconv_last_error().decode()
+
+
+def spconv_options_init() -> spconv_options:
+    o = spconv_options()
+    load_library().spconv_options_init(ctypes.byref(o))
+    return o
+
+
+def spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias=None, act="none",
+                       storage="f32", options: Optional[spconv_options] = None, check: bool = True):
+    """Create a plan from host CSR / 1xk block-CSR arrays.  Returns the plan handle (int).
+
+    With ``check=False`` returns ``(status, handle)`` instead of raising.
+    """
+    lib = load_library()
+    rp = _arr(row_ptr, np.int32)
+    ci = _arr(col_idx, np.int32)
+    va = _arr(values, np.float32)
+    bi = _arr(bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    if options is None:
+        status = lib.spconv_plan_create(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
+                                        _ptr(ci), _ptr(va), _ptr(bi), a, st)
+    else:
+        status = lib.spconv_plan_create_ex(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
+                                           _ptr(ci), _ptr(va), _ptr(bi), a, st, ctypes.byref(options))
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
+
+
+def _devptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def spconv_run(plan, x, y, n, h, w, stream=None, check: bool = True):
+    """Queue y = act(W x + b) on ``stream`` (torch stream, raw hipStream_t int, or None for torch's current)."""
+    lib = load_library()
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream().cuda_stream
+    elif not isinstance(stream, int):
+        stream = stream.cuda_stream
+    status = lib.spconv_run(plan, _devptr(x), _devptr(y), int(n), int(h), int(w), stream or None)
+    if check:
+        _check(status)
+    return status
+
+
+def spconv_destroy(plan):
+    _check(load_library().spconv_destroy(plan))
+
+
+def spconv_plan_get_info(plan) -> dict:
+    info = spconv_plan_info()
+    _check(load_library().spconv_plan_get_info(plan, ctypes.byref(info)))
+    return info.as_dict()
+
+
+def spconv_plan_unpack(plan):
+    """Return (row_ptr, col_idx, values, perm) rebuilt from the plan's packed host image."""
+    info = spconv_plan_get_info(plan)
+    rows = info["cout"] // info["block_rows"]
+    rp = np.zeros(rows + 1, np.int32)
+    ci = np.zeros(max(info["nnzb"], 1), np.int32)
+    va = np.zeros(max(info["nnzb"] * info["block_rows"], 1), np.float32)
+    perm = np.zeros(rows, np.int32)
+    _check(load_library().spconv_plan_unpack(plan, _ptr(rp), _ptr(ci), _ptr(va), _ptr(perm)))
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * info["block_rows"]], perm
+
+
+class Plan:
+    """Owning wrapper: ``Plan(...).run(x, y)`` with torch tensors [N, C, H, W]."""
+
+    def __init__(self, cout, cin, block_rows, row_ptr, col_idx, values, bias=None, act="none",
+                 storage="f32", **options):
+        opts = None
+        if options:
+            opts = spconv_options_init()
+            for k, v in options.items():
+                setattr(opts, k, int(v))
+        self.handle = spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage,
+                                         options=opts)
+        self.cout, self.cin, self.storage = int(cout), int(cin), storage
+
+    @classmethod
+    def from_layer(cls, layer, **options):
+        return cls(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
+                   layer.bias, layer.act, layer.storage, **options)
+
+    def info(self) -> dict:
+        return spconv_plan_get_info(self.handle)
+
+    def run(self, x, y=None, stream=None):
+        import torch
+        n, c, h, w = x.shape
+        if c != self.cin:
+            raise ValueError("x has %d channels, plan expects %d" % (c, self.cin))
+        if y is None:
+            y = torch.empty((n, self.cout, h, w), dtype=x.dtype, device=x.device)
+        spconv_run(self.handle, x, y, n, h, w, stream)
+        return y
+
+    def close(self):
+        if self.handle:
+            spconv_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

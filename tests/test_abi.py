@@ -1,0 +1,272 @@
+"""The C ABI and the host planner, without a GPU.
+
+* libspconv.so loads and exports every function include/spconv.h declares;
+* malformed CSR / block-CSR input is rejected with the documented status
+  before any device work;
+* host-only plans: the packed image unpacks back to the input exactly, the
+  processing order is a permutation sorted by nonzero count, the wave
+  assignment is balanced, fp16 storage rounds weights to nearest-even.
+"""
+
+import ctypes
+import os
+import re
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+import paper_1911_09723_amd as sp
+from paper_1911_09723_amd import spconv as spmod
+from synth import make_layer
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "spconv.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(spconv_[a-z_]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_header_declares_the_boundary():
+    names = _declared_functions()
+    for required in ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error"):
+        assert required in names
+    assert set(names) == set(spmod.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(spmod.LIBRARY_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", spmod.LIBRARY_PATH], capture_output=True, text=True)
+    exported = set(re.findall(r" T (spconv_\w+)", out.stdout))
+    assert set(_declared_functions()) <= exported
+
+
+def _host_opts(**kw):
+    o = sp.spconv_options_init()
+    o.host_only = 1
+    for k, v in kw.items():
+        setattr(o, k, v)
+    return o
+
+
+def _create(layer=None, check=True, **kw):
+    args = dict(cout=64, cin=32, block_rows=1, row_ptr=None, col_idx=None, values=None, bias=None,
+                act="relu", storage="f32")
+    if layer is not None:
+        args.update(cout=layer.cout, cin=layer.cin, block_rows=layer.block_rows, row_ptr=layer.row_ptr,
+                    col_idx=layer.col_idx, values=layer.values, bias=layer.bias, act=layer.act,
+                    storage=layer.storage)
+    opts = kw.pop("options", None) or _host_opts()
+    args.update(kw)
+    return sp.spconv_plan_create(args["cout"], args["cin"], args["block_rows"], args["row_ptr"],
+                                 args["col_idx"], args["values"], args["bias"], args["act"], args["storage"],
+                                 options=opts, check=check)
+
+
+def _status(**kw):
+    layer = kw.pop("layer", None) or make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    st, h = _create(layer, check=False, **kw)
+    if h:
+        sp.spconv_destroy(h)
+    return st, sp.spconv_last_error()
+
+
+def test_valid_host_plan():
+    st, msg = _status()
+    assert st == sp.spconv.OK and msg == ""
+
+
+@pytest.mark.parametrize("mutate,expect,words", [
+    (lambda L: L.row_ptr.__setitem__(0, 1), sp.spconv.E_FORMAT, "row_ptr[0]"),
+    (lambda L: L.row_ptr.__setitem__(5, L.row_ptr[4] - 1), sp.spconv.E_FORMAT, "decreases"),
+    (lambda L: L.col_idx.__setitem__(3, 32), sp.spconv.E_FORMAT, "outside"),
+    (lambda L: L.col_idx.__setitem__(0, -1), sp.spconv.E_FORMAT, "outside"),
+    (lambda L: L.values.__setitem__(2, np.nan), sp.spconv.E_FORMAT, "not finite"),
+    (lambda L: L.values.__setitem__(2, np.inf), sp.spconv.E_FORMAT, "not finite"),
+    (lambda L: L.bias.__setitem__(2, np.inf), sp.spconv.E_FORMAT, "bias"),
+])
+def test_malformed_csr_rejected(mutate, expect, words):
+    layer = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    mutate(layer)
+    st, msg = _status(layer=layer)
+    assert st == expect and words in msg, (st, msg)
+
+
+def test_duplicate_or_unsorted_columns_rejected():
+    layer = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    s = layer.row_ptr[3]
+    assert layer.row_ptr[4] - s >= 2
+    layer.col_idx[s + 1] = layer.col_idx[s]
+    st, msg = _status(layer=layer)
+    assert st == sp.spconv.E_FORMAT and "ascending" in msg
+
+
+@pytest.mark.parametrize("kw,expect", [
+    (dict(cout=63, block_rows=4), sp.spconv.E_SHAPE),
+    (dict(cout=0), sp.spconv.E_SHAPE),
+    (dict(cin=0), sp.spconv.E_SHAPE),
+    (dict(block_rows=2), sp.spconv.E_UNSUPPORTED),
+    (dict(block_rows=0), sp.spconv.E_ARG),
+    (dict(act=7), sp.spconv.E_ARG),
+    (dict(storage=5), sp.spconv.E_ARG),
+    (dict(row_ptr=None), sp.spconv.E_ARG),
+])
+def test_bad_arguments(kw, expect):
+    layer = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    if kw.get("row_ptr", 1) is None:
+        layer.row_ptr = None
+        kw = {}
+    st, msg = _status(layer=layer, **kw)
+    assert st == expect and msg, (st, msg)
+
+
+def test_null_arrays_with_nonzeros_rejected():
+    layer = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    layer.col_idx = None
+    st, msg = _status(layer=layer)
+    assert st == sp.spconv.E_ARG and "NULL" in msg
+
+
+def test_options_validated():
+    for kw in (dict(lanes_per_row=12), dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3)):
+        st, msg = _status(options=_host_opts(**kw))
+        assert st == sp.spconv.E_ARG, kw
+    o = _host_opts()
+    o.struct_size = 4
+    st, msg = _status(options=o)
+    assert st == sp.spconv.E_ARG and "struct_size" in msg
+
+
+def test_out_null_and_destroy_null():
+    lib = sp.load_library()
+    assert lib.spconv_plan_create(None, 4, 4, 1, None, None, None, None, 0, 0) == sp.spconv.E_ARG
+    assert lib.spconv_destroy(None) == sp.spconv.OK
+
+
+def test_run_refuses_host_only_plan_and_null_plan():
+    layer = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False)
+    h = _create(layer)
+    try:
+        assert sp.spconv_run(h, 1 << 20, 2 << 20, 1, 2, 2, stream=0, check=False) == sp.spconv.E_ARG
+        assert "host_only" in sp.spconv_last_error()
+    finally:
+        sp.spconv_destroy(h)
+    assert sp.load_library().spconv_run(None, None, None, 1, 1, 1, None) == sp.spconv.E_ARG
+
+
+def test_injected_allocation_failure_reports_nomem():
+    code = ("import paper_1911_09723_amd as sp; from synth import make_layer;"
+            "L = make_layer(32, 64, 2, 2, 1, 0.8, seed=1, with_x=False);"
+            "st, h = sp.spconv_plan_create(L.cout, L.cin, 1, L.row_ptr, L.col_idx, L.values, L.bias,"
+            " 'relu', 'f32', check=False);"
+            "print(st, h, sp.spconv_last_error())")
+    env = dict(os.environ, SPCONV_FAULT="alloc", PYTHONPATH=ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, env=env, cwd=ROOT)
+    assert out.returncode == 0, out.stderr
+    st, h, msg = out.stdout.split(" ", 2)
+    assert int(st) == sp.spconv.E_NOMEM and h == "None" and "SPCONV_FAULT" in msg
+
+
+@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("pattern", ["uniform", "beta"])
+@pytest.mark.parametrize("lanes", [0, 8, 16, 32, 64])
+def test_pack_unpack_round_trip_and_order(k, pattern, lanes):
+    if pattern == "beta" and k == 4:
+        pytest.skip("beta row densities are defined for unstructured masks")
+    layer = make_layer(96, 160, 2, 2, 1, 0.85, block_rows=k, pattern=pattern, seed=4, with_x=False)
+    h = _create(layer, options=_host_opts(lanes_per_row=lanes))
+    try:
+        info = sp.spconv_plan_get_info(h)
+        rp, ci, va, perm = sp.spconv_plan_unpack(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert np.array_equal(rp, layer.row_ptr) and np.array_equal(ci, layer.col_idx)
+    assert np.array_equal(va, layer.values)
+    rows = 160 // k
+    assert sorted(perm.tolist()) == list(range(rows))
+    counts = np.diff(layer.row_ptr)[perm]
+    assert np.all(np.diff(counts) <= 0), "rows not in descending nonzero order"
+    ties = [perm[i] < perm[i + 1] for i in range(rows - 1) if counts[i] == counts[i + 1]]
+    assert all(ties), "equal-length rows not kept in index order"
+    assert info["nnzb"] == layer.nnzb and info["slots"] >= layer.nnzb
+    assert info["lanes_per_row"] == (lanes or 16) and info["groups"] * info["lanes_per_row"] == 64
+
+
+def test_natural_order_when_reorder_off():
+    layer = make_layer(64, 64, 2, 2, 1, 0.8, seed=5, with_x=False)
+    h = _create(layer, options=_host_opts(reorder=0))
+    try:
+        _, _, _, perm = sp.spconv_plan_unpack(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert np.array_equal(perm, np.arange(64))
+
+
+def test_lpt_balance_on_uniform_rows():
+    layer = make_layer(512, 512, 1, 1, 1, 0.9, seed=2020, with_x=False)
+    h = _create(layer)
+    try:
+        info = sp.spconv_plan_get_info(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert info["max_wave_cost"] <= 1.05 * info["sum_wave_cost"] / info["waves"]
+    assert info["slots"] <= 1.02 * layer.nnzb
+
+
+def test_lpt_balance_on_heavy_tailed_rows():
+    layer = make_layer(960, 160, 1, 1, 1, 0.85, pattern="beta", seed=3070, with_x=False)
+    h = _create(layer)
+    try:
+        info = sp.spconv_plan_get_info(h)
+    finally:
+        sp.spconv_destroy(h)
+    mean = info["sum_wave_cost"] / info["waves"]
+    # LPT bound: max load <= mean + largest single job
+    counts = np.sort(np.diff(layer.row_ptr))[::-1]
+    largest_bundle = counts[0] + 3
+    assert info["max_wave_cost"] <= mean + largest_bundle
+
+
+def test_geometry_choice():
+    def info_for(cin, storage):
+        layer = make_layer(cin, 32, 1, 1, 1, 0.9, storage=storage, seed=1, with_x=False)
+        h = _create(layer)
+        try:
+            return sp.spconv_plan_get_info(h)
+        finally:
+            sp.spconv_destroy(h)
+    i = info_for(512, "f32")
+    assert (i["kernel"], i["lanes_per_row"], i["tile_cols"], i["lds_bytes"]) == (0, 16, 64, 512 * 256)
+    i = info_for(512, "f16")
+    assert (i["kernel"], i["lanes_per_row"], i["tile_cols"], i["cols_per_lane"]) == (0, 16, 128, 8)
+    i = info_for(1024, "f32")
+    assert (i["kernel"], i["lanes_per_row"], i["lds_bytes"]) == (0, 8, 1024 * 128)
+    i = info_for(1500, "f32")
+    assert i["kernel"] == 1 and i["lds_bytes"] == 0
+
+
+def test_f16_weights_rounded_to_nearest_even():
+    rng = np.random.default_rng(0)
+    special = np.array([1.0, 1 + 2 ** -11, 1 + 3 * 2 ** -11, 65504.0, 65519.0, 6e-8, 2.0 ** -25,
+                        3 * 2.0 ** -26, -2.0 ** -24, 1e-10, 0.0, -0.0, 5.96e-8, 6.1e-5, 6.09e-5],
+                       dtype=np.float32)
+    vals = np.concatenate([special, (rng.standard_normal(4000) * rng.choice([1e-6, 1e-3, 1, 300], 4000))
+                           .astype(np.float32)])
+    n = vals.size
+    cin = n
+    rp = np.array([0, n], np.int32)
+    ci = np.arange(n, dtype=np.int32)
+    h = sp.spconv_plan_create(1, cin, 1, rp, ci, vals, None, "none", "f16", options=_host_opts())
+    try:
+        _, _, va, _ = sp.spconv_plan_unpack(h)
+    finally:
+        sp.spconv_destroy(h)
+    expect = vals.astype(np.float16).astype(np.float32)
+    assert np.array_equal(va.view(np.uint32), expect.view(np.uint32))
