@@ -125,7 +125,13 @@ typedef struct {
     int32_t reorder;       /* 1 (default): process rows in descending nonzero order; 0: natural order */
     int32_t host_only;     /* 1: plan on the host only, no device memory; spconv_run refuses it */
     int32_t lanes_per_row; /* 0 = choose automatically; else 8, 16, 32 or 64 lanes share one row */
-    int32_t waves;         /* 0 = choose automatically; else 1..16 wavefronts per workgroup */
+    int32_t waves;         /* 0 = choose automatically; else the number of compute wavefronts per
+                              workgroup (with the loader wavefronts, at most 16 in all) */
+    int32_t vecs_per_lane; /* 0 = choose automatically; else 1 or 2 16-byte X vectors per lane
+                              and nonzero (the lane then owns 4 or 8 fp32 / 8 or 16 fp16 columns) */
+    int32_t prefetch;      /* 1 (default): loader wavefronts fetch the next strip while the others
+                              compute; 0: every wavefront computes and strips are copied between
+                              tiles */
 } spconv_options;
 
 /* Fill *opts with the defaults used by spconv_plan_create. */
@@ -142,9 +148,11 @@ typedef struct {
     int32_t storage, act;
     int32_t kernel;        /* 0: LDS-strip kernel; 1: direct-load kernel for wide inputs */
     int32_t lanes_per_row; /* lanes sharing one (block) row */
+    int32_t vecs_per_lane; /* 16-byte X vectors each lane reads per nonzero */
     int32_t cols_per_lane; /* output columns each lane accumulates */
     int32_t tile_cols;     /* columns per workgroup tile = lanes_per_row * cols_per_lane */
-    int32_t waves;         /* wavefronts per workgroup */
+    int32_t waves;         /* compute wavefronts per workgroup */
+    int32_t loader_waves;  /* wavefronts per workgroup that prefetch the next strip */
     int32_t groups;        /* row groups (rows processed together by one wavefront) */
     int32_t lds_bytes;     /* LDS per workgroup */
     int64_t nnzb;          /* stored blocks */

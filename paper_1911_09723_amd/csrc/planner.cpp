@@ -163,25 +163,61 @@ namespace {
 // Per-bundle fixed cost (epilogue, header loads) in units of one slot step.
 constexpr int64_t kBundleOverhead = 3;
 
+// Bytes of the per-bundle table (rows and biases) the strip kernel keeps in LDS.
+int64_t table_bytes(const Input &in, int g) {
+    const int64_t groups = 64 / g;
+    const int64_t rows = in.cout / in.block_rows;
+    const int64_t bundles = (rows + groups - 1) / groups;
+    return ((bundles * groups * (1 + in.block_rows) * 4) + 15) & ~int64_t(15);
+}
+
 void choose_geometry(const Input &in, const Options &opt, PackedPlan &p) {
     const int e = in.storage == 1 ? 2 : 4;
-    p.cols_per_lane = kLaneBytes / e;
-    auto strip_bytes = [&](int g) { return static_cast<int64_t>(in.cin) * g * kLaneBytes; };
-    int g = opt.lanes_per_row;
-    if (g == 0) {
-        g = 16;
-        if (strip_bytes(16) > kMaxLdsBytes && strip_bytes(8) <= kMaxLdsBytes)
+    auto strip_bytes = [&](int g, int nv) { return static_cast<int64_t>(in.cin) * g * nv * kLaneBytes; };
+    auto fits = [&](int g, int nv) { return strip_bytes(g, nv) + table_bytes(in, g) <= kMaxLdsBytes; };
+    // Strip rows of 256 bytes: 16 lanes x one 16-byte vector read 256
+    // contiguous bytes (all 64 LDS banks) per row, so the four lane groups of a
+    // wavefront take four conflict-free LDS cycles.  Wider inputs fall back to
+    // 128-byte rows (8 lanes), then to the direct-load kernel.
+    int g = opt.lanes_per_row, nv = opt.vecs_per_lane;
+    if (g == 0 && nv == 0) {
+        if (fits(16, 1)) {
+            g = 16;
+            nv = 1;
+        } else if (fits(8, 1)) {
             g = 8;
+            nv = 1;
+        } else {
+            g = 16;
+            nv = 1;
+        }
+    } else {
+        if (g == 0)
+            g = 16;
+        if (nv == 0)
+            nv = 1;
     }
+    const bool strip = fits(g, nv);
+    if (!strip)
+        nv = 1;  // the direct-load kernel reads one vector per lane
     p.lanes_per_row = g;
+    p.vecs_per_lane = nv;
     p.groups = 64 / g;
+    p.cols_per_lane = nv * kLaneBytes / e;
     p.tile_cols = g * p.cols_per_lane;
-    if (strip_bytes(g) <= kMaxLdsBytes) {
+    if (strip) {
         p.kernel = KERNEL_STRIP;
-        p.lds_bytes = static_cast<int32_t>(strip_bytes(g));
+        p.strip_bytes = static_cast<int32_t>(strip_bytes(g, nv));
+        p.lds_bytes = static_cast<int32_t>(strip_bytes(g, nv) + table_bytes(in, g));
+        p.loader_waves = opt.prefetch
+                             ? static_cast<int32_t>((strip_bytes(g, nv) + kLoaderBytesPerWave - 1) /
+                                                    kLoaderBytesPerWave)
+                             : 0;
     } else {
         p.kernel = KERNEL_DIRECT;
+        p.strip_bytes = 0;
         p.lds_bytes = 0;
+        p.loader_waves = 0;
     }
 }
 
@@ -200,8 +236,20 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         err = "waves must be in [0, 16]";
         return E_ARG;
     }
+    if (opt.vecs_per_lane != 0 && opt.vecs_per_lane != 1 && opt.vecs_per_lane != 2) {
+        err = "vecs_per_lane must be 0, 1 or 2";
+        return E_ARG;
+    }
+    if (opt.lanes_per_row == 64 && opt.vecs_per_lane == 2) {
+        err = "lanes_per_row = 64 takes one vector per lane";
+        return E_ARG;
+    }
     if (opt.reorder != 0 && opt.reorder != 1) {
         err = "reorder must be 0 or 1";
+        return E_ARG;
+    }
+    if (opt.prefetch != 0 && opt.prefetch != 1) {
+        err = "prefetch must be 0 or 1";
         return E_ARG;
     }
 
@@ -234,9 +282,18 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     for (int32_t b = 0; b < nb; ++b)
         for (int32_t g = 0; g < G && b * G + g < rows; ++g)
             blen[b] = std::max(blen[b], len(p.perm[b * G + g]));
+    // padded to whole steps of 4 slots, at least one step
+    for (int32_t b = 0; b < nb; ++b)
+        blen[b] = std::max<int32_t>(4, (blen[b] + 3) & ~3);
 
     // 3. longest-processing-time-first assignment of bundles to waves
-    int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(16, std::max<int32_t>(nb, 1));
+    const int32_t max_waves = kMaxWaves - p.loader_waves;
+    if (opt.waves > max_waves) {
+        err = "waves = " + std::to_string(opt.waves) + " plus " + std::to_string(p.loader_waves) +
+              " loader waves exceeds " + std::to_string(kMaxWaves) + " wavefronts per workgroup";
+        return E_ARG;
+    }
+    int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(max_waves, std::max<int32_t>(nb, 1));
     p.waves = waves;
     std::vector<int32_t> order(nb);
     std::iota(order.begin(), order.end(), 0);
@@ -258,23 +315,23 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     p.max_wave_cost = waves ? *std::max_element(load.begin(), load.end()) : 0;
     p.sum_wave_cost = std::accumulate(load.begin(), load.end(), int64_t(0));
 
-    // 4. pack, bundles stored in wave order
+    // 4. pack, bundles stored in wave order; every bundle is a whole number
+    // of steps (4 slots per lane group) and at least one step long
     p.wave_ptr.assign(waves + 1, 0);
     p.hdr.reserve(4 * static_cast<size_t>(nb));
     p.rows.reserve(static_cast<size_t>(G) * nb);
+    p.bundle_bias.reserve(static_cast<size_t>(G) * nb * k);
     int64_t slot = 0;
     for (int32_t w = 0; w < waves; ++w) {
         for (int32_t b : lists[w]) {
             const int32_t L = blen[b];
-            const int32_t L4 = L & ~3;
-            slot = (slot + 3) & ~int64_t(3);
             if (slot + static_cast<int64_t>(L) * G > (int64_t(1) << 30)) {
                 err = "packed plan too large";
                 return E_SHAPE;
             }
             p.hdr.push_back(static_cast<int32_t>(slot));
-            p.hdr.push_back(L4);
-            p.hdr.push_back(L - L4);
+            p.hdr.push_back(L / 4);
+            p.hdr.push_back(0);
             p.hdr.push_back(0);
             const size_t need = static_cast<size_t>(slot + static_cast<int64_t>(L) * G);
             p.idx.resize(need, 0);
@@ -283,17 +340,17 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
                 const int32_t pos = b * G + g;
                 const int32_t rb = pos < rows ? p.perm[pos] : -1;
                 p.rows.push_back(rb);
+                for (int32_t i = 0; i < k; ++i)
+                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + i] : 0.0f);
+                // the last step of the bundle is marked in its first slot
+                p.idx[slot + (static_cast<int64_t>(L / 4 - 1) * G + g) * 4] |= kLastStepFlag;
                 if (rb < 0)
                     continue;
                 const int32_t s0 = in.row_ptr[rb];
                 const int32_t n = len(rb);
                 for (int32_t t = 0; t < n; ++t) {
-                    int64_t sl;
-                    if (t < L4)
-                        sl = slot + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
-                    else
-                        sl = slot + static_cast<int64_t>(L4) * G + static_cast<int64_t>(t - L4) * G + g;
-                    p.idx[sl] = in.col_idx[s0 + t];
+                    const int64_t sl = slot + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
+                    p.idx[sl] = (p.idx[sl] & kLastStepFlag) | in.col_idx[s0 + t];
                     for (int32_t i = 0; i < k; ++i) {
                         float v = in.values[static_cast<int64_t>(s0 + t) * k + i];
                         if (in.storage == 1)
@@ -306,15 +363,18 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         }
         p.wave_ptr[w + 1] = static_cast<int32_t>(p.hdr.size() / 4);
     }
-    // keep every stream a whole number of 16-byte vectors, non-empty
-    slot = std::max<int64_t>((slot + 3) & ~int64_t(3), 4);
+    // Keep every stream a whole number of 16-byte vectors and leave
+    // kLookaheadSteps main-loop steps (4 slots per lane group each) of padding
+    // after the last bundle: the kernel fetches slots of later steps before it
+    // knows whether the bundle continues.
+    slot = ((slot + 3) & ~int64_t(3)) + (kLookaheadSteps + 1) * 4 * static_cast<int64_t>(G) + 4;
     p.idx.resize(static_cast<size_t>(slot), 0);
     p.val.resize(static_cast<size_t>(slot) * k, 0.0f);
     p.slots = slot;
     if (p.hdr.empty())
         p.hdr.assign(4, 0);
-    if (p.rows.empty())
-        p.rows.assign(G, -1);
+    // LDS copy of the per-bundle rows and biases, after the strip
+    p.meta_bytes = static_cast<int32_t>(p.rows.size() * sizeof(int32_t) + p.bundle_bias.size() * sizeof(float));
 
     p.bias.assign(in.cout, 0.0f);
     if (in.bias)
@@ -332,18 +392,13 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
     // each row's real entries are the first row_nnz[rb] slots of its sequence
     for (int32_t b = 0; b < nb; ++b) {
         const int64_t S = p.hdr[4 * b];
-        const int32_t L4 = p.hdr[4 * b + 1];
         for (int32_t g = 0; g < G; ++g) {
             const int32_t rb = p.rows[static_cast<size_t>(b) * G + g];
             if (rb < 0)
                 continue;
             for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
-                int64_t sl;
-                if (t < L4)
-                    sl = S + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
-                else
-                    sl = S + static_cast<int64_t>(L4) * G + static_cast<int64_t>(t - L4) * G + g;
-                cols[rb].push_back(p.idx[sl]);
+                const int64_t sl = S + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
+                cols[rb].push_back(p.idx[sl] & ~kLastStepFlag);
                 for (int32_t i = 0; i < k; ++i)
                     vals[rb].push_back(p.val[sl * k + i]);
             }

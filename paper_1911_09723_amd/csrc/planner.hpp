@@ -13,24 +13,26 @@
 //   wavefront processes at the same time, one row per lane group.  Bundles
 //   are made of consecutive rows in processing order (descending nonzero
 //   count unless reordering is off), so the rows of a bundle have similar
-//   lengths.  Its length L is the longest of its rows; shorter rows are padded
-//   with (channel 0, weight 0) slots, which add an exact zero.
+//   lengths.  Its length L is the longest of its rows rounded up to a multiple
+//   of 4 (at least 4); shorter rows are padded with (channel 0, weight 0)
+//   slots, which add an exact zero.  A *step* is 4 slots of every row.
 //
 //   hdr[4*b + 0]  first slot of bundle b (a multiple of 4)
-//   hdr[4*b + 1]  L4 = 4 * floor(L / 4): slots in the unrolled main part, per row
-//   hdr[4*b + 2]  L - L4: slots in the tail, per row
-//   rows[groups*b + g]  block row handled by lane group g, or -1 (padding group)
+//   hdr[4*b + 1]  L / 4: steps of bundle b
+//   rows[groups*b + g]         block row handled by lane group g, or -1 (padding group)
+//   bundle_bias[(groups*b + g)*k + i]  bias of row rows[..]*k + i (0 for padding)
 //
 //   Slot numbering inside bundle b (base S = hdr[4*b]):
-//     main part: slot S + (t4 * groups + g) * 4 + u   for step t4 < L4/4, u < 4
-//     tail:      slot S + L4 * groups + t * groups + g  for t < L - L4
+//     slot S + (t4 * groups + g) * 4 + u   for step t4 < L/4, u < 4
 //   so one 16-byte load fetches the next 4 channel indices of a row.
-//   idx[slot]        input channel c
+//   idx[slot]        input channel c; the first slot of a bundle's last step
+//                    also carries kLastStepFlag
 //   val[slot*k + i]  weight of block row element i (fp16-rounded for fp16 storage)
 //
 //   Bundles are assigned to the `waves` wavefronts of a workgroup by longest
 //   processing time first; wave_ptr[w] .. wave_ptr[w+1] are wave w's bundles,
-//   which are stored contiguously in that order.
+//   which are stored contiguously in that order, so each wavefront reads one
+//   continuous stream of steps.
 //
 // The per-row summation order is ascending input channel (the CSR order), with
 // padding zeros in between; it does not depend on the bundle grouping, so the
@@ -49,8 +51,19 @@ enum Kernel { KERNEL_STRIP = 0, KERNEL_DIRECT = 1 };
 
 // Largest LDS footprint of one workgroup on gfx950 (160 KiB per CU).
 constexpr int64_t kMaxLdsBytes = 160 * 1024;
-// Every lane reads 16 bytes of X per nonzero: 4 fp32 or 8 fp16 columns.
+// Every X read of a lane is one 16-byte vector: 4 fp32 or 8 fp16 columns.
 constexpr int kLaneBytes = 16;
+// Wavefronts per workgroup (1024 threads).
+constexpr int32_t kMaxWaves = 16;
+// Bit set in the channel index of the first slot of a bundle's last step.  It
+// lies above any valid channel and above the bits that survive the kernels'
+// scaling of the channel to a byte offset, so the kernels read it without
+// masking it out.
+constexpr int32_t kLastStepFlag = 1 << 30;
+// Main-loop steps the kernels may fetch past the end of a bundle.
+constexpr int64_t kLookaheadSteps = 4;
+// Strip bytes one loader wavefront holds in registers: 64 lanes x 16 vectors.
+constexpr int64_t kLoaderBytesPerWave = 64 * 16 * 16;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -67,6 +80,8 @@ struct Options {
     int32_t host_only = 0;
     int32_t lanes_per_row = 0;
     int32_t waves = 0;
+    int32_t vecs_per_lane = 0;
+    int32_t prefetch = 1;
 };
 
 struct PackedPlan {
@@ -75,11 +90,14 @@ struct PackedPlan {
     // launch geometry
     int32_t kernel = KERNEL_STRIP;
     int32_t lanes_per_row = 16;  // G
+    int32_t vecs_per_lane = 1;   // 16-byte X vectors each lane reads per nonzero
     int32_t groups = 4;          // 64 / G
-    int32_t cols_per_lane = 4;   // 16 bytes / element size
+    int32_t cols_per_lane = 4;   // vecs_per_lane * 16 bytes / element size
     int32_t tile_cols = 64;      // G * cols_per_lane
-    int32_t waves = 1;
-    int32_t lds_bytes = 0;
+    int32_t waves = 1;           // compute wavefronts (each owns a list of bundles)
+    int32_t loader_waves = 0;    // wavefronts that prefetch the next strip (strip kernel)
+    int32_t lds_bytes = 0;       // strip + bundle table (strip kernel)
+    int32_t strip_bytes = 0;
     // packed streams
     std::vector<int32_t> idx;
     std::vector<float> val;
@@ -87,6 +105,8 @@ struct PackedPlan {
     std::vector<int32_t> rows;
     std::vector<int32_t> wave_ptr;
     std::vector<float> bias;
+    std::vector<float> bundle_bias;  // bias of the row of each (bundle, group, block element)
+    int32_t meta_bytes = 0;          // rows + bundle_bias, copied into LDS by the strip kernel
     std::vector<int32_t> perm;     // block rows in processing order
     std::vector<int32_t> row_nnz;  // stored blocks per block row (host only; for unpacking)
     // statistics

@@ -13,6 +13,7 @@
 #include <cstring>
 #include <new>
 #include <string>
+#include <vector>
 
 #include "launch.hpp"
 #include "planner.hpp"
@@ -67,17 +68,21 @@ spconv::Input make_input(int32_t cout, int32_t cin, int32_t block_rows, const in
 
 spconv_status upload(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
+    // bundle table: rows, then the biases of those rows as fp32 bit patterns
+    std::vector<int32_t> meta(h.rows.begin(), h.rows.end());
+    meta.resize(h.rows.size() + h.bundle_bias.size());
+    if (!h.bundle_bias.empty())
+        std::memcpy(meta.data() + h.rows.size(), h.bundle_bias.data(), h.bundle_bias.size() * sizeof(float));
     struct Part {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[6] = {
+    } parts[5] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
-        {h.rows.data(), h.rows.size() * sizeof(int32_t), 0},
+        {meta.data(), meta.size() * sizeof(int32_t), 0},
         {h.wave_ptr.data(), h.wave_ptr.size() * sizeof(int32_t), 0},
-        {h.bias.data(), h.bias.size() * sizeof(float), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -110,9 +115,8 @@ spconv_status upload(spconv_plan_s *pl) {
     d.idx = reinterpret_cast<const int32_t *>(base + parts[0].off);
     d.val = reinterpret_cast<const float *>(base + parts[1].off);
     d.hdr = reinterpret_cast<const int32_t *>(base + parts[2].off);
-    d.rows = reinterpret_cast<const int32_t *>(base + parts[3].off);
+    d.meta = reinterpret_cast<const int32_t *>(base + parts[3].off);
     d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[4].off);
-    d.bias = reinterpret_cast<const float *>(base + parts[5].off);
     return SPCONV_OK;
 }
 
@@ -121,14 +125,21 @@ void fill_device_geometry(spconv_plan_s *pl) {
     spconv::DevicePlan &d = pl->dev;
     d.kernel = h.kernel;
     d.lanes_per_row = h.lanes_per_row;
+    d.vecs_per_lane = h.vecs_per_lane;
     d.tile_cols = h.tile_cols;
     d.waves = h.waves;
+    d.loader_waves = h.loader_waves;
     d.lds_bytes = h.lds_bytes;
     d.k = h.k;
     d.storage = h.storage;
     d.act = h.act;
     d.cin = h.cin;
     d.cout = h.cout;
+    d.idx_bytes = static_cast<int32_t>(h.idx.size() * sizeof(int32_t));
+    d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
+    d.nbundles = static_cast<int32_t>(h.hdr.size() / 4);
+    d.meta_words = static_cast<int32_t>(h.rows.size() + h.bundle_bias.size());
+    d.strip_bytes = h.strip_bytes;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -146,6 +157,7 @@ void spconv_options_init(spconv_options *opts) {
     std::memset(opts, 0, sizeof(*opts));
     opts->struct_size = static_cast<int32_t>(sizeof(spconv_options));
     opts->reorder = 1;
+    opts->prefetch = 1;
 }
 
 spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
@@ -170,6 +182,8 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     po.host_only = o.host_only;
     po.lanes_per_row = o.lanes_per_row;
     po.waves = o.waves;
+    po.vecs_per_lane = o.vecs_per_lane;
+    po.prefetch = o.prefetch;
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
     if (!pl)
@@ -191,6 +205,11 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     pl->host_only = o.host_only == 1;
     if (!pl->host_only) {
         spconv_status us = upload(pl);
+        if (us == SPCONV_OK) {
+            hipError_t pe = spconv::prepare_launch(pl->dev);
+            if (pe != hipSuccess)
+                us = hip_fail("kernel launch set-up", pe);
+        }
         if (us != SPCONV_OK) {
             if (pl->dmem)
                 (void)hipFree(pl->dmem);
@@ -242,10 +261,10 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     if (dev != plan->device)
         return fail(SPCONV_E_ARG, "plan was created on device " + std::to_string(plan->device) +
                                       " but the current device is " + std::to_string(dev));
-    const int32_t q = p.cols_per_lane;
-    const int32_t vec = (hw % q == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+    const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
+    const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    he = spconv::launch_spmm(plan->dev, x, y, m, static_cast<int32_t>(hw), vec,
+    he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
                              static_cast<hipStream_t>(stream));
     if (he != hipSuccess)
         return hip_fail("kernel launch", he);
@@ -281,9 +300,11 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->act = p.act;
     info->kernel = p.kernel;
     info->lanes_per_row = p.lanes_per_row;
+    info->vecs_per_lane = p.vecs_per_lane;
     info->cols_per_lane = p.cols_per_lane;
     info->tile_cols = p.tile_cols;
     info->waves = p.waves;
+    info->loader_waves = p.loader_waves;
     info->groups = p.groups;
     info->lds_bytes = p.lds_bytes;
     info->nnzb = p.nnzb;

@@ -135,7 +135,8 @@ def test_null_arrays_with_nonzeros_rejected():
 
 
 def test_options_validated():
-    for kw in (dict(lanes_per_row=12), dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3)):
+    for kw in (dict(lanes_per_row=12), dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3),
+               dict(vecs_per_lane=3), dict(lanes_per_row=64, vecs_per_lane=2)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw
     o = _host_opts()
@@ -196,7 +197,8 @@ def test_pack_unpack_round_trip_and_order(k, pattern, lanes):
     ties = [perm[i] < perm[i + 1] for i in range(rows - 1) if counts[i] == counts[i + 1]]
     assert all(ties), "equal-length rows not kept in index order"
     assert info["nnzb"] == layer.nnzb and info["slots"] >= layer.nnzb
-    assert info["lanes_per_row"] == (lanes or 16) and info["groups"] * info["lanes_per_row"] == 64
+    assert info["lanes_per_row"] == (lanes or 16)
+    assert info["groups"] * info["lanes_per_row"] == 64
 
 
 def test_natural_order_when_reorder_off():
@@ -217,7 +219,8 @@ def test_lpt_balance_on_uniform_rows():
     finally:
         sp.spconv_destroy(h)
     assert info["max_wave_cost"] <= 1.05 * info["sum_wave_cost"] / info["waves"]
-    assert info["slots"] <= 1.02 * layer.nnzb
+    # bundles are whole steps of 4 slots: about 1.5 padding slots per row, plus the look-ahead pad
+    assert info["slots"] <= 1.06 * layer.nnzb
 
 
 def test_lpt_balance_on_heavy_tailed_rows():
@@ -235,21 +238,39 @@ def test_lpt_balance_on_heavy_tailed_rows():
 
 
 def test_geometry_choice():
-    def info_for(cin, storage):
-        layer = make_layer(cin, 32, 1, 1, 1, 0.9, storage=storage, seed=1, with_x=False)
+    def info_for(cin, storage, k=1):
+        layer = make_layer(cin, 32, 1, 1, 1, 0.9, block_rows=k, storage=storage, seed=1, with_x=False)
         h = _create(layer)
         try:
             return sp.spconv_plan_get_info(h)
         finally:
             sp.spconv_destroy(h)
-    i = info_for(512, "f32")
-    assert (i["kernel"], i["lanes_per_row"], i["tile_cols"], i["lds_bytes"]) == (0, 16, 64, 512 * 256)
-    i = info_for(512, "f16")
-    assert (i["kernel"], i["lanes_per_row"], i["tile_cols"], i["cols_per_lane"]) == (0, 16, 128, 8)
-    i = info_for(1024, "f32")
-    assert (i["kernel"], i["lanes_per_row"], i["lds_bytes"]) == (0, 8, 1024 * 128)
+    keys = ("kernel", "lanes_per_row", "vecs_per_lane", "tile_cols", "lds_bytes", "loader_waves")
+
+    def table(cout, k, lanes):
+        # per-bundle output rows and biases kept in LDS after the strip, 16-byte rounded
+        groups = 64 // lanes
+        bundles = -(-(cout // k) // groups)
+        return -(-(bundles * groups * (1 + k) * 4) // 16) * 16
+    # 256-byte strip rows: 16 lanes x one 16-byte vector
+    assert tuple(info_for(512, "f32")[k] for k in keys) == (0, 16, 1, 64, 512 * 256 + table(32, 1, 16), 8)
+    assert tuple(info_for(512, "f32", 4)[k] for k in keys) == (0, 16, 1, 64, 512 * 256 + table(32, 4, 16), 8)
+    assert tuple(info_for(320, "f16", 4)[k] for k in keys) == (0, 16, 1, 128, 320 * 256 + table(32, 4, 16), 5)
+    assert tuple(info_for(24, "f32")[k] for k in keys) == (0, 16, 1, 64, 24 * 256 + table(32, 1, 16), 1)
+    # wider inputs: 128-byte rows, then the direct-load kernel
+    assert tuple(info_for(1024, "f32")[k] for k in keys) == (0, 8, 1, 32, 1024 * 128 + table(32, 1, 8), 8)
     i = info_for(1500, "f32")
-    assert i["kernel"] == 1 and i["lds_bytes"] == 0
+    assert i["kernel"] == 1 and i["lds_bytes"] == 0 and i["loader_waves"] == 0 and i["vecs_per_lane"] == 1
+    i = info_for(512, "f32")
+    assert i["waves"] + i["loader_waves"] <= 16
+
+
+def test_too_many_waves_with_loaders_rejected():
+    layer = make_layer(512, 64, 1, 1, 1, 0.9, seed=1, with_x=False)
+    st, msg = _status(layer=layer, options=_host_opts(waves=9))
+    assert st == sp.spconv.E_ARG and "loader" in msg
+    st, msg = _status(layer=layer, options=_host_opts(waves=8))
+    assert st == sp.spconv.OK
 
 
 def test_f16_weights_rounded_to_nearest_even():

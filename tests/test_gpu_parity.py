@@ -123,8 +123,10 @@ def test_run_is_deterministic_and_independent_of_planning():
     note("determinism")
     base = gpu_run(layer)
     assert np.array_equal(base, gpu_run(layer))
-    for opts in (dict(reorder=0), dict(lanes_per_row=8), dict(lanes_per_row=32), dict(lanes_per_row=64),
-                 dict(waves=1), dict(waves=5), dict(waves=16, reorder=0)):
+    for opts in (dict(reorder=0), dict(lanes_per_row=16, vecs_per_lane=1), dict(lanes_per_row=8, vecs_per_lane=1),
+                 dict(lanes_per_row=32), dict(lanes_per_row=32, vecs_per_lane=2), dict(lanes_per_row=64),
+                 dict(waves=1), dict(waves=5), dict(waves=12, reorder=0), dict(prefetch=0),
+                 dict(prefetch=0, waves=16, lanes_per_row=16, vecs_per_lane=1)):
         note("determinism %s" % opts)
         assert np.array_equal(base, gpu_run(layer, **opts)), opts
 
