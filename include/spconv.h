@@ -121,17 +121,20 @@ const char *spconv_last_error(void);
  * ------------------------------------------------------------------------- */
 
 typedef struct {
-    int32_t struct_size;   /* sizeof(spconv_options) */
-    int32_t reorder;       /* 1 (default): process rows in descending nonzero order; 0: natural order */
-    int32_t host_only;     /* 1: plan on the host only, no device memory; spconv_run refuses it */
-    int32_t lanes_per_row; /* 0 = choose automatically; else 8, 16, 32 or 64 lanes share one row */
-    int32_t waves;         /* 0 = choose automatically; else the number of compute wavefronts per
-                              workgroup (with the loader wavefronts, at most 16 in all) */
-    int32_t vecs_per_lane; /* 0 = choose automatically; else 1 or 2 16-byte X vectors per lane
-                              and nonzero (the lane then owns 4 or 8 fp32 / 8 or 16 fp16 columns) */
-    int32_t prefetch;      /* 1 (default): loader wavefronts fetch the next strip while the others
-                              compute; 0: every wavefront computes and strips are copied between
-                              tiles */
+    int32_t struct_size; /* sizeof(spconv_options) */
+    int32_t reorder;     /* 1 (default): process rows in descending nonzero order; 0: natural order */
+    int32_t host_only;   /* 1: plan on the host only, no device memory; spconv_run refuses it */
+    int32_t kernel;      /* 0 = choose automatically; 1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED
+                            when the strip of cin channels does not fit in LDS); 2 = direct-load
+                            kernel */
+    int32_t vec_bytes;   /* 0 = choose automatically; else 8 or 16 bytes of X each lane reads per
+                            nonzero (16 lanes share a row, so a tile is 16 * vec_bytes bytes wide);
+                            the direct kernel takes 16 only */
+    int32_t waves;       /* 0 = choose automatically; else the number of compute wavefronts per
+                            workgroup (with the loader wavefronts, at most 16 in all) */
+    int32_t prefetch;    /* 1 (default): loader wavefronts fetch the next strip while the others
+                            compute; 0: every wavefront computes and strips are copied between
+                            tiles */
 } spconv_options;
 
 /* Fill *opts with the defaults used by spconv_plan_create. */
@@ -147,16 +150,16 @@ typedef struct {
     int32_t cout, cin, block_rows;
     int32_t storage, act;
     int32_t kernel;        /* 0: LDS-strip kernel; 1: direct-load kernel for wide inputs */
-    int32_t lanes_per_row; /* lanes sharing one (block) row */
-    int32_t vecs_per_lane; /* 16-byte X vectors each lane reads per nonzero */
-    int32_t cols_per_lane; /* output columns each lane accumulates */
-    int32_t tile_cols;     /* columns per workgroup tile = lanes_per_row * cols_per_lane */
+    int32_t vec_bytes;     /* bytes of X each lane reads per nonzero */
+    int32_t cols_per_lane; /* output columns each lane accumulates (vec_bytes / element size) */
+    int32_t tile_cols;     /* columns per workgroup tile = 16 * cols_per_lane */
     int32_t waves;         /* compute wavefronts per workgroup */
     int32_t loader_waves;  /* wavefronts per workgroup that prefetch the next strip */
-    int32_t groups;        /* row groups (rows processed together by one wavefront) */
+    int32_t groups;        /* block rows one wavefront processes together (16 lanes each) */
     int32_t lds_bytes;     /* LDS per workgroup */
+    int32_t max_parts;     /* most workgroups that may share the rows of one tile */
     int64_t nnzb;          /* stored blocks */
-    int64_t slots;         /* packed (index, value) slots including padding */
+    int64_t slots;         /* packed (index, value) entries including padding */
     int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
     int64_t sum_wave_cost; /* total of the per-wavefront work estimates */
     int64_t device_bytes;  /* device memory the plan holds */

@@ -13,8 +13,7 @@ namespace spconv {
 // the launch facts fixed at plan creation.
 struct DevicePlan {
     int32_t kernel = KERNEL_STRIP;
-    int32_t lanes_per_row = 16;
-    int32_t vecs_per_lane = 1;
+    int32_t vec_bytes = 16;
     int32_t tile_cols = 64;
     int32_t waves = 1;
     int32_t loader_waves = 0;
@@ -30,11 +29,14 @@ struct DevicePlan {
     int32_t strip_bytes = 0;    // LDS bytes of the X strip (the bundle table follows it)
     int32_t meta_words = 0;     // 32-bit words of the bundle table
     int32_t nbundles = 0;
+    int32_t max_parts = 1;      // most workgroups that may share one tile
     const int32_t *idx = nullptr;
     const float *val = nullptr;
-    const int32_t *hdr = nullptr;
-    const int32_t *meta = nullptr;  // rows[nbundles * groups], then bundle_bias as fp32 bits
-    const int32_t *wave_ptr = nullptr;
+    const int32_t *hdr = nullptr;         // (first step, steps) per bundle
+    const int32_t *meta = nullptr;        // rows, biases (fp32 bits), steps
+    const int32_t *wave_ptr = nullptr;    // bundles of each wave
+    const int32_t *wave_chunk = nullptr;  // first chunk of each wave
+    const int32_t *split = nullptr;       // 65 part boundaries per wave
 };
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when

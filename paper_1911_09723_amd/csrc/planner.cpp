@@ -160,65 +160,65 @@ Status validate(const Input &in, std::string &err) {
 
 namespace {
 
-// Per-bundle fixed cost (epilogue, header loads) in units of one slot step.
+// Per-bundle fixed cost (epilogue, table reads) in units of one slot step.
 constexpr int64_t kBundleOverhead = 3;
 
-// Bytes of the per-bundle table (rows and biases) the strip kernel keeps in LDS.
-int64_t table_bytes(const Input &in, int g) {
-    const int64_t groups = 64 / g;
+// Bytes of the per-bundle table the strip kernel keeps in LDS, 16-byte rounded.
+int64_t table_bytes(const Input &in) {
     const int64_t rows = in.cout / in.block_rows;
-    const int64_t bundles = (rows + groups - 1) / groups;
-    return ((bundles * groups * (1 + in.block_rows) * 4) + 15) & ~int64_t(15);
+    const int64_t bundles = (rows + kGroups - 1) / kGroups;
+    return (bundles * (kGroups * (1 + in.block_rows) + 1) * 4 + 15) & ~int64_t(15);
 }
 
-void choose_geometry(const Input &in, const Options &opt, PackedPlan &p) {
+Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::string &err) {
     const int e = in.storage == 1 ? 2 : 4;
-    auto strip_bytes = [&](int g, int nv) { return static_cast<int64_t>(in.cin) * g * nv * kLaneBytes; };
-    auto fits = [&](int g, int nv) { return strip_bytes(g, nv) + table_bytes(in, g) <= kMaxLdsBytes; };
-    // Strip rows of 256 bytes: 16 lanes x one 16-byte vector read 256
-    // contiguous bytes (all 64 LDS banks) per row, so the four lane groups of a
-    // wavefront take four conflict-free LDS cycles.  Wider inputs fall back to
-    // 128-byte rows (8 lanes), then to the direct-load kernel.
-    int g = opt.lanes_per_row, nv = opt.vecs_per_lane;
-    if (g == 0 && nv == 0) {
-        if (fits(16, 1)) {
-            g = 16;
-            nv = 1;
-        } else if (fits(8, 1)) {
-            g = 8;
-            nv = 1;
-        } else {
-            g = 16;
-            nv = 1;
+    // One strip row is 16 lanes x vec_bytes: 256 bytes read by 16 lanes at a
+    // time touch all 64 LDS banks once.  Wider inputs fall back to 128-byte
+    // rows, then to the direct-load kernel, which keeps 16-byte vectors.
+    auto strip_bytes = [&](int vb) { return static_cast<int64_t>(in.cin) * kLanesPerRow * vb; };
+    auto fits = [&](int vb) { return strip_bytes(vb) + table_bytes(in) <= kMaxLdsBytes; };
+    int vb = opt.vec_bytes;
+    bool strip;
+    if (opt.kernel == 2) {
+        strip = false;
+        if (vb == 0)
+            vb = 16;
+    } else if (vb == 0) {
+        vb = fits(16) ? 16 : 8;
+        strip = fits(vb);
+        if (!strip)
+            vb = 16;
+        if (opt.kernel == 1 && !strip) {
+            err = "the X strip of cin = " + std::to_string(in.cin) + " channels does not fit in LDS";
+            return E_UNSUPPORTED;
         }
     } else {
-        if (g == 0)
-            g = 16;
-        if (nv == 0)
-            nv = 1;
+        strip = fits(vb);
+        if (!strip && opt.kernel == 1) {
+            err = "the X strip of cin = " + std::to_string(in.cin) + " channels at vec_bytes = " +
+                  std::to_string(vb) + " does not fit in LDS";
+            return E_UNSUPPORTED;
+        }
     }
-    const bool strip = fits(g, nv);
-    if (!strip)
-        nv = 1;  // the direct-load kernel reads one vector per lane
-    p.lanes_per_row = g;
-    p.vecs_per_lane = nv;
-    p.groups = 64 / g;
-    p.cols_per_lane = nv * kLaneBytes / e;
-    p.tile_cols = g * p.cols_per_lane;
+    p.vec_bytes = vb;
+    p.cols_per_lane = vb / e;
+    p.tile_cols = kLanesPerRow * p.cols_per_lane;
     if (strip) {
         p.kernel = KERNEL_STRIP;
-        p.strip_bytes = static_cast<int32_t>(strip_bytes(g, nv));
-        p.lds_bytes = static_cast<int32_t>(strip_bytes(g, nv) + table_bytes(in, g));
-        p.loader_waves = opt.prefetch
-                             ? static_cast<int32_t>((strip_bytes(g, nv) + kLoaderBytesPerWave - 1) /
-                                                    kLoaderBytesPerWave)
-                             : 0;
+        p.row_scale = kLanesPerRow * vb;
+        p.strip_bytes = static_cast<int32_t>(strip_bytes(vb));
+        p.lds_bytes = static_cast<int32_t>(strip_bytes(vb) + table_bytes(in));
+        p.loader_waves = opt.prefetch ? static_cast<int32_t>((strip_bytes(vb) + kLoaderBytesPerWave - 1) /
+                                                             kLoaderBytesPerWave)
+                                      : 0;
     } else {
         p.kernel = KERNEL_DIRECT;
+        p.row_scale = 1;
         p.strip_bytes = 0;
         p.lds_bytes = 0;
         p.loader_waves = 0;
     }
+    return OK;
 }
 
 }  // namespace
@@ -227,21 +227,20 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     Status st = validate(in, err);
     if (st != OK)
         return st;
-    if (opt.lanes_per_row != 0 && opt.lanes_per_row != 8 && opt.lanes_per_row != 16 &&
-        opt.lanes_per_row != 32 && opt.lanes_per_row != 64) {
-        err = "lanes_per_row must be 0, 8, 16, 32 or 64";
+    if (opt.kernel < 0 || opt.kernel > 2) {
+        err = "kernel must be 0 (automatic), 1 (strip) or 2 (direct)";
         return E_ARG;
     }
-    if (opt.waves < 0 || opt.waves > 16) {
+    if (opt.vec_bytes != 0 && opt.vec_bytes != 8 && opt.vec_bytes != 16) {
+        err = "vec_bytes must be 0, 8 or 16";
+        return E_ARG;
+    }
+    if (opt.kernel == 2 && opt.vec_bytes == 8) {
+        err = "the direct kernel reads 16-byte vectors (vec_bytes 0 or 16)";
+        return E_ARG;
+    }
+    if (opt.waves < 0 || opt.waves > kMaxWaves) {
         err = "waves must be in [0, 16]";
-        return E_ARG;
-    }
-    if (opt.vecs_per_lane != 0 && opt.vecs_per_lane != 1 && opt.vecs_per_lane != 2) {
-        err = "vecs_per_lane must be 0, 1 or 2";
-        return E_ARG;
-    }
-    if (opt.lanes_per_row == 64 && opt.vecs_per_lane == 2) {
-        err = "lanes_per_row = 64 takes one vector per lane";
         return E_ARG;
     }
     if (opt.reorder != 0 && opt.reorder != 1) {
@@ -259,11 +258,13 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     p.k = in.block_rows;
     p.act = in.act;
     p.storage = in.storage;
-    choose_geometry(in, opt, p);
+    st = choose_geometry(in, opt, p, err);
+    if (st != OK)
+        return st;
 
     const int32_t k = in.block_rows;
     const int32_t rows = in.cout / k;
-    const int32_t G = p.groups;
+    constexpr int32_t G = kGroups;
     p.nnzb = in.row_ptr[rows];
 
     // 1. processing order: descending nonzero count, ties by row index (stable)
@@ -273,18 +274,19 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     if (opt.reorder)
         std::stable_sort(p.perm.begin(), p.perm.end(), [&](int32_t a, int32_t b) { return len(a) > len(b); });
 
-    // 2. bundles of G consecutive rows in that order
+    // 2. bundles of G consecutive rows in that order, each a whole number of
+    // steps of 4 slots and at least one step long
     p.row_nnz.resize(rows);
     for (int32_t r = 0; r < rows; ++r)
         p.row_nnz[r] = len(r);
     const int32_t nb = (rows + G - 1) / G;
-    std::vector<int32_t> blen(nb, 0);
-    for (int32_t b = 0; b < nb; ++b)
+    std::vector<int32_t> bsteps(nb, 0);
+    for (int32_t b = 0; b < nb; ++b) {
+        int32_t l = 0;
         for (int32_t g = 0; g < G && b * G + g < rows; ++g)
-            blen[b] = std::max(blen[b], len(p.perm[b * G + g]));
-    // padded to whole steps of 4 slots, at least one step
-    for (int32_t b = 0; b < nb; ++b)
-        blen[b] = std::max<int32_t>(4, (blen[b] + 3) & ~3);
+            l = std::max(l, len(p.perm[b * G + g]));
+        bsteps[b] = std::max<int32_t>(1, (l + 3) / 4);
+    }
 
     // 3. longest-processing-time-first assignment of bundles to waves
     const int32_t max_waves = kMaxWaves - p.loader_waves;
@@ -293,11 +295,11 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
               " loader waves exceeds " + std::to_string(kMaxWaves) + " wavefronts per workgroup";
         return E_ARG;
     }
-    int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(max_waves, std::max<int32_t>(nb, 1));
+    const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(max_waves, std::max<int32_t>(nb, 1));
     p.waves = waves;
     std::vector<int32_t> order(nb);
     std::iota(order.begin(), order.end(), 0);
-    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return blen[a] > blen[b]; });
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return bsteps[a] > bsteps[b]; });
     using Item = std::pair<int64_t, int32_t>;  // (load, wave)
     std::priority_queue<Item, std::vector<Item>, std::greater<Item>> heap;
     for (int32_t w = 0; w < waves; ++w)
@@ -308,99 +310,111 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         Item it = heap.top();
         heap.pop();
         lists[it.second].push_back(b);
-        it.first += blen[b] + kBundleOverhead;
+        it.first += 4 * static_cast<int64_t>(bsteps[b]) + kBundleOverhead;
         load[it.second] = it.first;
         heap.push(it);
     }
     p.max_wave_cost = waves ? *std::max_element(load.begin(), load.end()) : 0;
     p.sum_wave_cost = std::accumulate(load.begin(), load.end(), int64_t(0));
 
-    // 4. pack, bundles stored in wave order; every bundle is a whole number
-    // of steps (4 slots per lane group) and at least one step long
+    // 4. pack: bundles in wave order; each wave's steps in chunks of 4 steps
     p.wave_ptr.assign(waves + 1, 0);
-    p.hdr.reserve(4 * static_cast<size_t>(nb));
+    p.wave_chunk.assign(waves + 1, 0);
+    p.split.assign(static_cast<size_t>(waves) * (kMaxParts + 1), 0);
+    p.hdr.reserve(2 * static_cast<size_t>(nb));
     p.rows.reserve(static_cast<size_t>(G) * nb);
     p.bundle_bias.reserve(static_cast<size_t>(G) * nb * k);
-    int64_t slot = 0;
+    int64_t chunk0 = 0;  // first chunk of the current wave
+    int32_t bglob = 0;   // bundles packed so far
+    int32_t max_bundles = 0;
     for (int32_t w = 0; w < waves; ++w) {
-        for (int32_t b : lists[w]) {
-            const int32_t L = blen[b];
-            if (slot + static_cast<int64_t>(L) * G > (int64_t(1) << 30)) {
-                err = "packed plan too large";
-                return E_SHAPE;
-            }
-            p.hdr.push_back(static_cast<int32_t>(slot));
-            p.hdr.push_back(L / 4);
-            p.hdr.push_back(0);
-            p.hdr.push_back(0);
-            const size_t need = static_cast<size_t>(slot + static_cast<int64_t>(L) * G);
-            p.idx.resize(need, 0);
-            p.val.resize(need * k, 0.0f);
+        int64_t total = 0;
+        for (int32_t b : lists[w])
+            total += bsteps[b];
+        const int64_t nchunks = (total + kChunkSteps - 1) / kChunkSteps;
+        if ((chunk0 + nchunks) * 64 * k > (int64_t(1) << 29)) {  // stream byte sizes stay below 2^31
+            err = "packed plan too large";
+            return E_SHAPE;
+        }
+        p.idx.resize(static_cast<size_t>((chunk0 + nchunks) * 64), 0);
+        p.val.resize(static_cast<size_t>((chunk0 + nchunks) * 64 * k), 0.0f);
+        // split[i]: first bundle whose first step is at or after i/64 of the stream
+        std::vector<int64_t> start(lists[w].size() + 1, 0);
+        for (size_t i = 0; i < lists[w].size(); ++i)
+            start[i + 1] = start[i] + bsteps[lists[w][i]];
+        for (int32_t i = 0; i <= kMaxParts; ++i) {
+            size_t j = 0;
+            while (j < lists[w].size() && start[j] * kMaxParts < static_cast<int64_t>(i) * total)
+                ++j;
+            if (i == kMaxParts)
+                j = lists[w].size();
+            p.split[static_cast<size_t>(w) * (kMaxParts + 1) + i] = bglob + static_cast<int32_t>(j);
+        }
+        for (size_t i = 0; i < lists[w].size(); ++i) {
+            const int32_t b = lists[w][i];
+            const int64_t s_first = start[i];
+            p.hdr.push_back(static_cast<int32_t>(s_first));
+            p.hdr.push_back(bsteps[b]);
             for (int32_t g = 0; g < G; ++g) {
                 const int32_t pos = b * G + g;
                 const int32_t rb = pos < rows ? p.perm[pos] : -1;
                 p.rows.push_back(rb);
-                for (int32_t i = 0; i < k; ++i)
-                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + i] : 0.0f);
-                // the last step of the bundle is marked in its first slot
-                p.idx[slot + (static_cast<int64_t>(L / 4 - 1) * G + g) * 4] |= kLastStepFlag;
+                for (int32_t ii = 0; ii < k; ++ii)
+                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + ii] : 0.0f);
                 if (rb < 0)
                     continue;
-                const int32_t s0 = in.row_ptr[rb];
-                const int32_t n = len(rb);
-                for (int32_t t = 0; t < n; ++t) {
-                    const int64_t sl = slot + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
-                    p.idx[sl] = (p.idx[sl] & kLastStepFlag) | in.col_idx[s0 + t];
-                    for (int32_t i = 0; i < k; ++i) {
-                        float v = in.values[static_cast<int64_t>(s0 + t) * k + i];
+                const int32_t r0 = in.row_ptr[rb];
+                for (int32_t t = 0; t < len(rb); ++t) {
+                    const int64_t s = s_first + t / 4;
+                    const int64_t e = 64 * (chunk0 + s / kChunkSteps) + kLanesPerRow * g + 4 * (s % kChunkSteps) +
+                                      (t % 4);
+                    p.idx[e] = in.col_idx[r0 + t] * p.row_scale;
+                    for (int32_t ii = 0; ii < k; ++ii) {
+                        float v = in.values[static_cast<int64_t>(r0 + t) * k + ii];
                         if (in.storage == 1)
                             v = half_to_float(float_to_half_rne(v));
-                        p.val[sl * k + i] = v;
+                        p.val[e * k + ii] = v;
                     }
                 }
             }
-            slot += static_cast<int64_t>(L) * G;
         }
-        p.wave_ptr[w + 1] = static_cast<int32_t>(p.hdr.size() / 4);
+        bglob += static_cast<int32_t>(lists[w].size());
+        max_bundles = std::max<int32_t>(max_bundles, static_cast<int32_t>(lists[w].size()));
+        p.wave_ptr[w + 1] = bglob;
+        chunk0 += nchunks;
+        p.wave_chunk[w + 1] = static_cast<int32_t>(chunk0);
     }
-    // Keep every stream a whole number of 16-byte vectors and leave
-    // kLookaheadSteps main-loop steps (4 slots per lane group each) of padding
-    // after the last bundle: the kernel fetches slots of later steps before it
-    // knows whether the bundle continues.
-    slot = ((slot + 3) & ~int64_t(3)) + (kLookaheadSteps + 1) * 4 * static_cast<int64_t>(G) + 4;
-    p.idx.resize(static_cast<size_t>(slot), 0);
-    p.val.resize(static_cast<size_t>(slot) * k, 0.0f);
-    p.slots = slot;
-    if (p.hdr.empty())
-        p.hdr.assign(4, 0);
-    // LDS copy of the per-bundle rows and biases, after the strip
-    p.meta_bytes = static_cast<int32_t>(p.rows.size() * sizeof(int32_t) + p.bundle_bias.size() * sizeof(float));
-
-    p.bias.assign(in.cout, 0.0f);
-    if (in.bias)
-        std::copy(in.bias, in.bias + in.cout, p.bias.begin());
+    p.slots = chunk0 * 64;
+    // A tile is shared by at most as many workgroups as the busiest wave has bundles.
+    p.max_parts = 1;
+    while (p.max_parts * 2 <= std::min<int32_t>(kMaxParts, max_bundles))
+        p.max_parts *= 2;
     return OK;
 }
 
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm) {
     const int32_t k = p.k;
     const int32_t rows = p.cout / k;
-    const int32_t G = p.groups;
+    constexpr int32_t G = kGroups;
     std::vector<std::vector<int32_t>> cols(rows);
     std::vector<std::vector<float>> vals(rows);
-    const int32_t nb = static_cast<int32_t>(p.wave_ptr.back());
+    const int32_t waves = static_cast<int32_t>(p.wave_ptr.size()) - 1;
     // each row's real entries are the first row_nnz[rb] slots of its sequence
-    for (int32_t b = 0; b < nb; ++b) {
-        const int64_t S = p.hdr[4 * b];
-        for (int32_t g = 0; g < G; ++g) {
-            const int32_t rb = p.rows[static_cast<size_t>(b) * G + g];
-            if (rb < 0)
-                continue;
-            for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
-                const int64_t sl = S + (static_cast<int64_t>(t >> 2) * G + g) * 4 + (t & 3);
-                cols[rb].push_back(p.idx[sl] & ~kLastStepFlag);
-                for (int32_t i = 0; i < k; ++i)
-                    vals[rb].push_back(p.val[sl * k + i]);
+    for (int32_t w = 0; w < waves; ++w) {
+        for (int32_t b = p.wave_ptr[w]; b < p.wave_ptr[w + 1]; ++b) {
+            const int64_t s_first = p.hdr[2 * b];
+            for (int32_t g = 0; g < G; ++g) {
+                const int32_t rb = p.rows[static_cast<size_t>(b) * G + g];
+                if (rb < 0)
+                    continue;
+                for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
+                    const int64_t s = s_first + t / 4;
+                    const int64_t e = 64 * (p.wave_chunk[w] + s / kChunkSteps) + kLanesPerRow * g +
+                                      4 * (s % kChunkSteps) + (t % 4);
+                    cols[rb].push_back(p.idx[e] / p.row_scale);
+                    for (int32_t i = 0; i < k; ++i)
+                        vals[rb].push_back(p.val[e * k + i]);
+                }
             }
         }
     }

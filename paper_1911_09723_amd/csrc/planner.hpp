@@ -7,36 +7,44 @@
 // channels sharing one input channel).  Output is the packed image the GPU
 // kernels stream.
 //
-// Packed layout (all int32 / fp32, little-endian, every array 16-byte aligned):
+// Packed layout (all int32 / fp32, little-endian):
 //
-//   A *bundle* is `groups` (= 64 / lanes_per_row) block rows that one
-//   wavefront processes at the same time, one row per lane group.  Bundles
-//   are made of consecutive rows in processing order (descending nonzero
-//   count unless reordering is off), so the rows of a bundle have similar
-//   lengths.  Its length L is the longest of its rows rounded up to a multiple
-//   of 4 (at least 4); shorter rows are padded with (channel 0, weight 0)
-//   slots, which add an exact zero.  A *step* is 4 slots of every row.
-//
-//   hdr[4*b + 0]  first slot of bundle b (a multiple of 4)
-//   hdr[4*b + 1]  L / 4: steps of bundle b
-//   rows[groups*b + g]         block row handled by lane group g, or -1 (padding group)
-//   bundle_bias[(groups*b + g)*k + i]  bias of row rows[..]*k + i (0 for padding)
-//
-//   Slot numbering inside bundle b (base S = hdr[4*b]):
-//     slot S + (t4 * groups + g) * 4 + u   for step t4 < L/4, u < 4
-//   so one 16-byte load fetches the next 4 channel indices of a row.
-//   idx[slot]        input channel c; the first slot of a bundle's last step
-//                    also carries kLastStepFlag
-//   val[slot*k + i]  weight of block row element i (fp16-rounded for fp16 storage)
+//   A *bundle* is 4 block rows that one wavefront processes at the same time,
+//   one row per group of 16 lanes.  Bundles are made of consecutive rows in
+//   processing order (descending nonzero count unless reordering is off), so
+//   the rows of a bundle have similar lengths.  Its length is the longest of
+//   its rows rounded up to a whole number of *steps* of 4 slots (at least one
+//   step); shorter rows are padded with (channel 0, weight 0) slots, which add
+//   an exact zero.
 //
 //   Bundles are assigned to the `waves` wavefronts of a workgroup by longest
-//   processing time first; wave_ptr[w] .. wave_ptr[w+1] are wave w's bundles,
-//   which are stored contiguously in that order, so each wavefront reads one
-//   continuous stream of steps.
+//   processing time first; wave_ptr[w] .. wave_ptr[w+1] are wave w's bundles.
+//   A wavefront's bundles, in that order, form one continuous stream of steps,
+//   stored as *chunks* of 4 steps: chunk q holds, for lane group g and slot
+//   u < 16 of that group's 16 slots in the chunk (steps 4q .. 4q+3, 4 slots
+//   each), entry
+//       e = 64 * (wave_chunk[w] + q) + 16 * g + u
+//   so lane L of a wavefront loads entry 64 * chunk + L: one coalesced load
+//   per chunk.
+//   idx[e]           input channel * row_scale (row_scale = bytes of one LDS
+//                    strip row for the strip kernel, 1 for the direct kernel)
+//   val[e*k + i]     weight of block row element i (fp16-rounded for fp16 storage)
+//
+//   hdr[2*b + 0]     first step of bundle b within its wavefront's stream
+//   hdr[2*b + 1]     steps of bundle b
+//   meta: the table the strip kernel copies into LDS, in three arrays
+//     rows[4*b + g]              block row of lane group g, or -1 (padding group)
+//     bias[(4*b + g)*k + i]      bias of output channel rows[..]*k + i (0 for padding), fp32 bits
+//     steps[b]                   = hdr[2*b + 1]
+//   split[65*w + i]  first bundle of part i of 64 of wave w's stream (parts cut
+//                    at bundle boundaries, each about 1/64 of the steps);
+//                    split[65*w + 64] = wave_ptr[w + 1].  A tile shared by P
+//                    workgroups (P a power of two up to 64) gives part p the
+//                    bundles split[65*w + p*64/P] .. split[65*w + (p+1)*64/P].
 //
 // The per-row summation order is ascending input channel (the CSR order), with
 // padding zeros in between; it does not depend on the bundle grouping, so the
-// result is bitwise independent of reordering and wave assignment.
+// result is bitwise independent of reordering, wave assignment and splitting.
 #pragma once
 
 #include <cstdint>
@@ -51,17 +59,17 @@ enum Kernel { KERNEL_STRIP = 0, KERNEL_DIRECT = 1 };
 
 // Largest LDS footprint of one workgroup on gfx950 (160 KiB per CU).
 constexpr int64_t kMaxLdsBytes = 160 * 1024;
-// Every X read of a lane is one 16-byte vector: 4 fp32 or 8 fp16 columns.
-constexpr int kLaneBytes = 16;
+// Lanes sharing one block row: one 16-lane DPP row of a wavefront.
+constexpr int32_t kLanesPerRow = 16;
+// Block rows per bundle (lane groups per wavefront).
+constexpr int32_t kGroups = 64 / kLanesPerRow;
+// Slots per lane group in one chunk (one per lane) and steps per chunk.
+constexpr int32_t kChunkSlots = kLanesPerRow;
+constexpr int32_t kChunkSteps = kChunkSlots / 4;
+// Finest split of a wavefront's stream.
+constexpr int32_t kMaxParts = 64;
 // Wavefronts per workgroup (1024 threads).
 constexpr int32_t kMaxWaves = 16;
-// Bit set in the channel index of the first slot of a bundle's last step.  It
-// lies above any valid channel and above the bits that survive the kernels'
-// scaling of the channel to a byte offset, so the kernels read it without
-// masking it out.
-constexpr int32_t kLastStepFlag = 1 << 30;
-// Main-loop steps the kernels may fetch past the end of a bundle.
-constexpr int64_t kLookaheadSteps = 4;
 // Strip bytes one loader wavefront holds in registers: 64 lanes x 16 vectors.
 constexpr int64_t kLoaderBytesPerWave = 64 * 16 * 16;
 
@@ -78,9 +86,9 @@ struct Input {
 struct Options {
     int32_t reorder = 1;
     int32_t host_only = 0;
-    int32_t lanes_per_row = 0;
+    int32_t kernel = 0;     // 0 automatic, 1 strip, 2 direct
+    int32_t vec_bytes = 0;  // 0 automatic, else 8 or 16 bytes of X per lane and nonzero
     int32_t waves = 0;
-    int32_t vecs_per_lane = 0;
     int32_t prefetch = 1;
 };
 
@@ -89,31 +97,35 @@ struct PackedPlan {
     int32_t cout = 0, cin = 0, k = 1, act = 0, storage = 0;
     // launch geometry
     int32_t kernel = KERNEL_STRIP;
-    int32_t lanes_per_row = 16;  // G
-    int32_t vecs_per_lane = 1;   // 16-byte X vectors each lane reads per nonzero
-    int32_t groups = 4;          // 64 / G
-    int32_t cols_per_lane = 4;   // vecs_per_lane * 16 bytes / element size
-    int32_t tile_cols = 64;      // G * cols_per_lane
+    int32_t vec_bytes = 16;      // bytes of X each lane reads per nonzero
+    int32_t cols_per_lane = 4;   // vec_bytes / element size
+    int32_t tile_cols = 64;      // kLanesPerRow * cols_per_lane
+    int32_t row_scale = 256;     // idx = channel * row_scale
     int32_t waves = 1;           // compute wavefronts (each owns a list of bundles)
     int32_t loader_waves = 0;    // wavefronts that prefetch the next strip (strip kernel)
     int32_t lds_bytes = 0;       // strip + bundle table (strip kernel)
     int32_t strip_bytes = 0;
+    int32_t max_parts = 1;       // most workgroups that may share one tile
     // packed streams
     std::vector<int32_t> idx;
     std::vector<float> val;
     std::vector<int32_t> hdr;
     std::vector<int32_t> rows;
+    std::vector<float> bundle_bias;  // bias of each (bundle, group, block element)
     std::vector<int32_t> wave_ptr;
-    std::vector<float> bias;
-    std::vector<float> bundle_bias;  // bias of the row of each (bundle, group, block element)
-    int32_t meta_bytes = 0;          // rows + bundle_bias, copied into LDS by the strip kernel
+    std::vector<int32_t> wave_chunk;
+    std::vector<int32_t> split;
     std::vector<int32_t> perm;     // block rows in processing order
     std::vector<int32_t> row_nnz;  // stored blocks per block row (host only; for unpacking)
     // statistics
     int64_t nnzb = 0;
-    int64_t slots = 0;
+    int64_t slots = 0;  // packed entries including padding (64 per chunk)
     int64_t max_wave_cost = 0;
     int64_t sum_wave_cost = 0;
+
+    int32_t nbundles() const { return static_cast<int32_t>(hdr.size() / 2); }
+    // 32-bit words of the LDS bundle table: rows, biases, steps
+    int32_t meta_words() const { return nbundles() * (kGroups * (1 + k) + 1); }
 };
 
 // Round an fp32 value to the nearest IEEE binary16 value, ties to even, and

@@ -9,6 +9,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <new>
@@ -68,26 +69,31 @@ spconv::Input make_input(int32_t cout, int32_t cin, int32_t block_rows, const in
 
 spconv_status upload(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
-    // bundle table: rows, then the biases of those rows as fp32 bit patterns
-    std::vector<int32_t> meta(h.rows.begin(), h.rows.end());
-    meta.resize(h.rows.size() + h.bundle_bias.size());
+    // bundle table: rows, the biases of those rows as fp32 bit patterns, steps
+    const size_t nb = static_cast<size_t>(h.nbundles());
+    std::vector<int32_t> meta(static_cast<size_t>(h.meta_words()));
+    std::copy(h.rows.begin(), h.rows.end(), meta.begin());
     if (!h.bundle_bias.empty())
         std::memcpy(meta.data() + h.rows.size(), h.bundle_bias.data(), h.bundle_bias.size() * sizeof(float));
+    for (size_t b = 0; b < nb; ++b)
+        meta[h.rows.size() + h.bundle_bias.size() + b] = h.hdr[2 * b + 1];
     struct Part {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[5] = {
+    } parts[7] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
         {meta.data(), meta.size() * sizeof(int32_t), 0},
         {h.wave_ptr.data(), h.wave_ptr.size() * sizeof(int32_t), 0},
+        {h.wave_chunk.data(), h.wave_chunk.size() * sizeof(int32_t), 0},
+        {h.split.data(), h.split.size() * sizeof(int32_t), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
         p.off = total;
-        total = align_up(total + p.bytes, 256);
+        total = align_up(total + std::max<size_t>(p.bytes, 16), 256);
     }
     if (fault_alloc())
         return fail(SPCONV_E_NOMEM, "device allocation failed (SPCONV_FAULT=alloc)");
@@ -106,7 +112,8 @@ spconv_status upload(spconv_plan_s *pl) {
     pl->dbytes = total;
     std::string image(total, '\0');
     for (const Part &p : parts)
-        std::memcpy(&image[p.off], p.src, p.bytes);
+        if (p.bytes)
+            std::memcpy(&image[p.off], p.src, p.bytes);
     e = hipMemcpy(pl->dmem, image.data(), total, hipMemcpyHostToDevice);
     if (e != hipSuccess)
         return hip_fail("hipMemcpy (plan upload)", e);
@@ -117,6 +124,8 @@ spconv_status upload(spconv_plan_s *pl) {
     d.hdr = reinterpret_cast<const int32_t *>(base + parts[2].off);
     d.meta = reinterpret_cast<const int32_t *>(base + parts[3].off);
     d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[4].off);
+    d.wave_chunk = reinterpret_cast<const int32_t *>(base + parts[5].off);
+    d.split = reinterpret_cast<const int32_t *>(base + parts[6].off);
     return SPCONV_OK;
 }
 
@@ -124,8 +133,7 @@ void fill_device_geometry(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
     spconv::DevicePlan &d = pl->dev;
     d.kernel = h.kernel;
-    d.lanes_per_row = h.lanes_per_row;
-    d.vecs_per_lane = h.vecs_per_lane;
+    d.vec_bytes = h.vec_bytes;
     d.tile_cols = h.tile_cols;
     d.waves = h.waves;
     d.loader_waves = h.loader_waves;
@@ -137,9 +145,10 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.cout = h.cout;
     d.idx_bytes = static_cast<int32_t>(h.idx.size() * sizeof(int32_t));
     d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
-    d.nbundles = static_cast<int32_t>(h.hdr.size() / 4);
-    d.meta_words = static_cast<int32_t>(h.rows.size() + h.bundle_bias.size());
+    d.nbundles = h.nbundles();
+    d.meta_words = h.meta_words();
     d.strip_bytes = h.strip_bytes;
+    d.max_parts = h.max_parts;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -180,9 +189,9 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     spconv::Options po;
     po.reorder = o.reorder;
     po.host_only = o.host_only;
-    po.lanes_per_row = o.lanes_per_row;
+    po.kernel = o.kernel;
+    po.vec_bytes = o.vec_bytes;
     po.waves = o.waves;
-    po.vecs_per_lane = o.vecs_per_lane;
     po.prefetch = o.prefetch;
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
@@ -299,13 +308,13 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->storage = p.storage;
     info->act = p.act;
     info->kernel = p.kernel;
-    info->lanes_per_row = p.lanes_per_row;
-    info->vecs_per_lane = p.vecs_per_lane;
+    info->vec_bytes = p.vec_bytes;
     info->cols_per_lane = p.cols_per_lane;
     info->tile_cols = p.tile_cols;
     info->waves = p.waves;
     info->loader_waves = p.loader_waves;
-    info->groups = p.groups;
+    info->groups = spconv::kGroups;
+    info->max_parts = p.max_parts;
     info->lds_bytes = p.lds_bytes;
     info->nnzb = p.nnzb;
     info->slots = p.slots;

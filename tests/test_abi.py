@@ -135,8 +135,8 @@ def test_null_arrays_with_nonzeros_rejected():
 
 
 def test_options_validated():
-    for kw in (dict(lanes_per_row=12), dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3),
-               dict(vecs_per_lane=3), dict(lanes_per_row=64, vecs_per_lane=2)):
+    for kw in (dict(vec_bytes=12), dict(vec_bytes=4), dict(waves=17), dict(waves=-1), dict(reorder=2),
+               dict(host_only=3), dict(kernel=3), dict(kernel=-1), dict(kernel=2, vec_bytes=8), dict(prefetch=2)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw
     o = _host_opts()
@@ -177,12 +177,12 @@ def test_injected_allocation_failure_reports_nomem():
 
 @pytest.mark.parametrize("k", [1, 4])
 @pytest.mark.parametrize("pattern", ["uniform", "beta"])
-@pytest.mark.parametrize("lanes", [0, 8, 16, 32, 64])
-def test_pack_unpack_round_trip_and_order(k, pattern, lanes):
+@pytest.mark.parametrize("kernel,vec_bytes", [(0, 0), (1, 8), (1, 16), (2, 0)])
+def test_pack_unpack_round_trip_and_order(k, pattern, kernel, vec_bytes):
     if pattern == "beta" and k == 4:
         pytest.skip("beta row densities are defined for unstructured masks")
     layer = make_layer(96, 160, 2, 2, 1, 0.85, block_rows=k, pattern=pattern, seed=4, with_x=False)
-    h = _create(layer, options=_host_opts(lanes_per_row=lanes))
+    h = _create(layer, options=_host_opts(kernel=kernel, vec_bytes=vec_bytes))
     try:
         info = sp.spconv_plan_get_info(h)
         rp, ci, va, perm = sp.spconv_plan_unpack(h)
@@ -197,8 +197,10 @@ def test_pack_unpack_round_trip_and_order(k, pattern, lanes):
     ties = [perm[i] < perm[i + 1] for i in range(rows - 1) if counts[i] == counts[i + 1]]
     assert all(ties), "equal-length rows not kept in index order"
     assert info["nnzb"] == layer.nnzb and info["slots"] >= layer.nnzb
-    assert info["lanes_per_row"] == (lanes or 16)
-    assert info["groups"] * info["lanes_per_row"] == 64
+    assert info["vec_bytes"] == (vec_bytes or 16) and info["groups"] == 4
+    assert info["kernel"] == (1 if kernel == 2 else 0)
+    # chunks of 4 steps x 4 slots x 4 lane groups
+    assert info["slots"] % 64 == 0
 
 
 def test_natural_order_when_reorder_off():
@@ -245,22 +247,21 @@ def test_geometry_choice():
             return sp.spconv_plan_get_info(h)
         finally:
             sp.spconv_destroy(h)
-    keys = ("kernel", "lanes_per_row", "vecs_per_lane", "tile_cols", "lds_bytes", "loader_waves")
+    keys = ("kernel", "vec_bytes", "tile_cols", "lds_bytes", "loader_waves")
 
-    def table(cout, k, lanes):
-        # per-bundle output rows and biases kept in LDS after the strip, 16-byte rounded
-        groups = 64 // lanes
-        bundles = -(-(cout // k) // groups)
-        return -(-(bundles * groups * (1 + k) * 4) // 16) * 16
+    def table(cout, k):
+        # per bundle of 4 block rows: their rows, biases and step count, 16-byte rounded
+        bundles = -(-(cout // k) // 4)
+        return -(-(bundles * (4 * (1 + k) + 1) * 4) // 16) * 16
     # 256-byte strip rows: 16 lanes x one 16-byte vector
-    assert tuple(info_for(512, "f32")[k] for k in keys) == (0, 16, 1, 64, 512 * 256 + table(32, 1, 16), 8)
-    assert tuple(info_for(512, "f32", 4)[k] for k in keys) == (0, 16, 1, 64, 512 * 256 + table(32, 4, 16), 8)
-    assert tuple(info_for(320, "f16", 4)[k] for k in keys) == (0, 16, 1, 128, 320 * 256 + table(32, 4, 16), 5)
-    assert tuple(info_for(24, "f32")[k] for k in keys) == (0, 16, 1, 64, 24 * 256 + table(32, 1, 16), 1)
+    assert tuple(info_for(512, "f32")[k] for k in keys) == (0, 16, 64, 512 * 256 + table(32, 1), 8)
+    assert tuple(info_for(512, "f32", 4)[k] for k in keys) == (0, 16, 64, 512 * 256 + table(32, 4), 8)
+    assert tuple(info_for(320, "f16", 4)[k] for k in keys) == (0, 16, 128, 320 * 256 + table(32, 4), 5)
+    assert tuple(info_for(24, "f32")[k] for k in keys) == (0, 16, 64, 24 * 256 + table(32, 1), 1)
     # wider inputs: 128-byte rows, then the direct-load kernel
-    assert tuple(info_for(1024, "f32")[k] for k in keys) == (0, 8, 1, 32, 1024 * 128 + table(32, 1, 8), 8)
+    assert tuple(info_for(1024, "f32")[k] for k in keys) == (0, 8, 32, 1024 * 128 + table(32, 1), 8)
     i = info_for(1500, "f32")
-    assert i["kernel"] == 1 and i["lds_bytes"] == 0 and i["loader_waves"] == 0 and i["vecs_per_lane"] == 1
+    assert i["kernel"] == 1 and i["lds_bytes"] == 0 and i["loader_waves"] == 0 and i["vec_bytes"] == 16
     i = info_for(512, "f32")
     assert i["waves"] + i["loader_waves"] <= 16
 

@@ -30,7 +30,7 @@ SMALL = [
     (200, 120, 9, 9, 2, 0.9, 1, "f16", "relu"),
     (200, 120, 9, 9, 2, 0.9, 4, "f16", "none"),
     (512, 64, 14, 14, 3, 0.9, 1, "f32", "relu"),
-    (700, 64, 7, 7, 2, 0.9, 1, "f32", "relu6"),     # 8 lanes per row
+    (700, 64, 7, 7, 2, 0.9, 1, "f32", "relu6"),     # 8-byte lane vectors
     (1280, 32, 7, 7, 2, 0.9, 4, "f32", "relu6"),
     (1500, 48, 6, 6, 2, 0.9, 1, "f32", "relu"),     # direct-load kernel
     (1500, 48, 6, 6, 2, 0.9, 4, "f16", "relu"),
@@ -123,12 +123,32 @@ def test_run_is_deterministic_and_independent_of_planning():
     note("determinism")
     base = gpu_run(layer)
     assert np.array_equal(base, gpu_run(layer))
-    for opts in (dict(reorder=0), dict(lanes_per_row=16, vecs_per_lane=1), dict(lanes_per_row=8, vecs_per_lane=1),
-                 dict(lanes_per_row=32), dict(lanes_per_row=32, vecs_per_lane=2), dict(lanes_per_row=64),
+    for opts in (dict(reorder=0), dict(vec_bytes=8), dict(kernel=2), dict(kernel=1, vec_bytes=8, prefetch=0),
                  dict(waves=1), dict(waves=5), dict(waves=12, reorder=0), dict(prefetch=0),
-                 dict(prefetch=0, waves=16, lanes_per_row=16, vecs_per_lane=1)):
+                 dict(prefetch=0, waves=16)):
         note("determinism %s" % opts)
         assert np.array_equal(base, gpu_run(layer, **opts)), opts
+
+
+@pytest.mark.parametrize("n", [1, 3, 83, 84, 85, 128])
+@pytest.mark.parametrize("k", [1, 4])
+def test_shared_tail_tiles(n, k):
+    """Batch sizes around one round of tiles: the tiles left after the whole
+    rounds are split by rows over several workgroups (up to 16 here)."""
+    layer = make_layer(512, 512, 14, 14, n, 0.9, block_rows=k, act="relu", seed=11 + n)
+    note("tail split n=%d k=%d" % (n, k))
+    assert_parity(layer, gpu_run(layer), what="tail n=%d k=%d" % (n, k))
+
+
+def test_split_does_not_change_bits():
+    """The per-row summation order is fixed, so how tiles are shared between
+    workgroups does not change a single bit: image i of a batch of 85 equals
+    image i of a batch of 84 (different tail splits)."""
+    big = make_layer(512, 512, 14, 14, 85, 0.9, act="none", seed=12)
+    small = make_layer(512, 512, 14, 14, 84, 0.9, act="none", seed=12)
+    small.x = np.ascontiguousarray(big.x[:84])
+    note("split bits")
+    assert np.array_equal(gpu_run(big)[:84], gpu_run(small))
 
 
 def test_blocked_equals_expanded_csr_bitwise():
