@@ -14,11 +14,21 @@ last-level cache.  Kernel durations come from HIP events recorded on the
 launch stream around every launch.
 
 Prints one JSON line.  ``--gpus`` above 1 is refused: this build measures one GPU.
+
+Two more modes produce the HBM-traffic figures of the ``roofline`` object:
+  --profile-run            a few launches of each variant, then a plain copy
+                           kernel of known size (run under rocprofv3 --pmc)
+  --traffic-summary F W    read the FETCH_SIZE (F) and WRITE_SIZE (W) counter
+                           directories of two such runs, scale each counter by
+                           what it read for the copy, and write
+                           profiles/traffic_spmm_strip_512_14_b256.{json,md}
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
 import hashlib
 import json
 import os
@@ -28,11 +38,14 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-HBM_PEAK_GBS = 8000.0        # MI355X HBM3E peak
+HBM_PEAK_GBS = 8000.0         # MI355X HBM3E peak
 FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector peak (packed FMA)
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_spmm_strip_512_14_b256.json")
+TRAFFIC_BASE = os.path.join(ROOT, "profiles", "traffic_spmm_strip_512_14_b256")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_09723_amd", "csrc", f)
                   for f in ("spmm_kernels.hip", "planner.cpp", "planner.hpp")]
+COPY_BYTES = 256 << 20        # calibration copy: 256 MiB read + 256 MiB written
+CALIBRATION_KERNEL = "neg_kernel"  # torch.neg(a, out=b): a plain elementwise copy
+METRIC = "effective GFLOP/s (2*nnz*HW*N) + HBM GB/s % peak, sparse 1x1 conv"
 
 
 def log(*a):
@@ -48,16 +61,27 @@ def kernel_source_hash() -> str:
 
 
 def measured_traffic():
-    """Per-launch HBM bytes from the committed rocprofv3 counter runs, if they
-    were taken on the current kernel source; else None."""
+    """Per-launch HBM bytes from the committed counter runs, if they were taken
+    on the current kernel source; else None."""
     try:
-        with open(TRAFFIC_FILE) as f:
+        with open(TRAFFIC_BASE + ".json") as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
     if t.get("kernel_source_hash") != kernel_source_hash():
         return None
     return t
+
+
+def headline_layers():
+    from synth.configs import TARGET, config_layers, build
+    specs = [s for s in config_layers(TARGET["config"]) if s["layer"] == TARGET["layer"]]
+    out = {}
+    for spec in specs:
+        tag = "1x%d" % spec["block_rows"]
+        log("bench: generating %s" % spec["name"])
+        out[tag] = build(TARGET["config"], spec)
+    return out
 
 
 def time_variant(layer, steps, warmup, sets):
@@ -73,7 +97,6 @@ def time_variant(layer, steps, warmup, sets):
     stream = torch.cuda.current_stream()
     for i in range(warmup):
         spconv_run(plan.handle, xs[i % sets], ys[i % sets], n, h, w, stream)
-    torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
@@ -97,25 +120,32 @@ def time_variant(layer, steps, warmup, sets):
 
 
 def cpu_baseline(layer, budget_s=12.0):
-    """The oracle on the first images of the batch, timed on this host."""
+    """The oracle, as it stands, timed on this host on a bounded sample of the
+    same layer (the first images of the batch, repeated to fill the budget)."""
     import numpy as np
     import oracle
 
     oracle.build(force=False)
     t0 = time.perf_counter()
     oracle.spconv_ref_layer(layer, x=layer.x[:1], with_scale=False)
-    t1 = time.perf_counter() - t0
-    n_s = int(max(1, min(layer.n, budget_s / max(t1, 1e-6))))
+    t1 = max(time.perf_counter() - t0, 1e-6)
+    n_s = int(max(1, min(layer.n, budget_s / t1)))
+    xs = np.ascontiguousarray(layer.x[:n_s])
+    reps = 0
     t0 = time.perf_counter()
-    oracle.spconv_ref_layer(layer, x=np.ascontiguousarray(layer.x[:n_s]), with_scale=False)
-    dt = time.perf_counter() - t0
+    while True:
+        oracle.spconv_ref_layer(layer, x=xs, with_scale=False)
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= 0.8 * budget_s or reps >= 1000:
+            break
     return {
-        "value": round(layer.flops(n_s) / dt / 1e9, 3),
-        "unit": "effective GFLOP/s",
+        "value": round(layer.flops(n_s) * reps / dt / 1e9, 3),
+        "unit": "GFLOP/s",
         "cores": oracle.threads(),
         "kind": "oracle",
-        "sample": "%d of %d images of the same layer (fp64 accumulation, OpenMP over images x rows), %.1f s"
-                  % (n_s, layer.n, dt),
+        "sample": "%d pass(es) over %d of %d images of the same layer (fp64 accumulation, OpenMP over "
+                  "images x rows), %.1f s" % (reps, n_s, layer.n, dt),
     }
 
 
@@ -126,7 +156,9 @@ def summarize(layer, r):
     t_kern = float(np.mean(r["kernel_ms"])) / 1e3
     flops = layer.flops()
     b_alg = layer.alg_bytes()
-    t_roof = max(b_alg / (HBM_PEAK_GBS * 1e9), flops / (FP32_VECTOR_PEAK_TFS * 1e12))
+    t_hbm = b_alg / (HBM_PEAK_GBS * 1e9)
+    t_alu = flops / (FP32_VECTOR_PEAK_TFS * 1e12)
+    t_roof = max(t_hbm, t_alu)
     return {
         "gflops_effective": round(flops / t_step / 1e9, 1),
         "ms_per_step": round(t_step * 1e3, 5),
@@ -135,42 +167,137 @@ def summarize(layer, r):
         "hbm_gbs_algorithmic": round(b_alg / t_kern / 1e9, 1),
         "roofline_us": round(t_roof * 1e6, 3),
         "roofline_frac": round(t_roof / t_kern, 4),
-        "bound": "hbm" if b_alg / (HBM_PEAK_GBS * 1e9) >= flops / (FP32_VECTOR_PEAK_TFS * 1e12) else "fp32",
+        "bound": "hbm" if t_hbm >= t_alu else "alu",
         "nnz": layer.nnz,
         "alg_bytes": b_alg,
         "flops": flops,
-        "plan": {k: r["info"][k] for k in ("kernel", "lanes_per_row", "tile_cols", "waves", "lds_bytes",
-                                           "slots")},
+        "plan": {k: r["info"][k] for k in ("kernel", "vec_bytes", "tile_cols", "waves", "loader_waves",
+                                           "lds_bytes", "slots", "max_parts")},
     }
+
+
+def profile_run(reps: int):
+    """A few launches of each variant, then the calibration copy (for rocprofv3)."""
+    import torch
+    from paper_1911_09723_amd import Plan, spconv_run
+
+    dev = torch.device("cuda:0")
+    for tag, layer in headline_layers().items():
+        plan = Plan.from_layer(layer)
+        n, c, h, w = layer.x.shape
+        x0 = torch.from_numpy(layer.x).to(dev)
+        xs = [x0, x0.clone(), x0.clone()]  # the bench's three rotating buffer sets
+        ys = [torch.empty((n, layer.cout, h, w), dtype=x0.dtype, device=dev) for _ in range(3)]
+        for i in range(reps):
+            spconv_run(plan.handle, xs[i % 3], ys[i % 3], n, h, w)
+        torch.cuda.synchronize()
+        plan.close()
+        del xs, ys, x0
+        torch.cuda.empty_cache()
+        log("profile-run: %s done" % tag)
+    a = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device=dev)
+    b = torch.empty_like(a)
+    for _ in range(reps):
+        torch.neg(a, out=b)  # a plain copy: reads and writes COPY_BYTES once each
+    torch.cuda.synchronize()
+    log("profile-run: copy of %d bytes done" % COPY_BYTES)
+
+
+def _read_counter_dir(d, counter):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % d)
+    per = {}
+    for f in files:
+        for row in csv.DictReader(open(f)):
+            if row["Counter_Name"] != counter:
+                continue
+            key = (row["Kernel_Name"], int(row["Dispatch_Id"]))
+            per[key] = per.get(key, 0.0) + float(row["Counter_Value"])
+    return per
+
+
+def traffic_summary(fetch_dir, write_dir, commands, out_base):
+    """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) by the copy kernel's
+    reading and write the per-launch HBM traffic of the headline kernel."""
+    import numpy as np
+    out = {"kernel_source_hash": kernel_source_hash(), "copy_bytes": COPY_BYTES, "commands": commands}
+    for counter, d in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        per = _read_counter_dir(d, counter)
+        copy = [v for (k, _), v in per.items() if CALIBRATION_KERNEL in k]
+        if not copy:
+            raise SystemExit("no calibration copy dispatch found in %s" % d)
+        copy_kib = float(np.median(copy))
+        factor = COPY_BYTES / (copy_kib * 1024.0)
+        out[counter] = {"copy_kib_per_dispatch": copy_kib, "factor": factor, "kernels": {}}
+        kinds = sorted({k for (k, _) in per if "spmm" in k})
+        for k in kinds:
+            vals = [v for (kk, _), v in per.items() if kk == k]
+            out[counter]["kernels"][k] = {"kib_per_dispatch": float(np.median(vals)), "dispatches": len(vals),
+                                          "bytes_scaled": float(np.median(vals)) * 1024.0 * factor}
+    # the headline (unstructured, 16-byte vectors) kernel
+    head = [k for k in out["FETCH_SIZE"]["kernels"] if "spmm_strip<16, 1, false, true>" in k]
+    if head:
+        k = head[0]
+        out["headline_kernel"] = k
+        out["bytes_per_launch"] = round(out["FETCH_SIZE"]["kernels"][k]["bytes_scaled"] +
+                                        out["WRITE_SIZE"]["kernels"].get(k, {}).get("bytes_scaled", 0.0))
+    os.makedirs(os.path.dirname(out_base), exist_ok=True)
+    with open(out_base + ".json", "w") as f:
+        json.dump(out, f, indent=1, sort_keys=True)
+    lines = ["# HBM traffic per launch: sparse 1x1 conv 512->512 @14x14, batch 256, 90%", "",
+             "Counters FETCH_SIZE and WRITE_SIZE (KiB per dispatch), each from its own rocprofv3 run, "
+             "scaled by the factor that maps the same counter's reading for a plain copy of %d bytes "
+             "(read once, written once) to that size." % COPY_BYTES, "", "Commands:", ""]
+    lines += ["    " + c for c in commands]
+    lines += ["", "| counter | copy KiB/dispatch | factor |", "|---|---|---|"]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        lines.append("| %s | %.0f | %.4f |" % (c, out[c]["copy_kib_per_dispatch"], out[c]["factor"]))
+    lines += ["", "| kernel | counter | KiB/dispatch | scaled MB |", "|---|---|---|---|"]
+    for c in ("FETCH_SIZE", "WRITE_SIZE"):
+        for k, v in out[c]["kernels"].items():
+            lines.append("| %s | %s | %.0f | %.2f |" % (k.split("(")[0], c, v["kib_per_dispatch"],
+                                                        v["bytes_scaled"] / 1e6))
+    if "bytes_per_launch" in out:
+        lines += ["", "Headline kernel: %.2f MB per launch (fetch + write, scaled)." % (out["bytes_per_launch"] / 1e6)]
+    lines += ["", "kernel source hash: %s" % out["kernel_source_hash"]]
+    with open(out_base + ".md", "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({k: out[k] for k in ("bytes_per_launch", "headline_kernel") if k in out}))
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--sets", type=int, default=3, help="rotating (X, Y) buffer sets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
+    ap.add_argument("--profile-run", action="store_true", help="launches for rocprofv3 counter passes")
+    ap.add_argument("--reps", type=int, default=5, help="launches per variant in --profile-run")
+    ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--command", action="append", default=[], help="command lines recorded in the summary")
+    ap.add_argument("--out", default=TRAFFIC_BASE, help="output path (without extension) of --traffic-summary")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (got --gpus %d)" % args.gpus,
               file=sys.stderr)
         sys.exit(2)
+    if args.traffic_summary:
+        traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.command, args.out)
+        return
 
     import torch
-    from synth.configs import TARGET, config_layers, build
-
     if not torch.cuda.is_available():
         raise RuntimeError("bench.py needs a ROCm GPU")
-    specs = [s for s in config_layers(TARGET["config"]) if s["layer"] == TARGET["layer"]]
+    if args.profile_run:
+        profile_run(args.reps)
+        return
+
+    layers = headline_layers()
     results = {}
-    layers = {}
-    for spec in specs:
-        tag = "1x%d" % spec["block_rows"]
-        log("bench: generating %s" % spec["name"])
-        layer = build(TARGET["config"], spec)
-        layers[tag] = layer
+    for tag, layer in layers.items():
         log("bench: timing %s (%d warmup, %d steps, %d buffer sets)" % (tag, args.warmup, args.steps, args.sets))
         r = time_variant(layer, args.steps, args.warmup, args.sets)
         results[tag] = summarize(layer, r)
@@ -181,7 +308,7 @@ def main():
     traffic = measured_traffic()
     achieved = head["hbm_gbs_algorithmic"]
     line = {
-        "metric": "effective GFLOP/s (2*nnz*HW*N) + HBM GB/s % peak, sparse 1x1 conv",
+        "metric": METRIC,
         "value": head["gflops_effective"],
         "unit": "GFLOP/s",
         "n_gpus": 1,
@@ -206,7 +333,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None if traffic is None else traffic["bytes_per_launch"],
+            "traffic": None if traffic is None else traffic.get("bytes_per_launch"),
         },
         "variants": results,
         "device": torch.cuda.get_device_name(0),

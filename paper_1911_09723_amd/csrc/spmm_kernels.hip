@@ -402,34 +402,49 @@ struct StripArgs {
     int32_t idx_bytes, val_bytes;
     int32_t strip_bytes, meta_words, nbundles;
     int32_t tiles;        // tiles of the launch
-    int32_t whole_tiles;  // tiles processed whole, round-robin over the grid
+    int32_t whole_tiles;  // tiles processed whole: a multiple of the grid
     int32_t tail_parts;   // workgroups sharing each remaining tile (a power of two)
+    int32_t nxcd;         // workgroup i runs on XCD i % nxcd; the grid is a multiple of it
 };
 
 // A workgroup's unit of work: a tile, whole (part < 0) or one of tail_parts
-// parts of its rows; tile < 0 when none is left.
+// parts of its rows; tile < 0 when none is left.  `round` counts the whole
+// tiles (-1 for a shared one).
+//
+// Tiles are laid out so that the workgroups of one XCD work on neighbouring
+// tiles: XCD x owns the whole tiles [x * W, (x + 1) * W), W = whole_tiles /
+// nxcd, and its workgroups take them 1 per round in order.  A strip row of a
+// tile rarely starts or ends on a 128-byte line, and the neighbouring tile
+// needs the rest of that line: on the same XCD it finds it in L2.  All parts
+// of a shared tile run on one XCD, so its strip is fetched from memory once.
 struct Work {
-    int32_t tile, part;
+    int32_t tile, part, round;
 };
 
 __device__ __forceinline__ Work tail_work(const StripArgs &a) {
-    const int32_t i = static_cast<int32_t>(blockIdx.x);
-    if (i < (a.tiles - a.whole_tiles) * a.tail_parts)
-        return Work{a.whole_tiles + i / a.tail_parts, a.tail_parts > 1 ? i % a.tail_parts : -1};
-    return Work{-1, -1};
+    const int32_t b = static_cast<int32_t>(blockIdx.x);
+    const int32_t x = b % a.nxcd, lb = b / a.nxcd;
+    const int32_t u = x + a.nxcd * (lb / a.tail_parts);  // remaining tile of this workgroup
+    if (u < a.tiles - a.whole_tiles)
+        return Work{a.whole_tiles + u, a.tail_parts > 1 ? lb % a.tail_parts : -1, -1};
+    return Work{-1, -1, -1};
+}
+
+__device__ __forceinline__ Work whole_work(const StripArgs &a, int32_t r) {
+    const int32_t b = static_cast<int32_t>(blockIdx.x);
+    const int32_t bpx = static_cast<int32_t>(gridDim.x) / a.nxcd;  // workgroups per XCD
+    return Work{(b % a.nxcd) * (a.whole_tiles / a.nxcd) + r * bpx + b / a.nxcd, -1, r};
 }
 
 __device__ __forceinline__ Work first_work(const StripArgs &a) {
-    const int32_t i = static_cast<int32_t>(blockIdx.x);
-    return i < a.whole_tiles ? Work{i, -1} : tail_work(a);
+    return a.whole_tiles > 0 ? whole_work(a, 0) : tail_work(a);
 }
 
 __device__ __forceinline__ Work next_work(const StripArgs &a, Work w) {
-    if (w.tile >= 0 && w.tile < a.whole_tiles) {
-        const int32_t t = w.tile + static_cast<int32_t>(gridDim.x);
-        return t < a.whole_tiles ? Work{t, -1} : tail_work(a);
-    }
-    return Work{-1, -1};
+    if (w.round >= 0)
+        return (w.round + 1) * static_cast<int32_t>(gridDim.x) < a.whole_tiles ? whole_work(a, w.round + 1)
+                                                                               : tail_work(a);
+    return Work{-1, -1, -1};
 }
 
 constexpr int kLoaderVecs = 16;  // 16-byte strip vectors one loader lane holds
@@ -812,6 +827,9 @@ hipError_t prepare_strip(DevicePlan &p) {
     return hipSuccess;
 }
 
+// XCDs of an MI355X: consecutive workgroups of a launch go to consecutive XCDs.
+constexpr int64_t kXcds = 8;
+
 int64_t pow2_floor(int64_t v) {
     int64_t r = 1;
     while (r * 2 <= v)
@@ -829,11 +847,16 @@ hipError_t launch_strip(const DevicePlan &p, const void *x, void *y, int32_t m, 
     if (slots < 1)
         return hipErrorInvalidConfiguration;
     // whole rounds of `slots` tiles, then each remaining tile shared by up to
-    // slots / remaining workgroups (a power of two, at most the plan's max_parts)
-    const int64_t whole = tiles >= slots ? tiles / slots * slots : 0;
+    // (workgroups per XCD) / (remaining tiles per XCD) workgroups of one XCD
+    // (a power of two, at most the plan's max_parts).  The grid is always
+    // `slots` workgroups; those left without work leave at once.
+    const int64_t nxcd = slots % kXcds == 0 ? kXcds : 1;
+    const int64_t whole = tiles / slots * slots;
     const int64_t rest = tiles - whole;
-    const int64_t parts = rest ? std::max<int64_t>(1, std::min<int64_t>(pow2_floor(slots / rest), p.max_parts)) : 1;
-    const int64_t grid = whole ? slots : rest * parts;
+    const int64_t per_xcd = (rest + nxcd - 1) / nxcd;
+    const int64_t parts =
+        rest ? std::max<int64_t>(1, std::min<int64_t>(pow2_floor(slots / nxcd / per_xcd), p.max_parts)) : 1;
+    const int64_t grid = slots;
     StripArgs a;
     a.cin = p.cin;
     a.cout = p.cout;
@@ -849,6 +872,7 @@ hipError_t launch_strip(const DevicePlan &p, const void *x, void *y, int32_t m, 
     a.tiles = static_cast<int32_t>(tiles);
     a.whole_tiles = static_cast<int32_t>(whole);
     a.tail_parts = static_cast<int32_t>(parts);
+    a.nxcd = static_cast<int32_t>(nxcd);
     if (vec)
         hipLaunchKernelGGL((spmm_strip<VB, K, F16, true>), dim3(static_cast<unsigned>(grid)), dim3(threads),
                            p.lds_bytes, stream, x, y, p.idx, p.val, p.hdr, p.meta, p.wave_ptr, p.wave_chunk, p.split,
