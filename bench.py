@@ -32,6 +32,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -256,8 +257,9 @@ def traffic_summary(fetch_dir, write_dir, commands, out_base):
     lines += ["", "| kernel | counter | KiB/dispatch | scaled MB |", "|---|---|---|---|"]
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         for k, v in out[c]["kernels"].items():
-            lines.append("| %s | %s | %.0f | %.2f |" % (k.split("(")[0], c, v["kib_per_dispatch"],
-                                                        v["bytes_scaled"] / 1e6))
+            m = re.search(r"spmm_\w+<[^>]*>", k)
+            lines.append("| `%s` | %s | %.0f | %.2f |" % (m.group(0) if m else k, c, v["kib_per_dispatch"],
+                                                          v["bytes_scaled"] / 1e6))
     if "bytes_per_launch" in out:
         lines += ["", "Headline kernel: %.2f MB per launch (fetch + write, scaled)." % (out["bytes_per_launch"] / 1e6)]
     lines += ["", "kernel source hash: %s" % out["kernel_source_hash"]]
