@@ -172,8 +172,8 @@ def summarize(layer, r):
         "nnz": layer.nnz,
         "alg_bytes": b_alg,
         "flops": flops,
-        "plan": {k: r["info"][k] for k in ("kernel", "vec_bytes", "tile_cols", "waves", "loader_waves",
-                                           "lds_bytes", "slots", "max_parts")},
+        "plan": {k: r["info"][k] for k in ("kernel", "group_lanes", "tile_cols", "waves", "lds_bytes", "slots",
+                                           "max_parts")},
     }
 
 

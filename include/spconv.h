@@ -101,7 +101,9 @@ spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, in
  *
  * Errors: SPCONV_E_ARG (NULL plan/x/y with work to do, negative sizes, overlap,
  * other device, host-only plan), SPCONV_E_SHAPE (sizes beyond 2^31 columns or
- * elements beyond 2^62), SPCONV_E_HIP (launch failure).  Faults during
+ * elements beyond 2^62), SPCONV_E_UNSUPPORTED ((tile columns + h * w) * cin
+ * elements of one tile's images span 2^31 bytes or more), SPCONV_E_HIP
+ * (launch failure).  Faults during
  * execution surface at the caller's next synchronization.
  */
 spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
@@ -127,14 +129,13 @@ typedef struct {
     int32_t kernel;      /* 0 = choose automatically; 1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED
                             when the strip of cin channels does not fit in LDS); 2 = direct-load
                             kernel */
-    int32_t vec_bytes;   /* 0 = choose automatically; else 8 or 16 bytes of X each lane reads per
-                            nonzero (16 lanes share a row, so a tile is 16 * vec_bytes bytes wide);
-                            the direct kernel takes 16 only */
-    int32_t waves;       /* 0 = choose automatically; else the number of compute wavefronts per
-                            workgroup (with the loader wavefronts, at most 16 in all) */
-    int32_t prefetch;    /* 1 (default): loader wavefronts fetch the next strip while the others
-                            compute; 0: every wavefront computes and strips are copied between
-                            tiles */
+    int32_t group_lanes; /* 0 = choose automatically; else 4, 8 or 16 lanes per (block) row: each
+                            lane accumulates 16 / group_lanes vectors of 16 bytes of the tile's
+                            columns, and a wavefront works on 64 / group_lanes rows at a time
+                            (SPCONV_E_UNSUPPORTED when a lane would hold more than 64 fp32
+                            accumulators) */
+    int32_t waves;       /* 0 = choose automatically; else the number of wavefronts per
+                            workgroup, 1 to 16 */
 } spconv_options;
 
 /* Fill *opts with the defaults used by spconv_plan_create. */
@@ -150,16 +151,15 @@ typedef struct {
     int32_t cout, cin, block_rows;
     int32_t storage, act;
     int32_t kernel;        /* 0: LDS-strip kernel; 1: direct-load kernel for wide inputs */
-    int32_t vec_bytes;     /* bytes of X each lane reads per nonzero */
-    int32_t cols_per_lane; /* output columns each lane accumulates (vec_bytes / element size) */
-    int32_t tile_cols;     /* columns per workgroup tile = 16 * cols_per_lane */
-    int32_t waves;         /* compute wavefronts per workgroup */
-    int32_t loader_waves;  /* wavefronts per workgroup that prefetch the next strip */
-    int32_t groups;        /* block rows one wavefront processes together (16 lanes each) */
+    int32_t group_lanes;   /* lanes per (block) row */
+    int32_t bundle_rows;   /* (block) rows a wavefront works on at a time = 64 / group_lanes */
+    int32_t cols_per_lane; /* output columns each lane accumulates */
+    int32_t tile_cols;     /* columns per workgroup tile (256 bytes of one channel) */
+    int32_t waves;         /* wavefronts per workgroup */
     int32_t lds_bytes;     /* LDS per workgroup */
     int32_t max_parts;     /* most workgroups that may share the rows of one tile */
     int64_t nnzb;          /* stored blocks */
-    int64_t slots;         /* packed (index, value) entries including padding */
+    int64_t slots;         /* packed (channel, weight) slots including padding */
     int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
     int64_t sum_wave_cost; /* total of the per-wavefront work estimates */
     int64_t device_bytes;  /* device memory the plan holds */

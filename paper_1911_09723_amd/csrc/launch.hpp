@@ -13,30 +13,30 @@ namespace spconv {
 // the launch facts fixed at plan creation.
 struct DevicePlan {
     int32_t kernel = KERNEL_STRIP;
-    int32_t vec_bytes = 16;
+    int32_t group_lanes = 4;
     int32_t tile_cols = 64;
     int32_t waves = 1;
-    int32_t loader_waves = 0;
     int32_t lds_bytes = 0;
     int32_t k = 1;
     int32_t storage = 0;
     int32_t act = 0;
     int32_t cin = 0, cout = 0;
-    int32_t idx_bytes = 0;      // size of the index stream (bounds of its buffer resource)
+    int32_t strip_rows = 0;     // channels of the LDS strip (cin rounded up to 4); 0 for the direct kernel
+    int32_t split_rows = 0;     // rows of the strip's lower part
+    int32_t busy_waves = 0;     // wavefronts with at least one bundle
+    int32_t idx_bytes = 0;      // size of the channel stream (bounds of its buffer resource)
     int32_t val_bytes = 0;      // size of the weight stream
     int32_t num_cus = 0;        // compute units of the plan's device
-    int32_t blocks_per_cu = 0;  // resident workgroups per CU of the strip kernel
-    int32_t strip_bytes = 0;    // LDS bytes of the X strip (the bundle table follows it)
-    int32_t meta_words = 0;     // 32-bit words of the bundle table
+    int32_t blocks_per_cu = 0;  // resident workgroups per CU
     int32_t nbundles = 0;
     int32_t max_parts = 1;      // most workgroups that may share one tile
     const int32_t *idx = nullptr;
     const float *val = nullptr;
-    const int32_t *hdr = nullptr;         // (first step, steps) per bundle
-    const int32_t *meta = nullptr;        // rows, biases (fp32 bits), steps
-    const int32_t *wave_ptr = nullptr;    // bundles of each wave
-    const int32_t *wave_chunk = nullptr;  // first chunk of each wave
-    const int32_t *split = nullptr;       // 65 part boundaries per wave
+    const int32_t *hdr = nullptr;       // (first step, steps) per bundle
+    const int32_t *table = nullptr;     // rows, then biases (fp32 bits), per (bundle, group)
+    const int32_t *rank = nullptr;      // longest-first rank of each bundle
+    const int32_t *wave_ptr = nullptr;  // bundles of each wave
+    const int32_t *wave_meta = nullptr; // per wave: lower part released after, upper part first needed at
 };
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when
@@ -45,8 +45,9 @@ hipError_t prepare_launch(DevicePlan &p);
 
 // Queue one launch computing all m = N * hw columns.  `vec` != 0 promises
 // that hw is a multiple of the columns in one 16-byte vector and that x and y
-// are 16-byte aligned, enabling 16-byte global loads and stores.
+// are 16-byte aligned, enabling 16-byte loads and stores.  `x_bytes` and
+// `y_bytes` are the sizes of x and y.
 hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, int32_t hw, int32_t vec,
-                       hipStream_t stream);
+                       int64_t x_bytes, int64_t y_bytes, hipStream_t stream);
 
 }  // namespace spconv

@@ -160,63 +160,69 @@ Status validate(const Input &in, std::string &err) {
 
 namespace {
 
-// Per-bundle fixed cost (epilogue, table reads) in units of one slot step.
+// Per-bundle fixed cost (epilogue, table reads) in units of one slot.
 constexpr int64_t kBundleOverhead = 3;
+// Most fp32 accumulators one lane may hold (k rows x its columns), and the
+// most the automatic choice uses (a 1xk block's k weights per slot also sit
+// in the lane's registers, so wider blocks take narrower column sets).
+constexpr int32_t kMaxAccumulators = 64;
+constexpr int32_t kAutoAccumulators = 32;
 
-// Bytes of the per-bundle table the strip kernel keeps in LDS, 16-byte rounded.
-int64_t table_bytes(const Input &in) {
-    const int64_t rows = in.cout / in.block_rows;
-    const int64_t bundles = (rows + kGroups - 1) / kGroups;
-    return (bundles * (kGroups * (1 + in.block_rows) + 1) * 4 + 15) & ~int64_t(15);
+int32_t bundles_of(int32_t rows, int32_t nb) { return (rows + nb - 1) / nb; }
+
+// Bytes of the per-bundle table the kernels keep in LDS, 16-byte rounded.
+int64_t table_bytes(int32_t nbundles, int32_t nb, int32_t k) {
+    return (static_cast<int64_t>(nbundles) * nb * (1 + k) * 4 + 15) & ~int64_t(15);
 }
 
 Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::string &err) {
-    const int e = in.storage == 1 ? 2 : 4;
-    // One strip row is 16 lanes x vec_bytes: 256 bytes read by 16 lanes at a
-    // time touch all 64 LDS banks once.  Wider inputs fall back to 128-byte
-    // rows, then to the direct-load kernel, which keeps 16-byte vectors.
-    auto strip_bytes = [&](int vb) { return static_cast<int64_t>(in.cin) * kLanesPerRow * vb; };
-    auto fits = [&](int vb) { return strip_bytes(vb) + table_bytes(in) <= kMaxLdsBytes; };
-    int vb = opt.vec_bytes;
-    bool strip;
-    if (opt.kernel == 2) {
-        strip = false;
-        if (vb == 0)
-            vb = 16;
-    } else if (vb == 0) {
-        vb = fits(16) ? 16 : 8;
-        strip = fits(vb);
-        if (!strip)
-            vb = 16;
-        if (opt.kernel == 1 && !strip) {
-            err = "the X strip of cin = " + std::to_string(in.cin) + " channels does not fit in LDS";
-            return E_UNSUPPORTED;
-        }
-    } else {
-        strip = fits(vb);
-        if (!strip && opt.kernel == 1) {
-            err = "the X strip of cin = " + std::to_string(in.cin) + " channels at vec_bytes = " +
-                  std::to_string(vb) + " does not fit in LDS";
-            return E_UNSUPPORTED;
-        }
+    const int32_t e = in.storage == 1 ? 2 : 4;
+    const int32_t k = in.block_rows;
+    const int32_t rows = in.cout / k;
+    auto accumulators = [&](int32_t g) { return k * (16 / g) * (16 / e); };
+    int32_t g = opt.group_lanes;
+    if (g == 0) {
+        // 4 lanes per row (16 bytes of X per lane and slot, 4 vectors) unless
+        // the accumulators would not fit; wider groups when there are too few
+        // bundles to occupy the workgroup's wavefronts
+        g = 4;
+        while (g < 16 && accumulators(g) > kAutoAccumulators)
+            g *= 2;
+        while (g < 16 && bundles_of(rows, 64 / g) < 8)
+            g *= 2;
+    } else if (accumulators(g) > kMaxAccumulators) {
+        err = "group_lanes = " + std::to_string(g) + " needs " + std::to_string(accumulators(g)) +
+              " accumulators per lane (limit " + std::to_string(kMaxAccumulators) + ")";
+        return E_UNSUPPORTED;
     }
-    p.vec_bytes = vb;
-    p.cols_per_lane = vb / e;
-    p.tile_cols = kLanesPerRow * p.cols_per_lane;
-    if (strip) {
+    p.group_lanes = g;
+    p.bundle_rows = 64 / g;
+    p.cols_per_lane = (16 / g) * (16 / e);
+    p.tile_cols = kRowBytes / e;
+    const int32_t nbundles = bundles_of(rows, p.bundle_rows);
+    const int64_t table = table_bytes(nbundles, p.bundle_rows, k) + kCtlBytes;
+    const int32_t strip_rows = (in.cin + 3) / 4 * 4;
+    const int64_t strip = static_cast<int64_t>(strip_rows) * kRowBytes;
+    const bool fits = strip + table <= kMaxLdsBytes;
+    if (opt.kernel == 1 && !fits) {
+        err = "the X strip of cin = " + std::to_string(in.cin) + " channels does not fit in LDS";
+        return E_UNSUPPORTED;
+    }
+    if (table > kMaxLdsBytes) {
+        err = "the bundle table of cout = " + std::to_string(in.cout) + " rows does not fit in LDS";
+        return E_UNSUPPORTED;
+    }
+    if (opt.kernel != 2 && fits) {
         p.kernel = KERNEL_STRIP;
-        p.row_scale = kLanesPerRow * vb;
-        p.strip_bytes = static_cast<int32_t>(strip_bytes(vb));
-        p.lds_bytes = static_cast<int32_t>(strip_bytes(vb) + table_bytes(in));
-        p.loader_waves = opt.prefetch ? static_cast<int32_t>((strip_bytes(vb) + kLoaderBytesPerWave - 1) /
-                                                             kLoaderBytesPerWave)
-                                      : 0;
+        p.row_scale = kRowBytes;
+        p.strip_rows = strip_rows;
+        p.split_rows = (strip_rows / 4 + 1) / 2 * 4;
+        p.lds_bytes = static_cast<int32_t>(strip + table);
     } else {
         p.kernel = KERNEL_DIRECT;
         p.row_scale = 1;
-        p.strip_bytes = 0;
-        p.lds_bytes = 0;
-        p.loader_waves = 0;
+        p.strip_rows = 0;
+        p.lds_bytes = static_cast<int32_t>(table);
     }
     return OK;
 }
@@ -231,12 +237,8 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         err = "kernel must be 0 (automatic), 1 (strip) or 2 (direct)";
         return E_ARG;
     }
-    if (opt.vec_bytes != 0 && opt.vec_bytes != 8 && opt.vec_bytes != 16) {
-        err = "vec_bytes must be 0, 8 or 16";
-        return E_ARG;
-    }
-    if (opt.kernel == 2 && opt.vec_bytes == 8) {
-        err = "the direct kernel reads 16-byte vectors (vec_bytes 0 or 16)";
+    if (opt.group_lanes != 0 && opt.group_lanes != 4 && opt.group_lanes != 8 && opt.group_lanes != 16) {
+        err = "group_lanes must be 0, 4, 8 or 16";
         return E_ARG;
     }
     if (opt.waves < 0 || opt.waves > kMaxWaves) {
@@ -245,10 +247,6 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     }
     if (opt.reorder != 0 && opt.reorder != 1) {
         err = "reorder must be 0 or 1";
-        return E_ARG;
-    }
-    if (opt.prefetch != 0 && opt.prefetch != 1) {
-        err = "prefetch must be 0 or 1";
         return E_ARG;
     }
 
@@ -264,7 +262,7 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
 
     const int32_t k = in.block_rows;
     const int32_t rows = in.cout / k;
-    constexpr int32_t G = kGroups;
+    const int32_t NB = p.bundle_rows;
     p.nnzb = in.row_ptr[rows];
 
     // 1. processing order: descending nonzero count, ties by row index (stable)
@@ -274,28 +272,22 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     if (opt.reorder)
         std::stable_sort(p.perm.begin(), p.perm.end(), [&](int32_t a, int32_t b) { return len(a) > len(b); });
 
-    // 2. bundles of G consecutive rows in that order, each a whole number of
+    // 2. bundles of NB consecutive rows in that order, each a whole number of
     // steps of 4 slots and at least one step long
     p.row_nnz.resize(rows);
     for (int32_t r = 0; r < rows; ++r)
         p.row_nnz[r] = len(r);
-    const int32_t nb = (rows + G - 1) / G;
+    const int32_t nb = bundles_of(rows, NB);
     std::vector<int32_t> bsteps(nb, 0);
     for (int32_t b = 0; b < nb; ++b) {
         int32_t l = 0;
-        for (int32_t g = 0; g < G && b * G + g < rows; ++g)
-            l = std::max(l, len(p.perm[b * G + g]));
-        bsteps[b] = std::max<int32_t>(1, (l + 3) / 4);
+        for (int32_t q = 0; q < NB && b * NB + q < rows; ++q)
+            l = std::max(l, len(p.perm[b * NB + q]));
+        bsteps[b] = std::max<int32_t>(1, (l + kStepSlots - 1) / kStepSlots);
     }
 
     // 3. longest-processing-time-first assignment of bundles to waves
-    const int32_t max_waves = kMaxWaves - p.loader_waves;
-    if (opt.waves > max_waves) {
-        err = "waves = " + std::to_string(opt.waves) + " plus " + std::to_string(p.loader_waves) +
-              " loader waves exceeds " + std::to_string(kMaxWaves) + " wavefronts per workgroup";
-        return E_ARG;
-    }
-    const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(max_waves, std::max<int32_t>(nb, 1));
+    const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(kMaxWaves, nb);
     p.waves = waves;
     std::vector<int32_t> order(nb);
     std::iota(order.begin(), order.end(), 0);
@@ -306,88 +298,100 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         heap.push({0, w});
     std::vector<std::vector<int32_t>> lists(waves);
     std::vector<int64_t> load(waves, 0);
-    for (int32_t b : order) {
+    std::vector<int32_t> rank_of(nb, 0);
+    for (int32_t i = 0; i < nb; ++i) {
+        const int32_t b = order[i];
+        rank_of[b] = i;
         Item it = heap.top();
         heap.pop();
         lists[it.second].push_back(b);
-        it.first += 4 * static_cast<int64_t>(bsteps[b]) + kBundleOverhead;
+        it.first += kStepSlots * static_cast<int64_t>(bsteps[b]) + kBundleOverhead;
         load[it.second] = it.first;
         heap.push(it);
     }
     p.max_wave_cost = waves ? *std::max_element(load.begin(), load.end()) : 0;
     p.sum_wave_cost = std::accumulate(load.begin(), load.end(), int64_t(0));
 
-    // 4. pack: bundles in wave order; each wave's steps in chunks of 4 steps
+    // 4. pack: bundles in wave order, each wave's bundles one continuous stream
+    int64_t total_steps = 0;
+    for (int32_t b = 0; b < nb; ++b)
+        total_steps += bsteps[b];
+    if (total_steps * NB * kStepSlots * k * 4 >= (int64_t(1) << 31)) {
+        err = "packed plan too large";
+        return E_SHAPE;
+    }
+    const int32_t pad_channel = p.kernel == KERNEL_STRIP ? p.strip_rows - 1 : 0;
+    p.idx.assign(static_cast<size_t>(total_steps * NB * kStepSlots), pad_channel * p.row_scale);
+    p.val.assign(static_cast<size_t>(total_steps * NB * kStepSlots * k), 0.0f);
     p.wave_ptr.assign(waves + 1, 0);
-    p.wave_chunk.assign(waves + 1, 0);
-    p.split.assign(static_cast<size_t>(waves) * (kMaxParts + 1), 0);
     p.hdr.reserve(2 * static_cast<size_t>(nb));
-    p.rows.reserve(static_cast<size_t>(G) * nb);
-    p.bundle_bias.reserve(static_cast<size_t>(G) * nb * k);
-    int64_t chunk0 = 0;  // first chunk of the current wave
-    int32_t bglob = 0;   // bundles packed so far
-    int32_t max_bundles = 0;
+    p.rows.reserve(static_cast<size_t>(NB) * nb);
+    p.bundle_bias.reserve(static_cast<size_t>(NB) * nb * k);
+    p.rank.reserve(nb);
+    p.wave_meta.assign(2 * static_cast<size_t>(waves), 0);
+    // slots of a row that read the strip's lower part (ascending channels)
+    auto lower = [&](int32_t rb) {
+        int32_t n = 0;
+        while (n < len(rb) && in.col_idx[in.row_ptr[rb] + n] < p.split_rows)
+            ++n;
+        return n;
+    };
+    int64_t step = 0;   // first step of the next bundle
+    int32_t bglob = 0;  // bundles packed so far
     for (int32_t w = 0; w < waves; ++w) {
-        int64_t total = 0;
-        for (int32_t b : lists[w])
-            total += bsteps[b];
-        const int64_t nchunks = (total + kChunkSteps - 1) / kChunkSteps;
-        if ((chunk0 + nchunks) * 64 * k > (int64_t(1) << 29)) {  // stream byte sizes stay below 2^31
-            err = "packed plan too large";
-            return E_SHAPE;
-        }
-        p.idx.resize(static_cast<size_t>((chunk0 + nchunks) * 64), 0);
-        p.val.resize(static_cast<size_t>((chunk0 + nchunks) * 64 * k), 0.0f);
-        // split[i]: first bundle whose first step is at or after i/64 of the stream
-        std::vector<int64_t> start(lists[w].size() + 1, 0);
-        for (size_t i = 0; i < lists[w].size(); ++i)
-            start[i + 1] = start[i] + bsteps[lists[w][i]];
-        for (int32_t i = 0; i <= kMaxParts; ++i) {
-            size_t j = 0;
-            while (j < lists[w].size() && start[j] * kMaxParts < static_cast<int64_t>(i) * total)
-                ++j;
-            if (i == kMaxParts)
-                j = lists[w].size();
-            p.split[static_cast<size_t>(w) * (kMaxParts + 1) + i] = bglob + static_cast<int32_t>(j);
-        }
-        for (size_t i = 0; i < lists[w].size(); ++i) {
-            const int32_t b = lists[w][i];
-            const int64_t s_first = start[i];
-            p.hdr.push_back(static_cast<int32_t>(s_first));
+        const int64_t wstart = step;
+        int64_t rel0 = 0, need1 = -1;
+        for (int32_t b : lists[w]) {
+            // a0: steps until every row has passed its lower-part channels;
+            // a1: first step in which some row reads the upper part (a padding
+            // group or a row's padding slots do from their first slot)
+            int64_t a0 = 0, a1 = bsteps[b];
+            for (int32_t q = 0; q < NB; ++q) {
+                const int32_t pos = b * NB + q;
+                const int32_t n0 = pos < rows ? lower(p.perm[pos]) : 0;
+                const int32_t n = pos < rows ? len(p.perm[pos]) : 0;
+                a0 = std::max<int64_t>(a0, (n0 + kStepSlots - 1) / kStepSlots);
+                if (n0 < static_cast<int64_t>(bsteps[b]) * kStepSlots && (n0 < n || n < bsteps[b] * kStepSlots))
+                    a1 = std::min<int64_t>(a1, n0 / kStepSlots);
+            }
+            rel0 = std::max(rel0, step - wstart + a0);
+            if (a1 < bsteps[b] && need1 < 0)
+                need1 = step - wstart + a1;
+            p.hdr.push_back(static_cast<int32_t>(step));
             p.hdr.push_back(bsteps[b]);
-            for (int32_t g = 0; g < G; ++g) {
-                const int32_t pos = b * G + g;
+            p.rank.push_back(rank_of[b]);
+            for (int32_t q = 0; q < NB; ++q) {
+                const int32_t pos = b * NB + q;
                 const int32_t rb = pos < rows ? p.perm[pos] : -1;
                 p.rows.push_back(rb);
-                for (int32_t ii = 0; ii < k; ++ii)
-                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + ii] : 0.0f);
+                for (int32_t i = 0; i < k; ++i)
+                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + i] : 0.0f);
                 if (rb < 0)
                     continue;
                 const int32_t r0 = in.row_ptr[rb];
                 for (int32_t t = 0; t < len(rb); ++t) {
-                    const int64_t s = s_first + t / 4;
-                    const int64_t e = 64 * (chunk0 + s / kChunkSteps) + kLanesPerRow * g + 4 * (s % kChunkSteps) +
-                                      (t % 4);
+                    const int64_t e = ((step + t / kStepSlots) * NB + q) * kStepSlots + t % kStepSlots;
                     p.idx[e] = in.col_idx[r0 + t] * p.row_scale;
-                    for (int32_t ii = 0; ii < k; ++ii) {
-                        float v = in.values[static_cast<int64_t>(r0 + t) * k + ii];
+                    for (int32_t i = 0; i < k; ++i) {
+                        float v = in.values[static_cast<int64_t>(r0 + t) * k + i];
                         if (in.storage == 1)
                             v = half_to_float(float_to_half_rne(v));
-                        p.val[e * k + ii] = v;
+                        p.val[e * k + i] = v;
                     }
                 }
             }
+            step += bsteps[b];
+            ++bglob;
         }
-        bglob += static_cast<int32_t>(lists[w].size());
-        max_bundles = std::max<int32_t>(max_bundles, static_cast<int32_t>(lists[w].size()));
         p.wave_ptr[w + 1] = bglob;
-        chunk0 += nchunks;
-        p.wave_chunk[w + 1] = static_cast<int32_t>(chunk0);
+        p.wave_meta[2 * w] = static_cast<int32_t>(rel0);
+        p.wave_meta[2 * w + 1] = static_cast<int32_t>(need1 < 0 ? step - wstart : need1);
+        if (!lists[w].empty())
+            ++p.busy_waves;
     }
-    p.slots = chunk0 * 64;
-    // A tile is shared by at most as many workgroups as the busiest wave has bundles.
+    p.slots = total_steps * NB * kStepSlots;
     p.max_parts = 1;
-    while (p.max_parts * 2 <= std::min<int32_t>(kMaxParts, max_bundles))
+    while (p.max_parts * 2 <= std::min<int32_t>(kMaxParts, nb))
         p.max_parts *= 2;
     return OK;
 }
@@ -395,26 +399,21 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm) {
     const int32_t k = p.k;
     const int32_t rows = p.cout / k;
-    constexpr int32_t G = kGroups;
+    const int32_t NB = p.bundle_rows;
     std::vector<std::vector<int32_t>> cols(rows);
     std::vector<std::vector<float>> vals(rows);
-    const int32_t waves = static_cast<int32_t>(p.wave_ptr.size()) - 1;
     // each row's real entries are the first row_nnz[rb] slots of its sequence
-    for (int32_t w = 0; w < waves; ++w) {
-        for (int32_t b = p.wave_ptr[w]; b < p.wave_ptr[w + 1]; ++b) {
-            const int64_t s_first = p.hdr[2 * b];
-            for (int32_t g = 0; g < G; ++g) {
-                const int32_t rb = p.rows[static_cast<size_t>(b) * G + g];
-                if (rb < 0)
-                    continue;
-                for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
-                    const int64_t s = s_first + t / 4;
-                    const int64_t e = 64 * (p.wave_chunk[w] + s / kChunkSteps) + kLanesPerRow * g +
-                                      4 * (s % kChunkSteps) + (t % 4);
-                    cols[rb].push_back(p.idx[e] / p.row_scale);
-                    for (int32_t i = 0; i < k; ++i)
-                        vals[rb].push_back(p.val[e * k + i]);
-                }
+    for (int32_t b = 0; b < p.nbundles(); ++b) {
+        const int64_t s_first = p.hdr[2 * b];
+        for (int32_t q = 0; q < NB; ++q) {
+            const int32_t rb = p.rows[static_cast<size_t>(b) * NB + q];
+            if (rb < 0)
+                continue;
+            for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
+                const int64_t e = ((s_first + t / kStepSlots) * NB + q) * kStepSlots + t % kStepSlots;
+                cols[rb].push_back(p.idx[e] / p.row_scale);
+                for (int32_t i = 0; i < k; ++i)
+                    vals[rb].push_back(p.val[e * k + i]);
             }
         }
     }

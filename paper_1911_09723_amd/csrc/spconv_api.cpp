@@ -69,14 +69,11 @@ spconv::Input make_input(int32_t cout, int32_t cin, int32_t block_rows, const in
 
 spconv_status upload(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
-    // bundle table: rows, the biases of those rows as fp32 bit patterns, steps
-    const size_t nb = static_cast<size_t>(h.nbundles());
-    std::vector<int32_t> meta(static_cast<size_t>(h.meta_words()));
-    std::copy(h.rows.begin(), h.rows.end(), meta.begin());
+    // bundle table: rows, then the biases of those rows as fp32 bit patterns
+    std::vector<int32_t> table(static_cast<size_t>(h.table_words()));
+    std::copy(h.rows.begin(), h.rows.end(), table.begin());
     if (!h.bundle_bias.empty())
-        std::memcpy(meta.data() + h.rows.size(), h.bundle_bias.data(), h.bundle_bias.size() * sizeof(float));
-    for (size_t b = 0; b < nb; ++b)
-        meta[h.rows.size() + h.bundle_bias.size() + b] = h.hdr[2 * b + 1];
+        std::memcpy(table.data() + h.rows.size(), h.bundle_bias.data(), h.bundle_bias.size() * sizeof(float));
     struct Part {
         const void *src;
         size_t bytes;
@@ -85,10 +82,10 @@ spconv_status upload(spconv_plan_s *pl) {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
-        {meta.data(), meta.size() * sizeof(int32_t), 0},
+        {table.data(), table.size() * sizeof(int32_t), 0},
+        {h.rank.data(), h.rank.size() * sizeof(int32_t), 0},
         {h.wave_ptr.data(), h.wave_ptr.size() * sizeof(int32_t), 0},
-        {h.wave_chunk.data(), h.wave_chunk.size() * sizeof(int32_t), 0},
-        {h.split.data(), h.split.size() * sizeof(int32_t), 0},
+        {h.wave_meta.data(), h.wave_meta.size() * sizeof(int32_t), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -122,10 +119,10 @@ spconv_status upload(spconv_plan_s *pl) {
     d.idx = reinterpret_cast<const int32_t *>(base + parts[0].off);
     d.val = reinterpret_cast<const float *>(base + parts[1].off);
     d.hdr = reinterpret_cast<const int32_t *>(base + parts[2].off);
-    d.meta = reinterpret_cast<const int32_t *>(base + parts[3].off);
-    d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[4].off);
-    d.wave_chunk = reinterpret_cast<const int32_t *>(base + parts[5].off);
-    d.split = reinterpret_cast<const int32_t *>(base + parts[6].off);
+    d.table = reinterpret_cast<const int32_t *>(base + parts[3].off);
+    d.rank = reinterpret_cast<const int32_t *>(base + parts[4].off);
+    d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[5].off);
+    d.wave_meta = reinterpret_cast<const int32_t *>(base + parts[6].off);
     return SPCONV_OK;
 }
 
@@ -133,21 +130,21 @@ void fill_device_geometry(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
     spconv::DevicePlan &d = pl->dev;
     d.kernel = h.kernel;
-    d.vec_bytes = h.vec_bytes;
+    d.group_lanes = h.group_lanes;
     d.tile_cols = h.tile_cols;
     d.waves = h.waves;
-    d.loader_waves = h.loader_waves;
     d.lds_bytes = h.lds_bytes;
     d.k = h.k;
     d.storage = h.storage;
     d.act = h.act;
     d.cin = h.cin;
     d.cout = h.cout;
+    d.strip_rows = h.strip_rows;
+    d.split_rows = h.split_rows;
+    d.busy_waves = h.busy_waves;
     d.idx_bytes = static_cast<int32_t>(h.idx.size() * sizeof(int32_t));
     d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
     d.nbundles = h.nbundles();
-    d.meta_words = h.meta_words();
-    d.strip_bytes = h.strip_bytes;
     d.max_parts = h.max_parts;
 }
 
@@ -166,7 +163,6 @@ void spconv_options_init(spconv_options *opts) {
     std::memset(opts, 0, sizeof(*opts));
     opts->struct_size = static_cast<int32_t>(sizeof(spconv_options));
     opts->reorder = 1;
-    opts->prefetch = 1;
 }
 
 spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
@@ -190,9 +186,8 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     po.reorder = o.reorder;
     po.host_only = o.host_only;
     po.kernel = o.kernel;
-    po.vec_bytes = o.vec_bytes;
+    po.group_lanes = o.group_lanes;
     po.waves = o.waves;
-    po.prefetch = o.prefetch;
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
     if (!pl)
@@ -273,7 +268,14 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
+    // the kernels address X relative to the first image of a tile with 32-bit
+    // byte offsets: a tile's images must span less than 2^31 bytes
+    if ((static_cast<int64_t>(p.tile_cols) + hw) * std::max(p.cin, p.cout) * static_cast<int64_t>(e) >=
+        (int64_t(1) << 31) - 16)
+        return fail(SPCONV_E_UNSUPPORTED,
+                    "h * w * channels too large: one tile's images must span less than 2^31 bytes");
     he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
+                             xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e),
                              static_cast<hipStream_t>(stream));
     if (he != hipSuccess)
         return hip_fail("kernel launch", he);
@@ -308,12 +310,11 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->storage = p.storage;
     info->act = p.act;
     info->kernel = p.kernel;
-    info->vec_bytes = p.vec_bytes;
+    info->group_lanes = p.group_lanes;
+    info->bundle_rows = p.bundle_rows;
     info->cols_per_lane = p.cols_per_lane;
     info->tile_cols = p.tile_cols;
     info->waves = p.waves;
-    info->loader_waves = p.loader_waves;
-    info->groups = spconv::kGroups;
     info->max_parts = p.max_parts;
     info->lds_bytes = p.lds_bytes;
     info->nnzb = p.nnzb;

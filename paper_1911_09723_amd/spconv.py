@@ -39,16 +39,15 @@ class SpconvError(RuntimeError):
 
 class spconv_options(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_int32), ("reorder", ctypes.c_int32), ("host_only", ctypes.c_int32),
-                ("kernel", ctypes.c_int32), ("vec_bytes", ctypes.c_int32), ("waves", ctypes.c_int32),
-                ("prefetch", ctypes.c_int32)]
+                ("kernel", ctypes.c_int32), ("group_lanes", ctypes.c_int32), ("waves", ctypes.c_int32)]
 
 
 class spconv_plan_info(ctypes.Structure):
     _fields_ = [("cout", ctypes.c_int32), ("cin", ctypes.c_int32), ("block_rows", ctypes.c_int32),
                 ("storage", ctypes.c_int32), ("act", ctypes.c_int32), ("kernel", ctypes.c_int32),
-                ("vec_bytes", ctypes.c_int32), ("cols_per_lane", ctypes.c_int32), ("tile_cols", ctypes.c_int32),
-                ("waves", ctypes.c_int32), ("loader_waves", ctypes.c_int32), ("groups", ctypes.c_int32),
-                ("lds_bytes", ctypes.c_int32), ("max_parts", ctypes.c_int32), ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
+                ("group_lanes", ctypes.c_int32), ("bundle_rows", ctypes.c_int32), ("cols_per_lane", ctypes.c_int32),
+                ("tile_cols", ctypes.c_int32), ("waves", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
+                ("max_parts", ctypes.c_int32), ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64)]
 

@@ -135,8 +135,9 @@ def test_null_arrays_with_nonzeros_rejected():
 
 
 def test_options_validated():
-    for kw in (dict(vec_bytes=12), dict(vec_bytes=4), dict(waves=17), dict(waves=-1), dict(reorder=2),
-               dict(host_only=3), dict(kernel=3), dict(kernel=-1), dict(kernel=2, vec_bytes=8), dict(prefetch=2)):
+    for kw in (dict(group_lanes=2), dict(group_lanes=12), dict(group_lanes=32), dict(group_lanes=-4),
+               dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=3),
+               dict(kernel=-1)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw
     o = _host_opts()
@@ -177,12 +178,12 @@ def test_injected_allocation_failure_reports_nomem():
 
 @pytest.mark.parametrize("k", [1, 4])
 @pytest.mark.parametrize("pattern", ["uniform", "beta"])
-@pytest.mark.parametrize("kernel,vec_bytes", [(0, 0), (1, 8), (1, 16), (2, 0)])
-def test_pack_unpack_round_trip_and_order(k, pattern, kernel, vec_bytes):
+@pytest.mark.parametrize("kernel,group_lanes", [(0, 0), (1, 4), (1, 8), (1, 16), (2, 0), (2, 8)])
+def test_pack_unpack_round_trip_and_order(k, pattern, kernel, group_lanes):
     if pattern == "beta" and k == 4:
         pytest.skip("beta row densities are defined for unstructured masks")
     layer = make_layer(96, 160, 2, 2, 1, 0.85, block_rows=k, pattern=pattern, seed=4, with_x=False)
-    h = _create(layer, options=_host_opts(kernel=kernel, vec_bytes=vec_bytes))
+    h = _create(layer, options=_host_opts(kernel=kernel, group_lanes=group_lanes))
     try:
         info = sp.spconv_plan_get_info(h)
         rp, ci, va, perm = sp.spconv_plan_unpack(h)
@@ -197,10 +198,12 @@ def test_pack_unpack_round_trip_and_order(k, pattern, kernel, vec_bytes):
     ties = [perm[i] < perm[i + 1] for i in range(rows - 1) if counts[i] == counts[i + 1]]
     assert all(ties), "equal-length rows not kept in index order"
     assert info["nnzb"] == layer.nnzb and info["slots"] >= layer.nnzb
-    assert info["vec_bytes"] == (vec_bytes or 16) and info["groups"] == 4
+    assert info["group_lanes"] in (4, 8, 16) and (group_lanes == 0 or info["group_lanes"] == group_lanes)
+    assert info["bundle_rows"] * info["group_lanes"] == 64
+    assert info["cols_per_lane"] == (16 // info["group_lanes"]) * 4
     assert info["kernel"] == (1 if kernel == 2 else 0)
-    # chunks of 4 steps x 4 slots x 4 lane groups
-    assert info["slots"] % 64 == 0
+    # whole steps of 4 slots for every group of a bundle
+    assert info["slots"] % (4 * info["bundle_rows"]) == 0
 
 
 def test_natural_order_when_reorder_off():
@@ -220,8 +223,10 @@ def test_lpt_balance_on_uniform_rows():
         info = sp.spconv_plan_get_info(h)
     finally:
         sp.spconv_destroy(h)
-    assert info["max_wave_cost"] <= 1.05 * info["sum_wave_cost"] / info["waves"]
-    # bundles are whole steps of 4 slots: about 1.5 padding slots per row, plus the look-ahead pad
+    # 32 bundles of 16 rows on 16 wavefronts: two each, longest paired with shortest
+    assert info["group_lanes"] == 4 and info["waves"] == 16
+    assert info["max_wave_cost"] <= 1.07 * info["sum_wave_cost"] / info["waves"]
+    # bundles are whole steps of 4 slots padded to their longest row (rows sorted by length)
     assert info["slots"] <= 1.06 * layer.nnzb
 
 
@@ -240,38 +245,59 @@ def test_lpt_balance_on_heavy_tailed_rows():
 
 
 def test_geometry_choice():
-    def info_for(cin, storage, k=1):
-        layer = make_layer(cin, 32, 1, 1, 1, 0.9, block_rows=k, storage=storage, seed=1, with_x=False)
-        h = _create(layer)
+    def info_for(cin, cout, storage, k=1, **opts):
+        layer = make_layer(cin, cout, 1, 1, 1, 0.9, block_rows=k, storage=storage, seed=1, with_x=False)
+        h = _create(layer, options=_host_opts(**opts))
         try:
             return sp.spconv_plan_get_info(h)
         finally:
             sp.spconv_destroy(h)
-    keys = ("kernel", "vec_bytes", "tile_cols", "lds_bytes", "loader_waves")
 
-    def table(cout, k):
-        # per bundle of 4 block rows: their rows, biases and step count, 16-byte rounded
-        bundles = -(-(cout // k) // 4)
-        return -(-(bundles * (4 * (1 + k) + 1) * 4) // 16) * 16
-    # 256-byte strip rows: 16 lanes x one 16-byte vector
-    assert tuple(info_for(512, "f32")[k] for k in keys) == (0, 16, 64, 512 * 256 + table(32, 1), 8)
-    assert tuple(info_for(512, "f32", 4)[k] for k in keys) == (0, 16, 64, 512 * 256 + table(32, 4), 8)
-    assert tuple(info_for(320, "f16", 4)[k] for k in keys) == (0, 16, 128, 320 * 256 + table(32, 4), 5)
-    assert tuple(info_for(24, "f32")[k] for k in keys) == (0, 16, 64, 24 * 256 + table(32, 1), 1)
-    # wider inputs: 128-byte rows, then the direct-load kernel
-    assert tuple(info_for(1024, "f32")[k] for k in keys) == (0, 8, 32, 1024 * 128 + table(32, 1), 8)
-    i = info_for(1500, "f32")
-    assert i["kernel"] == 1 and i["lds_bytes"] == 0 and i["loader_waves"] == 0 and i["vec_bytes"] == 16
-    i = info_for(512, "f32")
-    assert i["waves"] + i["loader_waves"] <= 16
+    def table(cout, k, nb):
+        # per bundle: the block row and the k biases of each of its nb groups, 16-byte rounded,
+        # then 16 bytes of counters
+        bundles = -(-(cout // k) // nb)
+        return -(-(bundles * nb * (1 + k) * 4) // 16) * 16 + 16
+
+    def check(i, kernel, g, tile_cols, cin, cout, k):
+        nb = 64 // g
+        assert (i["kernel"], i["group_lanes"], i["bundle_rows"], i["tile_cols"]) == (kernel, g, nb, tile_cols)
+        strip = 0 if kernel == 1 else -(-cin // 4) * 4 * 256
+        assert i["lds_bytes"] == strip + table(cout, k, nb)
+        assert i["waves"] == min(16, -(-(cout // k) // nb))
+
+    # unstructured fp32: 4 lanes per row, 16 columns per lane, 256-byte strip rows
+    check(info_for(512, 512, "f32"), 0, 4, 64, 512, 512, 1)
+    # 1x4 blocks: 4 x 16 accumulators would crowd the registers, so 8 lanes per row
+    check(info_for(512, 512, "f32", 4), 0, 8, 64, 512, 512, 4)
+    # fp16: 128 columns per tile; 1x4 blocks take 16 lanes per row
+    check(info_for(320, 1280, "f16", 4), 0, 16, 128, 320, 1280, 4)
+    check(info_for(320, 1280, "f16", 1), 0, 4, 128, 320, 1280, 1)
+    # few rows: wider lane groups keep enough bundles for the wavefronts
+    check(info_for(24, 32, "f32"), 0, 16, 64, 24, 32, 1)
+    check(info_for(144, 24, "f32"), 0, 16, 64, 144, 24, 1)
+    # inputs too wide for an LDS strip: the direct-load kernel
+    check(info_for(1024, 256, "f32"), 1, 4, 64, 1024, 256, 1)
+    check(info_for(600, 256, "f32"), 0, 4, 64, 600, 256, 1)
+    check(info_for(640, 256, "f32"), 1, 4, 64, 640, 256, 1)
+    # forced choices
+    i = info_for(512, 512, "f32", group_lanes=16, waves=7)
+    assert i["group_lanes"] == 16 and i["waves"] == 7
+    assert info_for(512, 512, "f32", kernel=2)["kernel"] == 1
 
 
-def test_too_many_waves_with_loaders_rejected():
-    layer = make_layer(512, 64, 1, 1, 1, 0.9, seed=1, with_x=False)
-    st, msg = _status(layer=layer, options=_host_opts(waves=9))
-    assert st == sp.spconv.E_ARG and "loader" in msg
-    st, msg = _status(layer=layer, options=_host_opts(waves=8))
+def test_group_lanes_beyond_the_accumulator_limit_rejected():
+    layer = make_layer(64, 64, 1, 1, 1, 0.9, block_rows=4, storage="f16", seed=1, with_x=False)
+    st, msg = _status(layer=layer, options=_host_opts(group_lanes=4))
+    assert st == sp.spconv.E_UNSUPPORTED and "accumulators" in msg
+    st, msg = _status(layer=layer, options=_host_opts(group_lanes=8))
     assert st == sp.spconv.OK
+
+
+def test_strip_refused_when_it_does_not_fit():
+    layer = make_layer(1024, 64, 1, 1, 1, 0.9, seed=1, with_x=False)
+    st, msg = _status(layer=layer, options=_host_opts(kernel=1))
+    assert st == sp.spconv.E_UNSUPPORTED and "LDS" in msg
 
 
 def test_f16_weights_rounded_to_nearest_even():

@@ -30,9 +30,11 @@ SMALL = [
     (200, 120, 9, 9, 2, 0.9, 1, "f16", "relu"),
     (200, 120, 9, 9, 2, 0.9, 4, "f16", "none"),
     (512, 64, 14, 14, 3, 0.9, 1, "f32", "relu"),
-    (700, 64, 7, 7, 2, 0.9, 1, "f32", "relu6"),     # 8-byte lane vectors
+    (600, 96, 7, 7, 2, 0.9, 1, "f32", "relu6"),     # largest strip
+    (601, 96, 7, 7, 2, 0.9, 4, "f32", "relu6"),     # direct-load kernel from here on
+    (700, 64, 7, 7, 2, 0.9, 1, "f32", "relu6"),
     (1280, 32, 7, 7, 2, 0.9, 4, "f32", "relu6"),
-    (1500, 48, 6, 6, 2, 0.9, 1, "f32", "relu"),     # direct-load kernel
+    (1500, 48, 6, 6, 2, 0.9, 1, "f32", "relu"),
     (1500, 48, 6, 6, 2, 0.9, 4, "f16", "relu"),
     (1300, 48, 8, 8, 2, 0.9, 1, "f16", "none"),
 ]
@@ -123,9 +125,9 @@ def test_run_is_deterministic_and_independent_of_planning():
     note("determinism")
     base = gpu_run(layer)
     assert np.array_equal(base, gpu_run(layer))
-    for opts in (dict(reorder=0), dict(vec_bytes=8), dict(kernel=2), dict(kernel=1, vec_bytes=8, prefetch=0),
-                 dict(waves=1), dict(waves=5), dict(waves=12, reorder=0), dict(prefetch=0),
-                 dict(prefetch=0, waves=16)):
+    for opts in (dict(reorder=0), dict(group_lanes=8), dict(group_lanes=16), dict(kernel=2),
+                 dict(kernel=2, group_lanes=16), dict(waves=1), dict(waves=5), dict(waves=12, reorder=0),
+                 dict(group_lanes=8, waves=16)):
         note("determinism %s" % opts)
         assert np.array_equal(base, gpu_run(layer, **opts)), opts
 
@@ -134,7 +136,7 @@ def test_run_is_deterministic_and_independent_of_planning():
 @pytest.mark.parametrize("k", [1, 4])
 def test_shared_tail_tiles(n, k):
     """Batch sizes around one round of tiles: the tiles left after the whole
-    rounds are split by rows over several workgroups (up to 16 here)."""
+    rounds are split by bundles over several workgroups."""
     layer = make_layer(512, 512, 14, 14, n, 0.9, block_rows=k, act="relu", seed=11 + n)
     note("tail split n=%d k=%d" % (n, k))
     assert_parity(layer, gpu_run(layer), what="tail n=%d k=%d" % (n, k))
