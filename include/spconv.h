@@ -136,6 +136,13 @@ typedef struct {
                             accumulators) */
     int32_t waves;       /* 0 = choose automatically; else the number of wavefronts per
                             workgroup, 1 to 16 */
+    int32_t pipe_sets;   /* LDS-strip kernel: 0 = choose automatically; 1 or 2 bundles of rows a
+                            wavefront interleaves by input channel so that it reads each tile's
+                            channels in ascending order once (2 needs twice the accumulators:
+                            SPCONV_E_UNSUPPORTED beyond 32 per lane) */
+    int32_t regions;     /* LDS-strip kernel: 0 = choose automatically; else 1 to 4 parts of the
+                            strip, each refilled with the next tile's channels as soon as every
+                            wavefront is done with it */
 } spconv_options;
 
 /* Fill *opts with the defaults used by spconv_plan_create. */
@@ -158,6 +165,8 @@ typedef struct {
     int32_t waves;         /* wavefronts per workgroup */
     int32_t lds_bytes;     /* LDS per workgroup */
     int32_t max_parts;     /* most workgroups that may share the rows of one tile */
+    int32_t pipe_sets;     /* bundles a wavefront interleaves (0 for the direct-load kernel) */
+    int32_t regions;       /* strip parts refilled independently (0 for the direct-load kernel) */
     int64_t nnzb;          /* stored blocks */
     int64_t slots;         /* packed (channel, weight) slots including padding */
     int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
@@ -176,6 +185,18 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info);
  */
 spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
                                  int32_t *perm);
+
+/*
+ * The same reconstruction from the interleaved weight streams the pipelined
+ * LDS-strip kernel reads (row_ptr, col_idx, values as above, each may be
+ * NULL), walking them with the kernel's own bookkeeping: per step, the
+ * accumulator set and last-step bits pick the bundle, and every strip channel
+ * read must fall between the need and release events of its strip part.
+ * Host only.  SPCONV_E_FORMAT (message set) when the streams are inconsistent
+ * or the plan uses the direct-load kernel, which has none.
+ */
+spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
+                                             float *values);
 
 #ifdef __cplusplus
 }

@@ -16,5 +16,6 @@ from .spconv import (  # noqa: F401
     spconv_plan_create,
     spconv_plan_get_info,
     spconv_plan_unpack,
+    spconv_plan_unpack_interleaved,
     spconv_run,
 )

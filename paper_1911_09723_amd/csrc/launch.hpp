@@ -22,7 +22,9 @@ struct DevicePlan {
     int32_t act = 0;
     int32_t cin = 0, cout = 0;
     int32_t strip_rows = 0;     // channels of the LDS strip (cin rounded up to 4); 0 for the direct kernel
-    int32_t split_rows = 0;     // rows of the strip's lower part
+    int32_t pipe_sets = 1;      // bundles a wavefront interleaves in the pipelined kernel
+    int32_t regions = 1;        // strip parts refilled independently
+    int32_t region_rows = 0;    // channels per part
     int32_t busy_waves = 0;     // wavefronts with at least one bundle
     int32_t idx_bytes = 0;      // size of the channel stream (bounds of its buffer resource)
     int32_t val_bytes = 0;      // size of the weight stream
@@ -36,7 +38,11 @@ struct DevicePlan {
     const int32_t *table = nullptr;     // rows, then biases (fp32 bits), per (bundle, group)
     const int32_t *rank = nullptr;      // longest-first rank of each bundle
     const int32_t *wave_ptr = nullptr;  // bundles of each wave
-    const int32_t *wave_meta = nullptr; // per wave: lower part released after, upper part first needed at
+    const int32_t *pidx = nullptr;      // interleaved streams and their per-wave tables
+    const float *pval = nullptr;
+    const uint32_t *psel = nullptr;
+    const int32_t *sel_ptr = nullptr;
+    const int32_t *wave_ev = nullptr;
 };
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when

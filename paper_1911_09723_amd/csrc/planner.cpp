@@ -202,7 +202,8 @@ Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::
     const int32_t nbundles = bundles_of(rows, p.bundle_rows);
     const int64_t table = table_bytes(nbundles, p.bundle_rows, k) + kCtlBytes;
     const int32_t strip_rows = (in.cin + 3) / 4 * 4;
-    const int64_t strip = static_cast<int64_t>(strip_rows) * kRowBytes;
+    // the strip and the row of zeros that padding slots read
+    const int64_t strip = static_cast<int64_t>(strip_rows + 1) * kRowBytes;
     const bool fits = strip + table <= kMaxLdsBytes;
     if (opt.kernel == 1 && !fits) {
         err = "the X strip of cin = " + std::to_string(in.cin) + " channels does not fit in LDS";
@@ -216,7 +217,6 @@ Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::
         p.kernel = KERNEL_STRIP;
         p.row_scale = kRowBytes;
         p.strip_rows = strip_rows;
-        p.split_rows = (strip_rows / 4 + 1) / 2 * 4;
         p.lds_bytes = static_cast<int32_t>(strip + table);
     } else {
         p.kernel = KERNEL_DIRECT;
@@ -225,6 +225,104 @@ Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::
         p.lds_bytes = static_cast<int32_t>(table);
     }
     return OK;
+}
+
+// The strip parts each channel of a step reads, as a bit mask, and the
+// step's merge key (lowest + highest channel it reads; padding reads none).
+struct StepReads {
+    uint32_t regions = 0;
+    int64_t key = 0;
+};
+
+StepReads step_reads(const PackedPlan &p, int64_t step) {
+    const int64_t rec = static_cast<int64_t>(p.bundle_rows) * kStepSlots;
+    StepReads r;
+    int32_t lo = INT32_MAX, hi = -1;
+    for (int64_t e = step * rec; e < (step + 1) * rec; ++e) {
+        const int32_t c = p.idx[e] / p.row_scale;
+        if (c >= p.strip_rows)
+            continue;  // padding: the row of zeros
+        lo = std::min(lo, c);
+        hi = std::max(hi, c);
+        r.regions |= 1u << (c / p.region_rows);
+    }
+    r.key = hi < 0 ? 0 : static_cast<int64_t>(lo) + hi;
+    return r;
+}
+
+// Interleaved streams, selector words and region events (planner.hpp).
+void build_interleaved(PackedPlan &p) {
+    const int32_t NB = p.bundle_rows, k = p.k, S = p.pipe_sets;
+    const int64_t rec = static_cast<int64_t>(NB) * kStepSlots;
+    p.pidx.assign(p.idx.size(), 0);
+    p.pval.assign(p.val.size(), 0.0f);
+    p.psel.clear();
+    p.sel_ptr.assign(p.waves + 1, 0);
+    p.wave_ev.assign(static_cast<size_t>(p.waves) * kWaveEvents, INT32_MAX);
+    for (int32_t w = 0; w < p.waves; ++w) {
+        const int32_t b0 = p.wave_ptr[w], b1 = p.wave_ptr[w + 1];
+        p.sel_ptr[w + 1] = p.sel_ptr[w];
+        if (b0 == b1)
+            continue;
+        const int64_t ws0 = p.hdr[2 * b0];
+        // merge each set group's steps by key, each bundle's steps in order
+        std::vector<int64_t> src;
+        std::vector<uint32_t> bits;
+        for (int32_t g = b0; g < b1; g += S) {
+            const int32_t ng = std::min(S, b1 - g);
+            std::vector<int32_t> next(ng, 0);
+            for (;;) {
+                int32_t best = -1;
+                int64_t best_key = 0;
+                for (int32_t i = 0; i < ng; ++i) {
+                    const int32_t b = g + i;
+                    if (next[i] == p.hdr[2 * b + 1])
+                        continue;
+                    const int64_t key = step_reads(p, p.hdr[2 * b] + next[i]).key;
+                    if (best < 0 || key < best_key) {
+                        best = i;
+                        best_key = key;
+                    }
+                }
+                if (best < 0)
+                    break;
+                const int32_t b = g + best;
+                src.push_back(p.hdr[2 * b] + next[best]);
+                ++next[best];
+                bits.push_back(static_cast<uint32_t>(best) | (next[best] == p.hdr[2 * b + 1] ? 2u : 0u));
+            }
+        }
+        const int64_t len = static_cast<int64_t>(src.size());
+        std::vector<int64_t> need(kMaxRegions, INT64_MAX), rel(kMaxRegions, -1);
+        for (int64_t i = 0; i < len; ++i) {
+            const int64_t d = ws0 + i;
+            std::copy(p.idx.begin() + src[i] * rec, p.idx.begin() + (src[i] + 1) * rec, p.pidx.begin() + d * rec);
+            std::copy(p.val.begin() + src[i] * rec * k, p.val.begin() + (src[i] + 1) * rec * k,
+                      p.pval.begin() + d * rec * k);
+            const uint32_t m = step_reads(p, src[i]).regions;
+            for (int32_t q = 0; q < p.regions; ++q)
+                if (m >> q & 1u) {
+                    need[q] = std::min(need[q], i);
+                    rel[q] = i;
+                }
+        }
+        const int64_t words = (len + kSelSteps - 1) / kSelSteps;
+        const size_t base = p.psel.size();
+        p.psel.resize(base + words, 0u);
+        for (int64_t i = 0; i < len; ++i)
+            p.psel[base + i / kSelSteps] |= bits[i] << (2 * (i % kSelSteps));
+        p.sel_ptr[w + 1] = static_cast<int32_t>(p.psel.size());
+        std::vector<int32_t> ne, re;
+        for (int32_t q = 0; q < p.regions; ++q) {
+            if (need[q] != INT64_MAX)
+                ne.push_back(static_cast<int32_t>(need[q] << 4 | q));
+            re.push_back(static_cast<int32_t>((rel[q] < 0 ? 0 : rel[q]) << 4 | q));
+        }
+        std::sort(ne.begin(), ne.end());
+        std::sort(re.begin(), re.end());
+        std::copy(ne.begin(), ne.end(), p.wave_ev.begin() + static_cast<size_t>(w) * kWaveEvents);
+        std::copy(re.begin(), re.end(), p.wave_ev.begin() + static_cast<size_t>(w) * kWaveEvents + kMaxRegions);
+    }
 }
 
 }  // namespace
@@ -247,6 +345,14 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     }
     if (opt.reorder != 0 && opt.reorder != 1) {
         err = "reorder must be 0 or 1";
+        return E_ARG;
+    }
+    if (opt.pipe_sets < 0 || opt.pipe_sets > 2) {
+        err = "pipe_sets must be 0, 1 or 2";
+        return E_ARG;
+    }
+    if (opt.regions < 0 || opt.regions > kMaxRegions) {
+        err = "regions must be in [0, " + std::to_string(kMaxRegions) + "]";
         return E_ARG;
     }
 
@@ -320,7 +426,7 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         err = "packed plan too large";
         return E_SHAPE;
     }
-    const int32_t pad_channel = p.kernel == KERNEL_STRIP ? p.strip_rows - 1 : 0;
+    const int32_t pad_channel = p.kernel == KERNEL_STRIP ? p.strip_rows : 0;
     p.idx.assign(static_cast<size_t>(total_steps * NB * kStepSlots), pad_channel * p.row_scale);
     p.val.assign(static_cast<size_t>(total_steps * NB * kStepSlots * k), 0.0f);
     p.wave_ptr.assign(waves + 1, 0);
@@ -328,35 +434,10 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     p.rows.reserve(static_cast<size_t>(NB) * nb);
     p.bundle_bias.reserve(static_cast<size_t>(NB) * nb * k);
     p.rank.reserve(nb);
-    p.wave_meta.assign(2 * static_cast<size_t>(waves), 0);
-    // slots of a row that read the strip's lower part (ascending channels)
-    auto lower = [&](int32_t rb) {
-        int32_t n = 0;
-        while (n < len(rb) && in.col_idx[in.row_ptr[rb] + n] < p.split_rows)
-            ++n;
-        return n;
-    };
     int64_t step = 0;   // first step of the next bundle
     int32_t bglob = 0;  // bundles packed so far
     for (int32_t w = 0; w < waves; ++w) {
-        const int64_t wstart = step;
-        int64_t rel0 = 0, need1 = -1;
         for (int32_t b : lists[w]) {
-            // a0: steps until every row has passed its lower-part channels;
-            // a1: first step in which some row reads the upper part (a padding
-            // group or a row's padding slots do from their first slot)
-            int64_t a0 = 0, a1 = bsteps[b];
-            for (int32_t q = 0; q < NB; ++q) {
-                const int32_t pos = b * NB + q;
-                const int32_t n0 = pos < rows ? lower(p.perm[pos]) : 0;
-                const int32_t n = pos < rows ? len(p.perm[pos]) : 0;
-                a0 = std::max<int64_t>(a0, (n0 + kStepSlots - 1) / kStepSlots);
-                if (n0 < static_cast<int64_t>(bsteps[b]) * kStepSlots && (n0 < n || n < bsteps[b] * kStepSlots))
-                    a1 = std::min<int64_t>(a1, n0 / kStepSlots);
-            }
-            rel0 = std::max(rel0, step - wstart + a0);
-            if (a1 < bsteps[b] && need1 < 0)
-                need1 = step - wstart + a1;
             p.hdr.push_back(static_cast<int32_t>(step));
             p.hdr.push_back(bsteps[b]);
             p.rank.push_back(rank_of[b]);
@@ -384,8 +465,6 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
             ++bglob;
         }
         p.wave_ptr[w + 1] = bglob;
-        p.wave_meta[2 * w] = static_cast<int32_t>(rel0);
-        p.wave_meta[2 * w + 1] = static_cast<int32_t>(need1 < 0 ? step - wstart : need1);
         if (!lists[w].empty())
             ++p.busy_waves;
     }
@@ -393,6 +472,23 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     p.max_parts = 1;
     while (p.max_parts * 2 <= std::min<int32_t>(kMaxParts, nb))
         p.max_parts *= 2;
+
+    // 5. interleaved streams for the pipelined strip kernel: two accumulator
+    // sets when both fit in the automatic accumulator budget
+    if (p.kernel == KERNEL_STRIP) {
+        const int32_t acc = k * (p.cols_per_lane);
+        const int32_t max_sets = 2 * acc <= kAutoAccumulators ? 2 : 1;
+        if (opt.pipe_sets > max_sets) {
+            err = "pipe_sets = 2 needs " + std::to_string(2 * acc) + " accumulators per lane (limit " +
+                  std::to_string(kAutoAccumulators) + ")";
+            return E_UNSUPPORTED;
+        }
+        p.pipe_sets = opt.pipe_sets ? opt.pipe_sets : max_sets;
+        p.regions = opt.regions ? std::min(opt.regions, p.strip_rows / 4) : std::min(kMaxRegions, p.strip_rows / 4);
+        p.region_rows = (p.strip_rows / 4 + p.regions - 1) / p.regions * 4;
+        p.regions = (p.strip_rows + p.region_rows - 1) / p.region_rows;  // none left empty
+        build_interleaved(p);
+    }
     return OK;
 }
 
@@ -431,6 +527,100 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
     }
     if (perm)
         std::copy(p.perm.begin(), p.perm.end(), perm);
+}
+
+Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values,
+                          std::string &err) {
+    if (p.kernel != KERNEL_STRIP || p.pidx.size() != p.idx.size()) {
+        err = "the plan has no interleaved streams (direct kernel)";
+        return E_FORMAT;
+    }
+    const int32_t k = p.k, NB = p.bundle_rows, S = p.pipe_sets;
+    const int32_t rows = p.cout / k;
+    std::vector<std::vector<int32_t>> cols(rows);
+    std::vector<std::vector<float>> vals(rows);
+    auto bad = [&](const std::string &m) {
+        err = m;
+        return E_FORMAT;
+    };
+    for (int32_t w = 0; w < p.waves; ++w) {
+        const int32_t b0 = p.wave_ptr[w], b1 = p.wave_ptr[w + 1];
+        if (b0 == b1)
+            continue;
+        const int64_t ws0 = p.hdr[2 * b0];
+        int64_t len = 0;
+        for (int32_t b = b0; b < b1; ++b)
+            len += p.hdr[2 * b + 1];
+        // decode the events: first and last step allowed to read each region
+        std::vector<int64_t> lo(kMaxRegions, INT64_MAX), hi(kMaxRegions, -1);
+        for (int32_t i = 0; i < kMaxRegions; ++i) {
+            const int32_t n = p.wave_ev[static_cast<size_t>(w) * kWaveEvents + i];
+            const int32_t r = p.wave_ev[static_cast<size_t>(w) * kWaveEvents + kMaxRegions + i];
+            if (n != INT32_MAX)
+                lo[n & 15] = n >> 4;
+            if (r != INT32_MAX)
+                hi[r & 15] = r >> 4;
+        }
+        std::vector<int32_t> bset(S), cnt(S, 0);
+        for (int32_t i = 0; i < S; ++i)
+            bset[i] = b0 + i;
+        for (int64_t i = 0; i < len; ++i) {
+            const uint32_t bits = p.psel[p.sel_ptr[w] + i / kSelSteps] >> (2 * (i % kSelSteps)) & 3u;
+            const int32_t set = static_cast<int32_t>(bits & 1u);
+            if (set >= S)
+                return bad("selector names a set the plan does not have");
+            const int32_t b = bset[set];
+            if (b >= b1 || cnt[set] >= p.hdr[2 * b + 1])
+                return bad("selector runs past a wavefront's bundles");
+            const int64_t step = ws0 + i;
+            for (int32_t q = 0; q < NB; ++q) {
+                const int32_t rb = p.rows[static_cast<size_t>(b) * NB + q];
+                for (int32_t u = 0; u < kStepSlots; ++u) {
+                    const int64_t e = (step * NB + q) * kStepSlots + u;
+                    const int32_t c = p.pidx[e] / p.row_scale;
+                    const int32_t t = cnt[set] * kStepSlots + u;
+                    if (rb < 0 || t >= p.row_nnz[rb]) {
+                        if (c != p.strip_rows)
+                            return bad("a padding slot reads a strip channel");
+                        for (int32_t j = 0; j < k; ++j)
+                            if (p.pval[e * k + j] != 0.0f)
+                                return bad("a padding slot has a nonzero weight");
+                        continue;
+                    }
+                    const int32_t r = c / p.region_rows;
+                    if (c < 0 || c >= p.strip_rows || i < lo[r] || i > hi[r])
+                        return bad("a step reads a strip part outside its need / release events");
+                    cols[rb].push_back(c);
+                    for (int32_t j = 0; j < k; ++j)
+                        vals[rb].push_back(p.pval[e * k + j]);
+                }
+            }
+            ++cnt[set];
+            const bool last = cnt[set] == p.hdr[2 * b + 1];
+            if (last != ((bits & 2u) != 0))
+                return bad("a last-step bit disagrees with the bundle length");
+            if (last) {
+                bset[set] += S;
+                cnt[set] = 0;
+            }
+        }
+        for (int32_t i = 0; i < S; ++i)
+            if (bset[i] < b1)
+                return bad("a wavefront's stream ends before its bundles do");
+    }
+    int32_t acc = 0;
+    if (row_ptr)
+        row_ptr[0] = 0;
+    for (int32_t r = 0; r < rows; ++r) {
+        if (col_idx)
+            std::copy(cols[r].begin(), cols[r].end(), col_idx + acc);
+        if (values)
+            std::copy(vals[r].begin(), vals[r].end(), values + static_cast<int64_t>(acc) * k);
+        acc += static_cast<int32_t>(cols[r].size());
+        if (row_ptr)
+            row_ptr[r + 1] = acc;
+    }
+    return OK;
 }
 
 }  // namespace spconv

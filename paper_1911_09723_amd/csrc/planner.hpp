@@ -21,8 +21,7 @@
 //   in processing order (descending nonzero count unless reordering is off),
 //   so the rows of a bundle have similar lengths.  Its length is the longest
 //   of its rows rounded up to a whole number of *steps* of 4 slots (at least
-//   one step); shorter rows are padded with (channel 0, weight 0) slots, which
-//   add an exact zero.
+//   one step); shorter rows are padded with weight-0 slots (below).
 //
 //   Bundles are assigned to the `waves` wavefronts of a workgroup by longest
 //   processing time first; wave_ptr[w] .. wave_ptr[w+1] are wave w's bundles,
@@ -36,8 +35,9 @@
 //   so the lanes of group q read idx bytes (s*NB + q)*16 .. +15 and val bytes
 //   (s*NB + q)*16k .. +16k-1: the 4 slots of their row in step s.
 //
-//   Padding slots read strip row strip_rows - 1 (channel 0 for the direct
-//   kernel): a row of the strip's upper part (below).
+//   Padding slots read channel strip_rows (strip kernel: an LDS row of zeros
+//   after the strip, so they add an exact zero whatever X holds) or channel 0
+//   (direct kernel).
 //
 //   hdr[2*b + 0]     first (global) step of bundle b
 //   hdr[2*b + 1]     steps of bundle b
@@ -47,21 +47,31 @@
 //                    shared by P workgroups (P a power of two up to max_parts)
 //                    gives part p the bundles with rank % P == p.
 //
-//   Strip halves.  The strip's rows are split at split_rows (a multiple of 4):
-//   the lower part holds channels [0, split_rows), the upper part the rest.
-//   Since every row reads its channels in ascending order, a bundle stops
-//   reading the lower part after a few steps and starts reading the upper part
-//   after a few steps; per wave (stream offsets from its first step):
-//   wave_meta[2*w + 0]  steps after which the wave no longer reads the lower part
-//   wave_meta[2*w + 1]  first step that reads the upper part (stream length if none)
-//   A kernel can then refill the lower part with the next tile's channels while
-//   the wavefronts finish the current tile in the upper part, and the other way
-//   round.
+// Interleaved streams (strip kernel).  The pipelined kernel keeps the strip as
+// `regions` parts of region_rows channels (the last may be shorter) and
+// refills each part with the next tile's channels as soon as every wavefront
+// is done with it.  That only overlaps copying with computing when each
+// wavefront reads the channels of a tile roughly in ascending order once, so
+// its stream interleaves the steps of `pipe_sets` bundles at a time (one
+// accumulator set each): the bundles wave_ptr[w] + j*S .. + S - 1 (S =
+// pipe_sets) form its j-th set group, bundle wave_ptr[w] + j*S + i uses set
+// i, and the group's steps are merged by the mean of the lowest and highest
+// channel each step reads, keeping every bundle's own step order (so every
+// row still sums in ascending channel order).  pidx / pval hold the same
+// records as idx / val, with each wave's steps (same global step range) in
+// that order.  Per wave:
+//   psel[sel_ptr[w] + i / 16] bits 2*(i % 16), +1   set of the wave's i-th step,
+//                    and whether it is its bundle's last step
+//   wave_ev[8*w + 0 .. 3]   (pos << 4) | region for each region the wave reads,
+//                    sorted by pos: the first step that reads it ("need")
+//   wave_ev[8*w + 4 .. 7]   the same for the last step that reads it
+//                    ("release"; step 0 for a region it never reads)
+//   unused entries hold INT32_MAX.
 //
 // The per-row summation order is ascending input channel (the CSR order), with
 // padding zeros after the last stored block; it does not depend on the bundle
 // grouping, so the result is bitwise independent of reordering, lane-group
-// width, wave assignment and splitting.
+// width, wave assignment, interleaving and splitting.
 #pragma once
 
 #include <cstdint>
@@ -84,8 +94,15 @@ constexpr int32_t kStepSlots = 4;
 constexpr int32_t kMaxWaves = 16;
 // Finest split of a tile over workgroups.
 constexpr int32_t kMaxParts = 64;
-// LDS bytes of the strip-refill counters at the end of a workgroup's LDS.
-constexpr int32_t kCtlBytes = 16;
+// Most parts of the strip the pipelined kernel refills independently.
+constexpr int32_t kMaxRegions = 4;
+// LDS bytes of the strip-refill counters at the end of a workgroup's LDS
+// (per region: wavefronts done with it, copies of it landed).
+constexpr int32_t kCtlBytes = 8 * kMaxRegions;
+// Steps per selector word of the interleaved streams (2 bits each).
+constexpr int32_t kSelSteps = 16;
+// Events per wavefront in wave_ev.
+constexpr int32_t kWaveEvents = 2 * kMaxRegions;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -103,6 +120,8 @@ struct Options {
     int32_t kernel = 0;       // 0 automatic, 1 strip, 2 direct
     int32_t group_lanes = 0;  // 0 automatic, else 4, 8 or 16 lanes per block row
     int32_t waves = 0;        // 0 automatic, else 1 .. 16 wavefronts per workgroup
+    int32_t pipe_sets = 0;    // 0 automatic, else 1 or 2 bundles interleaved per wavefront
+    int32_t regions = 0;      // 0 automatic, else 1 .. kMaxRegions strip parts
 };
 
 struct PackedPlan {
@@ -117,9 +136,11 @@ struct PackedPlan {
     int32_t row_scale = kRowBytes;
     int32_t waves = 1;           // wavefronts per workgroup (each owns a list of bundles)
     int32_t strip_rows = 0;      // cin rounded up to a multiple of 4 (strip kernel)
-    int32_t split_rows = 0;      // rows of the strip's lower part (a multiple of 4)
     int32_t busy_waves = 0;      // wavefronts with at least one bundle
-    int32_t lds_bytes = 0;       // strip + bundle table (strip kernel)
+    int32_t lds_bytes = 0;       // strip, zero row, bundle table, counters (strip kernel)
+    int32_t pipe_sets = 1;       // bundles a wavefront interleaves (strip kernel)
+    int32_t regions = 1;         // strip parts refilled independently (strip kernel)
+    int32_t region_rows = 0;     // channels per part, a multiple of 4
     int32_t max_parts = 1;       // most workgroups that may share one tile
     // packed streams
     std::vector<int32_t> idx;
@@ -129,7 +150,11 @@ struct PackedPlan {
     std::vector<float> bundle_bias;
     std::vector<int32_t> rank;
     std::vector<int32_t> wave_ptr;
-    std::vector<int32_t> wave_meta;
+    std::vector<int32_t> pidx;     // interleaved streams (strip kernel)
+    std::vector<float> pval;
+    std::vector<uint32_t> psel;
+    std::vector<int32_t> sel_ptr;
+    std::vector<int32_t> wave_ev;
     std::vector<int32_t> perm;     // block rows in processing order
     std::vector<int32_t> row_nnz;  // stored blocks per block row (host only; for unpacking)
     // statistics
@@ -159,5 +184,12 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &out, std::str
 // Rebuild block-CSR arrays (and the processing order) from a packed plan.
 // Any output pointer may be null.
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm);
+
+// The same from the interleaved streams, walking them as the pipelined kernel
+// does (selector bits, set groups) and checking that every strip read lies
+// between its region's need and release events.  Returns OK, or E_FORMAT with
+// `err` set when the streams are inconsistent or the plan has none.
+Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values,
+                          std::string &err);
 
 }  // namespace spconv

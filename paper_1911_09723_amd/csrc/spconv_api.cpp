@@ -78,14 +78,18 @@ spconv_status upload(spconv_plan_s *pl) {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[7] = {
+    } parts[11] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
         {table.data(), table.size() * sizeof(int32_t), 0},
         {h.rank.data(), h.rank.size() * sizeof(int32_t), 0},
         {h.wave_ptr.data(), h.wave_ptr.size() * sizeof(int32_t), 0},
-        {h.wave_meta.data(), h.wave_meta.size() * sizeof(int32_t), 0},
+        {h.pidx.data(), h.pidx.size() * sizeof(int32_t), 0},
+        {h.pval.data(), h.pval.size() * sizeof(float), 0},
+        {h.psel.data(), h.psel.size() * sizeof(uint32_t), 0},
+        {h.sel_ptr.data(), h.sel_ptr.size() * sizeof(int32_t), 0},
+        {h.wave_ev.data(), h.wave_ev.size() * sizeof(int32_t), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -122,7 +126,11 @@ spconv_status upload(spconv_plan_s *pl) {
     d.table = reinterpret_cast<const int32_t *>(base + parts[3].off);
     d.rank = reinterpret_cast<const int32_t *>(base + parts[4].off);
     d.wave_ptr = reinterpret_cast<const int32_t *>(base + parts[5].off);
-    d.wave_meta = reinterpret_cast<const int32_t *>(base + parts[6].off);
+    d.pidx = reinterpret_cast<const int32_t *>(base + parts[6].off);
+    d.pval = reinterpret_cast<const float *>(base + parts[7].off);
+    d.psel = reinterpret_cast<const uint32_t *>(base + parts[8].off);
+    d.sel_ptr = reinterpret_cast<const int32_t *>(base + parts[9].off);
+    d.wave_ev = reinterpret_cast<const int32_t *>(base + parts[10].off);
     return SPCONV_OK;
 }
 
@@ -140,7 +148,9 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.cin = h.cin;
     d.cout = h.cout;
     d.strip_rows = h.strip_rows;
-    d.split_rows = h.split_rows;
+    d.pipe_sets = h.pipe_sets;
+    d.regions = h.regions;
+    d.region_rows = h.region_rows;
     d.busy_waves = h.busy_waves;
     d.idx_bytes = static_cast<int32_t>(h.idx.size() * sizeof(int32_t));
     d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
@@ -188,6 +198,8 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     po.kernel = o.kernel;
     po.group_lanes = o.group_lanes;
     po.waves = o.waves;
+    po.pipe_sets = o.pipe_sets;
+    po.regions = o.regions;
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
     if (!pl)
@@ -316,6 +328,8 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->tile_cols = p.tile_cols;
     info->waves = p.waves;
     info->max_parts = p.max_parts;
+    info->pipe_sets = p.kernel == spconv::KERNEL_STRIP ? p.pipe_sets : 0;
+    info->regions = p.kernel == spconv::KERNEL_STRIP ? p.regions : 0;
     info->lds_bytes = p.lds_bytes;
     info->nnzb = p.nnzb;
     info->slots = p.slots;
@@ -331,6 +345,18 @@ spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *co
     if (!plan)
         return fail(SPCONV_E_ARG, "plan is NULL");
     spconv::unpack_plan(plan->host, row_ptr, col_idx, values, perm);
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
+                                             float *values) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    std::string err;
+    const spconv::Status st = spconv::unpack_interleaved(plan->host, row_ptr, col_idx, values, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
     return SPCONV_OK;
 }
 

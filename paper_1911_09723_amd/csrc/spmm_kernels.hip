@@ -115,7 +115,8 @@ struct Args {
     int32_t cin, cout, hw, m, act;
     int32_t vec;         // 16-byte global loads and stores (see launch_spmm)
     int32_t strip_rows;  // LDS strip channels (a multiple of 4); 0 for the direct kernel
-    int32_t split_rows;  // rows of the strip's lower part (pipelined kernel)
+    int32_t regions;     // strip parts refilled independently (pipelined kernel)
+    int32_t region_rows; // channels per part, a multiple of 4
     int32_t table_off;   // LDS byte offset of the bundle table
     int32_t ctl_off;     // LDS byte offset of the strip-refill counters (pipelined kernel)
     int32_t nbundles;
@@ -535,8 +536,8 @@ template <int G, int K, bool F16, bool DIRECT, bool VEC>
 __global__ void __launch_bounds__(1024)
 spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__restrict__ idx,
             const float *__restrict__ val, const int32_t *__restrict__ hdr, const int32_t *__restrict__ table,
-            const int32_t *__restrict__ rank, const int32_t *__restrict__ wave_ptr,
-            const int32_t *__restrict__ wave_meta, Args a) {
+            const int32_t *__restrict__ rank, const int32_t *__restrict__ wave_ptr, const int32_t *, const float *,
+            const uint32_t *, const int32_t *, const int32_t *, Args a) {
     using GE = Geo<G, F16>;
     using T = typename GE::T;
     extern __shared__ __align__(16) unsigned char lds[];
@@ -555,6 +556,11 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
     const float *bias_lds = reinterpret_cast<const float *>(rows_lds + a.nbundles * GE::NB);
     for (int i = tid; i < a.nbundles * GE::NB * (1 + K); i += blockDim.x)
         rows_lds[i] = table[i];
+    if constexpr (!DIRECT) {
+        // the row of zeros that padding slots read
+        if (tid < kRowBytes / 16)
+            *reinterpret_cast<u4 *>(lds + a.strip_rows * kRowBytes + 16 * tid) = u4{0u, 0u, 0u, 0u};
+    }
     const Rsrc ri = make_rsrc(idx, static_cast<uint32_t>(a.idx_bytes));
     const Rsrc rv = make_rsrc(val, static_cast<uint32_t>(a.val_bytes));
     // the activation as a clamp: [-inf, inf] none, [0, inf] ReLU, [0, 6] ReLU6
@@ -581,38 +587,39 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
 }
 
 // ---------------------------------------------------------------------------
-// Pipelined strip kernel (16-byte vectors): the next tile's strip streams
-// into LDS while the current one is computed.
+// Pipelined strip kernel (16-byte vectors): the strip is a ring of `regions`
+// parts, each refilled with the next tile's channels while the wavefronts
+// compute on the others.
 //
-// The strip's rows are split into a lower part (channels below split_rows)
-// and an upper part.  Rows read their channels in ascending order, so each
-// wavefront finishes with the lower part of tile t a few steps before the
-// end of its tile and needs the upper part of tile t + 1 only a few steps
-// into it (wave_meta).  Four LDS counters coordinate the workgroup:
-//   free0 / free1  count wavefronts done with the lower / upper part of a tile
-//   fill0 / fill1  count the copies of a part that have landed
-// When free0 reaches busy * (t + 1), every wavefront issues its 1/nwaves share
-// of the copies of tile t + 1's lower part (buffer loads with the LDS
-// destination bit); the same for the upper part with free1.  A wavefront
-// counts its share in fill0 / fill1 once its own vector-memory counter proves
-// the copies landed: D steps later (the share is then older than every record
-// fetched since, and those complete in issue order), or at once when it has
-// nothing else to do.  A wavefront starts tile t + 1 once fill0 reaches
-// nwaves * (t + 2) and reads its upper part once fill1 does.  The records are
-// fetched D steps ahead so that a share in flight does not hold up the ring.
+// Each wavefront walks its interleaved stream (planner.hpp): its bundles, two
+// at a time with one accumulator set each, merged so that the wavefront reads
+// a tile's channels roughly in ascending order once.  Per strip part q, two
+// LDS counters coordinate the workgroup:
+//   free[q]  wavefronts (with bundles) done with part q, summed over tiles
+//   fill[q]  copies of part q that have landed, summed over tiles
+// A wavefront waits for fill[q] >= nwaves * (t + 1) before its first read of
+// part q in tile t (a "need" event) and counts free[q] after its last one (a
+// "release" event).  Every wavefront copies a 1/nwaves share of each part of
+// every tile, in order: part q of tile t once free[q] >= busy * t, with
+// buffer loads that write LDS directly.  It counts the share in fill[q] one
+// ring turn later, when a record fetched after the share has arrived (vector
+// memory operations complete in issue order), or at once when waiting.  Each
+// part of tile t + 1 can thus stream in while the wavefronts are still busy
+// with other parts of tile t, and fast wavefronts run ahead into tile t + 1
+// without a workgroup barrier.
 //
 // The copies are issued with inline assembly: the compiler would otherwise
-// drain every vector-memory access before the next LDS read.  Every wait
-// on a counter is bounded, so a logic error cannot hang the device.  The
-// tiles left after the whole rounds take the simple path.
+// drain every vector-memory access before the next LDS read.  Every wait on a
+// counter is bounded, so a logic error cannot hang the device.  The tiles
+// left after the whole rounds take the simple path.
 // ---------------------------------------------------------------------------
 
 // Steps of records fetched ahead: as many as fit beside the accumulators and
-// X vectors in a 128-register budget (each entry costs 4 + 4k registers).
-template <int G, int K, bool F16>
+// X vectors in an 88-register budget (each entry costs 4 + 4k registers).
+template <int G, int K, bool F16, int M>
 struct PipeDepth {
-    static constexpr int A = K * (16 / G) * (16 / (F16 ? 2 : 4));  // accumulators
-    static constexpr int FREE = 96 - A - 4 * (16 / G);
+    static constexpr int A = M * K * (16 / G) * (16 / (F16 ? 2 : 4));  // accumulators
+    static constexpr int FREE = 88 - A - 4 * (16 / G);
     static constexpr int RAW = FREE / (4 + 4 * K) - 1;
     static constexpr int D = RAW < 2 ? 2 : (RAW > 6 ? 6 : RAW);
     static constexpr int NR = D + 1;
@@ -628,17 +635,18 @@ __device__ __forceinline__ void count_once(int32_t *p, int lane) {
         atomicAdd(p, 1);
 }
 
-template <int G, int K, bool F16>
+template <int G, int K, bool F16, int M>
 __global__ void __launch_bounds__(1024)
 spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__restrict__ idx,
           const float *__restrict__ val, const int32_t *__restrict__ hdr, const int32_t *__restrict__ table,
           const int32_t *__restrict__ rank, const int32_t *__restrict__ wave_ptr,
-          const int32_t *__restrict__ wave_meta, Args a) {
+          const int32_t *__restrict__ pidx, const float *__restrict__ pval, const uint32_t *__restrict__ psel,
+          const int32_t *__restrict__ sel_ptr, const int32_t *__restrict__ wave_ev, Args a) {
     using GE = Geo<G, F16>;
     using T = typename GE::T;
-    using DP = PipeDepth<G, K, F16>;
+    using DP = PipeDepth<G, K, F16, M>;
     constexpr int D = DP::D, NR = DP::NR;
-    constexpr int LPE = 1 + K;        // vector loads per ring entry
+    constexpr int LPE = 1 + K;          // vector loads per ring entry
     constexpr int32_t kSpin = 1 << 22;  // bound of every wait on a counter
 
     extern __shared__ __align__(16) unsigned char lds[];
@@ -656,15 +664,15 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
     const float *bias_lds = reinterpret_cast<const float *>(rows_lds + a.nbundles * GE::NB);
     for (int i = tid; i < a.nbundles * GE::NB * (1 + K); i += blockDim.x)
         rows_lds[i] = table[i];
-    int32_t *ctl = reinterpret_cast<int32_t *>(lds + a.ctl_off);  // free0, free1, fill0, fill1
-    if (tid == 0) {
-        ctl[0] = 0;
-        ctl[1] = 0;
-        ctl[2] = nwaves;  // tile 0 is copied by everyone below
-        ctl[3] = nwaves;
+    if (tid < kRowBytes / 16)
+        *reinterpret_cast<u4 *>(lds + a.strip_rows * kRowBytes + 16 * tid) = u4{0u, 0u, 0u, 0u};
+    int32_t *ctl = reinterpret_cast<int32_t *>(lds + a.ctl_off);  // free[kMaxRegions], fill[kMaxRegions]
+    if (tid < kMaxRegions) {
+        ctl[tid] = 0;
+        ctl[kMaxRegions + tid] = nwaves;  // tile 0 is copied by everyone below
     }
-    const Rsrc ri = make_rsrc(idx, static_cast<uint32_t>(a.idx_bytes));
-    const Rsrc rv = make_rsrc(val, static_cast<uint32_t>(a.val_bytes));
+    const Rsrc rpi = make_rsrc(pidx, static_cast<uint32_t>(a.idx_bytes));
+    const Rsrc rpv = make_rsrc(pval, static_cast<uint32_t>(a.val_bytes));
     const float lo = a.act == 0 ? -__builtin_huge_valf() : 0.0f;
     const float hi = a.act == 2 ? 6.0f : __builtin_huge_valf();
     const int32_t wb0 = wave_ptr[wave], wb1 = wave_ptr[wave + 1];
@@ -673,151 +681,177 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
     if (R > 0)
         copy_share<G, F16>(a, x, lds_base, whole_work(a, 0).tile, 0, a.strip_rows, wave, nwaves, lane);
     wait_vmcnt<0>();
-    __syncthreads();  // table, counters and tile 0 ready
+    __syncthreads();  // table, zero row, counters and tile 0 ready
 
     // ---- whole rounds ----
-    // share bookkeeping: next tile whose lower / upper part this wave copies,
-    // and the step at which a share in flight is counted (-1: none)
-    int32_t sh0 = 1, sh1 = 1, pub0 = -1, pub1 = -1;
-    auto publish_now = [&]() __attribute__((always_inline)) {
-        if (pub0 >= 0 || pub1 >= 0) {
+    // the next share this wave copies (part cq of tile ct) and the parts whose
+    // shares are in flight
+    int32_t cq = 0, ct = 1;
+    uint32_t pend = 0;
+    auto publish = [&]() __attribute__((always_inline)) {
+        static_for<kMaxRegions>([&](auto qc) __attribute__((always_inline)) {
+            constexpr int Q = decltype(qc)::value;
+            if (pend & (1u << Q))
+                count_once(&ctl[kMaxRegions + Q], lane);
+        });
+        pend = 0;
+    };
+    // copy the next share if its part is free; `idle`: count it at once
+    auto service = [&](bool idle) __attribute__((always_inline)) {
+        if (ct < R && lds_load_volatile(&ctl[cq]) >= a.busy_waves * ct) {
+            const int32_t r0 = cq * a.region_rows;
+            const int32_t r1 = std::min(r0 + a.region_rows, a.strip_rows);
+            copy_share<G, F16>(a, x, lds_base, whole_work(a, ct).tile, r0, r1, wave, nwaves, lane);
+            pend |= 1u << cq;
+            if (++cq == a.regions) {
+                cq = 0;
+                ++ct;
+            }
+            if (idle) {
+                wait_vmcnt<0>();
+                publish();
+            }
+        }
+    };
+    auto wait_fill = [&](int32_t q, int32_t target) __attribute__((always_inline)) {
+        if (pend) {
             wait_vmcnt<0>();
-            if (pub0 >= 0)
-                count_once(&ctl[2], lane);
-            if (pub1 >= 0)
-                count_once(&ctl[3], lane);
-            pub0 = pub1 = -1;
+            publish();
         }
-    };
-    // issue this wave's shares whose parts are free; `idle`: count them at once.
-    // done0 / done1: tiles whose lower part / all of which this wave is done with
-    // (a share for tile t needs tile t - 1 done by every wave, this one included)
-    int32_t done0 = R, done1 = R;  // a wave without bundles is done with everything
-    auto service = [&](bool idle, int32_t g) __attribute__((always_inline)) {
-        if (sh0 < R && sh0 <= done0 && lds_load_volatile(&ctl[0]) >= a.busy_waves * sh0) {
-            copy_share<G, F16>(a, x, lds_base, whole_work(a, sh0).tile, 0, a.split_rows, wave, nwaves, lane);
-            ++sh0;
-            pub0 = g + D;
-            if (idle)
-                publish_now();
-        }
-        if (sh1 < R && sh1 <= done1 && lds_load_volatile(&ctl[1]) >= a.busy_waves * sh1) {
-            copy_share<G, F16>(a, x, lds_base, whole_work(a, sh1).tile, a.split_rows, a.strip_rows, wave, nwaves,
-                               lane);
-            ++sh1;
-            pub1 = g + D;
-            if (idle)
-                publish_now();
-        }
-    };
-    auto wait_fill = [&](int c, int32_t target, int32_t g) __attribute__((always_inline)) {
-        publish_now();
-        for (int32_t n = 0; n < kSpin && lds_load_volatile(&ctl[c]) < target; ++n) {
-            service(true, g);
+        for (int32_t n = 0; n < kSpin && lds_load_volatile(&ctl[kMaxRegions + q]) < target; ++n) {
+            service(true);
             __builtin_amdgcn_s_sleep(1);
         }
         // strip reads stay after the wait
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     };
     // done with a part: earlier strip reads stay before the count
-    auto release = [&](int c) __attribute__((always_inline)) {
+    auto release = [&](int32_t q) __attribute__((always_inline)) {
         __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-        count_once(&ctl[c], lane);
+        count_once(&ctl[q], lane);
     };
 
     if (R > 0 && wb0 < wb1) {
         const int32_t ws0 = hdr[2 * wb0];
         const int32_t len = hdr[2 * (wb1 - 1)] + hdr[2 * (wb1 - 1) + 1] - ws0;  // steps per tile
-        const int32_t rel0 = wave_meta[2 * wave], need1 = wave_meta[2 * wave + 1];
         const int32_t total = R * len;
-        done0 = done1 = 0;
+        const uint32_t *__restrict__ sel = psel + sel_ptr[wave];
+        const int32_t *__restrict__ ev = wave_ev + kWaveEvents * wave;
         // LDS byte addresses of the lane's vectors in strip row 0
         uint32_t lrow[GE::V];
 #pragma unroll
         for (int j = 0; j < GE::V; ++j)
             lrow[j] = lds_base + static_cast<uint32_t>(L.lb[j]);
 
-        float acc[K][GE::V][GE::QE];
+        float acc[M][K][GE::V][GE::QE];
 #pragma unroll
-        for (int kk = 0; kk < K; ++kk)
+        for (int s = 0; s < M; ++s)
 #pragma unroll
-            for (int j = 0; j < GE::V; ++j)
+            for (int kk = 0; kk < K; ++kk)
 #pragma unroll
-                for (int e = 0; e < GE::QE; ++e)
-                    acc[kk][j][e] = 0.0f;
-        int32_t b = wb0, rb = 0, left = 0;
-        float bv[K];
-        auto start_bundle = [&]() __attribute__((always_inline)) {
-            rb = rows_lds[b * GE::NB + L.q];
+                for (int j = 0; j < GE::V; ++j)
+#pragma unroll
+                    for (int e = 0; e < GE::QE; ++e)
+                        acc[s][kk][j][e] = 0.0f;
+        int32_t bset[M];  // bundle in progress of each set
+        // this tile's next need and release events and their indices in ev
+        int32_t need = INT32_MAX, rel = INT32_MAX, ni = 0, ri_ = 0;
+        uint32_t selw = 0;  // selector bits of the steps ahead (2 per step)
+        TileAddr<G, F16> ta;
+        // one step of set S: 4 slots of strip reads and FMAs
+        auto step = [&](auto sc, const Entry<K> &en) __attribute__((always_inline)) {
+            constexpr int S = decltype(sc)::value;
+            static_for<4>([&](auto uc) __attribute__((always_inline)) {
+                constexpr int U = decltype(uc)::value;
+                u4 xr[GE::V];
+#pragma unroll
+                for (int j = 0; j < GE::V; ++j)
+                    xr[j] = *reinterpret_cast<const __attribute__((address_space(3))) u4 *>(
+                        static_cast<uintptr_t>(en.off[U] + lrow[j]));
+                fma_slot<G, K, F16, U>(acc[S], en, xr);
+            });
+        };
+        // after a bundle's last step: bias, activation and store from set S,
+        // which continues with its next bundle
+        auto finish = [&](auto sc) __attribute__((always_inline)) {
+            constexpr int S = decltype(sc)::value;
+            const int32_t b = bset[S];
+            float bv[K];
 #pragma unroll
             for (int kk = 0; kk < K; ++kk)
                 bv[kk] = bias_lds[(b * GE::NB + L.q) * K + kk];
-            left = hdr[2 * b + 1];
+            finish_rows<G, K, F16, true>(a, L, ta, y, acc[S], bv, rows_lds[b * GE::NB + L.q], lo, hi);
+            bset[S] = b + M;
         };
-        start_bundle();
 
-        TileAddr<G, F16> ta;
         int32_t it = 0, pos = 0;   // tile (round) and step within the wave's stream
+        int32_t pre = 0;           // next step with tile-start, selector or need-event work
         int32_t lpos = D % len;    // stream position of the next record fetch
         Entry<K> cr[NR];
 #pragma unroll
-        for (int d = 0; d < D; ++d)
-            cr[d] = load_entry<G, K>(ri, rv, L.q, ws0 + d % len);
+        for (int dd = 0; dd < D; ++dd)
+            cr[dd] = load_entry<G, K>(rpi, rpv, L.q, ws0 + dd % len);
         for (int32_t g0 = 0; g0 < total; g0 += NR) {
             static_for<NR>([&](auto kc) __attribute__((always_inline)) {
                 constexpr int KI = decltype(kc)::value;
-                const int32_t g = g0 + KI;
-                if (g < total) {
-                    cr[(KI + D) % NR] = load_entry<G, K>(ri, rv, L.q, ws0 + lpos);
+                if (g0 + KI < total) {
+                    cr[(KI + D) % NR] = load_entry<G, K>(rpi, rpv, L.q, ws0 + lpos);
                     lpos = lpos + 1 == len ? 0 : lpos + 1;
-                    if (pos == 0) {
-                        if (it > 0)
-                            wait_fill(2, nwaves * (it + 1), g);
-                        ta.set(a, L, x, y, whole_work(a, it).tile);
-                        if (rel0 == 0) {
-                            release(0);  // this wave reads no lower-part channel
-                            done0 = it + 1;
-                        }
-                    }
-                    if (pos == need1)
-                        wait_fill(3, nwaves * (it + 1), g);
-                    static_for<4>([&](auto uc) __attribute__((always_inline)) {
-                        constexpr int U = decltype(uc)::value;
-                        u4 xr[GE::V];
+                    if (pos == pre) {
+                        if (pos == 0) {
+                            ni = ri_ = 0;
+                            need = ev[0];
+                            rel = ev[kMaxRegions];
+                            ta.set(a, L, x, y, whole_work(a, it).tile);
 #pragma unroll
-                        for (int j = 0; j < GE::V; ++j)
-                            xr[j] = *reinterpret_cast<const __attribute__((address_space(3))) u4 *>(
-                                static_cast<uintptr_t>(cr[KI].off[U] + lrow[j]));
-                        fma_slot<G, K, F16, U>(acc, cr[KI], xr);
-                    });
-                    if (--left == 0) {
-                        finish_rows<G, K, F16, true>(a, L, ta, y, acc, bv, rb, lo, hi);
-                        b = b + 1 == wb1 ? wb0 : b + 1;
-                        start_bundle();
-                    }
-                    if (pos == rel0 - 1) {
-                        release(0);  // done with the lower part of this tile
-                        done0 = it + 1;
-                    }
-                    if (pos == len - 1) {
-                        release(1);  // done with this tile
-                        done1 = it + 1;
-                    }
-                    service(false, g);
-                    if (pub0 == g || pub1 == g) {
-                        // the shares were issued D fetches ago and complete before them
-                        wait_vmcnt<D * LPE>();
-                        if (pub0 == g) {
-                            count_once(&ctl[2], lane);
-                            pub0 = -1;
+                            for (int s2 = 0; s2 < M; ++s2)
+                                bset[s2] = wb0 + s2;
                         }
-                        if (pub1 == g) {
-                            count_once(&ctl[3], lane);
-                            pub1 = -1;
+                        if ((pos & (kSelSteps - 1)) == 0)
+                            selw = sel[pos / kSelSteps];
+                        while ((need >> 4) == pos) {
+                            wait_fill(need & 15, nwaves * (it + 1));
+                            need = ++ni < kMaxRegions ? ev[ni] : INT32_MAX;
                         }
+                        pre = std::min(need >> 4, (pos | (kSelSteps - 1)) + 1);
+                    }
+                    // the step's set as two one-sided branches on conditions the
+                    // compiler cannot relate: with an if / else it copies one
+                    // set's accumulators at the join
+                    uint32_t c1 = selw & 1u, c0 = c1 ^ 1u;
+                    asm volatile("" : "+s"(c1), "+s"(c0));
+                    if constexpr (M > 1) {
+                        if (c1)
+                            step(std::integral_constant<int, M - 1>{}, cr[KI]);
+                    }
+                    if (M == 1 || c0)
+                        step(std::integral_constant<int, 0>{}, cr[KI]);
+                    if constexpr (KI == 0) {
+                        // shares issued one ring turn ago precede the record just used
+                        if (pend) {
+                            wait_vmcnt<D * LPE>();
+                            publish();
+                        }
+                        service(false);
+                    }
+                    if (selw & 2u) {
+                        if constexpr (M > 1) {
+                            if (c1)
+                                finish(std::integral_constant<int, M - 1>{});
+                        }
+                        if (M == 1 || c0)
+                            finish(std::integral_constant<int, 0>{});
+                    }
+                    selw >>= 2;
+                    if ((rel >> 4) == pos) {
+                        do {
+                            release(rel & 15);
+                            rel = ++ri_ < kMaxRegions ? ev[kMaxRegions + ri_] : INT32_MAX;
+                        } while ((rel >> 4) == pos);
                     }
                     if (++pos == len) {
                         pos = 0;
+                        pre = 0;
                         ++it;
                     }
                 }
@@ -825,12 +859,13 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         }
     }
     // shares not issued yet (a wave without bundles issues all of its shares here)
-    for (int32_t n = 0; n < kSpin && (sh0 < R || sh1 < R); ++n) {
-        service(true, 0);
+    for (int32_t n = 0; n < kSpin && ct < R; ++n) {
+        service(true);
         __builtin_amdgcn_s_sleep(1);
     }
-    publish_now();
     wait_vmcnt<0>();
+    if (pend)
+        publish();
     __syncthreads();  // every copy landed and every wave is done with the strip
 
     // ---- the shared tiles left after the whole rounds ----
@@ -841,6 +876,8 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         copy_share<G, F16>(a, x, lds_base, wk.tile, 0, a.strip_rows, wave, nwaves, lane);
         wait_vmcnt<0>();
         __syncthreads();  // strip ready
+        const Rsrc ri = make_rsrc(idx, static_cast<uint32_t>(a.idx_bytes));
+        const Rsrc rv = make_rsrc(val, static_cast<uint32_t>(a.val_bytes));
         run_item<G, K, F16, false, true>(a, L, ta, x, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
                                          wk.part, lo, hi);
     }
@@ -851,7 +888,8 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
 // ---------------------------------------------------------------------------
 
 using KernelFn = void (*)(const void *, void *, const int32_t *, const float *, const int32_t *, const int32_t *,
-                          const int32_t *, const int32_t *, const int32_t *, Args);
+                          const int32_t *, const int32_t *, const int32_t *, const float *, const uint32_t *,
+                          const int32_t *, const int32_t *, Args);
 
 template <int K, bool F16, bool DIRECT, bool VEC>
 KernelFn pick_g(int g) {
@@ -866,15 +904,29 @@ KernelFn pick_g(int g) {
     }
 }
 
+// Accumulators of one set of a lane.
+template <int G, int K, bool F16>
+constexpr int kSetAcc = K * (16 / G) * (16 / (F16 ? 2 : 4));
+
+template <int G, int K, bool F16>
+KernelFn pick_pipe_m(int m) {
+    if constexpr (kSetAcc<G, K, F16> <= 64) {
+        if (m == 1)
+            return spmm_pipe<G, K, F16, 1>;
+        if constexpr (2 * kSetAcc<G, K, F16> <= 32) {
+            if (m == 2)
+                return spmm_pipe<G, K, F16, 2>;
+        }
+    }
+    return nullptr;
+}
+
 template <int K, bool F16>
-KernelFn pick_pipe(int g) {
+KernelFn pick_pipe(int g, int m) {
     switch (g) {
-    case 4:
-        if constexpr (K * 4 * (16 / (F16 ? 2 : 4)) <= 64)
-            return spmm_pipe<4, K, F16>;
-        return nullptr;
-    case 8: return spmm_pipe<8, K, F16>;
-    case 16: return spmm_pipe<16, K, F16>;
+    case 4: return pick_pipe_m<4, K, F16>(m);
+    case 8: return pick_pipe_m<8, K, F16>(m);
+    case 16: return pick_pipe_m<16, K, F16>(m);
     default: return nullptr;
     }
 }
@@ -883,8 +935,10 @@ template <int K, bool F16>
 KernelFn pick_kv(const DevicePlan &p, bool vec) {
     if (p.kernel == KERNEL_DIRECT)
         return vec ? pick_g<K, F16, true, true>(p.group_lanes) : pick_g<K, F16, true, false>(p.group_lanes);
-    if (vec && p.split_rows < p.strip_rows)
-        return pick_pipe<K, F16>(p.group_lanes);
+    // 1xk blocks keep the simple loop: their records take too many registers
+    // for the pipelined kernel's fetch depth
+    if (vec && K == 1)
+        return pick_pipe<K, F16>(p.group_lanes, p.pipe_sets);
     return vec ? pick_g<K, F16, false, true>(p.group_lanes) : pick_g<K, F16, false, false>(p.group_lanes);
 }
 
@@ -966,8 +1020,9 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.act = p.act;
     a.vec = vec;
     a.strip_rows = p.strip_rows;
-    a.split_rows = p.split_rows;
-    a.table_off = p.kernel == KERNEL_DIRECT ? 0 : p.strip_rows * kRowBytes;
+    a.regions = p.regions;
+    a.region_rows = p.region_rows;
+    a.table_off = p.kernel == KERNEL_DIRECT ? 0 : (p.strip_rows + 1) * kRowBytes;
     a.ctl_off = p.lds_bytes - kCtlBytes;
     a.nbundles = p.nbundles;
     a.busy_waves = p.busy_waves;
@@ -980,7 +1035,8 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.tail_parts = static_cast<int32_t>(parts);
     a.nxcd = static_cast<int32_t>(nxcd);
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(slots)), dim3(p.waves * 64), p.lds_bytes, stream, x, y,
-                       p.idx, p.val, p.hdr, p.table, p.rank, p.wave_ptr, p.wave_meta, a);
+                       p.idx, p.val, p.hdr, p.table, p.rank, p.wave_ptr, p.pidx, p.pval, p.psel, p.sel_ptr,
+                       p.wave_ev, a);
     return hipGetLastError();
 }
 

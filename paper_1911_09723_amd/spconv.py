@@ -27,7 +27,8 @@ _DTYPES = {"f32": F32, "f16": F16}
 
 # Symbols declared in include/spconv.h.
 EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error",
-            "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack")
+            "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
+            "spconv_plan_unpack_interleaved")
 
 
 class SpconvError(RuntimeError):
@@ -39,7 +40,8 @@ class SpconvError(RuntimeError):
 
 class spconv_options(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_int32), ("reorder", ctypes.c_int32), ("host_only", ctypes.c_int32),
-                ("kernel", ctypes.c_int32), ("group_lanes", ctypes.c_int32), ("waves", ctypes.c_int32)]
+                ("kernel", ctypes.c_int32), ("group_lanes", ctypes.c_int32), ("waves", ctypes.c_int32),
+                ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32)]
 
 
 class spconv_plan_info(ctypes.Structure):
@@ -47,7 +49,8 @@ class spconv_plan_info(ctypes.Structure):
                 ("storage", ctypes.c_int32), ("act", ctypes.c_int32), ("kernel", ctypes.c_int32),
                 ("group_lanes", ctypes.c_int32), ("bundle_rows", ctypes.c_int32), ("cols_per_lane", ctypes.c_int32),
                 ("tile_cols", ctypes.c_int32), ("waves", ctypes.c_int32), ("lds_bytes", ctypes.c_int32),
-                ("max_parts", ctypes.c_int32), ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
+                ("max_parts", ctypes.c_int32), ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32),
+                ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64)]
 
@@ -85,6 +88,8 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_get_info.argtypes = [vp, ctypes.POINTER(spconv_plan_info)]
     lib.spconv_plan_unpack.restype = i32
     lib.spconv_plan_unpack.argtypes = [vp, vp, vp, vp, vp]
+    lib.spconv_plan_unpack_interleaved.restype = i32
+    lib.spconv_plan_unpack_interleaved.argtypes = [vp, vp, vp, vp]
     if path is None:
         _lib = lib
     return lib
@@ -183,6 +188,17 @@ def spconv_plan_unpack(plan):
     perm = np.zeros(rows, np.int32)
     _check(load_library().spconv_plan_unpack(plan, _ptr(rp), _ptr(ci), _ptr(va), _ptr(perm)))
     return rp, ci[:info["nnzb"]], va[:info["nnzb"] * info["block_rows"]], perm
+
+
+def spconv_plan_unpack_interleaved(plan):
+    """Return (row_ptr, col_idx, values) rebuilt from the pipelined kernel's interleaved streams."""
+    info = spconv_plan_get_info(plan)
+    rows = info["cout"] // info["block_rows"]
+    rp = np.zeros(rows + 1, np.int32)
+    ci = np.zeros(max(info["nnzb"], 1), np.int32)
+    va = np.zeros(max(info["nnzb"] * info["block_rows"], 1), np.float32)
+    _check(load_library().spconv_plan_unpack_interleaved(plan, _ptr(rp), _ptr(ci), _ptr(va)))
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * info["block_rows"]]
 
 
 class Plan:

@@ -137,7 +137,7 @@ def test_null_arrays_with_nonzeros_rejected():
 def test_options_validated():
     for kw in (dict(group_lanes=2), dict(group_lanes=12), dict(group_lanes=32), dict(group_lanes=-4),
                dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=3),
-               dict(kernel=-1)):
+               dict(kernel=-1), dict(pipe_sets=3), dict(pipe_sets=-1), dict(regions=5), dict(regions=-1)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw
     o = _host_opts()
@@ -187,10 +187,18 @@ def test_pack_unpack_round_trip_and_order(k, pattern, kernel, group_lanes):
     try:
         info = sp.spconv_plan_get_info(h)
         rp, ci, va, perm = sp.spconv_plan_unpack(h)
+        if info["kernel"] == 0:
+            irp, ici, iva = sp.spconv_plan_unpack_interleaved(h)
+        else:
+            with pytest.raises(sp.SpconvError) as ei:
+                sp.spconv_plan_unpack_interleaved(h)
+            assert ei.value.status == sp.spconv.E_FORMAT
+            irp, ici, iva = rp, ci, va
     finally:
         sp.spconv_destroy(h)
     assert np.array_equal(rp, layer.row_ptr) and np.array_equal(ci, layer.col_idx)
     assert np.array_equal(va, layer.values)
+    assert np.array_equal(irp, rp) and np.array_equal(ici, ci) and np.array_equal(iva, va)
     rows = 160 // k
     assert sorted(perm.tolist()) == list(range(rows))
     counts = np.diff(layer.row_ptr)[perm]
@@ -204,6 +212,55 @@ def test_pack_unpack_round_trip_and_order(k, pattern, kernel, group_lanes):
     assert info["kernel"] == (1 if kernel == 2 else 0)
     # whole steps of 4 slots for every group of a bundle
     assert info["slots"] % (4 * info["bundle_rows"]) == 0
+
+
+@pytest.mark.parametrize("sets", [0, 1, 2])
+@pytest.mark.parametrize("regions", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("shape", [(512, 512, 1, "uniform", 1), (37, 80, 1, "uniform", 1),
+                                   (200, 120, 1, "beta", 0), (3, 8, 1, "uniform", 1), (96, 64, 4, "uniform", 1),
+                                   (601, 48, 1, "uniform", 1)])
+def test_interleaved_streams_walk_back_to_the_input(shape, regions, sets):
+    """The pipelined kernel's streams, walked with its own bookkeeping (set and
+    last-step bits, strip parts between need and release events), give back
+    every row's blocks in order."""
+    cin, cout, k, pattern, reorder = shape
+    layer = make_layer(cin, cout, 1, 1, 1, 0.85, block_rows=k, pattern=pattern, seed=cin + cout,
+                       with_x=False)
+    opts = _host_opts(pipe_sets=sets, regions=regions, reorder=reorder, group_lanes=16 if k == 4 else 0)
+    st, h = _create(layer, options=opts, check=False)
+    if sets == 2 and k == 4 and st == sp.spconv.E_UNSUPPORTED:
+        return
+    assert st == sp.spconv.OK, sp.spconv_last_error()
+    try:
+        info = sp.spconv_plan_get_info(h)
+        rp, ci, va = sp.spconv_plan_unpack_interleaved(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert info["kernel"] == 0
+    assert info["pipe_sets"] == (sets or info["pipe_sets"]) and info["pipe_sets"] in (1, 2)
+    strip_rows = -(-cin // 4) * 4
+    assert 1 <= info["regions"] <= min(regions or 4, strip_rows // 4)
+    assert np.array_equal(rp, layer.row_ptr) and np.array_equal(ci, layer.col_idx)
+    assert np.array_equal(va, layer.values)
+
+
+def test_headline_plan_interleaves_two_bundles_over_four_parts():
+    layer = make_layer(512, 512, 1, 1, 1, 0.9, seed=5, with_x=False)
+    h = _create(layer)
+    try:
+        info = sp.spconv_plan_get_info(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert (info["group_lanes"], info["waves"], info["pipe_sets"], info["regions"]) == (4, 16, 2, 4)
+
+
+def test_two_sets_refused_when_accumulators_do_not_fit():
+    # 1x4 blocks take 8 lanes per block row: 4 x 8 accumulators per set
+    layer = make_layer(256, 512, 1, 1, 1, 0.9, block_rows=4, seed=1, with_x=False)
+    st, msg = _status(layer=layer, options=_host_opts(pipe_sets=2))
+    assert st == sp.spconv.E_UNSUPPORTED and "accumulators" in msg
+    st, msg = _status(layer=layer, options=_host_opts(pipe_sets=2, group_lanes=16))
+    assert st == sp.spconv.OK
 
 
 def test_natural_order_when_reorder_off():
@@ -255,14 +312,15 @@ def test_geometry_choice():
 
     def table(cout, k, nb):
         # per bundle: the block row and the k biases of each of its nb groups, 16-byte rounded,
-        # then 16 bytes of counters
+        # then 32 bytes of counters
         bundles = -(-(cout // k) // nb)
-        return -(-(bundles * nb * (1 + k) * 4) // 16) * 16 + 16
+        return -(-(bundles * nb * (1 + k) * 4) // 16) * 16 + 32
 
     def check(i, kernel, g, tile_cols, cin, cout, k):
         nb = 64 // g
         assert (i["kernel"], i["group_lanes"], i["bundle_rows"], i["tile_cols"]) == (kernel, g, nb, tile_cols)
-        strip = 0 if kernel == 1 else -(-cin // 4) * 4 * 256
+        # the strip's rows and one row of zeros for padding slots
+        strip = 0 if kernel == 1 else (-(-cin // 4) * 4 + 1) * 256
         assert i["lds_bytes"] == strip + table(cout, k, nb)
         assert i["waves"] == min(16, -(-(cout // k) // nb))
 

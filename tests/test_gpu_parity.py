@@ -127,7 +127,8 @@ def test_run_is_deterministic_and_independent_of_planning():
     assert np.array_equal(base, gpu_run(layer))
     for opts in (dict(reorder=0), dict(group_lanes=8), dict(group_lanes=16), dict(kernel=2),
                  dict(kernel=2, group_lanes=16), dict(waves=1), dict(waves=5), dict(waves=12, reorder=0),
-                 dict(group_lanes=8, waves=16)):
+                 dict(group_lanes=8, waves=16), dict(pipe_sets=1), dict(regions=1), dict(regions=3),
+                 dict(pipe_sets=1, regions=2), dict(pipe_sets=2, waves=7)):
         note("determinism %s" % opts)
         assert np.array_equal(base, gpu_run(layer, **opts)), opts
 
@@ -140,6 +141,21 @@ def test_shared_tail_tiles(n, k):
     layer = make_layer(512, 512, 14, 14, n, 0.9, block_rows=k, act="relu", seed=11 + n)
     note("tail split n=%d k=%d" % (n, k))
     assert_parity(layer, gpu_run(layer), what="tail n=%d k=%d" % (n, k))
+
+
+@pytest.mark.parametrize("opts", [dict(), dict(pipe_sets=1), dict(regions=1), dict(regions=2),
+                                  dict(pipe_sets=1, regions=3), dict(waves=9), dict(group_lanes=8)],
+                         ids=lambda o: "-".join("%s%d" % kv for kv in o.items()) or "auto")
+def test_pipelined_rounds_bitwise_equal_simple_path(opts):
+    """Batch 256 of the 512 -> 512 layer: three whole rounds of tiles through
+    the pipelined kernel plus a shared tail; every planner choice gives the
+    same bits, and they match the oracle."""
+    layer = make_layer(512, 512, 14, 14, 256, 0.9, act="relu", seed=21)
+    note("pipelined rounds %s" % opts)
+    y = gpu_run(layer, **opts)
+    ref = gpu_run(layer, kernel=2)  # direct-load kernel: no strip, no pipeline
+    assert np.array_equal(y, ref), opts
+    assert_parity(layer, y, what="pipelined %s" % opts)
 
 
 def test_split_does_not_change_bits():
