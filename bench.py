@@ -41,7 +41,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0         # MI355X HBM3E peak
 FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector peak (packed FMA)
-TRAFFIC_BASE = os.path.join(ROOT, "profiles", "traffic_spmm_strip_512_14_b256")
+TRAFFIC_BASE = os.path.join(ROOT, "profiles", "traffic_spmm_pipe_512x512_14x14_b256")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_09723_amd", "csrc", f)
                   for f in ("spmm_kernels.hip", "planner.cpp", "planner.hpp")]
 COPY_BYTES = 256 << 20        # calibration copy: 256 MiB read + 256 MiB written
@@ -171,6 +171,9 @@ def summarize(layer, r):
         "bound": "hbm" if t_hbm >= t_alu else "alu",
         "nnz": layer.nnz,
         "alg_bytes": b_alg,
+        # strip reads from LDS: every packed slot reads one 256-byte strip row
+        # per tile (the on-chip traffic that bounds the unstructured kernel)
+        "lds_strip_read_bytes": r["info"]["slots"] * 256 * -(-layer.n * layer.hw // r["info"]["tile_cols"]),
         "flops": flops,
         "plan": {k: r["info"][k] for k in ("kernel", "group_lanes", "tile_cols", "waves", "lds_bytes", "slots",
                                            "max_parts")},
@@ -236,10 +239,11 @@ def traffic_summary(fetch_dir, write_dir, commands, out_base):
             vals = [v for (kk, _), v in per.items() if kk == k]
             out[counter]["kernels"][k] = {"kib_per_dispatch": float(np.median(vals)), "dispatches": len(vals),
                                           "bytes_scaled": float(np.median(vals)) * 1024.0 * factor}
-    # the headline (unstructured, 16-byte vectors) kernel
-    head = [k for k in out["FETCH_SIZE"]["kernels"] if "spmm_strip<16, 1, false, true>" in k]
-    if head:
-        k = head[0]
+    # the headline kernel: --profile-run launches the unstructured layer first,
+    # so its kernel is the spmm kernel of the lowest dispatch id
+    firsts = sorted((d, k) for (k, d) in _read_counter_dir(fetch_dir, "FETCH_SIZE") if "spmm" in k)
+    if firsts:
+        k = firsts[0][1]
         out["headline_kernel"] = k
         out["bytes_per_launch"] = round(out["FETCH_SIZE"]["kernels"][k]["bytes_scaled"] +
                                         out["WRITE_SIZE"]["kernels"].get(k, {}).get("bytes_scaled", 0.0))
