@@ -51,15 +51,15 @@ typedef enum { SPCONV_ACT_NONE = 0, SPCONV_ACT_RELU = 1, SPCONV_ACT_RELU6 = 2 } 
 
 /*
  * Build a plan from CSR (block_rows = 1) or 1 x block_rows block-CSR weights
- * (Sec. 3.2: k consecutive output channels share one column pattern; k = 4 is
- * the blocking the paper's models use).  Validates the arrays, orders the
+ * (Sec. 3.2: k consecutive output channels share one column pattern; the
+ * paper's kernels block by 2 and 4 output channels).  Validates the arrays, orders the
  * (block) rows by nonzero count for load balance, packs column indices and
  * values into the layout the kernels stream, and copies the result to the
  * current HIP device.  Synchronous.
  *
  *   out         receives the plan; set to NULL on failure
  *   cout, cin   output / input channels; cout % block_rows == 0, both >= 1
- *   block_rows  1 or 4
+ *   block_rows  1, 2 or 4
  *   row_ptr     host, cout/block_rows + 1 entries: row_ptr[0] = 0, non-decreasing
  *   col_idx     host, row_ptr[cout/block_rows] entries, each in [0, cin), strictly
  *               ascending within a (block) row
@@ -74,7 +74,7 @@ typedef enum { SPCONV_ACT_NONE = 0, SPCONV_ACT_RELU = 1, SPCONV_ACT_RELU6 = 2 } 
  *
  * Errors: SPCONV_E_ARG (NULL out/row_ptr, NULL col_idx/values with nonzeros,
  * bad enum), SPCONV_E_SHAPE, SPCONV_E_FORMAT (message names the first bad
- * entry), SPCONV_E_UNSUPPORTED (block_rows not 1 or 4), SPCONV_E_NOMEM,
+ * entry), SPCONV_E_UNSUPPORTED (block_rows not 1, 2 or 4), SPCONV_E_NOMEM,
  * SPCONV_E_HIP (no usable device, allocation or copy failure).  Nothing is
  * leaked on failure.
  */
@@ -116,6 +116,58 @@ spconv_status spconv_destroy(spconv_plan plan);
 /* Message for the calling thread's most recent failure ("" if none).  The
  * pointer stays valid until the next spconv_* call on the same thread. */
 const char *spconv_last_error(void);
+
+/* ---------------------------------------------------------------------------
+ * Dense weights.  Sec. 3.3: a trained (pruned) model keeps its weights as a
+ * dense tensor with zeros, which the library converts to a block compressed
+ * sparse row form for inference; Sec. 3.2: blocks of 2 or 4 consecutive
+ * output channels that share one zero / nonzero pattern.  `dense` is host
+ * memory, row-major [cout][cin] fp32 (W[r][c] at dense[r * cin + c]); a
+ * weight is stored when it is not zero (-0.0 counts as zero); every value
+ * must be finite (SPCONV_E_FORMAT names the first one that is not).  Host
+ * only, synchronous; the caller keeps ownership of every array.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * The largest k in {4, 2, 1} that divides cout and for which every aligned
+ * group of k rows (rows k*b .. k*b + k - 1) has the same zero / nonzero
+ * pattern in every column, so that the 1 x k block-CSR stores no zero.
+ *   block_rows  out: the detected k
+ * Errors: SPCONV_E_ARG (NULL pointer), SPCONV_E_SHAPE (cout or cin < 1,
+ * cin > 2^24), SPCONV_E_FORMAT (a non-finite weight).
+ */
+spconv_status spconv_detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows);
+
+/*
+ * Convert a dense weight to 1 x block_rows block-CSR (the layout that
+ * spconv_plan_create takes): block (b, c) is stored when any of
+ * W[b*k .. b*k + k - 1][c] is nonzero, with all k of its weights (zeros
+ * included), columns ascending within a block row.
+ *   block_rows  1, 2 or 4; cout % block_rows == 0
+ *   row_ptr     out, cout/block_rows + 1 entries, or NULL
+ *   col_idx     out, `capacity` entries; NULL = only count the blocks
+ *   values      out, capacity * block_rows entries (required with col_idx)
+ *   capacity    blocks that col_idx / values can hold
+ *   nnzb        out: number of stored blocks (set also on SPCONV_E_ARG for
+ *               too small a capacity, so a caller can size its arrays with a
+ *               first call that passes col_idx = NULL)
+ * Errors: SPCONV_E_ARG (NULL dense / nnzb, values or row_ptr missing with
+ * col_idx, capacity too small), SPCONV_E_UNSUPPORTED (block_rows not 1, 2 or
+ * 4), SPCONV_E_SHAPE, SPCONV_E_FORMAT.
+ */
+spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t block_rows,
+                                   int32_t *row_ptr, int32_t *col_idx, float *values, int64_t capacity,
+                                   int64_t *nnzb);
+
+/*
+ * spconv_plan_create from a dense weight: block_rows = 0 detects the block
+ * height (spconv_detect_block_rows), else 1, 2 or 4; then converts
+ * (spconv_dense_to_bcsr) and plans.  Other arguments and errors as for
+ * spconv_plan_create.
+ */
+spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
+                                       int32_t block_rows, const float *bias, spconv_act act,
+                                       spconv_dtype storage);
 
 /* ---------------------------------------------------------------------------
  * Planner controls and introspection.  These let a caller (and the CPU-only

@@ -1,8 +1,9 @@
 """Sparse 1x1 convolution (sparse weights x dense CHW activations) for MI355X.
 
 The work happens in ``libspconv.so`` (C ABI in include/spconv.h): a host
-planner packs CSR / 1x4 block-CSR weights, and hand-written gfx950 HIP
-kernels compute act(W X + b) on NCHW fp32 or fp16 tensors.  This package is
+planner packs CSR / 1x2 / 1x4 block-CSR weights (or converts dense masked
+ones), and hand-written gfx950 HIP kernels compute act(W X + b) on NCHW fp32
+or fp16 tensors.  This package is
 the thin Python binding plus the in-tree build script.
 """
 
@@ -10,10 +11,13 @@ from .spconv import (  # noqa: F401
     Plan,
     SpconvError,
     load_library,
+    spconv_dense_to_bcsr,
     spconv_destroy,
+    spconv_detect_block_rows,
     spconv_last_error,
     spconv_options_init,
     spconv_plan_create,
+    spconv_plan_create_dense,
     spconv_plan_get_info,
     spconv_plan_unpack,
     spconv_plan_unpack_interleaved,

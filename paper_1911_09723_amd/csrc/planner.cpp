@@ -71,8 +71,8 @@ Status validate(const Input &in, std::string &err) {
         err = "block_rows must be positive";
         return E_ARG;
     }
-    if (in.block_rows != 1 && in.block_rows != 4) {
-        os << "block_rows = " << in.block_rows << " is not supported (1 or 4)";
+    if (in.block_rows != 1 && in.block_rows != 2 && in.block_rows != 4) {
+        os << "block_rows = " << in.block_rows << " is not supported (1, 2 or 4)";
         err = os.str();
         return E_UNSUPPORTED;
     }
@@ -154,6 +154,130 @@ Status validate(const Input &in, std::string &err) {
                 return E_FORMAT;
             }
         }
+    }
+    return OK;
+}
+
+namespace {
+
+Status check_dense(int32_t cout, int32_t cin, const float *dense, std::string &err) {
+    if (cout <= 0 || cin <= 0) {
+        err = "cout and cin must be >= 1 (got cout = " + std::to_string(cout) + ", cin = " + std::to_string(cin) + ")";
+        return E_SHAPE;
+    }
+    if (cin > (1 << 24)) {
+        err = "cin must be at most 2^24";
+        return E_SHAPE;
+    }
+    if (!dense) {
+        err = "dense is NULL";
+        return E_ARG;
+    }
+    const int64_t n = static_cast<int64_t>(cout) * cin;
+    for (int64_t i = 0; i < n; ++i) {
+        if (!std::isfinite(dense[i])) {
+            err = "dense[" + std::to_string(i / cin) + "][" + std::to_string(i % cin) + "] is not finite";
+            return E_FORMAT;
+        }
+    }
+    return OK;
+}
+
+}  // namespace
+
+Status detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t &k, std::string &err) {
+    const Status st = check_dense(cout, cin, dense, err);
+    if (st != OK)
+        return st;
+    for (int32_t cand : {4, 2}) {
+        if (cout % cand)
+            continue;
+        bool blocked = true;
+        for (int32_t rb = 0; blocked && rb < cout / cand; ++rb) {
+            const float *w0 = dense + static_cast<int64_t>(rb) * cand * cin;
+            for (int32_t i = 1; blocked && i < cand; ++i) {
+                const float *wi = w0 + static_cast<int64_t>(i) * cin;
+                for (int32_t c = 0; c < cin; ++c) {
+                    if ((w0[c] != 0.0f) != (wi[c] != 0.0f)) {
+                        blocked = false;
+                        break;
+                    }
+                }
+            }
+        }
+        if (blocked) {
+            k = cand;
+            return OK;
+        }
+    }
+    k = 1;
+    return OK;
+}
+
+Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t *row_ptr,
+                     int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err) {
+    nnzb = 0;
+    Status st = check_dense(cout, cin, dense, err);
+    if (st != OK)
+        return st;
+    if (k != 1 && k != 2 && k != 4) {
+        err = "block_rows = " + std::to_string(k) + " is not supported (1, 2 or 4)";
+        return k <= 0 ? E_ARG : E_UNSUPPORTED;
+    }
+    if (cout % k) {
+        err = "cout = " + std::to_string(cout) + " is not a multiple of block_rows = " + std::to_string(k);
+        return E_SHAPE;
+    }
+    const bool write = col_idx != nullptr;
+    if (write && (!row_ptr || !values)) {
+        err = "row_ptr and values must be given with col_idx";
+        return E_ARG;
+    }
+    auto stored = [&](int32_t rb, int32_t c) {
+        for (int32_t i = 0; i < k; ++i)
+            if (dense[(static_cast<int64_t>(rb) * k + i) * cin + c] != 0.0f)
+                return true;
+        return false;
+    };
+    int64_t total = 0;
+    for (int32_t rb = 0; rb < cout / k; ++rb)
+        for (int32_t c = 0; c < cin; ++c)
+            total += stored(rb, c) ? 1 : 0;
+    nnzb = total;
+    if (total * k > (int64_t(1) << 30)) {
+        err = "too many stored values (limit 2^30)";
+        return E_SHAPE;
+    }
+    if (!write) {
+        if (row_ptr) {
+            // row offsets only
+            int32_t acc = 0;
+            row_ptr[0] = 0;
+            for (int32_t rb = 0; rb < cout / k; ++rb) {
+                for (int32_t c = 0; c < cin; ++c)
+                    acc += stored(rb, c) ? 1 : 0;
+                row_ptr[rb + 1] = acc;
+            }
+        }
+        return OK;
+    }
+    if (total > capacity) {
+        err = "capacity of " + std::to_string(capacity) + " blocks is below the " + std::to_string(total) +
+              " blocks of the weight";
+        return E_ARG;
+    }
+    int32_t t = 0;
+    row_ptr[0] = 0;
+    for (int32_t rb = 0; rb < cout / k; ++rb) {
+        for (int32_t c = 0; c < cin; ++c) {
+            if (!stored(rb, c))
+                continue;
+            col_idx[t] = c;
+            for (int32_t i = 0; i < k; ++i)
+                values[static_cast<int64_t>(t) * k + i] = dense[(static_cast<int64_t>(rb) * k + i) * cin + c];
+            ++t;
+        }
+        row_ptr[rb + 1] = t;
     }
     return OK;
 }

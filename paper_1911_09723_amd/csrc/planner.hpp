@@ -175,6 +175,22 @@ uint16_t float_to_half_rne(float v);
 // Exact binary16 -> fp32 conversion.
 float half_to_float(uint16_t h);
 
+// Dense weights (Sec. 3.3: dense masked weights are converted to a block
+// compressed sparse row form for inference).  `dense` is row-major
+// [cout][cin]; a weight is stored when it is not zero (-0.0 counts as zero).
+//
+// The largest k in {4, 2, 1} dividing cout for which every aligned group of k
+// rows has a single zero / nonzero pattern in every column (Sec. 3.2: output
+// channel blocks of 2 and 4), so a 1 x k block-CSR stores no zero.
+Status detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t &k, std::string &err);
+// The 1 x k block-CSR of a dense weight: a block (aligned group of k rows,
+// one column) is stored when any of its k weights is nonzero, with its k
+// weights in block-major order (zeros included).  Sets nnzb and, when not
+// null, row_ptr[cout/k + 1]; with col_idx not null also writes col_idx[nnzb]
+// and values[nnzb * k] (E_ARG when nnzb exceeds `capacity` blocks).
+Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t *row_ptr,
+                     int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err);
+
 // Check the block-CSR arrays; on failure return the status and set `err`.
 Status validate(const Input &in, std::string &err);
 

@@ -244,6 +244,70 @@ spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, in
                                  nullptr);
 }
 
+spconv_status spconv_detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows) {
+    g_err.clear();
+    if (!block_rows)
+        return fail(SPCONV_E_ARG, "block_rows is NULL");
+    std::string err;
+    int32_t k = 1;
+    const spconv::Status st = spconv::detect_block_rows(cout, cin, dense, k, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    *block_rows = k;
+    return SPCONV_OK;
+}
+
+spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t block_rows,
+                                   int32_t *row_ptr, int32_t *col_idx, float *values, int64_t capacity,
+                                   int64_t *nnzb) {
+    g_err.clear();
+    if (!nnzb)
+        return fail(SPCONV_E_ARG, "nnzb is NULL");
+    std::string err;
+    int64_t n = 0;
+    const spconv::Status st =
+        spconv::dense_to_bcsr(cout, cin, dense, block_rows, row_ptr, col_idx, values, capacity, n, err);
+    *nnzb = n;
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
+                                       int32_t block_rows, const float *bias, spconv_act act,
+                                       spconv_dtype storage) {
+    g_err.clear();
+    if (!out)
+        return fail(SPCONV_E_ARG, "out is NULL");
+    *out = nullptr;
+    std::string err;
+    int32_t k = block_rows;
+    spconv::Status st = spconv::OK;
+    if (k == 0)
+        st = spconv::detect_block_rows(cout, cin, dense, k, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    int64_t nnzb = 0;
+    st = spconv::dense_to_bcsr(cout, cin, dense, k, nullptr, nullptr, nullptr, 0, nnzb, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    std::vector<int32_t> row_ptr, col_idx;
+    std::vector<float> values;
+    try {
+        row_ptr.resize(static_cast<size_t>(cout / k) + 1);
+        col_idx.resize(static_cast<size_t>(std::max<int64_t>(nnzb, 1)));
+        values.resize(static_cast<size_t>(std::max<int64_t>(nnzb, 1) * k));
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while converting the dense weight");
+    }
+    st = spconv::dense_to_bcsr(cout, cin, dense, k, row_ptr.data(), col_idx.data(), values.data(), nnzb, nnzb,
+                               err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    return spconv_plan_create(out, cout, cin, k, row_ptr.data(), col_idx.data(), values.data(), bias, act,
+                              storage);
+}
+
 spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
                          void *stream) {
     g_err.clear();

@@ -184,8 +184,8 @@ struct Geo {
 };
 
 // One step's records as one lane holds them: the channel offsets of its row's
-// 4 slots and their weights (K == 1: the 4 slots' weights; K == 4: w[u] = the
-// 4 rows' weights of slot u).
+// 4 slots and their weights, slot-major with K weights per slot (K == 1: the 4
+// slots' weights; K == 4: w[u] = the 4 rows' weights of slot u).
 template <int K>
 struct Entry {
     u4 off;
@@ -261,7 +261,9 @@ __device__ __forceinline__ void fma_slot(float (&acc)[K][16 / G][16 / (F16 ? 2 :
     using GE = Geo<G, F16>;
 #pragma unroll
     for (int kk = 0; kk < K; ++kk) {
-        const float w = __uint_as_float(K == 1 ? en.w[0][U] : en.w[U % K][kk]);
+        // the step's weights are slot-major, K per slot: weight kk of slot U is
+        // float U * K + kk of the lane's 4 K floats
+        const float w = __uint_as_float(en.w[(U * K + kk) / 4][(U * K + kk) % 4]);
 #pragma unroll
         for (int j = 0; j < GE::V; ++j) {
             if constexpr (F16) {
@@ -945,6 +947,8 @@ KernelFn pick_kv(const DevicePlan &p, bool vec) {
 KernelFn pick(const DevicePlan &p, bool vec) {
     if (p.k == 4)
         return p.storage == 1 ? pick_kv<4, true>(p, vec) : pick_kv<4, false>(p, vec);
+    if (p.k == 2)
+        return p.storage == 1 ? pick_kv<2, true>(p, vec) : pick_kv<2, false>(p, vec);
     return p.storage == 1 ? pick_kv<1, true>(p, vec) : pick_kv<1, false>(p, vec);
 }
 

@@ -28,7 +28,8 @@ _DTYPES = {"f32": F32, "f16": F16}
 # Symbols declared in include/spconv.h.
 EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error",
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
-            "spconv_plan_unpack_interleaved")
+            "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
+            "spconv_plan_create_dense")
 
 
 class SpconvError(RuntimeError):
@@ -90,6 +91,12 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_unpack.argtypes = [vp, vp, vp, vp, vp]
     lib.spconv_plan_unpack_interleaved.restype = i32
     lib.spconv_plan_unpack_interleaved.argtypes = [vp, vp, vp, vp]
+    lib.spconv_detect_block_rows.restype = i32
+    lib.spconv_detect_block_rows.argtypes = [i32, i32, vp, ctypes.POINTER(i32)]
+    lib.spconv_dense_to_bcsr.restype = i32
+    lib.spconv_dense_to_bcsr.argtypes = [i32, i32, vp, i32, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
+    lib.spconv_plan_create_dense.restype = i32
+    lib.spconv_plan_create_dense.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, vp, i32, i32]
     if path is None:
         _lib = lib
     return lib
@@ -140,6 +147,45 @@ def spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias=Non
     else:
         status = lib.spconv_plan_create_ex(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
                                            _ptr(ci), _ptr(va), _ptr(bi), a, st, ctypes.byref(options))
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
+
+
+def spconv_detect_block_rows(dense) -> int:
+    """Largest k in (4, 2, 1) for which the dense [Cout, Cin] weight is 1 x k blocked."""
+    d = _arr(dense, np.float32)
+    k = ctypes.c_int32()
+    _check(load_library().spconv_detect_block_rows(int(d.shape[0]), int(d.shape[1]), _ptr(d), ctypes.byref(k)))
+    return k.value
+
+
+def spconv_dense_to_bcsr(dense, block_rows: int):
+    """Convert a dense [Cout, Cin] weight to 1 x block_rows block-CSR: (row_ptr, col_idx, values)."""
+    lib = load_library()
+    d = _arr(dense, np.float32)
+    cout, cin = int(d.shape[0]), int(d.shape[1])
+    n = ctypes.c_int64()
+    _check(lib.spconv_dense_to_bcsr(cout, cin, _ptr(d), int(block_rows), None, None, None, 0, ctypes.byref(n)))
+    k = int(block_rows)
+    rp = np.zeros(cout // k + 1, np.int32)
+    ci = np.zeros(max(n.value, 1), np.int32)
+    va = np.zeros(max(n.value, 1) * k, np.float32)
+    _check(lib.spconv_dense_to_bcsr(cout, cin, _ptr(d), k, _ptr(rp), _ptr(ci), _ptr(va), n.value, ctypes.byref(n)))
+    return rp, ci[:n.value], va[:n.value * k]
+
+
+def spconv_plan_create_dense(dense, block_rows: int = 0, bias=None, act="none", storage="f32",
+                             check: bool = True):
+    """Create a plan from a dense [Cout, Cin] weight (block_rows 0 = detect).  Returns the handle."""
+    d = _arr(dense, np.float32)
+    bi = _arr(bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    status = load_library().spconv_plan_create_dense(ctypes.byref(out), int(d.shape[0]), int(d.shape[1]), _ptr(d),
+                                                     int(block_rows), _ptr(bi), a, st)
     if not check:
         return status, out.value
     _check(status)
@@ -214,6 +260,14 @@ class Plan:
         self.handle = spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage,
                                          options=opts)
         self.cout, self.cin, self.storage = int(cout), int(cin), storage
+
+    @classmethod
+    def from_dense(cls, dense, block_rows: int = 0, bias=None, act="none", storage="f32"):
+        """Plan for a dense masked [Cout, Cin] weight (block_rows 0 = detect the block height)."""
+        self = cls.__new__(cls)
+        self.handle = spconv_plan_create_dense(dense, block_rows, bias, act, storage)
+        self.cout, self.cin, self.storage = int(dense.shape[0]), int(dense.shape[1]), storage
+        return self
 
     @classmethod
     def from_layer(cls, layer, **options):

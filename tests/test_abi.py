@@ -112,7 +112,8 @@ def test_duplicate_or_unsorted_columns_rejected():
     (dict(cout=63, block_rows=4), sp.spconv.E_SHAPE),
     (dict(cout=0), sp.spconv.E_SHAPE),
     (dict(cin=0), sp.spconv.E_SHAPE),
-    (dict(block_rows=2), sp.spconv.E_UNSUPPORTED),
+    (dict(block_rows=3), sp.spconv.E_UNSUPPORTED),
+    (dict(block_rows=8), sp.spconv.E_UNSUPPORTED),
     (dict(block_rows=0), sp.spconv.E_ARG),
     (dict(act=7), sp.spconv.E_ARG),
     (dict(storage=5), sp.spconv.E_ARG),
@@ -176,11 +177,11 @@ def test_injected_allocation_failure_reports_nomem():
     assert int(st) == sp.spconv.E_NOMEM and h == "None" and "SPCONV_FAULT" in msg
 
 
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 @pytest.mark.parametrize("pattern", ["uniform", "beta"])
 @pytest.mark.parametrize("kernel,group_lanes", [(0, 0), (1, 4), (1, 8), (1, 16), (2, 0), (2, 8)])
 def test_pack_unpack_round_trip_and_order(k, pattern, kernel, group_lanes):
-    if pattern == "beta" and k == 4:
+    if pattern == "beta" and k > 1:
         pytest.skip("beta row densities are defined for unstructured masks")
     layer = make_layer(96, 160, 2, 2, 1, 0.85, block_rows=k, pattern=pattern, seed=4, with_x=False)
     h = _create(layer, options=_host_opts(kernel=kernel, group_lanes=group_lanes))
@@ -328,6 +329,8 @@ def test_geometry_choice():
     check(info_for(512, 512, "f32"), 0, 4, 64, 512, 512, 1)
     # 1x4 blocks: 4 x 16 accumulators would crowd the registers, so 8 lanes per row
     check(info_for(512, 512, "f32", 4), 0, 8, 64, 512, 512, 4)
+    # 1x2 blocks: 2 x 16 accumulators fit, so 4 lanes per row
+    check(info_for(512, 512, "f32", 2), 0, 4, 64, 512, 512, 2)
     # fp16: 128 columns per tile; 1x4 blocks take 16 lanes per row
     check(info_for(320, 1280, "f16", 4), 0, 16, 128, 320, 1280, 4)
     check(info_for(320, 1280, "f16", 1), 0, 4, 128, 320, 1280, 1)

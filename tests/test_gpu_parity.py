@@ -37,6 +37,13 @@ SMALL = [
     (1500, 48, 6, 6, 2, 0.9, 1, "f32", "relu"),
     (1500, 48, 6, 6, 2, 0.9, 4, "f16", "relu"),
     (1300, 48, 8, 8, 2, 0.9, 1, "f16", "none"),
+    # 1x2 output-channel blocks (the paper's 16x2 kernels)
+    (24, 40, 7, 7, 3, 0.8, 2, "f32", "relu6"),
+    (64, 36, 5, 5, 2, 0.5, 2, "f16", "none"),
+    (200, 120, 9, 9, 2, 0.9, 2, "f16", "relu"),
+    (512, 64, 14, 14, 3, 0.9, 2, "f32", "relu"),
+    (601, 96, 7, 7, 2, 0.9, 2, "f32", "relu6"),
+    (1500, 48, 6, 6, 2, 0.9, 2, "f16", "relu"),
 ]
 
 
@@ -77,7 +84,7 @@ def test_identity_weight_is_bitwise_x(storage):
     assert np.array_equal(y.view(np.uint8), layer.x.view(np.uint8))
 
 
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 @pytest.mark.parametrize("act", ["none", "relu", "relu6"])
 def test_all_zero_weight_gives_act_bias(k, act):
     layer = make_layer(64, 128, 7, 7, 2, 1.0, block_rows=k, act=act, seed=6)
@@ -134,7 +141,7 @@ def test_run_is_deterministic_and_independent_of_planning():
 
 
 @pytest.mark.parametrize("n", [1, 3, 83, 84, 85, 128])
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 def test_shared_tail_tiles(n, k):
     """Batch sizes around one round of tiles: the tiles left after the whole
     rounds are split by bundles over several workgroups."""
@@ -169,12 +176,13 @@ def test_split_does_not_change_bits():
     assert np.array_equal(gpu_run(big)[:84], gpu_run(small))
 
 
-def test_blocked_equals_expanded_csr_bitwise():
-    layer = make_layer(128, 96, 14, 14, 2, 0.8, block_rows=4, act="relu6", seed=10)
-    rp, ci, va = expand_blocks_to_csr(96, 4, layer.row_ptr, layer.col_idx, layer.values)
+@pytest.mark.parametrize("k", [2, 4])
+def test_blocked_equals_expanded_csr_bitwise(k):
+    layer = make_layer(128, 96, 14, 14, 2, 0.8, block_rows=k, act="relu6", seed=10)
+    rp, ci, va = expand_blocks_to_csr(96, k, layer.row_ptr, layer.col_idx, layer.values)
     csr = make_layer(128, 96, 14, 14, 2, 0.8, act="relu6", seed=10)
     csr.row_ptr, csr.col_idx, csr.values, csr.bias, csr.x = rp, ci, va, layer.bias, layer.x
-    note("blocked vs expanded")
+    note("blocked vs expanded k=%d" % k)
     assert np.array_equal(gpu_run(layer), gpu_run(csr))
 
 
@@ -243,3 +251,26 @@ def test_overlapping_x_y_rejected():
         assert ei.value.status == 1
     finally:
         plan.close()
+
+
+@pytest.mark.parametrize("k", [1, 2, 4])
+@pytest.mark.parametrize("storage", ["f32", "f16"])
+def test_dense_weight_plan_matches_block_csr_plan(k, storage):
+    """A plan built from the dense masked weight (block height detected, then
+    converted) computes the same bits as the plan from the block-CSR arrays."""
+    from paper_1911_09723_amd import Plan
+    from synth import densify
+    import torch
+    layer = make_layer(160, 96, 7, 7, 3, 0.85, block_rows=k, storage=storage, act="relu6", seed=30 + k)
+    dense = densify(96, 160, k, layer.row_ptr, layer.col_idx, layer.values).astype(np.float32)
+    note("dense plan k=%d %s" % (k, storage))
+    plan = Plan.from_dense(dense, 0, layer.bias, "relu6", storage)
+    try:
+        assert plan.info()["block_rows"] == k
+        y = plan.run(to_gpu(layer.x))
+        torch.cuda.synchronize()
+        y = y.cpu().numpy()
+    finally:
+        plan.close()
+    assert np.array_equal(y.view(np.uint8), gpu_run(layer).view(np.uint8))
+    assert_parity(layer, y, what="dense k=%d" % k)

@@ -57,7 +57,7 @@ def _battery(lib):
                 failed.append("hand:" + case["name"] + ":" + act)
             if not np.array_equal(s[0], np.asarray(case["scale"])):
                 failed.append("hand-scale:" + case["name"])
-    for k, storage in ((1, "f32"), (4, "f32"), (4, "f16")):
+    for k, storage in ((1, "f32"), (2, "f32"), (4, "f32"), (4, "f16")):
         layer = make_layer(12, 16, 3, 5, 2, 0.5, block_rows=k, storage=storage, act="relu6", seed=3)
         _, y64, s = oracle.spconv_ref(layer.cout, layer.cin, k, layer.row_ptr, layer.col_idx,
                                       layer.values, layer.bias, "relu6", layer.x, storage=storage, lib=lib)

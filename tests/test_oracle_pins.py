@@ -59,7 +59,7 @@ def test_hand_examples(case, act):
     assert np.array_equal(wd, np.asarray(case["dense_w"], dtype=np.float64))
 
 
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 @pytest.mark.parametrize("sparsity", [0.0, 0.5, 0.9, 1.0])
 @pytest.mark.parametrize("act", ["none", "relu", "relu6"])
 @pytest.mark.parametrize("storage", ["f32", "f16"])
@@ -75,7 +75,7 @@ def test_brute_force_small(k, sparsity, act, storage):
 
 
 @settings(max_examples=60, deadline=None)
-@given(cin=st.integers(1, 16), cout4=st.integers(1, 4), k=st.sampled_from([1, 4]),
+@given(cin=st.integers(1, 16), cout4=st.integers(1, 4), k=st.sampled_from([1, 2, 4]),
        hw=st.integers(1, 20), n=st.integers(1, 3),
        sparsity=st.sampled_from([0.0, 0.5, 0.9, 1.0]), act=st.sampled_from(["none", "relu", "relu6"]),
        seed=st.integers(0, 2 ** 31 - 1))
@@ -116,7 +116,7 @@ def test_identity_weight_returns_x(storage, act):
 
 @pytest.mark.parametrize("storage", ["f32", "f16"])
 @pytest.mark.parametrize("act", ["none", "relu", "relu6"])
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 def test_all_zero_weight_gives_act_bias(storage, act, k):
     layer = make_layer(16, 32, 5, 5, 2, 1.0, block_rows=k, storage=storage, act=act, seed=9)
     layer.bias[:4] = np.float32([7.5, -3.0, 0.0, 6.0])
@@ -126,7 +126,7 @@ def test_all_zero_weight_gives_act_bias(storage, act, k):
     assert np.array_equal(y, np.broadcast_to(expect[None, :, None, None], y.shape))
 
 
-@pytest.mark.parametrize("k", [1, 4])
+@pytest.mark.parametrize("k", [1, 2, 4])
 def test_power_of_two_scaling(k):
     layer = make_layer(32, 64, 6, 6, 2, 0.7, block_rows=k, act="none", seed=11)
     y, y64, _ = oracle.spconv_ref_layer(layer)
@@ -137,16 +137,17 @@ def test_power_of_two_scaling(k):
     assert np.array_equal(y2, 2 * y)
 
 
+@pytest.mark.parametrize("k", [2, 4])
 @pytest.mark.parametrize("storage", ["f32", "f16"])
-def test_blocked_equals_expanded_csr(storage):
-    layer = make_layer(40, 48, 4, 7, 2, 0.8, block_rows=4, storage=storage, act="relu6", seed=21)
-    rp, ci, va = expand_blocks_to_csr(48, 4, layer.row_ptr, layer.col_idx, layer.values)
+def test_blocked_equals_expanded_csr(storage, k):
+    layer = make_layer(40, 48, 4, 7, 2, 0.8, block_rows=k, storage=storage, act="relu6", seed=21)
+    rp, ci, va = expand_blocks_to_csr(48, k, layer.row_ptr, layer.col_idx, layer.values)
     _, y64b, sb = oracle.spconv_ref_layer(layer)
     _, y64c, sc = oracle.spconv_ref(48, 40, 1, rp, ci, va, layer.bias, "relu6", layer.x, storage=storage)
     assert np.array_equal(y64b, y64c) and np.array_equal(sb, sc)
     # every block row of the expansion shares one column pattern
-    for rb in range(12):
-        pats = [tuple(ci[rp[4 * rb + i]:rp[4 * rb + i + 1]]) for i in range(4)]
+    for rb in range(48 // k):
+        pats = [tuple(ci[rp[k * rb + i]:rp[k * rb + i + 1]]) for i in range(k)]
         assert len(set(pats)) == 1
 
 
