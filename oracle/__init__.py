@@ -14,6 +14,10 @@ share one pattern; Sec. 3.3: block-CSR weights) in double precision with the C
 code in ``spconv_ref.c``, then rounds each element once, to nearest-even, to
 the storage type.  It also returns the per-element error scale
 S = sum |W[r, c] * X[n, c, p]| that the parity tolerance is stated in.
+
+``dw3x3_ref`` and ``fused_ref`` evaluate the fused MobileNet block order
+(depthwise 3x3, then the sparse 1x1 on its output; paper Sec. 2 and Sec.
+3.3) the same way, in double.
 """
 
 from __future__ import annotations
@@ -50,6 +54,18 @@ def load_library(path: str):
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
         ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
         ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_run_f64.restype = ctypes.c_int
+    lib.spconv_ref_run_f64.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_dw3x3.restype = ctypes.c_int
+    lib.spconv_ref_dw3x3.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
     ]
     lib.spconv_ref_threads.restype = ctypes.c_int
     lib.spconv_ref_half_to_double.restype = ctypes.c_double
@@ -126,6 +142,53 @@ def spconv_ref_layer(layer, x=None, with_scale: bool = True):
     return spconv_ref(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx,
                       layer.values, layer.bias, layer.act, layer.x if x is None else x,
                       storage=layer.storage, with_scale=with_scale)
+
+
+def dw3x3_ref(x, k, bias, act, stride: int, lib=None):
+    """Depthwise 3x3, zero padding 1, stride ``stride`` over float32 x [N, C, H, W]
+    (k [C, 3, 3]); returns (d, sd) in double, [N, C, Ho, Wo]: the outputs and
+    their scale |b| + sum |K * X|."""
+    lib = _load() if lib is None else lib
+    xa = np.ascontiguousarray(x, dtype=np.float32)
+    ka = np.ascontiguousarray(k, dtype=np.float32)
+    ba = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    n, c, h, w = xa.shape
+    if ka.shape != (c, 3, 3):
+        raise ValueError("k must be [C, 3, 3]")
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    d = np.empty((n, c, ho, wo), dtype=np.float64)
+    sd = np.empty((n, c, ho, wo), dtype=np.float64)
+    rc = lib.spconv_ref_dw3x3(int(n), int(c), int(h), int(w), int(stride), _ptr(xa), _ptr(ka), _ptr(ba),
+                              _ACTS[act], _ptr(d), _ptr(sd))
+    if rc != 0:
+        raise ValueError("oracle rejected the depthwise input (code %d)" % rc)
+    return d, sd
+
+
+def fused_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x, dw_k, dw_bias, dw_act,
+              stride: int, lib=None):
+    """The depthwise 3x3 stage, then the sparse 1x1 over its exact (double)
+    output.  Returns (y float32, y64, scale) with scale
+    S = sum |W * D| + |W| * SD, SD the depthwise stage's own scale."""
+    lib = _load() if lib is None else lib
+    d, sd = dw3x3_ref(x, dw_k, dw_bias, dw_act, stride, lib=lib)
+    n, c, ho, wo = d.shape
+    if c != cin:
+        raise ValueError("x has %d channels, expected %d" % (c, cin))
+    row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+    values = np.ascontiguousarray(values, dtype=np.float32)
+    bias_a = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    hw = ho * wo
+    y64 = np.empty((n, cout, hw), dtype=np.float64)
+    scale = np.empty((n, cout, hw), dtype=np.float64)
+    rc = lib.spconv_ref_run_f64(int(cout), int(cin), int(block_rows), _ptr(row_ptr), _ptr(col_idx),
+                                _ptr(values), _ptr(bias_a), _ACTS[act], _ptr(d), _ptr(sd),
+                                int(n), int(hw), _ptr(y64), _ptr(scale))
+    if rc != 0:
+        raise ValueError("oracle rejected the input (code %d)" % rc)
+    shape = (n, cout, ho, wo)
+    return y64.astype(np.float32).reshape(shape), y64.reshape(shape), scale.reshape(shape)
 
 
 def tolerance(y_ref, scale, storage: str):

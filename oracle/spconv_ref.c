@@ -34,6 +34,9 @@
  * product and sum is rounded on its own.
  *
  * Returns 0, -1 if a column index is out of range, -2 if scratch allocation fails.
+ *
+ * Below it: the same stage over a double input (spconv_ref_run_f64) and a
+ * depthwise 3x3 stage (spconv_ref_dw3x3) for the fused depthwise -> 1x1 path.
  */
 #include <math.h>
 #include <stddef.h>
@@ -68,11 +71,15 @@ static double apply_act(double v, int act)
     return v;
 }
 
-int spconv_ref_run(int32_t cout, int32_t cin, int32_t k,
-                   const int32_t *row_ptr, const int32_t *col_idx,
-                   const float *values, const float *bias, int32_t act,
-                   const void *x, int32_t x_f16, int64_t n, int64_t hw,
-                   double *y, double *scale)
+/* The 1x1 stage.  x_kind: 0 float, 1 binary16 bits, 2 double.  xs (may be
+ * NULL): a per-input-element error scale of x itself, added to the output
+ * scale as |W[r, c]| * xs[n, c, p] (used when x is the exact output of an
+ * earlier stage that the GPU evaluates in fp32). */
+static int ref_spmm(int32_t cout, int32_t cin, int32_t k,
+                    const int32_t *row_ptr, const int32_t *col_idx,
+                    const float *values, const float *bias, int32_t act,
+                    const void *x, int32_t x_kind, const double *xs, int64_t n, int64_t hw,
+                    double *y, double *scale)
 {
     const int32_t rows = cout / k;
     int bad = 0;
@@ -108,12 +115,14 @@ int spconv_ref_run(int32_t cout, int32_t cin, int32_t k,
                         const double wv = (double)values[(int64_t)t * k + i];
                         const int64_t xrow = (img * cin + c) * hw;
                         for (int64_t p = 0; p < hw; ++p) {
-                            const double xv = x_f16
-                                ? spconv_ref_half_to_double(((const uint16_t *)x)[xrow + p])
+                            const double xv = x_kind == 2 ? ((const double *)x)[xrow + p]
+                                : x_kind == 1 ? spconv_ref_half_to_double(((const uint16_t *)x)[xrow + p])
                                 : (double)((const float *)x)[xrow + p];
                             const double prod = wv * xv;
                             acc[p] += prod;
                             s[p] += fabs(prod);
+                            if (xs)
+                                s[p] += fabs(wv) * xs[xrow + p];
                         }
                     }
                     const double b = bias ? (double)bias[r] : 0.0;
@@ -133,6 +142,79 @@ int spconv_ref_run(int32_t cout, int32_t cin, int32_t k,
     }
     if (nomem)
         return -2;
+    return 0;
+}
+
+int spconv_ref_run(int32_t cout, int32_t cin, int32_t k,
+                   const int32_t *row_ptr, const int32_t *col_idx,
+                   const float *values, const float *bias, int32_t act,
+                   const void *x, int32_t x_f16, int64_t n, int64_t hw,
+                   double *y, double *scale)
+{
+    return ref_spmm(cout, cin, k, row_ptr, col_idx, values, bias, act, x, x_f16 ? 1 : 0, NULL, n, hw, y,
+                    scale);
+}
+
+/* The 1x1 stage over a double-precision input x with its own error scale xs
+ * (both [n][cin][hw]); the output scale is sum |W * x| + |W| * xs. */
+int spconv_ref_run_f64(int32_t cout, int32_t cin, int32_t k,
+                       const int32_t *row_ptr, const int32_t *col_idx,
+                       const float *values, const float *bias, int32_t act,
+                       const double *x, const double *xs, int64_t n, int64_t hw,
+                       double *y, double *scale)
+{
+    return ref_spmm(cout, cin, k, row_ptr, col_idx, values, bias, act, x, 2, xs, n, hw, y, scale);
+}
+
+/*
+ * Depthwise 3x3 convolution with zero padding 1 and stride s over CHW images
+ * (the MobileNet block: a depthwise convolution per channel, then the 1x1;
+ * paper Sec. 2 and Sec. 3.3), evaluated in double:
+ *
+ *   D[n, c, oy, ox] = act( b[c] + sum_{dy, dx in 0..2} K[c, dy, dx] * X[n, c, s*oy + dy - 1, s*ox + dx - 1] )
+ *
+ * with X taken as zero outside the image; output size ho = (h - 1) / s + 1,
+ * wo = (w - 1) / s + 1.  x: float [n][c][h][w]; k: float [c][3][3];
+ * bias: [c] or NULL.  d: [n][c][ho][wo]; sd (may be NULL): the scale
+ * |b[c]| + sum |K * X| of each output.  Returns 0, or -1 for a bad stride.
+ */
+int spconv_ref_dw3x3(int64_t n, int32_t c, int32_t h, int32_t w, int32_t stride,
+                     const float *x, const float *k, const float *bias, int32_t act,
+                     double *d, double *sd)
+{
+    if (stride < 1)
+        return -1;
+    const int64_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t img = 0; img < n; ++img) {
+        for (int32_t ch = 0; ch < c; ++ch) {
+            const float *xc = x + (img * c + ch) * (int64_t)h * w;
+            const float *kc = k + (int64_t)ch * 9;
+            const double b = bias ? (double)bias[ch] : 0.0;
+            for (int64_t oy = 0; oy < ho; ++oy) {
+                for (int64_t ox = 0; ox < wo; ++ox) {
+                    double acc = 0.0, s = 0.0;
+                    for (int dy = 0; dy < 3; ++dy) {
+                        const int64_t iy = oy * stride + dy - 1;
+                        if (iy < 0 || iy >= h)
+                            continue;
+                        for (int dx = 0; dx < 3; ++dx) {
+                            const int64_t ix = ox * stride + dx - 1;
+                            if (ix < 0 || ix >= w)
+                                continue;
+                            const double prod = (double)kc[dy * 3 + dx] * (double)xc[iy * w + ix];
+                            acc += prod;
+                            s += fabs(prod);
+                        }
+                    }
+                    const int64_t o = ((img * c + ch) * ho + oy) * wo + ox;
+                    d[o] = apply_act(acc + b, act);
+                    if (sd)
+                        sd[o] = s + fabs(b);
+                }
+            }
+        }
+    }
     return 0;
 }
 

@@ -34,6 +34,13 @@ MUTANTS = {
     "half_exponent_bias": ("expo - 25", "expo - 24"),
     "half_implicit_bit": ("(frac | 0x400)", "frac"),
     "half_subnormal_scale": ("ldexp((double)frac, -24)", "ldexp((double)frac, -25)"),
+    "dw_tap_row_offset": ("oy * stride + dy - 1", "oy * stride + dy"),
+    "dw_column_stride": ("ox * stride + dx - 1", "ox + dx - 1"),
+    "dw_bias_dropped": ("d[o] = apply_act(acc + b, act);", "d[o] = apply_act(acc, act);"),
+    "dw_kernel_transposed": ("kc[dy * 3 + dx]", "kc[dx * 3 + dy]"),
+    "dw_scale_signed": ("            s += fabs(prod);", "            s += prod;"),
+    "dw_border_taps_kept": ("if (ix < 0 || ix >= w)", "if (ix < 0 || ix > w)"),
+    "input_scale_dropped": ("s[p] += fabs(wv) * xs[xrow + p];", "s[p] += 0.0;"),
 }
 
 
@@ -69,12 +76,48 @@ def _battery(lib):
             failed.append("brute:k%d:%s" % (k, storage))
         if not np.allclose(s.reshape(sref.shape), sref, rtol=1e-12, atol=0):
             failed.append("brute-scale:k%d:%s" % (k, storage))
+    failed += _dw_battery(lib)
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     ref = bits.view(np.float16).astype(np.float64)
     got = np.array([lib.spconv_ref_half_to_double(int(b)) for b in bits])
     ok = ~np.isnan(ref)
     if not np.array_equal(got[ok], ref[ok]):
         failed.append("half-decoder")
+    return failed
+
+
+def _dw_battery(lib):
+    """Pins of the depthwise stage and the fused path: torch's grouped conv2d in
+    fp64 (an independent library routine) for the outputs and, on absolute
+    values, for the scale; the fused output against densified W applied to it."""
+    import torch
+    failed = []
+    rng = np.random.default_rng(5)
+    for stride, (h, w) in ((1, (5, 6)), (2, (7, 5)), (2, (6, 6))):
+        x = rng.standard_normal((2, 4, h, w)).astype(np.float32)
+        k = rng.standard_normal((4, 3, 3)).astype(np.float32)
+        b = rng.standard_normal(4).astype(np.float32)
+        d, sd = oracle.dw3x3_ref(x, k, b, "none", stride, lib=lib)
+        conv = lambda xx, kk, bb: torch.nn.functional.conv2d(  # noqa: E731
+            torch.from_numpy(xx).double(), torch.from_numpy(kk).double()[:, None],
+            None if bb is None else torch.from_numpy(bb).double(), stride=stride, padding=1, groups=4).numpy()
+        ref = conv(x, k, b)
+        sref = conv(np.abs(x), np.abs(k), np.abs(b))
+        if d.shape != ref.shape or not np.all(np.abs(d - ref) <= 1e-12 * (sref + 1.0)):
+            failed.append("dw:s%d" % stride)
+        elif not np.allclose(sd, sref, rtol=1e-12, atol=0):
+            failed.append("dw-scale:s%d" % stride)
+        layer = make_layer(4, 8, 1, 1, 1, 0.5, block_rows=2, act="relu", seed=stride, with_x=False)
+        _, y64, s = oracle.fused_ref(8, 4, 2, layer.row_ptr, layer.col_idx, layer.values, layer.bias, "relu",
+                                     x, k, b, "none", stride, lib=lib)
+        wd = densify(8, 4, 2, layer.row_ptr, layer.col_idx, layer.values)
+        d2 = ref.reshape(2, 4, -1)
+        yref = _act(np.matmul(wd[None], d2) + layer.bias.astype(np.float64)[None, :, None], "relu")
+        syref = np.matmul(np.abs(wd)[None], np.abs(d2)) + np.matmul(np.abs(wd)[None], sref.reshape(2, 4, -1))
+        if not np.all(np.abs(y64.reshape(yref.shape) - yref) <= 1e-12 * (syref + 1.0)):
+            failed.append("fused:s%d" % stride)
+        elif not np.allclose(s.reshape(syref.shape), syref, rtol=1e-12, atol=1e-300):
+            failed.append("fused-scale:s%d" % stride)
     return failed
 
 
