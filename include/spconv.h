@@ -84,7 +84,9 @@ spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, in
                                  spconv_dtype storage);
 
 /*
- * Run the plan:  y = act(W x + b)  on NCHW tensors of the plan's storage type.
+ * Run the plan:  y = act(W x + b)  on NCHW tensors of the plan's storage type
+ * (for a plan with a depthwise stage, see spconv_plan_create_fused: x is that
+ * stage's input and y is n x cout x out_h x out_w).
  *
  *   x       device, n * cin * h * w elements, NCHW contiguous
  *   y       device, n * cout * h * w elements, NCHW contiguous; must not overlap x
@@ -206,6 +208,46 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
                                     const float *values, const float *bias, spconv_act act,
                                     spconv_dtype storage, const spconv_options *opts);
 
+/* ---------------------------------------------------------------------------
+ * Fused depthwise 3x3 -> sparse 1x1.  A MobileNet block runs a depthwise 3x3
+ * convolution (one 3x3 filter per channel) right before each 1x1 (Sec. 2;
+ * Sec. 3.3 lists the CHW depthwise kernels beside the sparse 1x1).  A fused
+ * plan computes both in one launch, keeping the depthwise output on chip:
+ *
+ *     D[n, c, oy, ox] = dw_act( dw_bias[c] + sum_{dy, dx in 0..2} dw_weights[c][dy][dx]
+ *                                  * X[n, c, s*oy + dy - 1, s*ox + dx - 1] )
+ *     Y[n, r, p]      = act( b[r] + sum_{stored (r, c)} W[r, c] * D[n, c, p] )
+ *
+ * with zero padding 1 (X reads outside the image give 0) and stride s, so an
+ * h x w input gives an out_h x out_w output, out_h = (h - 1) / s + 1,
+ * out_w = (w - 1) / s + 1.  D is evaluated in fp32 (fma in dy, dx order, then
+ * the bias, then dw_act) and is never written to memory.
+ * ------------------------------------------------------------------------- */
+
+/*
+ * As spconv_plan_create_ex, with a depthwise stage in front:
+ *   dw_weights  host, cin * 9 floats, [c][dy][dx]; must be finite
+ *   dw_bias     host, cin floats, or NULL for zeros; must be finite
+ *   dw_act      activation of the depthwise stage
+ *   dw_stride   1 or 2
+ *   storage     SPCONV_F32 only
+ *   opts        as for spconv_plan_create_ex; the plan always uses the
+ *               LDS-strip kernel with one bundle per accumulator set, so
+ *               kernel = 2, pipe_sets and regions are refused
+ * spconv_run on the plan takes x = the depthwise input (n x cin x h x w) and
+ * writes y = n x cout x out_h x out_w.
+ * Errors: as spconv_plan_create_ex; SPCONV_E_ARG (dw_stride not 1 or 2, NULL
+ * dw_weights, bad dw_act), SPCONV_E_FORMAT (a non-finite depthwise weight or
+ * bias), SPCONV_E_UNSUPPORTED (SPCONV_F16 storage, kernel = 2, pipe_sets or
+ * regions set, or a strip of cin channels that does not fit in LDS).
+ */
+spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                       const int32_t *row_ptr, const int32_t *col_idx,
+                                       const float *values, const float *bias, spconv_act act,
+                                       const float *dw_weights, const float *dw_bias, spconv_act dw_act,
+                                       int32_t dw_stride, spconv_dtype storage,
+                                       const spconv_options *opts);
+
 typedef struct {
     int32_t cout, cin, block_rows;
     int32_t storage, act;
@@ -217,13 +259,16 @@ typedef struct {
     int32_t waves;         /* wavefronts per workgroup */
     int32_t lds_bytes;     /* LDS per workgroup */
     int32_t max_parts;     /* most workgroups that may share the rows of one tile */
-    int32_t pipe_sets;     /* bundles a wavefront interleaves (0 for the direct-load kernel) */
-    int32_t regions;       /* strip parts refilled independently (0 for the direct-load kernel) */
+    int32_t pipe_sets;     /* bundles a wavefront interleaves (0: direct-load kernel or depthwise stage) */
+    int32_t regions;       /* strip parts refilled independently (0: direct-load kernel or depthwise
+                              stage) */
     int64_t nnzb;          /* stored blocks */
     int64_t slots;         /* packed (channel, weight) slots including padding */
     int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
     int64_t sum_wave_cost; /* total of the per-wavefront work estimates */
     int64_t device_bytes;  /* device memory the plan holds */
+    int32_t dw_stride;     /* fused depthwise stage: 0 none, else its stride */
+    int32_t dw_act;        /* its activation */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */
@@ -245,7 +290,7 @@ spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *co
  * accumulator set and last-step bits pick the bundle, and every strip channel
  * read must fall between the need and release events of its strip part.
  * Host only.  SPCONV_E_FORMAT (message set) when the streams are inconsistent
- * or the plan uses the direct-load kernel, which has none.
+ * or the plan has none (direct-load kernel, depthwise stage).
  */
 spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
                                              float *values);

@@ -3,7 +3,7 @@
 The work happens in ``libspconv.so`` (C ABI in include/spconv.h): a host
 planner packs CSR / 1x2 / 1x4 block-CSR weights (or converts dense masked
 ones), and hand-written gfx950 HIP kernels compute act(W X + b) on NCHW fp32
-or fp16 tensors.  This package is
+or fp16 tensors, optionally with a depthwise 3x3 stage fused in front.  This package is
 the thin Python binding plus the in-tree build script.
 """
 
@@ -18,6 +18,7 @@ from .spconv import (  # noqa: F401
     spconv_options_init,
     spconv_plan_create,
     spconv_plan_create_dense,
+    spconv_plan_create_fused,
     spconv_plan_get_info,
     spconv_plan_unpack,
     spconv_plan_unpack_interleaved,

@@ -32,6 +32,8 @@ struct DevicePlan {
     int32_t blocks_per_cu = 0;  // resident workgroups per CU
     int32_t nbundles = 0;
     int32_t max_parts = 1;      // most workgroups that may share one tile
+    int32_t dw_stride = 0;      // fused depthwise 3x3 stage: 0 none, else its stride
+    int32_t dw_act = 0;
     const int32_t *idx = nullptr;
     const float *val = nullptr;
     const int32_t *hdr = nullptr;       // (first step, steps) per bundle
@@ -43,17 +45,21 @@ struct DevicePlan {
     const uint32_t *psel = nullptr;
     const int32_t *sel_ptr = nullptr;
     const int32_t *wave_ev = nullptr;
+    const float *dw = nullptr;          // depthwise taps and biases, kDwParams per strip channel
 };
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when
 // needed and record num_cus and blocks_per_cu.
 hipError_t prepare_launch(DevicePlan &p);
 
-// Queue one launch computing all m = N * hw columns.  `vec` != 0 promises
-// that hw is a multiple of the columns in one 16-byte vector and that x and y
-// are 16-byte aligned, enabling 16-byte loads and stores.  `x_bytes` and
-// `y_bytes` are the sizes of x and y.
+// Queue one launch computing all m = N * hw output columns.  `vec` != 0
+// promises that hw is a multiple of the columns in one 16-byte vector and
+// that x and y are 16-byte aligned, enabling 16-byte loads and stores.
+// `x_bytes` and `y_bytes` are the sizes of x and y.  With a depthwise stage,
+// x is N x cin x in_h x in_w and hw = out_h * out_w (out_w given); otherwise
+// in_h, in_w and out_w are ignored.
 hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, int32_t hw, int32_t vec,
-                       int64_t x_bytes, int64_t y_bytes, hipStream_t stream);
+                       int64_t x_bytes, int64_t y_bytes, int32_t in_h, int32_t in_w, int32_t out_w,
+                       hipStream_t stream);
 
 }  // namespace spconv

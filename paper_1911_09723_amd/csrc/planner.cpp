@@ -451,6 +451,51 @@ void build_interleaved(PackedPlan &p) {
 
 }  // namespace
 
+// The fused depthwise stage's arguments: fp32 storage, the strip kernel,
+// stride 1 or 2, finite taps and biases.
+Status validate_depthwise(const Input &in, const Options &opt, std::string &err) {
+    if (in.dw_stride == 0)
+        return OK;
+    if (in.dw_stride != 1 && in.dw_stride != 2) {
+        err = "dw_stride must be 1 or 2 (got " + std::to_string(in.dw_stride) + ")";
+        return E_ARG;
+    }
+    if (!in.dw_weights) {
+        err = "dw_weights is NULL";
+        return E_ARG;
+    }
+    if (in.dw_act < 0 || in.dw_act > 2) {
+        err = "dw_act must be SPCONV_ACT_NONE, _RELU or _RELU6";
+        return E_ARG;
+    }
+    if (in.storage != 0) {
+        err = "the fused depthwise stage supports fp32 storage only";
+        return E_UNSUPPORTED;
+    }
+    if (opt.kernel == 2) {
+        err = "the fused depthwise stage needs the LDS-strip kernel (kernel = 2 was requested)";
+        return E_UNSUPPORTED;
+    }
+    if (opt.pipe_sets || opt.regions) {
+        err = "pipe_sets and regions select the pipelined kernel, which has no depthwise stage";
+        return E_UNSUPPORTED;
+    }
+    for (int64_t i = 0; i < static_cast<int64_t>(in.cin) * 9; ++i) {
+        if (!std::isfinite(in.dw_weights[i])) {
+            err = "dw_weights[" + std::to_string(i / 9) + "][" + std::to_string(i % 9 / 3) + "][" +
+                  std::to_string(i % 3) + "] is not finite";
+            return E_FORMAT;
+        }
+    }
+    for (int32_t c = 0; in.dw_bias && c < in.cin; ++c) {
+        if (!std::isfinite(in.dw_bias[c])) {
+            err = "dw_bias[" + std::to_string(c) + "] is not finite";
+            return E_FORMAT;
+        }
+    }
+    return OK;
+}
+
 Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::string &err) {
     Status st = validate(in, err);
     if (st != OK)
@@ -479,6 +524,9 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         err = "regions must be in [0, " + std::to_string(kMaxRegions) + "]";
         return E_ARG;
     }
+    st = validate_depthwise(in, opt, err);
+    if (st != OK)
+        return st;
 
     p = PackedPlan();
     p.cout = in.cout;
@@ -489,6 +537,23 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     st = choose_geometry(in, opt, p, err);
     if (st != OK)
         return st;
+    if (in.dw_stride) {
+        if (p.kernel != KERNEL_STRIP) {
+            err = "the fused depthwise stage needs the LDS-strip kernel, and the strip of cin = " +
+                  std::to_string(in.cin) + " channels does not fit in LDS";
+            return E_UNSUPPORTED;
+        }
+        p.dw_stride = in.dw_stride;
+        p.dw_act = in.dw_act;
+        p.pipe_sets = 0;
+        p.regions = 0;
+        p.dw.assign(static_cast<size_t>(p.strip_rows) * kDwParams, 0.0f);
+        for (int32_t c = 0; c < in.cin; ++c) {
+            for (int32_t t = 0; t < 9; ++t)
+                p.dw[static_cast<size_t>(c) * kDwParams + t] = in.dw_weights[static_cast<size_t>(c) * 9 + t];
+            p.dw[static_cast<size_t>(c) * kDwParams + 9] = in.dw_bias ? in.dw_bias[c] : 0.0f;
+        }
+    }
 
     const int32_t k = in.block_rows;
     const int32_t rows = in.cout / k;
@@ -598,8 +663,9 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         p.max_parts *= 2;
 
     // 5. interleaved streams for the pipelined strip kernel: two accumulator
-    // sets when both fit in the automatic accumulator budget
-    if (p.kernel == KERNEL_STRIP) {
+    // sets when both fit in the automatic accumulator budget (a plan with a
+    // depthwise stage runs the simple loop and needs none)
+    if (p.kernel == KERNEL_STRIP && !p.dw_stride) {
         const int32_t acc = k * (p.cols_per_lane);
         const int32_t max_sets = 2 * acc <= kAutoAccumulators ? 2 : 1;
         if (opt.pipe_sets > max_sets) {
@@ -656,7 +722,7 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
 Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values,
                           std::string &err) {
     if (p.kernel != KERNEL_STRIP || p.pidx.size() != p.idx.size()) {
-        err = "the plan has no interleaved streams (direct kernel)";
+        err = "the plan has no interleaved streams (direct kernel or depthwise stage)";
         return E_FORMAT;
     }
     const int32_t k = p.k, NB = p.bundle_rows, S = p.pipe_sets;

@@ -103,6 +103,8 @@ constexpr int32_t kCtlBytes = 8 * kMaxRegions;
 constexpr int32_t kSelSteps = 16;
 // Events per wavefront in wave_ev.
 constexpr int32_t kWaveEvents = 2 * kMaxRegions;
+// Floats per channel of a fused depthwise stage's parameters (9 taps, bias, padding to 64 bytes).
+constexpr int32_t kDwParams = 16;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -112,6 +114,15 @@ struct Input {
     const float *bias = nullptr;
     int32_t act = 0;      // 0 none, 1 relu, 2 relu6
     int32_t storage = 0;  // 0 fp32, 1 fp16
+    // Optional depthwise 3x3 stage run on the input first (the MobileNet block
+    // order, Sec. 2; the library's CHW depthwise kernels, Sec. 3.3):
+    //   D[n, c, oy, ox] = dw_act(dw_bias[c] + sum_{dy, dx} dw_weights[c][dy][dx]
+    //                               * X[n, c, s*oy + dy - 1, s*ox + dx - 1])
+    // with zero padding 1 and stride s = dw_stride; the 1x1 then reads D.
+    int32_t dw_stride = 0;               // 0: no depthwise stage; else 1 or 2
+    const float *dw_weights = nullptr;   // [cin][3][3]
+    const float *dw_bias = nullptr;      // [cin] or null for zeros
+    int32_t dw_act = 0;
 };
 
 struct Options {
@@ -142,6 +153,10 @@ struct PackedPlan {
     int32_t regions = 1;         // strip parts refilled independently (strip kernel)
     int32_t region_rows = 0;     // channels per part, a multiple of 4
     int32_t max_parts = 1;       // most workgroups that may share one tile
+    // fused depthwise 3x3 stage (Input::dw_stride); such a plan runs the simple
+    // strip loop, which computes each strip from the input instead of copying it
+    int32_t dw_stride = 0, dw_act = 0;
+    std::vector<float> dw;  // [strip_rows][kDwParams]: the 9 taps (dy-major), then the bias; 0 past cin
     // packed streams
     std::vector<int32_t> idx;
     std::vector<float> val;

@@ -78,7 +78,7 @@ spconv_status upload(spconv_plan_s *pl) {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[11] = {
+    } parts[12] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
@@ -90,6 +90,7 @@ spconv_status upload(spconv_plan_s *pl) {
         {h.psel.data(), h.psel.size() * sizeof(uint32_t), 0},
         {h.sel_ptr.data(), h.sel_ptr.size() * sizeof(int32_t), 0},
         {h.wave_ev.data(), h.wave_ev.size() * sizeof(int32_t), 0},
+        {h.dw.data(), h.dw.size() * sizeof(float), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -131,6 +132,7 @@ spconv_status upload(spconv_plan_s *pl) {
     d.psel = reinterpret_cast<const uint32_t *>(base + parts[8].off);
     d.sel_ptr = reinterpret_cast<const int32_t *>(base + parts[9].off);
     d.wave_ev = reinterpret_cast<const int32_t *>(base + parts[10].off);
+    d.dw = reinterpret_cast<const float *>(base + parts[11].off);
     return SPCONV_OK;
 }
 
@@ -156,6 +158,8 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
     d.nbundles = h.nbundles();
     d.max_parts = h.max_parts;
+    d.dw_stride = h.dw_stride;
+    d.dw_act = h.dw_act;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -163,23 +167,8 @@ bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) 
     return a0 < b0 + bbytes && b0 < a0 + abytes;
 }
 
-}  // namespace
-
-extern "C" {
-
-void spconv_options_init(spconv_options *opts) {
-    if (!opts)
-        return;
-    std::memset(opts, 0, sizeof(*opts));
-    opts->struct_size = static_cast<int32_t>(sizeof(spconv_options));
-    opts->reorder = 1;
-}
-
-spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
-                                    const int32_t *row_ptr, const int32_t *col_idx, const float *values,
-                                    const float *bias, spconv_act act, spconv_dtype storage,
-                                    const spconv_options *opts) {
-    g_err.clear();
+// Plan creation shared by every entry point: options, planning, upload.
+spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spconv_options *opts) {
     if (!out)
         return fail(SPCONV_E_ARG, "out is NULL");
     *out = nullptr;
@@ -207,8 +196,7 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     std::string err;
     spconv::Status st;
     try {
-        st = spconv::build_plan(make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage),
-                                po, pl->host, err);
+        st = spconv::build_plan(in, po, pl->host, err);
     } catch (const std::bad_alloc &) {
         delete pl;
         return fail(SPCONV_E_NOMEM, "host allocation failed while packing the plan");
@@ -235,6 +223,45 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
     }
     *out = pl;
     return SPCONV_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+void spconv_options_init(spconv_options *opts) {
+    if (!opts)
+        return;
+    std::memset(opts, 0, sizeof(*opts));
+    opts->struct_size = static_cast<int32_t>(sizeof(spconv_options));
+    opts->reorder = 1;
+}
+
+spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                    const int32_t *row_ptr, const int32_t *col_idx, const float *values,
+                                    const float *bias, spconv_act act, spconv_dtype storage,
+                                    const spconv_options *opts) {
+    g_err.clear();
+    return create_plan(out, make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage), opts);
+}
+
+spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                       const int32_t *row_ptr, const int32_t *col_idx, const float *values,
+                                       const float *bias, spconv_act act, const float *dw_weights,
+                                       const float *dw_bias, spconv_act dw_act, int32_t dw_stride,
+                                       spconv_dtype storage, const spconv_options *opts) {
+    g_err.clear();
+    spconv::Input in = make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage);
+    if (dw_stride != 1 && dw_stride != 2) {
+        if (out)
+            *out = nullptr;
+        return fail(SPCONV_E_ARG, "dw_stride must be 1 or 2 (got " + std::to_string(dw_stride) + ")");
+    }
+    in.dw_stride = dw_stride;
+    in.dw_weights = dw_weights;
+    in.dw_bias = dw_bias;
+    in.dw_act = static_cast<int32_t>(dw_act);
+    return create_plan(out, in, opts);
 }
 
 spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
@@ -317,17 +344,21 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
         return fail(SPCONV_E_ARG, "n, h and w must be >= 0");
     if (plan->host_only)
         return fail(SPCONV_E_ARG, "plan was created with host_only = 1 and has no device data");
-    const int64_t hw = static_cast<int64_t>(h) * w;
+    const spconv::PackedPlan &p = plan->host;
+    // a depthwise stage maps the h x w input to out_h x out_w (zero padding 1)
+    const int32_t s = p.dw_stride ? p.dw_stride : 1;
+    const int64_t oh = p.dw_stride ? (h > 0 ? (h - 1) / s + 1 : 0) : h;
+    const int64_t ow = p.dw_stride ? (w > 0 ? (w - 1) / s + 1 : 0) : w;
+    const int64_t hw = oh * ow, ihw = static_cast<int64_t>(h) * w;
     const int64_t m = static_cast<int64_t>(n) * hw;
     if (m == 0)
         return SPCONV_OK;
     if (!x || !y)
         return fail(SPCONV_E_ARG, "x or y is NULL");
-    if (hw > INT32_MAX || m > INT32_MAX)
+    if (ihw > INT32_MAX || static_cast<int64_t>(n) * ihw > INT32_MAX)
         return fail(SPCONV_E_SHAPE, "n * h * w must be below 2^31 columns");
-    const spconv::PackedPlan &p = plan->host;
     const size_t e = p.storage == 1 ? 2 : 4;
-    const int64_t xel = m * p.cin, yel = m * p.cout;
+    const int64_t xel = static_cast<int64_t>(n) * ihw * p.cin, yel = m * p.cout;
     if (xel > (int64_t(1) << 62) / 4 || yel > (int64_t(1) << 62) / 4)
         return fail(SPCONV_E_SHAPE, "tensor too large");
     if (reinterpret_cast<uintptr_t>(x) % e || reinterpret_cast<uintptr_t>(y) % e)
@@ -344,15 +375,15 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    // the kernels address X relative to the first image of a tile with 32-bit
-    // byte offsets: a tile's images must span less than 2^31 bytes
-    if ((static_cast<int64_t>(p.tile_cols) + hw) * std::max(p.cin, p.cout) * static_cast<int64_t>(e) >=
+    // the kernels address X and Y relative to the first image of a tile with
+    // 32-bit byte offsets: a tile's images must span less than 2^31 bytes
+    if ((static_cast<int64_t>(p.tile_cols) + ihw) * std::max(p.cin, p.cout) * static_cast<int64_t>(e) >=
         (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,
                     "h * w * channels too large: one tile's images must span less than 2^31 bytes");
     he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
-                             xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e),
-                             static_cast<hipStream_t>(stream));
+                             xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e), h, w,
+                             static_cast<int32_t>(ow), static_cast<hipStream_t>(stream));
     if (he != hipSuccess)
         return hip_fail("kernel launch", he);
     return SPCONV_OK;
@@ -400,6 +431,8 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->max_wave_cost = p.max_wave_cost;
     info->sum_wave_cost = p.sum_wave_cost;
     info->device_bytes = static_cast<int64_t>(plan->dbytes);
+    info->dw_stride = p.dw_stride;
+    info->dw_act = p.dw_act;
     return SPCONV_OK;
 }
 

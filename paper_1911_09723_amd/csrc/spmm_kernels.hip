@@ -127,6 +127,11 @@ struct Args {
     int32_t whole_tiles;  // tiles processed whole: a multiple of the grid
     int32_t tail_parts;   // workgroups sharing each remaining tile (a power of two)
     int32_t nxcd;         // workgroup i runs on XCD i % nxcd; the grid is a multiple of it
+    // fused depthwise stage (simple strip kernel, fp32): stride (0 = none), its
+    // activation, the input's height and width, the output width, and the
+    // taps and biases (kDwParams floats per strip channel)
+    int32_t dw_stride, dw_act, in_h, in_w, out_w;
+    const float *dw;
 };
 
 // A workgroup's unit of work: a tile, whole (part < 0) or one of tail_parts
@@ -529,9 +534,64 @@ __device__ __forceinline__ void load_strip_simple(const Args &a, const TileAddr<
     }
 }
 
+// The strip of a plan with a depthwise stage, computed instead of copied:
+// column j of strip row c is the depthwise output
+//     D[n, c, oy, ox] = act1(b1[c] + sum_{dy, dx} K[c][dy][dx] * X[n, c, s*oy + dy - 1, s*ox + dx - 1])
+// (zero padding 1, stride s) of output column j = (n, oy * out_w + ox).  The
+// taps are fp32 fma in dy, dx order from zero, then the bias, then the clamp.
+// Thread i computes vector i % 16 (4 columns) of row i / 16, so the 16 lanes
+// of a row read neighbouring X elements, mostly from L1 / L2: each input
+// element is read by up to 9 / s^2 output columns.  Rows past cin and columns
+// past the last one are zero.  The caller synchronizes.
+__device__ __forceinline__ void dw_strip(const Args &a, const float *__restrict__ x, unsigned char *lds,
+                                         int32_t tile, int tid, int nthreads) {
+    const float lo = a.dw_act == 0 ? -__builtin_huge_valf() : 0.0f;
+    const float hi = a.dw_act == 2 ? 6.0f : __builtin_huge_valf();
+    const int32_t s = a.dw_stride;
+    const int64_t ihw = static_cast<int64_t>(a.in_h) * a.in_w;
+    for (int i = tid; i < a.strip_rows * 16; i += nthreads) {
+        const int32_t row = i >> 4;
+        f4 v = {0.0f, 0.0f, 0.0f, 0.0f};
+        if (row < a.cin) {
+            const float *kp = a.dw + row * kDwParams;
+            float kw[10];
+#pragma unroll
+            for (int t = 0; t < 10; ++t)
+                kw[t] = kp[t];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int32_t c = tile * 64 + (i & 15) * 4 + e;
+                if (c < a.m) {
+                    const int32_t n = c / a.hw;
+                    const int32_t pp = c - n * a.hw;
+                    const int32_t oy = pp / a.out_w;
+                    const int32_t ox = pp - oy * a.out_w;
+                    const float *xc = x + (static_cast<int64_t>(n) * a.cin + row) * ihw;
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int dy = 0; dy < 3; ++dy) {
+                        const int32_t iy = oy * s + dy - 1;
+                        if (iy >= 0 && iy < a.in_h) {
+#pragma unroll
+                            for (int dx = 0; dx < 3; ++dx) {
+                                const int32_t ix = ox * s + dx - 1;
+                                if (ix >= 0 && ix < a.in_w)
+                                    acc = __builtin_fmaf(kw[dy * 3 + dx], xc[iy * a.in_w + ix], acc);
+                            }
+                        }
+                    }
+                    v[e] = fminf(fmaxf(acc + kw[9], lo), hi);
+                }
+            }
+        }
+        *reinterpret_cast<f4 *>(lds + i * 16) = v;
+    }
+}
+
 // ---------------------------------------------------------------------------
-// Simple kernel: for each work item, copy the strip (strip kernel), then every
-// wavefront runs its bundles; workgroup barriers around each strip.
+// Simple kernel: for each work item, copy the strip (strip kernel; computed by
+// the depthwise stage when the plan has one), then every wavefront runs its
+// bundles; workgroup barriers around each strip.
 // ---------------------------------------------------------------------------
 
 template <int G, int K, bool F16, bool DIRECT, bool VEC>
@@ -576,7 +636,16 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
     while (wk.tile >= 0) {
         ta.set(a, L, x, y, wk.tile);
         if constexpr (!DIRECT) {
-            load_strip_simple<G, F16, VEC>(a, ta, x, lds, lds_base, wk.tile, tid, blockDim.x, wave, nwaves, lane);
+            bool computed = false;
+            if constexpr (!F16) {
+                if (a.dw_stride) {
+                    dw_strip(a, x, lds, wk.tile, tid, blockDim.x);
+                    computed = true;
+                }
+            }
+            if (!computed)
+                load_strip_simple<G, F16, VEC>(a, ta, x, lds, lds_base, wk.tile, tid, blockDim.x, wave, nwaves,
+                                               lane);
             __syncthreads();  // strip ready
         }
         run_item<G, K, F16, DIRECT, VEC>(a, L, ta, x, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
@@ -939,7 +1008,8 @@ KernelFn pick_kv(const DevicePlan &p, bool vec) {
         return vec ? pick_g<K, F16, true, true>(p.group_lanes) : pick_g<K, F16, true, false>(p.group_lanes);
     // 1xk blocks keep the simple loop: their records take too many registers
     // for the pipelined kernel's fetch depth
-    if (vec && K == 1)
+    // (a depthwise stage computes the strip in the simple kernel)
+    if (vec && K == 1 && !p.dw_stride)
         return pick_pipe<K, F16>(p.group_lanes, p.pipe_sets);
     return vec ? pick_g<K, F16, false, true>(p.group_lanes) : pick_g<K, F16, false, false>(p.group_lanes);
 }
@@ -997,7 +1067,8 @@ hipError_t prepare_launch(DevicePlan &p) {
 }
 
 hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, int32_t hw, int32_t vec,
-                       int64_t x_bytes, int64_t y_bytes, hipStream_t stream) {
+                       int64_t x_bytes, int64_t y_bytes, int32_t in_h, int32_t in_w, int32_t out_w,
+                       hipStream_t stream) {
     KernelFn kern = pick(p, vec != 0);
     if (!kern)
         return hipErrorInvalidValue;
@@ -1038,6 +1109,12 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.whole_tiles = static_cast<int32_t>(whole);
     a.tail_parts = static_cast<int32_t>(parts);
     a.nxcd = static_cast<int32_t>(nxcd);
+    a.dw_stride = p.dw_stride;
+    a.dw_act = p.dw_act;
+    a.in_h = p.dw_stride ? in_h : 0;
+    a.in_w = p.dw_stride ? in_w : 0;
+    a.out_w = p.dw_stride ? out_w : 0;
+    a.dw = p.dw;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(slots)), dim3(p.waves * 64), p.lds_bytes, stream, x, y,
                        p.idx, p.val, p.hdr, p.table, p.rank, p.wave_ptr, p.pidx, p.pval, p.psel, p.sel_ptr,
                        p.wave_ev, a);

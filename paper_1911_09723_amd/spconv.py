@@ -29,7 +29,7 @@ _DTYPES = {"f32": F32, "f16": F16}
 EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error",
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
-            "spconv_plan_create_dense")
+            "spconv_plan_create_dense", "spconv_plan_create_fused")
 
 
 class SpconvError(RuntimeError):
@@ -53,7 +53,7 @@ class spconv_plan_info(ctypes.Structure):
                 ("max_parts", ctypes.c_int32), ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32),
                 ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
-                ("device_bytes", ctypes.c_int64)]
+                ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -97,6 +97,9 @@ def load_library(path: Optional[str] = None):
     lib.spconv_dense_to_bcsr.argtypes = [i32, i32, vp, i32, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
     lib.spconv_plan_create_dense.restype = i32
     lib.spconv_plan_create_dense.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, vp, i32, i32]
+    lib.spconv_plan_create_fused.restype = i32
+    lib.spconv_plan_create_fused.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
+                                             i32, i32, ctypes.POINTER(spconv_options)]
     if path is None:
         _lib = lib
     return lib
@@ -192,6 +195,31 @@ def spconv_plan_create_dense(dense, block_rows: int = 0, bias=None, act="none", 
     return out.value
 
 
+def spconv_plan_create_fused(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, dw_weights, dw_bias=None,
+                             dw_act="none", dw_stride=1, storage="f32", options: Optional[spconv_options] = None,
+                             check: bool = True):
+    """Create a plan for a depthwise 3x3 (weights [cin, 3, 3], zero padding 1,
+    stride ``dw_stride``) followed by the sparse 1x1.  Returns the handle."""
+    lib = load_library()
+    rp = _arr(row_ptr, np.int32)
+    ci = _arr(col_idx, np.int32)
+    va = _arr(values, np.float32)
+    bi = _arr(bias, np.float32)
+    kw = _arr(dw_weights, np.float32)
+    kb = _arr(dw_bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    da = _ACTS[dw_act] if isinstance(dw_act, str) else int(dw_act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    status = lib.spconv_plan_create_fused(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp), _ptr(ci),
+                                          _ptr(va), _ptr(bi), a, _ptr(kw), _ptr(kb), da, int(dw_stride), st,
+                                          ctypes.byref(options) if options is not None else None)
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
+
+
 def _devptr(t):
     if t is None:
         return None
@@ -259,15 +287,37 @@ class Plan:
                 setattr(opts, k, int(v))
         self.handle = spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage,
                                          options=opts)
-        self.cout, self.cin, self.storage = int(cout), int(cin), storage
+        self.cout, self.cin, self.storage, self.dw_stride = int(cout), int(cin), storage, 0
 
     @classmethod
     def from_dense(cls, dense, block_rows: int = 0, bias=None, act="none", storage="f32"):
         """Plan for a dense masked [Cout, Cin] weight (block_rows 0 = detect the block height)."""
         self = cls.__new__(cls)
         self.handle = spconv_plan_create_dense(dense, block_rows, bias, act, storage)
-        self.cout, self.cin, self.storage = int(dense.shape[0]), int(dense.shape[1]), storage
+        self.cout, self.cin, self.storage, self.dw_stride = int(dense.shape[0]), int(dense.shape[1]), storage, 0
         return self
+
+    @classmethod
+    def fused(cls, cout, cin, block_rows, row_ptr, col_idx, values, bias, act, dw_weights, dw_bias=None,
+              dw_act="none", dw_stride=1, **options):
+        """Plan for depthwise 3x3 (stride ``dw_stride``, zero padding 1) -> sparse 1x1, fp32."""
+        self = cls.__new__(cls)
+        opts = None
+        if options:
+            opts = spconv_options_init()
+            for k, v in options.items():
+                setattr(opts, k, int(v))
+        self.handle = spconv_plan_create_fused(cout, cin, block_rows, row_ptr, col_idx, values, bias, act,
+                                               dw_weights, dw_bias, dw_act, dw_stride, options=opts)
+        self.cout, self.cin, self.storage, self.dw_stride = int(cout), int(cin), "f32", int(dw_stride)
+        return self
+
+    def out_hw(self, h, w):
+        """Output spatial size for an h x w input."""
+        if not self.dw_stride:
+            return h, w
+        s = self.dw_stride
+        return ((h - 1) // s + 1 if h > 0 else 0), ((w - 1) // s + 1 if w > 0 else 0)
 
     @classmethod
     def from_layer(cls, layer, **options):
@@ -283,7 +333,7 @@ class Plan:
         if c != self.cin:
             raise ValueError("x has %d channels, plan expects %d" % (c, self.cin))
         if y is None:
-            y = torch.empty((n, self.cout, h, w), dtype=x.dtype, device=x.device)
+            y = torch.empty((n, self.cout) + self.out_hw(h, w), dtype=x.dtype, device=x.device)
         spconv_run(self.handle, x, y, n, h, w, stream)
         return y
 

@@ -6,12 +6,13 @@ oracle (``oracle/``) and the GPU library (``paper_1911_09723_amd``) can be
 fed from it without sharing any computation.
 """
 
-from .layers import Layer, make_layer, densify, expand_blocks_to_csr
+from .layers import Layer, make_layer, make_depthwise, densify, expand_blocks_to_csr
 from .configs import CONFIGS, config_layers, layer_seed, TARGET
 
 __all__ = [
     "Layer",
     "make_layer",
+    "make_depthwise",
     "densify",
     "expand_blocks_to_csr",
     "CONFIGS",

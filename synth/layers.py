@@ -214,3 +214,14 @@ def expand_blocks_to_csr(cout: int, block_rows: int, row_ptr, col_idx, values):
             rp.append(len(cols))
     return (np.asarray(rp, dtype=np.int32), np.asarray(cols, dtype=np.int32),
             np.asarray(vals, dtype=np.float32))
+
+
+def make_depthwise(cin: int, seed: int):
+    """Seeded depthwise 3x3 weights [cin, 3, 3] and biases [cin] for the stage
+    that precedes a 1x1 in a MobileNet block (Sec. 2): taps ~ N(0, variance
+    2 / 9) (fan-in 9), bias ~ N(0, variance 0.01), from
+    ``numpy.random.Generator(PCG64(seed))``."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    k = (rng.standard_normal((cin, 3, 3)) * np.sqrt(2.0 / 9.0)).astype(np.float32)
+    b = (rng.standard_normal(cin) * 0.1).astype(np.float32)
+    return k, b

@@ -54,3 +54,33 @@ def assert_parity(layer, y_gpu, x=None, what=""):
     assert bad == 0, "%s: %d of %d elements outside tolerance (worst error/tolerance %.3g)" % (
         what, bad, ratio.size, worst)
     return worst
+
+
+def gpu_run_fused(layer, dw_k, dw_b, dw_act, stride, x=None, **options):
+    """Run a fused depthwise 3x3 -> sparse 1x1 plan on layer.x (the depthwise input)."""
+    import torch
+    x = layer.x if x is None else x
+    plan = Plan.fused(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
+                      layer.bias, layer.act, dw_k, dw_b, dw_act, stride, **options)
+    try:
+        yt = plan.run(to_gpu(x))
+        torch.cuda.synchronize()
+        return yt.cpu().numpy()
+    finally:
+        plan.close()
+
+
+def assert_fused_parity(layer, dw_k, dw_b, dw_act, stride, y_gpu, x=None, what=""):
+    """Element-wise check of a fused run against the oracle, tolerance
+    1e-5 * S + 1e-6 with S = sum |W * D| + |W| * SD (SD: the depthwise stage's
+    sum of absolute terms), which bounds the fp32 error of both stages."""
+    x = layer.x if x is None else x
+    y_ref, _, scale = oracle.fused_ref(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx,
+                                       layer.values, layer.bias, layer.act, x, dw_k, dw_b, dw_act, stride)
+    assert y_gpu.shape == y_ref.shape and y_gpu.dtype == y_ref.dtype, (y_gpu.shape, y_ref.shape)
+    tol = oracle.tolerance(y_ref, scale, "f32")
+    ratio = np.abs(y_gpu.astype(np.float64) - y_ref.astype(np.float64)) / tol
+    bad = int((ratio > 1).sum())
+    assert bad == 0, "%s: %d of %d elements outside tolerance (worst error/tolerance %.3g)" % (
+        what, bad, ratio.size, float(ratio.max()))
+    return float(ratio.max()) if ratio.size else 0.0
