@@ -8,6 +8,8 @@ sweep point is reported beside it.  Inputs are seeded synthetic tensors with
 the paper's layer shapes (no trained weights or images are used).
 
 One step = one spconv_run over the whole batch (bias and activation fused).
+A third variant runs the same 1x1 behind a fused depthwise 3x3 (stride 1,
+ReLU6): one MobileNet v1 block at 512 channels.
 Inputs are resident in HBM before timing starts; three (X, Y) buffer sets,
 616 MB in all, rotate so no step finds its operands in the 256 MB
 last-level cache.  Kernel durations come from HIP events recorded on the
@@ -85,16 +87,28 @@ def headline_layers():
     return out
 
 
-def time_variant(layer, steps, warmup, sets):
+def fused_layer(layer):
+    """The headline layer's 1x1 weights and input with a depthwise 3x3 stage
+    (stride 1, ReLU6) in front: one MobileNet v1 block at 512 channels."""
+    from synth import make_depthwise
+    kw, kb = make_depthwise(layer.cin, 2021)
+    return kw, kb
+
+
+def time_variant(layer, steps, warmup, sets, dw=None):
     import torch
     from paper_1911_09723_amd import Plan, spconv_run
 
     dev = torch.device("cuda:0")
-    plan = Plan.from_layer(layer)
+    if dw is None:
+        plan = Plan.from_layer(layer)
+    else:
+        plan = Plan.fused(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
+                          layer.bias, layer.act, dw[0], dw[1], "relu6", 1)
     n, c, h, w = layer.x.shape
     x0 = torch.from_numpy(layer.x).to(dev)
     xs = [x0] + [x0.clone() for _ in range(sets - 1)]
-    ys = [torch.empty((n, layer.cout, h, w), dtype=x0.dtype, device=dev) for _ in range(sets)]
+    ys = [torch.empty((n, layer.cout) + plan.out_hw(h, w), dtype=x0.dtype, device=dev) for _ in range(sets)]
     stream = torch.cuda.current_stream()
     for i in range(warmup):
         spconv_run(plan.handle, xs[i % sets], ys[i % sets], n, h, w, stream)
@@ -150,13 +164,19 @@ def cpu_baseline(layer, budget_s=12.0):
     }
 
 
-def summarize(layer, r):
+def summarize(layer, r, dw=False):
     import numpy as np
     steps = len(r["kernel_ms"])
     t_step = r["region_ms"] / steps / 1e3
     t_kern = float(np.mean(r["kernel_ms"])) / 1e3
     flops = layer.flops()
     b_alg = layer.alg_bytes()
+    if dw:
+        # stride 1: the depthwise input has the output's size, so X and Y
+        # traffic are as for the 1x1 alone; add the 3x3 taps (2 flops each)
+        # and the depthwise parameters
+        flops += 2.0 * 9 * layer.cin * layer.hw * layer.n
+        b_alg += 4.0 * 10 * layer.cin
     t_hbm = b_alg / (HBM_PEAK_GBS * 1e9)
     t_alu = flops / (FP32_VECTOR_PEAK_TFS * 1e12)
     t_roof = max(t_hbm, t_alu)
@@ -181,13 +201,21 @@ def summarize(layer, r):
 
 
 def profile_run(reps: int):
-    """A few launches of each variant, then the calibration copy (for rocprofv3)."""
+    """A few launches of each variant (the unstructured layer first), then the
+    calibration copy (for rocprofv3)."""
     import torch
     from paper_1911_09723_amd import Plan, spconv_run
 
     dev = torch.device("cuda:0")
-    for tag, layer in headline_layers().items():
-        plan = Plan.from_layer(layer)
+    layers = headline_layers()
+    runs = [(tag, layer, None) for tag, layer in layers.items()]
+    runs.append(("dw3x3+1x1", layers["1x1"], fused_layer(layers["1x1"])))
+    for tag, layer, dw in runs:
+        if dw is None:
+            plan = Plan.from_layer(layer)
+        else:
+            plan = Plan.fused(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
+                              layer.bias, layer.act, dw[0], dw[1], "relu6", 1)
         n, c, h, w = layer.x.shape
         x0 = torch.from_numpy(layer.x).to(dev)
         xs = [x0, x0.clone(), x0.clone()]  # the bench's three rotating buffer sets
@@ -308,6 +336,12 @@ def main():
         r = time_variant(layer, args.steps, args.warmup, args.sets)
         results[tag] = summarize(layer, r)
         log("bench: %s %s" % (tag, json.dumps(results[tag])))
+    # the same 1x1 behind a fused depthwise 3x3 (stride 1, ReLU6)
+    tag = "dw3x3+1x1"
+    log("bench: timing %s" % tag)
+    r = time_variant(layers["1x1"], args.steps, args.warmup, args.sets, dw=fused_layer(layers["1x1"]))
+    results[tag] = summarize(layers["1x1"], r, dw=True)
+    log("bench: %s %s" % (tag, json.dumps(results[tag])))
 
     head = results["1x1"]
     layer = layers["1x1"]

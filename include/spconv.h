@@ -103,8 +103,9 @@ spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, in
  *
  * Errors: SPCONV_E_ARG (NULL plan/x/y with work to do, negative sizes, overlap,
  * other device, host-only plan), SPCONV_E_SHAPE (sizes beyond 2^31 columns or
- * elements beyond 2^62), SPCONV_E_UNSUPPORTED ((tile columns + h * w) * cin
- * elements of one tile's images span 2^31 bytes or more), SPCONV_E_HIP
+ * elements beyond 2^62), SPCONV_E_UNSUPPORTED (the images one tile of output
+ * columns touches, ((tile columns - 1) / (out_h * out_w) + 2) of them, span
+ * 2^31 bytes or more of x or of y), SPCONV_E_HIP
  * (launch failure).  Faults during
  * execution surface at the caller's next synchronization.
  */

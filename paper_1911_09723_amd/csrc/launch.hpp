@@ -34,6 +34,8 @@ struct DevicePlan {
     int32_t max_parts = 1;      // most workgroups that may share one tile
     int32_t dw_stride = 0;      // fused depthwise 3x3 stage: 0 none, else its stride
     int32_t dw_act = 0;
+    int32_t stage_off = 0;      // LDS staging area of the depthwise stage's input windows
+    int32_t stage_bytes = 0;
     const int32_t *idx = nullptr;
     const float *val = nullptr;
     const int32_t *hdr = nullptr;       // (first step, steps) per bundle

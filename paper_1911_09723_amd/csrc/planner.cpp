@@ -547,6 +547,10 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
         p.dw_act = in.dw_act;
         p.pipe_sets = 0;
         p.regions = 0;
+        // every LDS byte left after the strip and the bundle table stages input windows
+        p.stage_off = p.lds_bytes - kCtlBytes;
+        p.lds_bytes = static_cast<int32_t>(kMaxLdsBytes);
+        p.stage_bytes = (p.lds_bytes - kCtlBytes - p.stage_off) & ~15;
         p.dw.assign(static_cast<size_t>(p.strip_rows) * kDwParams, 0.0f);
         for (int32_t c = 0; c < in.cin; ++c) {
             for (int32_t t = 0; t < 9; ++t)

@@ -156,6 +156,8 @@ struct PackedPlan {
     // fused depthwise 3x3 stage (Input::dw_stride); such a plan runs the simple
     // strip loop, which computes each strip from the input instead of copying it
     int32_t dw_stride = 0, dw_act = 0;
+    int32_t stage_off = 0;    // LDS [stage_off, stage_off + stage_bytes): the depthwise input windows
+    int32_t stage_bytes = 0;  // (all LDS left after the strip and the bundle table)
     std::vector<float> dw;  // [strip_rows][kDwParams]: the 9 taps (dy-major), then the bias; 0 past cin
     // packed streams
     std::vector<int32_t> idx;

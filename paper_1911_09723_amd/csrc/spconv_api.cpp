@@ -160,6 +160,8 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.max_parts = h.max_parts;
     d.dw_stride = h.dw_stride;
     d.dw_act = h.dw_act;
+    d.stage_off = h.stage_off;
+    d.stage_bytes = h.stage_bytes;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -376,11 +378,12 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
     // the kernels address X and Y relative to the first image of a tile with
-    // 32-bit byte offsets: a tile's images must span less than 2^31 bytes
-    if ((static_cast<int64_t>(p.tile_cols) + ihw) * std::max(p.cin, p.cout) * static_cast<int64_t>(e) >=
-        (int64_t(1) << 31) - 16)
+    // 32-bit byte offsets: the images one tile's columns touch (at most
+    // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
+    const int64_t span = (p.tile_cols - 1) / hw + 2;
+    if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,
-                    "h * w * channels too large: one tile's images must span less than 2^31 bytes");
+                    "h * w * channels too large: the images of one tile must span less than 2^31 bytes");
     he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
                              xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e), h, w,
                              static_cast<int32_t>(ow), static_cast<hipStream_t>(stream));

@@ -131,6 +131,7 @@ struct Args {
     // activation, the input's height and width, the output width, and the
     // taps and biases (kDwParams floats per strip channel)
     int32_t dw_stride, dw_act, in_h, in_w, out_w;
+    int32_t stage_off, stage_bytes;  // LDS staging area of its input windows
     const float *dw;
 };
 
@@ -539,53 +540,215 @@ __device__ __forceinline__ void load_strip_simple(const Args &a, const TileAddr<
 //     D[n, c, oy, ox] = act1(b1[c] + sum_{dy, dx} K[c][dy][dx] * X[n, c, s*oy + dy - 1, s*ox + dx - 1])
 // (zero padding 1, stride s) of output column j = (n, oy * out_w + ox).  The
 // taps are fp32 fma in dy, dx order from zero, then the bias, then the clamp.
-// Thread i computes vector i % 16 (4 columns) of row i / 16, so the 16 lanes
-// of a row read neighbouring X elements, mostly from L1 / L2: each input
-// element is read by up to 9 / s^2 output columns.  Rows past cin and columns
-// past the last one are zero.  The caller synchronizes.
+//
+// Lane j owns column j of the tile for every row: its 9 tap offsets (relative
+// to the tile's first image) are computed once per tile, a tap in the padding
+// gets an offset past the buffer so its load returns 0 without touching
+// memory.  Each wavefront computes whole rows, 4 at a time (rows wave,
+// wave + nwaves, ...), so a row's taps and bias are wavefront-uniform and one
+// load instruction reads 64 neighbouring columns of one input plane.  Rows
+// past cin are zero.  The caller synchronizes.
 __device__ __forceinline__ void dw_strip(const Args &a, const float *__restrict__ x, unsigned char *lds,
-                                         int32_t tile, int tid, int nthreads) {
+                                         int32_t tile, int wave, int nwaves, int lane) {
     const float lo = a.dw_act == 0 ? -__builtin_huge_valf() : 0.0f;
     const float hi = a.dw_act == 2 ? 6.0f : __builtin_huge_valf();
     const int32_t s = a.dw_stride;
-    const int64_t ihw = static_cast<int64_t>(a.in_h) * a.in_w;
-    for (int i = tid; i < a.strip_rows * 16; i += nthreads) {
-        const int32_t row = i >> 4;
-        f4 v = {0.0f, 0.0f, 0.0f, 0.0f};
-        if (row < a.cin) {
-            const float *kp = a.dw + row * kDwParams;
-            float kw[10];
+    const int32_t ihw = a.in_h * a.in_w;
+    const int32_t col0 = tile * 64;
+    const int32_t n0 = col0 / a.hw;
+    const int32_t c = col0 + lane;
+    const bool ok = c < a.m;
+    int32_t off[9];
+    {
+        const int32_t n = c / a.hw;
+        const int32_t pp = c - n * a.hw;
+        const int32_t oy = pp / a.out_w;
+        const int32_t ox = pp - oy * a.out_w;
+        const int32_t plane = (n - n0) * a.cin * ihw;  // (n, channel 0) from (n0, channel 0), elements
 #pragma unroll
-            for (int t = 0; t < 10; ++t)
-                kw[t] = kp[t];
+        for (int t = 0; t < 9; ++t) {
+            const int32_t iy = oy * s + t / 3 - 1;
+            const int32_t ix = ox * s + t % 3 - 1;
+            const bool in = ok && iy >= 0 && iy < a.in_h && ix >= 0 && ix < a.in_w;
+            off[t] = in ? (plane + iy * a.in_w + ix) * 4 : kOutOfRange;
+        }
+    }
+    const int64_t xbase = static_cast<int64_t>(n0) * a.cin * ihw;
+    const int64_t xbytes = a.x_bytes - xbase * 4;
+    constexpr int R = 4;
+    for (int32_t r0 = wave; r0 < a.strip_rows; r0 += R * nwaves) {
+        float v[R];
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int32_t c = tile * 64 + (i & 15) * 4 + e;
-                if (c < a.m) {
-                    const int32_t n = c / a.hw;
-                    const int32_t pp = c - n * a.hw;
-                    const int32_t oy = pp / a.out_w;
-                    const int32_t ox = pp - oy * a.out_w;
-                    const float *xc = x + (static_cast<int64_t>(n) * a.cin + row) * ihw;
+        for (int u = 0; u < R; ++u) {
+            const int32_t row = r0 + u * nwaves;
+            v[u] = 0.0f;
+            if (row < a.cin) {
+                // channel row of the tile's first image: one buffer resource per row
+                const int64_t rowoff = static_cast<int64_t>(row) * ihw;
+                const Rsrc rx = make_rsrc(x + xbase + rowoff,
+                                          static_cast<uint32_t>(std::min<int64_t>(xbytes - rowoff * 4, kMaxRecords)));
+                const float *kp = a.dw + row * kDwParams;
+                float acc = 0.0f;
+#pragma unroll
+                for (int t = 0; t < 9; ++t)
+                    acc = __builtin_fmaf(kp[t], __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rx, off[t], 0, 0)), acc);
+                v[u] = fminf(fmaxf(acc + kp[9], lo), hi);  // columns past the last one: never stored
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < R; ++u) {
+            const int32_t row = r0 + u * nwaves;
+            if (row < a.strip_rows)
+                *reinterpret_cast<float *>(lds + row * kRowBytes + lane * 4) = v[u];
+        }
+    }
+}
+
+// The same strip through LDS: a tile's 64 output columns read, per channel, a
+// window of input rows -- for each image n0 .. n1 the tile touches, rows
+// iy_a(n) .. iy_b(n) of its plane, one contiguous span of memory each.  The
+// workgroup stages the windows of `ch` channels at a time with 16-byte loads
+// (each input element is fetched once per tile, not once per tap), and each
+// wavefront computes whole strip rows from there, lane j column j, 9 LDS
+// reads per output.  The loads of the next chunk are issued into registers
+// before the current chunk is computed, so their latency overlaps it.  Spans
+// start on 16-byte boundaries in LDS (piece n at base(n), lengths rounded up
+// to 4 floats), so the staging copy of vector i is simply LDS bytes 16 i ..
+// 16 i + 15 and no two threads write one word.  Returns false, doing nothing,
+// when one channel's window does not fit in the staging area.  Same
+// arithmetic as dw_strip.  The caller synchronizes after it.
+constexpr int kStageVecs = 4;  // staged 16-byte vectors per thread and chunk, at most
+
+// The depthwise parameters are read-only for the whole launch: reading them
+// through the constant address space lets wavefront-uniform reads become
+// scalar loads.
+using ConstF = const __attribute__((address_space(4))) float;
+__device__ __forceinline__ ConstF *as_constant(const float *p) { return (ConstF *)(p); }
+
+__device__ __forceinline__ bool dw_strip_staged(const Args &a, const float *__restrict__ x, unsigned char *lds,
+                                                int32_t tile, int tid, int nthreads, int wave, int nwaves,
+                                                int lane) {
+    const int32_t s = a.dw_stride;
+    const int32_t in_w = a.in_w;
+    const int32_t ihw = a.in_h * in_w;
+    // the tile's images and the rows of each it needs (uniform)
+    const int32_t col0 = tile * 64;
+    const int32_t clast = std::min(col0 + 63, a.m - 1);
+    const int32_t n0 = col0 / a.hw, n1 = clast / a.hw;
+    const int32_t ya0 = std::max(0, (col0 - n0 * a.hw) / a.out_w * s - 1);           // iy_a(n0)
+    const int32_t yb1 = std::min(a.in_h - 1, (clast - n1 * a.hw) / a.out_w * s + 1);  // iy_b(n1)
+    const int32_t yb0 = n1 == n0 ? yb1 : a.in_h - 1;                                  // iy_b(n0)
+    const int32_t ya1 = n1 == n0 ? ya0 : 0;                                           // iy_a(n1)
+    const int32_t len0 = (yb0 - ya0 + 1) * in_w, len1 = (yb1 - ya1 + 1) * in_w;
+    const int32_t pfull = (ihw + 3) & ~3;     // a whole plane (images between n0 and n1)
+    const int32_t p0 = (len0 + 3) & ~3;       // LDS floats of each piece
+    const int32_t p1 = (len1 + 3) & ~3;
+    const int32_t spc = n1 == n0 ? p0 : p0 + (n1 - n0 - 1) * pfull + p1;  // LDS floats per channel
+    const int32_t nv = spc / 4;  // 16-byte vectors per channel
+    const int32_t ch = std::min(a.stage_bytes / 4 / spc, kStageVecs * nthreads / nv);
+    if (ch == 0)
+        return false;
+
+    // this lane's taps: LDS float offsets in its channel's window, -1 in the padding
+    const int32_t c = col0 + lane;
+    const bool ok = c < a.m;
+    int32_t toff[9];
+    {
+        const int32_t n = ok ? c / a.hw : n0;
+        const int32_t pp = c - n * a.hw;
+        const int32_t oy = pp / a.out_w;
+        const int32_t ox = pp - oy * a.out_w;
+        const int32_t ya = n == n0 ? ya0 : 0;
+        const int32_t base = n == n0 ? 0 : p0 + (n - n0 - 1) * pfull;
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+            const int32_t iy = oy * s + t / 3 - 1;
+            const int32_t ix = ox * s + t % 3 - 1;
+            const bool in = ok && iy >= 0 && iy < a.in_h && ix >= 0 && ix < in_w;
+            toff[t] = in ? base + (iy - ya) * in_w + ix : -1;
+        }
+    }
+    // this thread's staging vectors i = tid + j * nthreads of a chunk: their
+    // channel within the chunk and their byte offset from channel 0 of the
+    // tile's first image (chunk c0 adds c0 planes)
+    int32_t vr[kStageVecs], vg[kStageVecs];
+#pragma unroll
+    for (int j = 0; j < kStageVecs; ++j) {
+        const int32_t i = tid + j * nthreads;
+        const int32_t r = i / nv;
+        const int32_t f = (i - r * nv) * 4;  // LDS float offset in the channel's window
+        int32_t n, off;
+        if (f < p0) {
+            n = n0;
+            off = f;
+        } else if (f < spc - p1) {
+            n = n0 + 1 + (f - p0) / pfull;
+            off = (f - p0) % pfull;
+        } else {
+            n = n1;
+            off = f - (spc - p1);
+        }
+        vr[j] = r < ch ? r : INT32_MAX;
+        vg[j] = r < ch ? (((n - n0) * a.cin + r) * ihw + (n == n0 ? ya0 : 0) * in_w + off) * 4 : 0;
+    }
+    const float lo = a.dw_act == 0 ? -__builtin_huge_valf() : 0.0f;
+    const float hi = a.dw_act == 2 ? 6.0f : __builtin_huge_valf();
+    const int64_t xbase = static_cast<int64_t>(n0) * a.cin * ihw;
+    const int64_t xrel = a.x_bytes - xbase * 4;  // bytes of x from the tile's first image on
+    const Rsrc rx = make_rsrc(x + xbase, static_cast<uint32_t>(std::min<int64_t>(xrel, kMaxRecords)));
+    float *stage = reinterpret_cast<float *>(lds + a.stage_off);
+
+    // A vector past the last element of x is padding, never read back; raw
+    // buffer loads check their bounds per dword, so the elements of a vector
+    // that straddles the end of x still arrive and the rest read 0.
+    u4 v[kStageVecs];
+    auto fetch = [&](int32_t c0) __attribute__((always_inline)) {
+        const int32_t nch = std::min(ch, a.cin - c0);
+#pragma unroll
+        for (int j = 0; j < kStageVecs; ++j)
+            v[j] = bload16(rx, vr[j] < nch ? vg[j] + c0 * ihw * 4 : kOutOfRange, 0);
+    };
+    fetch(0);
+    for (int32_t c0 = 0; c0 < a.cin; c0 += ch) {
+        const int32_t nch = std::min(ch, a.cin - c0);
+#pragma unroll
+        for (int j = 0; j < kStageVecs; ++j)
+            if (vr[j] < nch)
+                *reinterpret_cast<u4 *>(stage + 4 * (tid + j * nthreads)) = v[j];
+        __syncthreads();  // chunk staged
+        if (c0 + ch < a.cin)
+            fetch(c0 + ch);
+        // two rows per pass, their 18 LDS reads issued together; columns past
+        // the last one hold act1(b1), never stored
+        for (int32_t r0 = wave; r0 < nch; r0 += 2 * nwaves) {
+            float xv[2][9];
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const float *w = stage + std::min(r0 + u * nwaves, nch - 1) * spc;
+#pragma unroll
+                for (int t = 0; t < 9; ++t)
+                    xv[u][t] = w[toff[t] < 0 ? 0 : toff[t]];
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int32_t r = r0 + u * nwaves;
+                if (r < nch) {
+                    const ConstF *kp = as_constant(a.dw) + (c0 + r) * kDwParams;
                     float acc = 0.0f;
 #pragma unroll
-                    for (int dy = 0; dy < 3; ++dy) {
-                        const int32_t iy = oy * s + dy - 1;
-                        if (iy >= 0 && iy < a.in_h) {
-#pragma unroll
-                            for (int dx = 0; dx < 3; ++dx) {
-                                const int32_t ix = ox * s + dx - 1;
-                                if (ix >= 0 && ix < a.in_w)
-                                    acc = __builtin_fmaf(kw[dy * 3 + dx], xc[iy * a.in_w + ix], acc);
-                            }
-                        }
-                    }
-                    v[e] = fminf(fmaxf(acc + kw[9], lo), hi);
+                    for (int t = 0; t < 9; ++t)
+                        acc = __builtin_fmaf(kp[t], toff[t] < 0 ? 0.0f : xv[u][t], acc);
+                    *reinterpret_cast<float *>(lds + (c0 + r) * kRowBytes + lane * 4) =
+                        fminf(fmaxf(acc + kp[9], lo), hi);
                 }
             }
         }
-        *reinterpret_cast<f4 *>(lds + i * 16) = v;
+        __syncthreads();  // staging free again
     }
+    // channel rows past cin read as zero
+    for (int32_t row = a.cin + wave; row < a.strip_rows; row += nwaves)
+        *reinterpret_cast<float *>(lds + row * kRowBytes + lane * 4) = 0.0f;
+    return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -639,7 +802,8 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
             bool computed = false;
             if constexpr (!F16) {
                 if (a.dw_stride) {
-                    dw_strip(a, x, lds, wk.tile, tid, blockDim.x);
+                    if (!dw_strip_staged(a, x, lds, wk.tile, tid, blockDim.x, wave, nwaves, lane))
+                        dw_strip(a, x, lds, wk.tile, wave, nwaves, lane);
                     computed = true;
                 }
             }
@@ -1115,6 +1279,8 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.in_w = p.dw_stride ? in_w : 0;
     a.out_w = p.dw_stride ? out_w : 0;
     a.dw = p.dw;
+    a.stage_off = p.stage_off;
+    a.stage_bytes = p.stage_bytes;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(slots)), dim3(p.waves * 64), p.lds_bytes, stream, x, y,
                        p.idx, p.val, p.hdr, p.table, p.rank, p.wave_ptr, p.pidx, p.pval, p.psel, p.sel_ptr,
                        p.wave_ev, a);

@@ -18,7 +18,7 @@ pytestmark = pytest.mark.gpu
 
 # (cin, cout, h, w, n, sparsity, k, act, dw_act, stride): the MobileNet v1
 # block shapes (stride 1 and 2), ragged tails, odd and tiny images, every
-# block height, the widest strip.
+# block height, the widest strip, tiles that span several images.
 CASES = [
     (32, 64, 56, 56, 1, 0.9, 1, "relu", "relu6", 1),
     (32, 64, 56, 56, 1, 0.9, 1, "relu", "relu6", 2),
@@ -37,6 +37,10 @@ CASES = [
     (512, 512, 14, 14, 3, 0.9, 4, "relu", "relu6", 1),
     (512, 1024, 14, 14, 2, 0.9, 2, "relu6", "relu6", 2),
     (600, 96, 7, 7, 2, 0.9, 1, "relu6", "relu6", 1),
+    # input windows too wide for the LDS staging area: some tiles (row 1 of a
+    # 3 x 2500 image), then every tile (2 rows of 4096), take the direct loads
+    (512, 64, 3, 2500, 1, 0.9, 1, "relu", "relu6", 1),
+    (512, 64, 3, 4096, 1, 0.9, 1, "relu", "none", 2),
 ]
 
 
@@ -123,3 +127,27 @@ def test_fused_unaligned_pointers_and_odd_output():
     finally:
         plan.close()
     assert_fused_parity(layer, kw, kb, "relu", 2, y, what="unaligned")
+
+
+@pytest.mark.parametrize("fused", [False, True])
+def test_run_rejects_tiles_whose_images_span_2gib(fused):
+    """Two 1024 x 1024 images of 300 channels: one tile touches both, 2.5 GB
+    of x, beyond the kernels' 32-bit offsets.  The call is refused before any
+    launch (the addresses are never dereferenced)."""
+    from paper_1911_09723_amd import Plan, spconv
+    layer = make_layer(300, 8, 1, 1, 1, 0.5, act="relu", seed=91, with_x=False)
+    if fused:
+        kw, kb = make_depthwise(300, 92)
+        plan = Plan.fused(8, 300, 1, layer.row_ptr, layer.col_idx, layer.values, layer.bias, "relu", kw, kb,
+                          "none", 1)
+    else:
+        plan = Plan.from_layer(layer)
+    try:
+        note("span check fused=%s" % fused)
+        st = spconv.spconv_run(plan.handle, 1 << 44, 1 << 45, 2, 1024, 1024, check=False)
+        assert st == spconv.E_UNSUPPORTED and "2^31" in spconv.spconv_last_error()
+        # one image of the same size fits
+        st = spconv.spconv_run(plan.handle, 1 << 44, 1 << 45, 0, 1024, 1024, check=False)
+        assert st == spconv.OK
+    finally:
+        plan.close()
