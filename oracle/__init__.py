@@ -17,7 +17,10 @@ S = sum |W[r, c] * X[n, c, p]| that the parity tolerance is stated in.
 
 ``dw3x3_ref`` and ``fused_ref`` evaluate the fused MobileNet block order
 (depthwise 3x3, then the sparse 1x1 on its output; paper Sec. 2 and Sec.
-3.3) the same way, in double.
+3.3) the same way, in double.  ``conv3x3_hwc_ref`` (the dense first
+convolution from an HWC image to CHW, Sec. 3.1), ``gap_ref`` (global average
+pooling, Sec. 3.3) and ``mobilenet_v1_ref`` (the whole network, chaining
+the double-precision stages and their error scales) complete a network.
 """
 
 from __future__ import annotations
@@ -66,6 +69,22 @@ def load_library(path: str):
     lib.spconv_ref_dw3x3.argtypes = [
         ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_dw3x3_f64.restype = ctypes.c_int
+    lib.spconv_ref_dw3x3_f64.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_conv3x3_hwc.restype = ctypes.c_int
+    lib.spconv_ref_conv3x3_hwc.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+    ]
+    lib.spconv_ref_gap.restype = ctypes.c_int
+    lib.spconv_ref_gap.argtypes = [
+        ctypes.c_int64, ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+        ctypes.c_void_p,
     ]
     lib.spconv_ref_threads.restype = ctypes.c_int
     lib.spconv_ref_half_to_double.restype = ctypes.c_double
@@ -189,6 +208,108 @@ def fused_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x, dw_
         raise ValueError("oracle rejected the input (code %d)" % rc)
     shape = (n, cout, ho, wo)
     return y64.astype(np.float32).reshape(shape), y64.reshape(shape), scale.reshape(shape)
+
+
+def dw3x3_ref64(x, xs, k, bias, act, stride: int, lib=None):
+    """The depthwise 3x3 stage over a double input x [N, C, H, W] with its own
+    error scale xs (or None); returns (d, sd) as ``dw3x3_ref``, sd also
+    carrying sum |K| * xs."""
+    lib = _load() if lib is None else lib
+    xa = np.ascontiguousarray(x, dtype=np.float64)
+    xsa = None if xs is None else np.ascontiguousarray(xs, dtype=np.float64)
+    ka = np.ascontiguousarray(k, dtype=np.float32)
+    ba = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    n, c, h, w = xa.shape
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    d = np.empty((n, c, ho, wo), dtype=np.float64)
+    sd = np.empty((n, c, ho, wo), dtype=np.float64)
+    rc = lib.spconv_ref_dw3x3_f64(int(n), int(c), int(h), int(w), int(stride), _ptr(xa), _ptr(xsa), _ptr(ka),
+                                  _ptr(ba), _ACTS[act], _ptr(d), _ptr(sd))
+    if rc != 0:
+        raise ValueError("oracle rejected the depthwise input (code %d)" % rc)
+    return d, sd
+
+
+def spmm_ref64(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x, xs, lib=None):
+    """The sparse 1x1 over a double input x [N, Cin, H, W] with error scale xs
+    (or None); returns (y, scale) in double, scale = sum |W X| + |W| xs."""
+    lib = _load() if lib is None else lib
+    xa = np.ascontiguousarray(x, dtype=np.float64)
+    xsa = None if xs is None else np.ascontiguousarray(xs, dtype=np.float64)
+    n, c, h, w = xa.shape
+    if c != cin:
+        raise ValueError("x has %d channels, expected %d" % (c, cin))
+    rp = np.ascontiguousarray(row_ptr, dtype=np.int32)
+    ci = np.ascontiguousarray(col_idx, dtype=np.int32)
+    va = np.ascontiguousarray(values, dtype=np.float32)
+    ba = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    y = np.empty((n, cout, h * w), dtype=np.float64)
+    sc = np.empty((n, cout, h * w), dtype=np.float64)
+    rc = lib.spconv_ref_run_f64(int(cout), int(cin), int(block_rows), _ptr(rp), _ptr(ci), _ptr(va), _ptr(ba),
+                                _ACTS[act], _ptr(xa), _ptr(xsa), int(n), int(h * w), _ptr(y), _ptr(sc))
+    if rc != 0:
+        raise ValueError("oracle rejected the input (code %d)" % rc)
+    return y.reshape(n, cout, h, w), sc.reshape(n, cout, h, w)
+
+
+def conv3x3_hwc_ref(x, wt, bias, act, stride: int, lib=None):
+    """Dense 3x3 convolution (zero padding 1, stride ``stride``) of float32
+    HWC images x [N, H, W, Cin] with wt [Cout, 3, 3, Cin]; returns (y, ys) in
+    double, CHW [N, Cout, Ho, Wo], ys = |b| + sum |Wt X|."""
+    lib = _load() if lib is None else lib
+    xa = np.ascontiguousarray(x, dtype=np.float32)
+    wa = np.ascontiguousarray(wt, dtype=np.float32)
+    ba = None if bias is None else np.ascontiguousarray(bias, dtype=np.float32)
+    n, h, w, cin = xa.shape
+    cout = wa.shape[0]
+    if wa.shape != (cout, 3, 3, cin):
+        raise ValueError("wt must be [Cout, 3, 3, Cin]")
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    y = np.empty((n, cout, ho, wo), dtype=np.float64)
+    ys = np.empty((n, cout, ho, wo), dtype=np.float64)
+    rc = lib.spconv_ref_conv3x3_hwc(int(n), int(h), int(w), int(cin), int(cout), int(stride), _ptr(xa), _ptr(wa),
+                                    _ptr(ba), _ACTS[act], _ptr(y), _ptr(ys))
+    if rc != 0:
+        raise ValueError("oracle rejected the convolution input (code %d)" % rc)
+    return y, ys
+
+
+def gap_ref(x, xs=None, lib=None):
+    """Global average pooling of x [N, C, H, W] (any float type) with error
+    scale xs (or None); returns (y, ys) in double, [N, C]."""
+    lib = _load() if lib is None else lib
+    xa = np.ascontiguousarray(x, dtype=np.float64)
+    xsa = None if xs is None else np.ascontiguousarray(xs, dtype=np.float64)
+    n, c, h, w = xa.shape
+    y = np.empty((n, c), dtype=np.float64)
+    ys = np.empty((n, c), dtype=np.float64)
+    rc = lib.spconv_ref_gap(int(n), int(c), int(h * w), _ptr(xa), _ptr(xsa), _ptr(y), _ptr(ys))
+    if rc != 0:
+        raise ValueError("oracle rejected the pooling input (code %d)" % rc)
+    return y, ys
+
+
+def mobilenet_v1_ref(net, x, lib=None):
+    """A whole MobileNet v1 forward pass (``synth.MobileNetV1`` weights) on
+    HWC images x [N, H, W, 3], in double: the dense stem convolution (stride
+    2, ReLU6), 13 blocks of depthwise 3x3 (ReLU6) -> sparse 1x1 (ReLU6),
+    global average pooling, the dense classifier (no activation; the
+    classifier runs as a 1x1 over 1 x 1 images).  Returns (logits [N,
+    classes] double, their error scale S propagated through every layer)."""
+    d, s = conv3x3_hwc_ref(x, net.stem_w, net.stem_b, "relu6", 2, lib=lib)
+    for blk in net.blocks:
+        d, s = dw3x3_ref64(d, s, blk.dw_k, blk.dw_b, "relu6", blk.stride, lib=lib)
+        pw = blk.pw
+        d, s = spmm_ref64(pw.cout, pw.cin, pw.block_rows, pw.row_ptr, pw.col_idx, pw.values, pw.bias, "relu6",
+                          d, s, lib=lib)
+    g, gs = gap_ref(d, s, lib=lib)
+    n, c = g.shape
+    classes = net.fc_w.shape[0]
+    rp = np.arange(0, classes * c + 1, c, dtype=np.int32)
+    ci = np.tile(np.arange(c, dtype=np.int32), classes)
+    y, ys = spmm_ref64(classes, c, 1, rp, ci, net.fc_w.reshape(-1), net.fc_b, "none",
+                       g.reshape(n, c, 1, 1), gs.reshape(n, c, 1, 1), lib=lib)
+    return y.reshape(n, classes), ys.reshape(n, classes)
 
 
 def tolerance(y_ref, scale, storage: str):

@@ -35,8 +35,12 @@
  *
  * Returns 0, -1 if a column index is out of range, -2 if scratch allocation fails.
  *
- * Below it: the same stage over a double input (spconv_ref_run_f64) and a
- * depthwise 3x3 stage (spconv_ref_dw3x3) for the fused depthwise -> 1x1 path.
+ * Below it: the same stage over a double input (spconv_ref_run_f64), a
+ * depthwise 3x3 stage (spconv_ref_dw3x3, and spconv_ref_dw3x3_f64 over a
+ * double input) for the fused depthwise -> 1x1 path, and the other CHW
+ * operators of a whole network (paper Sec. 3.1 and Sec. 3.3): the dense 3x3
+ * convolution from an HWC image to CHW (spconv_ref_conv3x3_hwc) and global
+ * average pooling (spconv_ref_gap).
  */
 #include <math.h>
 #include <stddef.h>
@@ -213,6 +217,137 @@ int spconv_ref_dw3x3(int64_t n, int32_t c, int32_t h, int32_t w, int32_t stride,
                         sd[o] = s + fabs(b);
                 }
             }
+        }
+    }
+    return 0;
+}
+
+/*
+ * The depthwise 3x3 stage over a double input x [n][c][h][w] with its own
+ * error scale xs (same shape, may be NULL): as spconv_ref_dw3x3, and the
+ * output scale also carries sum |K| * xs over the taps inside the image.
+ */
+int spconv_ref_dw3x3_f64(int64_t n, int32_t c, int32_t h, int32_t w, int32_t stride,
+                         const double *x, const double *xs, const float *k, const float *bias, int32_t act,
+                         double *d, double *sd)
+{
+    if (stride < 1)
+        return -1;
+    const int64_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t img = 0; img < n; ++img) {
+        for (int32_t ch = 0; ch < c; ++ch) {
+            const int64_t plane = (img * c + ch) * (int64_t)h * w;
+            const float *kc = k + (int64_t)ch * 9;
+            const double b = bias ? (double)bias[ch] : 0.0;
+            for (int64_t oy = 0; oy < ho; ++oy) {
+                for (int64_t ox = 0; ox < wo; ++ox) {
+                    double acc = 0.0, s = 0.0;
+                    for (int dy = 0; dy < 3; ++dy) {
+                        const int64_t iy = oy * stride + dy - 1;
+                        if (iy < 0 || iy >= h)
+                            continue;
+                        for (int dx = 0; dx < 3; ++dx) {
+                            const int64_t ix = ox * stride + dx - 1;
+                            if (ix < 0 || ix >= w)
+                                continue;
+                            const double kv = (double)kc[dy * 3 + dx];
+                            const double prod = kv * x[plane + iy * w + ix];
+                            acc += prod;
+                            s += fabs(prod);
+                            if (xs)
+                                s += fabs(kv) * xs[plane + iy * w + ix];
+                        }
+                    }
+                    const int64_t o = ((img * c + ch) * ho + oy) * wo + ox;
+                    d[o] = apply_act(acc + b, act);
+                    if (sd)
+                        sd[o] = s + fabs(b);
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Dense 3x3 convolution from an HWC image to CHW (the network's first layer,
+ * which the paper keeps dense and runs on the image in HWC order, writing the
+ * CHW layout the sparse layers read; Sec. 3.1, Sec. 3.3):
+ *
+ *     Y[n, o, oy, ox] = act( b[o] + sum_{dy, dx in 0..2} sum_{i < cin}
+ *                                     Wt[o][dy][dx][i] * X[n, s*oy + dy - 1, s*ox + dx - 1, i] )
+ *
+ * with X zero outside the image (padding 1) and stride s: ho = (h - 1) / s + 1,
+ * wo = (w - 1) / s + 1.  x: float [n][h][w][cin]; wt: float
+ * [cout][3][3][cin]; bias [cout] or NULL.  y: double [n][cout][ho][wo]; ys
+ * (may be NULL): |b| + sum |Wt * X|.  Returns 0, or -1 for a bad stride.
+ */
+int spconv_ref_conv3x3_hwc(int64_t n, int32_t h, int32_t w, int32_t cin, int32_t cout, int32_t stride,
+                           const float *x, const float *wt, const float *bias, int32_t act,
+                           double *y, double *ys)
+{
+    if (stride < 1)
+        return -1;
+    const int64_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t img = 0; img < n; ++img) {
+        for (int32_t o = 0; o < cout; ++o) {
+            const double b = bias ? (double)bias[o] : 0.0;
+            for (int64_t oy = 0; oy < ho; ++oy) {
+                for (int64_t ox = 0; ox < wo; ++ox) {
+                    double acc = 0.0, s = 0.0;
+                    for (int dy = 0; dy < 3; ++dy) {
+                        const int64_t iy = oy * stride + dy - 1;
+                        if (iy < 0 || iy >= h)
+                            continue;
+                        for (int dx = 0; dx < 3; ++dx) {
+                            const int64_t ix = ox * stride + dx - 1;
+                            if (ix < 0 || ix >= w)
+                                continue;
+                            for (int32_t i = 0; i < cin; ++i) {
+                                const double prod = (double)wt[((int64_t)o * 9 + dy * 3 + dx) * cin + i] *
+                                                    (double)x[((img * h + iy) * w + ix) * cin + i];
+                                acc += prod;
+                                s += fabs(prod);
+                            }
+                        }
+                    }
+                    const int64_t q = ((img * cout + o) * ho + oy) * wo + ox;
+                    y[q] = apply_act(acc + b, act);
+                    if (ys)
+                        ys[q] = s + fabs(b);
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Global average pooling over CHW planes (Sec. 3.3): y[n][c] = (1 / hw) *
+ * sum_p x[n][c][p], the sum in ascending p from zero.  x: double
+ * [n][c][hw]; xs (may be NULL): its error scale, pooled the same way into ys
+ * together with sum |x| / hw.  Returns 0, or -1 for hw < 1.
+ */
+int spconv_ref_gap(int64_t n, int32_t c, int64_t hw, const double *x, const double *xs, double *y, double *ys)
+{
+    if (hw < 1)
+        return -1;
+#pragma omp parallel for collapse(2) schedule(static)
+    for (int64_t img = 0; img < n; ++img) {
+        for (int32_t ch = 0; ch < c; ++ch) {
+            const double *xp = x + (img * c + ch) * hw;
+            double acc = 0.0, s = 0.0;
+            for (int64_t p = 0; p < hw; ++p) {
+                acc += xp[p];
+                s += fabs(xp[p]);
+                if (xs)
+                    s += xs[(img * c + ch) * hw + p];
+            }
+            y[img * c + ch] = acc / (double)hw;
+            if (ys)
+                ys[img * c + ch] = s / (double)hw;
         }
     }
     return 0;

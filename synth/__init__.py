@@ -8,6 +8,7 @@ fed from it without sharing any computation.
 
 from .layers import Layer, make_layer, make_depthwise, densify, expand_blocks_to_csr
 from .configs import CONFIGS, config_layers, layer_seed, TARGET
+from .mobilenet import MBV1_BLOCKS, MobileNetV1, make_mobilenet_v1, make_image
 
 __all__ = [
     "Layer",
@@ -19,4 +20,8 @@ __all__ = [
     "config_layers",
     "layer_seed",
     "TARGET",
+    "MBV1_BLOCKS",
+    "MobileNetV1",
+    "make_mobilenet_v1",
+    "make_image",
 ]

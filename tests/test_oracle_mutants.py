@@ -34,14 +34,40 @@ MUTANTS = {
     "half_exponent_bias": ("expo - 25", "expo - 24"),
     "half_implicit_bit": ("(frac | 0x400)", "frac"),
     "half_subnormal_scale": ("ldexp((double)frac, -24)", "ldexp((double)frac, -25)"),
-    "dw_tap_row_offset": ("oy * stride + dy - 1", "oy * stride + dy"),
-    "dw_column_stride": ("ox * stride + dx - 1", "ox + dx - 1"),
-    "dw_bias_dropped": ("d[o] = apply_act(acc + b, act);", "d[o] = apply_act(acc, act);"),
-    "dw_kernel_transposed": ("kc[dy * 3 + dx]", "kc[dx * 3 + dy]"),
-    "dw_scale_signed": ("            s += fabs(prod);", "            s += prod;"),
-    "dw_border_taps_kept": ("if (ix < 0 || ix >= w)", "if (ix < 0 || ix > w)"),
+    "dw_tap_row_offset": ("spconv_ref_dw3x3", "oy * stride + dy - 1", "oy * stride + dy"),
+    "dw_column_stride": ("spconv_ref_dw3x3", "ox * stride + dx - 1", "ox + dx - 1"),
+    "dw_bias_dropped": ("spconv_ref_dw3x3", "d[o] = apply_act(acc + b, act);", "d[o] = apply_act(acc, act);"),
+    "dw_kernel_transposed": ("spconv_ref_dw3x3", "kc[dy * 3 + dx]", "kc[dx * 3 + dy]"),
+    "dw_scale_signed": ("spconv_ref_dw3x3", "            s += fabs(prod);", "            s += prod;"),
+    "dw_border_taps_kept": ("spconv_ref_dw3x3", "if (ix < 0 || ix >= w)", "if (ix < 0 || ix > w)"),
     "input_scale_dropped": ("s[p] += fabs(wv) * xs[xrow + p];", "s[p] += 0.0;"),
+    # the network-level stages: (function, anchor inside it, replacement)
+    "dw64_tap_row_offset": ("spconv_ref_dw3x3_f64", "oy * stride + dy - 1", "oy * stride + dy"),
+    "dw64_input_scale_dropped": ("spconv_ref_dw3x3_f64", "s += fabs(kv) * xs[plane + iy * w + ix];", "s += 0.0;"),
+    "stem_tap_transposed": ("spconv_ref_conv3x3_hwc", "(int64_t)o * 9 + dy * 3 + dx", "(int64_t)o * 9 + dx * 3 + dy"),
+    "stem_hwc_channel_stride": ("spconv_ref_conv3x3_hwc", "((img * h + iy) * w + ix) * cin + i",
+                                "((img * h + iy) * w + ix) + i"),
+    "stem_padding_shift": ("spconv_ref_conv3x3_hwc", "ox * stride + dx - 1", "ox * stride + dx"),
+    "stem_bias_dropped": ("spconv_ref_conv3x3_hwc", "y[q] = apply_act(acc + b, act);", "y[q] = apply_act(acc, act);"),
+    "gap_drops_last": ("spconv_ref_gap", "p < hw; ++p", "p < hw - 1; ++p"),
+    "gap_divisor": ("spconv_ref_gap", "acc / (double)hw", "acc / (double)(hw + 1)"),
+    "gap_input_scale_dropped": ("spconv_ref_gap", "s += xs[(img * c + ch) * hw + p];", "s += 0.0;"),
 }
+
+
+def _mutate(source, mutant):
+    """Apply one planted mistake: (anchor, replacement), the anchor unique in
+    the file, or (function, anchor, replacement), unique in that function."""
+    if len(mutant) == 2:
+        before, after = mutant
+        assert source.count(before) == 1, "mutation anchor not found exactly once: " + before
+        return source.replace(before, after)
+    func, before, after = mutant
+    start = source.index("\nint " + func + "(")
+    end = source.index("\n}\n", start)
+    body = source[start:end]
+    assert body.count(before) == 1, "mutation anchor not found exactly once in %s: %s" % (func, before)
+    return source[:start] + body.replace(before, after) + source[end:]
 
 
 def _act(v, act):
@@ -77,6 +103,7 @@ def _battery(lib):
         if not np.allclose(s.reshape(sref.shape), sref, rtol=1e-12, atol=0):
             failed.append("brute-scale:k%d:%s" % (k, storage))
     failed += _dw_battery(lib)
+    failed += _net_battery(lib)
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     ref = bits.view(np.float16).astype(np.float64)
     got = np.array([lib.spconv_ref_half_to_double(int(b)) for b in bits])
@@ -121,6 +148,46 @@ def _dw_battery(lib):
     return failed
 
 
+def _net_battery(lib):
+    """Stem convolution, pooling and the double-input depthwise stage against
+    torch / numpy in fp64, and the whole chain on 32 x 32 images."""
+    import torch
+    F = torch.nn.functional
+    failed = []
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((2, 9, 8, 3)).astype(np.float32)
+    wt = rng.standard_normal((4, 3, 3, 3)).astype(np.float32)
+    b = rng.standard_normal(4).astype(np.float32)
+    for stride in (1, 2):
+        y, ys = oracle.conv3x3_hwc_ref(x, wt, b, "none", stride, lib=lib)
+        xt = torch.from_numpy(x).double().permute(0, 3, 1, 2)
+        wtt = torch.from_numpy(wt).double().permute(0, 3, 1, 2)
+        ref = F.conv2d(xt, wtt, torch.from_numpy(b).double(), stride=stride, padding=1).numpy()
+        if y.shape != ref.shape or not np.allclose(y, ref, rtol=1e-12, atol=1e-12):
+            failed.append("stem:s%d" % stride)
+    g = rng.standard_normal((2, 3, 5, 4))
+    gs = np.abs(rng.standard_normal(g.shape))
+    y, ys = oracle.gap_ref(g, gs, lib=lib)
+    if not np.allclose(y, g.mean(axis=(2, 3)), rtol=1e-13, atol=1e-15):
+        failed.append("gap")
+    if not np.allclose(ys, (np.abs(g) + gs).mean(axis=(2, 3)), rtol=1e-13, atol=0):
+        failed.append("gap-scale")
+    d = rng.standard_normal((1, 3, 7, 6))
+    ds = np.abs(rng.standard_normal(d.shape))
+    k = rng.standard_normal((3, 3, 3)).astype(np.float32)
+    for stride in (1, 2):
+        o, os_ = oracle.dw3x3_ref64(d, ds, k, None, "none", stride, lib=lib)
+        kt = torch.from_numpy(k).double()[:, None]
+        ref = F.conv2d(torch.from_numpy(d), kt, None, stride=stride, padding=1, groups=3).numpy()
+        sref = F.conv2d(torch.from_numpy(np.abs(d) + ds), kt.abs(), None, stride=stride, padding=1,
+                        groups=3).numpy()
+        if o.shape != ref.shape or not np.allclose(o, ref, rtol=1e-12, atol=1e-12):
+            failed.append("dw64:s%d" % stride)
+        elif not np.allclose(os_, sref, rtol=1e-12, atol=0):
+            failed.append("dw64-scale:s%d" % stride)
+    return failed
+
+
 def _build(tmp_path, name, source):
     src = tmp_path / (name + ".c")
     so = tmp_path / ("lib" + name + ".so")
@@ -137,8 +204,5 @@ def test_unmodified_oracle_passes_battery(tmp_path):
 
 @pytest.mark.parametrize("name", sorted(MUTANTS))
 def test_planted_mistake_is_caught(tmp_path, name):
-    before, after = MUTANTS[name]
-    source = open(SRC).read()
-    assert source.count(before) == 1, "mutation anchor not found exactly once: " + before
-    lib = _build(tmp_path, name, source.replace(before, after))
+    lib = _build(tmp_path, name, _mutate(open(SRC).read(), MUTANTS[name]))
     assert _battery(lib), "planted mistake %r passed every pin" % name
