@@ -173,6 +173,51 @@ spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t c
                                        spconv_dtype storage);
 
 /* ---------------------------------------------------------------------------
+ * The other CHW operators of a network (Sec. 3.3: besides the sparse 1x1,
+ * the library provides the depthwise convolution, global average pooling
+ * and a dense 3x3 stride-2 convolution from the HWC image to CHW; Sec. 3.1:
+ * the first convolution stays dense).  fp32 only; every pointer is device
+ * memory owned by the caller; one asynchronous kernel launch on `stream`
+ * (NULL: the default stream); nothing is allocated and nothing synchronizes.
+ * Sizes of 0 are no-ops.  Outputs must not overlap inputs (SPCONV_E_ARG).
+ * ------------------------------------------------------------------------- */
+
+/*
+ * Dense 3x3 convolution, zero padding 1, from an HWC image to CHW:
+ *   y[n, o, oy, ox] = act( bias[o] + sum_{dy, dx, i} weight[o][dy][dx][i]
+ *                                     * x[n, s*oy + dy - 1, s*ox + dx - 1, i] )
+ *   x       [n][h][w][cin]          weight  [cout][3][3][cin]
+ *   bias    [cout] or NULL          y       [n][cout][(h-1)/s+1][(w-1)/s+1]
+ *   stride  1 or 2 (the network stem uses 2)
+ * Errors: SPCONV_E_ARG (NULL pointer with work to do, negative size, bad
+ * stride or act, overlap), SPCONV_E_SHAPE (cin or cout < 1, too many
+ * pixels), SPCONV_E_UNSUPPORTED (cin > 8 or cout * (9 cin + 1) > 16384:
+ * the weights are held in LDS), SPCONV_E_HIP.
+ */
+spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const float *bias, spconv_act act,
+                                 int32_t stride, float *y, int32_t n, int32_t h, int32_t w, int32_t cin,
+                                 int32_t cout, void *stream);
+
+/*
+ * Depthwise 3x3 convolution, zero padding 1, on CHW tensors (a standalone
+ * launch; spconv_plan_create_fused runs the same stage inside the 1x1):
+ *   y[n, c, oy, ox] = act( bias[c] + sum_{dy, dx} weight[c][dy][dx] * x[n, c, s*oy + dy - 1, s*ox + dx - 1] )
+ *   x [n][c][h][w], weight [c][3][3], bias [c] or NULL, y [n][c][(h-1)/s+1][(w-1)/s+1], stride 1 or 2.
+ * Errors: SPCONV_E_ARG, SPCONV_E_SHAPE (too many outputs), SPCONV_E_HIP.
+ */
+spconv_status spconv_depthwise3x3(const float *x, const float *weight, const float *bias, spconv_act act,
+                                  int32_t stride, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
+                                  void *stream);
+
+/*
+ * Global average pooling: y[n, c] = (1 / (h w)) * sum_p x[n, c, p], summed in
+ * ascending p in fp32.  x [n][c][h][w], y [n][c].
+ * Errors: SPCONV_E_ARG, SPCONV_E_SHAPE (h * w == 0 with n * c > 0), SPCONV_E_HIP.
+ */
+spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
+                                     void *stream);
+
+/* ---------------------------------------------------------------------------
  * Planner controls and introspection.  These let a caller (and the CPU-only
  * tests) see what the host-side planner decided without running a kernel.
  * ------------------------------------------------------------------------- */

@@ -12,7 +12,10 @@ from .spconv import (  # noqa: F401
     SpconvError,
     load_library,
     spconv_dense_to_bcsr,
+    spconv_conv3x3_hwc,
+    spconv_depthwise3x3,
     spconv_destroy,
+    spconv_global_avg_pool,
     spconv_detect_block_rows,
     spconv_last_error,
     spconv_options_init,

@@ -17,6 +17,7 @@
 #include <vector>
 
 #include "launch.hpp"
+#include "net_kernels.hpp"
 #include "planner.hpp"
 
 struct spconv_plan_s {
@@ -390,6 +391,81 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     if (he != hipSuccess)
         return hip_fail("kernel launch", he);
     return SPCONV_OK;
+}
+
+spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const float *bias, spconv_act act,
+                                 int32_t stride, float *y, int32_t n, int32_t h, int32_t w, int32_t cin,
+                                 int32_t cout, void *stream) {
+    g_err.clear();
+    if (n < 0 || h < 0 || w < 0)
+        return fail(SPCONV_E_ARG, "n, h and w must be >= 0");
+    if (stride != 1 && stride != 2)
+        return fail(SPCONV_E_ARG, "stride must be 1 or 2");
+    if (act < SPCONV_ACT_NONE || act > SPCONV_ACT_RELU6)
+        return fail(SPCONV_E_ARG, "act must be SPCONV_ACT_NONE, _RELU or _RELU6");
+    if (cin < 1 || cout < 1)
+        return fail(SPCONV_E_SHAPE, "cin and cout must be >= 1");
+    if (cin > 8 || static_cast<int64_t>(cout) * (9 * cin + 1) > 16384)
+        return fail(SPCONV_E_UNSUPPORTED,
+                    "the HWC convolution supports cin <= 8 and cout * (9 cin + 1) <= 16384 (its weights in LDS)");
+    if (static_cast<int64_t>(n) * h * w == 0)
+        return SPCONV_OK;
+    if (!x || !weight || !y)
+        return fail(SPCONV_E_ARG, "x, weight or y is NULL");
+    const int64_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
+    const int64_t xel = static_cast<int64_t>(n) * h * w * cin, yel = static_cast<int64_t>(n) * cout * ho * wo;
+    if (static_cast<int64_t>(n) * ho * wo > (int64_t(1) << 38))
+        return fail(SPCONV_E_SHAPE, "too many output pixels");
+    if (ranges_overlap(x, static_cast<size_t>(xel) * 4, y, static_cast<size_t>(yel) * 4))
+        return fail(SPCONV_E_ARG, "x and y overlap");
+    const hipError_t he = spconv::launch_conv3x3_hwc(x, weight, bias, y, n, h, w, cin, cout, stride,
+                                                     static_cast<int32_t>(act), static_cast<hipStream_t>(stream));
+    return he == hipSuccess ? SPCONV_OK : hip_fail("kernel launch", he);
+}
+
+spconv_status spconv_depthwise3x3(const float *x, const float *weight, const float *bias, spconv_act act,
+                                  int32_t stride, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
+                                  void *stream) {
+    g_err.clear();
+    if (n < 0 || c < 0 || h < 0 || w < 0)
+        return fail(SPCONV_E_ARG, "n, c, h and w must be >= 0");
+    if (stride != 1 && stride != 2)
+        return fail(SPCONV_E_ARG, "stride must be 1 or 2");
+    if (act < SPCONV_ACT_NONE || act > SPCONV_ACT_RELU6)
+        return fail(SPCONV_E_ARG, "act must be SPCONV_ACT_NONE, _RELU or _RELU6");
+    if (static_cast<int64_t>(n) * c * h * w == 0)
+        return SPCONV_OK;
+    if (!x || !weight || !y)
+        return fail(SPCONV_E_ARG, "x, weight or y is NULL");
+    const int64_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
+    const int64_t xel = static_cast<int64_t>(n) * c * h * w, yel = static_cast<int64_t>(n) * c * ho * wo;
+    if (yel > (int64_t(1) << 38))
+        return fail(SPCONV_E_SHAPE, "too many output elements");
+    if (ranges_overlap(x, static_cast<size_t>(xel) * 4, y, static_cast<size_t>(yel) * 4))
+        return fail(SPCONV_E_ARG, "x and y overlap");
+    const hipError_t he = spconv::launch_dw3x3(x, weight, bias, y, n, c, h, w, stride, static_cast<int32_t>(act),
+                                               static_cast<hipStream_t>(stream));
+    return he == hipSuccess ? SPCONV_OK : hip_fail("kernel launch", he);
+}
+
+spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
+                                     void *stream) {
+    g_err.clear();
+    if (n < 0 || c < 0 || h < 0 || w < 0)
+        return fail(SPCONV_E_ARG, "n, c, h and w must be >= 0");
+    if (static_cast<int64_t>(n) * c == 0)
+        return SPCONV_OK;
+    if (static_cast<int64_t>(h) * w == 0)
+        return fail(SPCONV_E_SHAPE, "h * w must be >= 1 to average");
+    if (!x || !y)
+        return fail(SPCONV_E_ARG, "x or y is NULL");
+    const int64_t planes = static_cast<int64_t>(n) * c, hw = static_cast<int64_t>(h) * w;
+    if (planes > (int64_t(1) << 38))
+        return fail(SPCONV_E_SHAPE, "too many planes");
+    if (ranges_overlap(x, static_cast<size_t>(planes * hw) * 4, y, static_cast<size_t>(planes) * 4))
+        return fail(SPCONV_E_ARG, "x and y overlap");
+    const hipError_t he = spconv::launch_gap(x, y, n, c, hw, static_cast<hipStream_t>(stream));
+    return he == hipSuccess ? SPCONV_OK : hip_fail("kernel launch", he);
 }
 
 spconv_status spconv_destroy(spconv_plan plan) {

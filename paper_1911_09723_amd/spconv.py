@@ -29,7 +29,8 @@ _DTYPES = {"f32": F32, "f16": F16}
 EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_error",
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
-            "spconv_plan_create_dense", "spconv_plan_create_fused")
+            "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
+            "spconv_global_avg_pool")
 
 
 class SpconvError(RuntimeError):
@@ -100,6 +101,12 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_create_fused.restype = i32
     lib.spconv_plan_create_fused.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
                                              i32, i32, ctypes.POINTER(spconv_options)]
+    lib.spconv_conv3x3_hwc.restype = i32
+    lib.spconv_conv3x3_hwc.argtypes = [vp, vp, vp, i32, i32, vp, i32, i32, i32, i32, i32, vp]
+    lib.spconv_depthwise3x3.restype = i32
+    lib.spconv_depthwise3x3.argtypes = [vp, vp, vp, i32, i32, vp, i32, i32, i32, i32, vp]
+    lib.spconv_global_avg_pool.restype = i32
+    lib.spconv_global_avg_pool.argtypes = [vp, vp, i32, i32, i32, i32, vp]
     if path is None:
         _lib = lib
     return lib
@@ -237,6 +244,43 @@ def spconv_run(plan, x, y, n, h, w, stream=None, check: bool = True):
     elif not isinstance(stream, int):
         stream = stream.cuda_stream
     status = lib.spconv_run(plan, _devptr(x), _devptr(y), int(n), int(h), int(w), stream or None)
+    if check:
+        _check(status)
+    return status
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return stream if isinstance(stream, int) else stream.cuda_stream
+
+
+def spconv_conv3x3_hwc(x, weight, bias, act, stride, y, n, h, w, cin, cout, stream=None, check: bool = True):
+    """Queue the dense 3x3 HWC -> CHW convolution (device tensors or addresses)."""
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    status = load_library().spconv_conv3x3_hwc(_devptr(x), _devptr(weight), _devptr(bias), a, int(stride),
+                                               _devptr(y), int(n), int(h), int(w), int(cin), int(cout),
+                                               _stream(stream) or None)
+    if check:
+        _check(status)
+    return status
+
+
+def spconv_depthwise3x3(x, weight, bias, act, stride, y, n, c, h, w, stream=None, check: bool = True):
+    """Queue a standalone depthwise 3x3 convolution on CHW tensors."""
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    status = load_library().spconv_depthwise3x3(_devptr(x), _devptr(weight), _devptr(bias), a, int(stride),
+                                                _devptr(y), int(n), int(c), int(h), int(w), _stream(stream) or None)
+    if check:
+        _check(status)
+    return status
+
+
+def spconv_global_avg_pool(x, y, n, c, h, w, stream=None, check: bool = True):
+    """Queue global average pooling [N, C, H, W] -> [N, C]."""
+    status = load_library().spconv_global_avg_pool(_devptr(x), _devptr(y), int(n), int(c), int(h), int(w),
+                                                   _stream(stream) or None)
     if check:
         _check(status)
     return status

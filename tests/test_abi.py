@@ -28,7 +28,7 @@ HEADER = os.path.join(ROOT, "include", "spconv.h")
 def _declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    names = re.findall(r"\b(spconv_[a-z_]+)\s*\(", text)
+    names = re.findall(r"\b(spconv_[a-z0-9_]+)\s*\(", text)
     return sorted(set(names))
 
 

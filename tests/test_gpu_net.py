@@ -1,0 +1,150 @@
+"""GPU parity of the network operators and of a whole MobileNet v1 forward
+pass (runs on an MI355X).
+
+Each operator is compared element by element with the oracle at
+|y_gpu - y_ref| <= 1e-5 * S + 1e-6 (S the sum of absolute terms).  The whole
+network is compared with the oracle's double-precision chain; its
+propagated worst-case scale is astronomically loose after 27 layers, so the
+chain test bounds the logits by 1e-4 * max |logit| instead: a wiring mistake
+(a wrong stride, layer order or buffer) moves logits by the order of the
+logits themselves, while fp32 rounding through the chain moves them by ~1e-6
+relative.  Graph replays must equal eager runs bit for bit (the kernels are
+deterministic).
+"""
+
+import numpy as np
+import pytest
+
+import oracle
+from synth import make_mobilenet_v1, make_image, make_depthwise
+from gpu_util import note, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _sync_np(t):
+    import torch
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def _check(y, y_ref, scale, what):
+    tol = 1e-5 * scale + 1e-6
+    err = np.abs(y.astype(np.float64) - y_ref)
+    bad = int((err > tol).sum())
+    assert y.shape == y_ref.shape, (y.shape, y_ref.shape)
+    assert bad == 0, "%s: %d of %d outside tolerance (worst %.3g)" % (what, bad, err.size, float((err / tol).max()))
+
+
+@pytest.mark.parametrize("n,h,w,cin,cout,stride,act,bias", [
+    (2, 224, 224, 3, 32, 2, "relu6", True),
+    (1, 17, 9, 3, 32, 2, "relu", True),
+    (3, 8, 8, 1, 5, 1, "none", False),
+    (1, 13, 11, 8, 24, 2, "relu6", True),
+    (2, 5, 7, 4, 64, 1, "none", True),
+    (1, 1, 1, 3, 7, 2, "relu", True),
+])
+def test_stem_conv_parity(n, h, w, cin, cout, stride, act, bias):
+    import torch
+    from paper_1911_09723_amd import spconv_conv3x3_hwc
+    rng = np.random.default_rng(h * 31 + w + cin)
+    x = rng.uniform(-1, 1, (n, h, w, cin)).astype(np.float32)
+    wt = (rng.standard_normal((cout, 3, 3, cin)) * 0.3).astype(np.float32)
+    b = (rng.standard_normal(cout) * 0.1).astype(np.float32) if bias else None
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    y = torch.full((n, cout, ho, wo), float("nan"), device="cuda:0")
+    note("stem %s" % ((n, h, w, cin, cout, stride, act, bias),))
+    spconv_conv3x3_hwc(to_gpu(x), to_gpu(wt), None if b is None else to_gpu(b), act, stride, y, n, h, w, cin, cout)
+    y_ref, s = oracle.conv3x3_hwc_ref(x, wt, b, act, stride)
+    _check(_sync_np(y), y_ref, s, "stem")
+
+
+@pytest.mark.parametrize("n,c,h,w,stride,act", [
+    (2, 1024, 7, 7, 1, "relu6"), (1, 64, 112, 112, 2, "relu"), (3, 5, 9, 4, 2, "none"), (1, 3, 1, 1, 1, "relu6"),
+])
+def test_standalone_depthwise_parity(n, c, h, w, stride, act):
+    import torch
+    from paper_1911_09723_amd import spconv_depthwise3x3
+    rng = np.random.default_rng(c + h)
+    x = np.maximum(rng.standard_normal((n, c, h, w)), 0).astype(np.float32)
+    k, b = make_depthwise(c, c + w)
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    y = torch.full((n, c, ho, wo), float("nan"), device="cuda:0")
+    note("depthwise %s" % ((n, c, h, w, stride, act),))
+    spconv_depthwise3x3(to_gpu(x), to_gpu(k), to_gpu(b), act, stride, y, n, c, h, w)
+    d, sd = oracle.dw3x3_ref(x, k, b, act, stride)
+    _check(_sync_np(y), d, sd, "depthwise")
+
+
+@pytest.mark.parametrize("n,c,h,w", [(64, 1024, 7, 7), (3, 5, 1, 1), (2, 7, 13, 3)])
+def test_global_avg_pool_parity(n, c, h, w):
+    import torch
+    from paper_1911_09723_amd import spconv_global_avg_pool
+    rng = np.random.default_rng(n * c)
+    x = rng.standard_normal((n, c, h, w)).astype(np.float32)
+    y = torch.full((n, c), float("nan"), device="cuda:0")
+    note("gap %s" % ((n, c, h, w),))
+    spconv_global_avg_pool(to_gpu(x), y, n, c, h, w)
+    g, gs = oracle.gap_ref(x)
+    _check(_sync_np(y), g, gs, "gap")
+
+
+def test_network_operators_reject_bad_arguments():
+    from paper_1911_09723_amd import spconv, spconv_conv3x3_hwc, spconv_depthwise3x3, spconv_global_avg_pool
+    assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 3, 1 << 42, 1, 4, 4, 3, 8, check=False) == spconv.E_ARG
+    assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 2, 1 << 42, 1, 4, 4, 9, 8, check=False) == \
+        spconv.E_UNSUPPORTED
+    assert spconv_conv3x3_hwc(None, None, None, "relu", 2, None, 0, 4, 4, 3, 8, check=False) == spconv.OK
+    assert spconv_depthwise3x3(1 << 40, 1 << 41, None, "relu", 2, 1 << 40, 1, 4, 4, 4, check=False) == spconv.E_ARG
+    assert spconv_global_avg_pool(1 << 40, 1 << 41, 1, 4, 0, 3, check=False) == spconv.E_SHAPE
+    assert spconv_global_avg_pool(None, None, 0, 4, 3, 3, check=False) == spconv.OK
+
+
+def _engine_case(batch, hw, classes, seed):
+    from paper_1911_09723_amd.mobilenet import MobileNetV1Engine
+    net = make_mobilenet_v1(seed=seed, classes=classes)
+    x = make_image(batch, hw, hw, seed=seed)
+    return net, x, MobileNetV1Engine(net, batch, hw, hw)
+
+
+@pytest.mark.parametrize("batch,hw,classes", [(2, 224, 1000), (3, 32, 10)])
+def test_mobilenet_v1_forward_matches_oracle(batch, hw, classes):
+    net, x, eng = _engine_case(batch, hw, classes, seed=batch)
+    try:
+        note("mobilenet v1 batch %d %dx%d (%d launches, %d fused blocks)" % (batch, hw, hw, eng.launches(),
+                                                                             eng.fused_blocks))
+        assert eng.fused_blocks == 12 and eng.launches() == 1 + 12 + 2 + 2
+        y = _sync_np(eng.forward(to_gpu(x)))
+    finally:
+        eng.close()
+    y_ref, s = oracle.mobilenet_v1_ref(net, x)
+    err = np.abs(y.astype(np.float64) - y_ref)
+    assert np.all(err <= 1e-5 * s + 1e-6)
+    bound = 1e-4 * np.abs(y_ref).max()
+    print("max |logit error| %.3g, bound %.3g" % (err.max(), bound))
+    assert err.max() <= bound
+    assert np.array_equal(y.argmax(axis=1), y_ref.argmax(axis=1))
+
+
+def test_mobilenet_v1_graph_replays_equal_eager_runs():
+    """Capture once, then alternate eager runs and replays on new inputs (with
+    synchronizations between); every replay must equal the eager result."""
+    import torch
+    net, x, eng = _engine_case(4, 64, 16, seed=11)
+    try:
+        note("mobilenet v1 graph capture")
+        ys = []
+        for i in range(3):
+            xi = to_gpu(make_image(4, 64, 64, seed=20 + i))
+            eager = _sync_np(eng.forward(xi)).copy()
+            if eng.graph is None:
+                eng.capture()
+                torch.cuda.synchronize()
+            eng.x.copy_(xi)
+            for _ in range(2):
+                rep = _sync_np(eng.replay()).copy()
+                assert np.array_equal(rep.view(np.uint32), eager.view(np.uint32)), "replay %d differs" % i
+            ys.append(eager)
+        assert not np.array_equal(ys[0], ys[1])
+    finally:
+        eng.close()
