@@ -9,7 +9,9 @@ the paper's layer shapes (no trained weights or images are used).
 
 One step = one spconv_run over the whole batch (bias and activation fused).
 A third variant runs the same 1x1 behind a fused depthwise 3x3 (stride 1,
-ReLU6): one MobileNet v1 block at 512 channels.
+ReLU6): one MobileNet v1 block at 512 channels.  The ``network`` entries time
+a whole synthetic MobileNet v1 forward pass (17 launches replayed as one
+graph) at batch 1 and 64.
 Inputs are resident in HBM before timing starts; three (X, Y) buffer sets,
 616 MB in all, rotate so no step finds its operands in the 256 MB
 last-level cache.  Kernel durations come from HIP events recorded on the
@@ -132,6 +134,44 @@ def time_variant(layer, steps, warmup, sets, dw=None):
     del xs, ys
     torch.cuda.empty_cache()
     return dict(region_ms=region_ms, wall_s=wall, kernel_ms=kern_ms, info=info)
+
+
+def time_network(batch, steps, warmup, graph=True):
+    """Whole MobileNet v1 forward passes (synthetic 90%-sparse weights,
+    224 x 224 images) replayed as one captured graph; per-replay time from
+    HIP events on the replay stream."""
+    import numpy as np
+    import torch
+    from paper_1911_09723_amd.mobilenet import MobileNetV1Engine
+    from synth import make_mobilenet_v1, make_image
+
+    net = make_mobilenet_v1(seed=0)
+    eng = MobileNetV1Engine(net, batch)
+    eng.x.copy_(torch.from_numpy(make_image(batch, seed=0)).to(eng.x.device))
+    if graph:
+        eng.capture()
+    run = eng.replay if graph else eng.forward
+    stream = torch.cuda.current_stream()
+    for _ in range(warmup):
+        run()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev[i][0].record(stream)
+        run()
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    ms = np.array([a.elapsed_time(b) for a, b in ev])
+    launches = eng.launches()
+    layers = list(eng.layers)
+    eng.close()
+    torch.cuda.empty_cache()
+    return {
+        "model": "MobileNet v1 1.0 224x224, 90%-sparse pointwise layers, synthetic weights",
+        "batch": batch, "graph": graph, "launches": launches, "layers": layers,
+        "ms_per_batch_mean": round(float(ms.mean()), 4), "ms_per_batch_min": round(float(ms.min()), 4),
+        "images_per_s": round(batch / (float(ms.mean()) / 1e3), 1),
+    }
 
 
 def cpu_baseline(layer, budget_s=12.0):
@@ -311,6 +351,8 @@ def main():
     ap.add_argument("--profile-run", action="store_true", help="launches for rocprofv3 counter passes")
     ap.add_argument("--reps", type=int, default=5, help="launches per variant in --profile-run")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--network-run", action="store_true",
+                    help="only the MobileNet v1 graph replays (batch 64), for rocprofv3 kernel traces")
     ap.add_argument("--command", action="append", default=[], help="command lines recorded in the summary")
     ap.add_argument("--out", default=TRAFFIC_BASE, help="output path (without extension) of --traffic-summary")
     args = ap.parse_args()
@@ -328,6 +370,9 @@ def main():
     if args.profile_run:
         profile_run(args.reps)
         return
+    if args.network_run:
+        print(json.dumps(time_network(64, args.steps, args.warmup)), flush=True)
+        return
 
     layers = headline_layers()
     results = {}
@@ -342,6 +387,12 @@ def main():
     r = time_variant(layers["1x1"], args.steps, args.warmup, args.sets, dw=fused_layer(layers["1x1"]))
     results[tag] = summarize(layers["1x1"], r, dw=True)
     log("bench: %s %s" % (tag, json.dumps(results[tag])))
+
+    network = []
+    for batch in (1, 64):
+        log("bench: MobileNet v1 forward, batch %d, graph replays" % batch)
+        network.append(time_network(batch, 50, 5))
+        log("bench: network %s" % json.dumps({k: v for k, v in network[-1].items() if k != "layers"}))
 
     head = results["1x1"]
     layer = layers["1x1"]
@@ -376,6 +427,7 @@ def main():
             "traffic": None if traffic is None else traffic.get("bytes_per_launch"),
         },
         "variants": results,
+        "network": network,
         "device": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:

@@ -255,6 +255,33 @@ struct TileAddr {
     }
 };
 
+// Per-element X offsets of a lane's columns for the direct kernel without
+// 16-byte vectors (H*W not a multiple of the vector width): byte offset of
+// column (vector vb[j], element e) from channel 0 of the tile's first image,
+// kOutOfRange past the last column.  Computed once per tile, so the inner
+// loop reads X with one buffer load per element and no division.
+template <int G, bool F16, bool ON>
+struct ColOff {
+    __device__ __forceinline__ void set(const Args &, const Lane<G, F16> &, int32_t) {}
+};
+template <int G, bool F16>
+struct ColOff<G, F16, true> {
+    using GE = Geo<G, F16>;
+    int32_t xe[GE::V][GE::QE];
+    __device__ __forceinline__ void set(const Args &a, const Lane<G, F16> &L, int32_t tile) {
+        const int32_t col0 = tile * GE::TC;
+        const int32_t n0 = col0 / a.hw;
+#pragma unroll
+        for (int j = 0; j < GE::V; ++j)
+#pragma unroll
+            for (int e = 0; e < GE::QE; ++e) {
+                const int32_t c = col0 + L.vb[j] * GE::QE + e;
+                const int32_t n = c / a.hw;
+                xe[j][e] = c < a.m ? ((n - n0) * a.cin * a.hw + (c - n * a.hw)) * GE::E : kOutOfRange;
+            }
+    }
+};
+
 __device__ __forceinline__ void bstore16(u4 v, Rsrc r, int32_t voff) {
     // plain write-back stores: the lane groups' pieces of a 128-byte line meet in L2
     __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, 0, 0);
@@ -335,24 +362,23 @@ __device__ __forceinline__ void finish_rows(const Args &a, const Lane<G, F16> &L
 // kernel, o = channel) from global memory.
 template <int G, bool F16, bool DIRECT, bool VEC>
 __device__ __forceinline__ u4 read_x(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
-                                     const typename Geo<G, F16>::T *x, const unsigned char *lds, uint32_t o,
-                                     int j) {
+                                     const ColOff<G, F16, DIRECT && !VEC> &co, const unsigned char *lds,
+                                     uint32_t o, int j) {
     using GE = Geo<G, F16>;
     using T = typename GE::T;
     if constexpr (DIRECT) {
+        const int32_t ro = static_cast<int32_t>(o) * a.hw * GE::E;  // channel o's plane
         if constexpr (VEC) {
-            return bload16(ta.rx, ta.xo[j] + static_cast<int32_t>(__umul24(o, a.hw * GE::E)), 0);
+            return bload16(ta.rx, ta.xo[j] + ro, 0);
         } else {
-            // any HW: element by element
+            // any HW: element by element (past the last column: zero)
             T v[GE::QE];
 #pragma unroll
             for (int e = 0; e < GE::QE; ++e) {
-                const int32_t c = ta.col0 + L.vb[j] * GE::QE + e;
-                v[e] = T(0);
-                if (c < a.m) {
-                    const int32_t n = c / a.hw;
-                    v[e] = x[(static_cast<int64_t>(n) * a.cin + o) * a.hw + (c - n * a.hw)];
-                }
+                if constexpr (F16)
+                    v[e] = __builtin_bit_cast(_Float16, __builtin_amdgcn_raw_buffer_load_b16(ta.rx, co.xe[j][e] + ro, 0, 0));
+                else
+                    v[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ta.rx, co.xe[j][e] + ro, 0, 0));
             }
             return *reinterpret_cast<const u4 *>(v);
         }
@@ -368,7 +394,7 @@ __device__ __forceinline__ u4 read_x(const Args &a, const Lane<G, F16> &L, const
 
 template <int G, int K, bool F16, bool DIRECT, bool VEC>
 __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
-                                           const typename Geo<G, F16>::T *x, typename Geo<G, F16>::T *y,
+                                           const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                            const unsigned char *lds, Rsrc ri, Rsrc rv,
                                            const int32_t *__restrict__ hdr, const int32_t *rows_lds,
                                            const float *bias_lds, int32_t b0, int32_t b1, float lo, float hi) {
@@ -415,7 +441,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
                     u4 xr[GE::V];
 #pragma unroll
                     for (int j = 0; j < GE::V; ++j)
-                        xr[j] = read_x<G, F16, DIRECT, VEC>(a, L, ta, x, lds, cr[KI].off[U], j);
+                        xr[j] = read_x<G, F16, DIRECT, VEC>(a, L, ta, co, lds, cr[KI].off[U], j);
                     fma_slot<G, K, F16, U>(acc, cr[KI], xr);
                 });
                 if (--left == 0) {
@@ -432,7 +458,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
 // bundles of rank % tail_parts == part (shared tile), one run each.
 template <int G, int K, bool F16, bool DIRECT, bool VEC>
 __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
-                                         const typename Geo<G, F16>::T *x, typename Geo<G, F16>::T *y,
+                                         const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                          const unsigned char *lds, Rsrc ri, Rsrc rv, const int32_t *__restrict__ hdr,
                                          const int32_t *__restrict__ rank, const int32_t *rows_lds,
                                          const float *bias_lds, int32_t wb0, int32_t wb1, int32_t part, float lo,
@@ -454,7 +480,7 @@ __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, c
             b1 = bnext + 1;
         }
         bnext = b1;
-        run_simple<G, K, F16, DIRECT, VEC>(a, L, ta, x, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo, hi);
+        run_simple<G, K, F16, DIRECT, VEC>(a, L, ta, co, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo, hi);
     }
 }
 
@@ -796,6 +822,7 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
     Work wk = first_work(a);
     __syncthreads();  // table ready
     TileAddr<G, F16> ta;
+    ColOff<G, F16, DIRECT && !VEC> co;
     while (wk.tile >= 0) {
         ta.set(a, L, x, y, wk.tile);
         if constexpr (!DIRECT) {
@@ -812,7 +839,8 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
                                                lane);
             __syncthreads();  // strip ready
         }
-        run_item<G, K, F16, DIRECT, VEC>(a, L, ta, x, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
+        co.set(a, L, wk.tile);
+        run_item<G, K, F16, DIRECT, VEC>(a, L, ta, co, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
                                          wk.part, lo, hi);
         const Work nx = next_work(a, wk);
         if constexpr (!DIRECT)
@@ -1113,8 +1141,8 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         __syncthreads();  // strip ready
         const Rsrc ri = make_rsrc(idx, static_cast<uint32_t>(a.idx_bytes));
         const Rsrc rv = make_rsrc(val, static_cast<uint32_t>(a.val_bytes));
-        run_item<G, K, F16, false, true>(a, L, ta, x, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
-                                         wk.part, lo, hi);
+        run_item<G, K, F16, false, true>(a, L, ta, ColOff<G, F16, false>{}, y, lds, ri, rv, hdr, rank, rows_lds,
+                                         bias_lds, wb0, wb1, wk.part, lo, hi);
     }
 }
 
