@@ -210,6 +210,17 @@ spconv_status spconv_depthwise3x3(const float *x, const float *weight, const flo
                                   void *stream);
 
 /*
+ * Dense fully connected layer (the network's classifier, kept dense as in
+ * Sec. 3.1 / Table 1):  y[n, r] = act( bias[r] + sum_c weight[r][c] * x[n][c] ),
+ * fp32 FMA in ascending c.  x [n][cin], weight [cout][cin] row-major, bias
+ * [cout] or NULL, y [n][cout].
+ * Errors: SPCONV_E_ARG (NULL pointer with work to do, negative size, bad act,
+ * overlap), SPCONV_E_SHAPE (cin == 0 with outputs, n > 262140), SPCONV_E_HIP.
+ */
+spconv_status spconv_linear(const float *x, const float *weight, const float *bias, spconv_act act, float *y,
+                            int32_t n, int32_t cin, int32_t cout, void *stream);
+
+/*
  * Global average pooling: y[n, c] = (1 / (h w)) * sum_p x[n, c, p], summed in
  * ascending p in fp32.  x [n][c][h][w], y [n][c].
  * Errors: SPCONV_E_ARG, SPCONV_E_SHAPE (h * w == 0 with n * c > 0), SPCONV_E_HIP.

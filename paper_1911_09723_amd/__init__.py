@@ -18,6 +18,7 @@ from .spconv import (  # noqa: F401
     spconv_global_avg_pool,
     spconv_detect_block_rows,
     spconv_last_error,
+    spconv_linear,
     spconv_options_init,
     spconv_plan_create,
     spconv_plan_create_dense,

@@ -1,8 +1,8 @@
 // gfx950 kernels for the CHW operators around the sparse 1x1 in a MobileNet
 // (Fast Sparse ConvNets, Sec. 3.1 and Sec. 3.3): the dense 3x3 convolution
 // that reads the HWC image and writes CHW, a standalone depthwise 3x3 (for
-// layers whose strip does not fit the fused strip kernel), and global
-// average pooling.  All three are memory-bound elementwise-style kernels:
+// layers whose strip does not fit the fused strip kernel), global average
+// pooling and the dense classifier.  All three are memory-bound elementwise-style kernels:
 // one thread per output element (per output pixel for the convolution), fp32
 // arithmetic, zero padding 1.
 #include <hip/hip_runtime.h>
@@ -13,6 +13,8 @@
 
 namespace spconv {
 namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float clamp_act(float v, int32_t act) {
     const float lo = act == 0 ? -__builtin_huge_valf() : 0.0f;
@@ -118,6 +120,56 @@ gap_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t planes, i
     y[q] = acc * inv;
 }
 
+// Dense fully connected layer (the classifier the paper keeps dense, Sec. 3.1):
+//   y[n, r] = act(b[r] + sum_c W[r, c] * x[n, c]),  W row-major [cout][cin].
+// A wavefront owns 64 consecutive rows (lane = row) and kImg images: each W
+// load feeds kImg FMAs, the x loads are the same address in every lane (one
+// line per instruction), and the stores are consecutive rows.  VEC: 16-byte
+// loads (cin a multiple of 4, pointers 16-byte aligned).  fp32 FMA in
+// ascending c from zero, then the bias, then the activation.
+constexpr int kImg = 4;
+
+template <bool VEC>
+__global__ void __launch_bounds__(64)
+linear_kernel(const float *__restrict__ x, const float *__restrict__ wt, const float *__restrict__ bias,
+              float *__restrict__ y, int32_t n, int32_t cin, int32_t cout, int32_t act) {
+    const int32_t r = blockIdx.x * 64 + threadIdx.x;
+    const int32_t n0 = blockIdx.y * kImg;
+    const int32_t rr = r < cout ? r : cout - 1;  // past the last row: compute row cout - 1, store nothing
+    const float *wr = wt + static_cast<int64_t>(rr) * cin;
+    const float *xi[kImg];
+#pragma unroll
+    for (int i = 0; i < kImg; ++i)
+        xi[i] = x + static_cast<int64_t>(n0 + i < n ? n0 + i : n - 1) * cin;
+    float acc[kImg] = {};
+    if constexpr (VEC) {
+        for (int32_t c = 0; c < cin; c += 4) {
+            const f4 wv = *reinterpret_cast<const f4 *>(wr + c);
+#pragma unroll
+            for (int i = 0; i < kImg; ++i) {
+                const f4 xv = *reinterpret_cast<const f4 *>(xi[i] + c);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    acc[i] = __builtin_fmaf(wv[e], xv[e], acc[i]);
+            }
+        }
+    } else {
+        for (int32_t c = 0; c < cin; ++c) {
+            const float wv = wr[c];
+#pragma unroll
+            for (int i = 0; i < kImg; ++i)
+                acc[i] = __builtin_fmaf(wv, xi[i][c], acc[i]);
+        }
+    }
+    if (r >= cout)
+        return;
+    const float b = bias ? bias[r] : 0.0f;
+#pragma unroll
+    for (int i = 0; i < kImg; ++i)
+        if (n0 + i < n)
+            y[static_cast<int64_t>(n0 + i) * cout + r] = clamp_act(acc[i] + b, act);
+}
+
 using ConvFn = void (*)(const float *, const float *, const float *, float *, int64_t, int32_t, int32_t, int32_t,
                         int32_t, int32_t, int32_t, int32_t);
 
@@ -161,6 +213,18 @@ hipError_t launch_dw3x3(const float *x, const float *k, const float *bias, float
     const int64_t blocks = (total + kThreads - 1) / kThreads;
     hipLaunchKernelGGL(dw3x3_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, x, k, bias,
                        y, total, c, h, w, ho, wo, stride, act);
+    return hipGetLastError();
+}
+
+hipError_t launch_linear(const float *x, const float *wt, const float *bias, float *y, int32_t n, int32_t cin,
+                         int32_t cout, int32_t act, hipStream_t stream) {
+    const bool vec = cin % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                     reinterpret_cast<uintptr_t>(wt) % 16 == 0;
+    const dim3 grid(static_cast<unsigned>((cout + 63) / 64), static_cast<unsigned>((n + kImg - 1) / kImg));
+    if (vec)
+        hipLaunchKernelGGL(linear_kernel<true>, grid, dim3(64), 0, stream, x, wt, bias, y, n, cin, cout, act);
+    else
+        hipLaunchKernelGGL(linear_kernel<false>, grid, dim3(64), 0, stream, x, wt, bias, y, n, cin, cout, act);
     return hipGetLastError();
 }
 

@@ -448,6 +448,28 @@ spconv_status spconv_depthwise3x3(const float *x, const float *weight, const flo
     return he == hipSuccess ? SPCONV_OK : hip_fail("kernel launch", he);
 }
 
+spconv_status spconv_linear(const float *x, const float *weight, const float *bias, spconv_act act, float *y,
+                            int32_t n, int32_t cin, int32_t cout, void *stream) {
+    g_err.clear();
+    if (n < 0 || cin < 0 || cout < 0)
+        return fail(SPCONV_E_ARG, "n, cin and cout must be >= 0");
+    if (act < SPCONV_ACT_NONE || act > SPCONV_ACT_RELU6)
+        return fail(SPCONV_E_ARG, "act must be SPCONV_ACT_NONE, _RELU or _RELU6");
+    if (static_cast<int64_t>(n) * cout == 0)
+        return SPCONV_OK;
+    if (cin == 0)
+        return fail(SPCONV_E_SHAPE, "cin must be >= 1");
+    if ((static_cast<int64_t>(n) + 3) / 4 > 65535)
+        return fail(SPCONV_E_SHAPE, "n must be at most 262140");
+    if (!x || !weight || !y)
+        return fail(SPCONV_E_ARG, "x, weight or y is NULL");
+    if (ranges_overlap(x, static_cast<size_t>(n) * cin * 4, y, static_cast<size_t>(n) * cout * 4))
+        return fail(SPCONV_E_ARG, "x and y overlap");
+    const hipError_t he = spconv::launch_linear(x, weight, bias, y, n, cin, cout, static_cast<int32_t>(act),
+                                                static_cast<hipStream_t>(stream));
+    return he == hipSuccess ? SPCONV_OK : hip_fail("kernel launch", he);
+}
+
 spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
                                      void *stream) {
     g_err.clear();

@@ -6,8 +6,8 @@ ReLU6); 13 blocks of depthwise 3x3 -> sparse 1x1 (ReLU6 after each), each one
 fused plan (``spconv_plan_create_fused``) -- a block whose input strip does
 not fit in LDS (the 1024-channel one) runs ``spconv_depthwise3x3`` and then a
 plain plan on the direct-load kernel; global average pooling
-(``spconv_global_avg_pool``); the dense classifier as a 1x1 plan over 1 x 1
-images (``spconv_plan_create_dense``, no activation).
+(``spconv_global_avg_pool``); the dense classifier (``spconv_linear``, no
+activation).
 
 Every step is one kernel launch on the caller's (torch's current) stream;
 nothing is allocated after construction.  ``capture`` records the whole
@@ -21,7 +21,7 @@ from __future__ import annotations
 from typing import List, Optional
 
 from .spconv import (E_UNSUPPORTED, Plan, SpconvError, spconv_conv3x3_hwc, spconv_depthwise3x3,
-                     spconv_global_avg_pool, spconv_run)
+                     spconv_global_avg_pool, spconv_linear, spconv_run)
 
 
 class MobileNetV1Engine:
@@ -82,10 +82,11 @@ class MobileNetV1Engine:
         self._steps.append(lambda: spconv_global_avg_pool(last, pooled, batch, ch, hh, ww))
         self.layers.append("global average pool %d @%dx%d" % (ch, hh, ww))
         self.classes = int(net.fc_w.shape[0])
-        fc = Plan.from_dense(net.fc_w, 0, net.fc_b, "none")
+        fc_w, fc_b = put(net.fc_w), put(net.fc_b)
         self.logits = torch.empty((batch, self.classes), dtype=f32, device=dev)
-        self._keep += [fc]
-        self._steps.append(self._run_step(fc, pooled, self.logits, batch, 1, 1))
+        self._keep += [fc_w, fc_b]
+        logits, classes = self.logits, self.classes
+        self._steps.append(lambda: spconv_linear(pooled, fc_w, fc_b, "none", logits, batch, ch, classes))
         self.layers.append("dense fc %d->%d" % (ch, self.classes))
         self.graph = None
 

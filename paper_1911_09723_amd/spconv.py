@@ -30,7 +30,7 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
-            "spconv_global_avg_pool")
+            "spconv_global_avg_pool", "spconv_linear")
 
 
 class SpconvError(RuntimeError):
@@ -105,6 +105,8 @@ def load_library(path: Optional[str] = None):
     lib.spconv_conv3x3_hwc.argtypes = [vp, vp, vp, i32, i32, vp, i32, i32, i32, i32, i32, vp]
     lib.spconv_depthwise3x3.restype = i32
     lib.spconv_depthwise3x3.argtypes = [vp, vp, vp, i32, i32, vp, i32, i32, i32, i32, vp]
+    lib.spconv_linear.restype = i32
+    lib.spconv_linear.argtypes = [vp, vp, vp, i32, vp, i32, i32, i32, vp]
     lib.spconv_global_avg_pool.restype = i32
     lib.spconv_global_avg_pool.argtypes = [vp, vp, i32, i32, i32, i32, vp]
     if path is None:
@@ -272,6 +274,16 @@ def spconv_depthwise3x3(x, weight, bias, act, stride, y, n, c, h, w, stream=None
     a = _ACTS[act] if isinstance(act, str) else int(act)
     status = load_library().spconv_depthwise3x3(_devptr(x), _devptr(weight), _devptr(bias), a, int(stride),
                                                 _devptr(y), int(n), int(c), int(h), int(w), _stream(stream) or None)
+    if check:
+        _check(status)
+    return status
+
+
+def spconv_linear(x, weight, bias, act, y, n, cin, cout, stream=None, check: bool = True):
+    """Queue the dense fully connected layer y = act(x W^T + b)."""
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    status = load_library().spconv_linear(_devptr(x), _devptr(weight), _devptr(bias), a, _devptr(y), int(n),
+                                          int(cin), int(cout), _stream(stream) or None)
     if check:
         _check(status)
     return status

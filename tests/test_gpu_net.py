@@ -89,8 +89,32 @@ def test_global_avg_pool_parity(n, c, h, w):
     _check(_sync_np(y), g, gs, "gap")
 
 
+@pytest.mark.parametrize("n,cin,cout,act,bias,offset", [
+    (64, 1024, 1000, "none", True, 0), (3, 7, 130, "relu6", True, 0), (5, 64, 64, "relu", False, 1),
+    (1, 1, 1, "none", True, 0),
+])
+def test_linear_parity(n, cin, cout, act, bias, offset):
+    """Against the oracle's 1x1 over 1 x 1 images with the dense weight as CSR;
+    offset 1 misaligns x (the element-by-element path)."""
+    import torch
+    from paper_1911_09723_amd import spconv_linear
+    rng = np.random.default_rng(n + cin + cout)
+    x = rng.standard_normal((n, cin)).astype(np.float32)
+    wt = (rng.standard_normal((cout, cin)) / np.sqrt(cin)).astype(np.float32)
+    b = rng.standard_normal(cout).astype(np.float32) if bias else None
+    xb = to_gpu(np.concatenate([np.zeros(offset, np.float32), x.ravel()]))[offset:]
+    y = torch.full((n, cout), float("nan"), device="cuda:0")
+    note("linear %s" % ((n, cin, cout, act, bias, offset),))
+    spconv_linear(xb, to_gpu(wt), None if b is None else to_gpu(b), act, y, n, cin, cout)
+    rp = np.arange(0, cout * cin + 1, cin, dtype=np.int32)
+    ci = np.tile(np.arange(cin, dtype=np.int32), cout)
+    _, y64, s = oracle.spconv_ref(cout, cin, 1, rp, ci, wt.ravel(), b, act, x.reshape(n, cin, 1, 1))
+    _check(_sync_np(y), y64.reshape(n, cout), s.reshape(n, cout), "linear")
+
+
 def test_network_operators_reject_bad_arguments():
-    from paper_1911_09723_amd import spconv, spconv_conv3x3_hwc, spconv_depthwise3x3, spconv_global_avg_pool
+    from paper_1911_09723_amd import (spconv, spconv_conv3x3_hwc, spconv_depthwise3x3, spconv_global_avg_pool,
+                                      spconv_linear)
     assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 3, 1 << 42, 1, 4, 4, 3, 8, check=False) == spconv.E_ARG
     assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 2, 1 << 42, 1, 4, 4, 9, 8, check=False) == \
         spconv.E_UNSUPPORTED
@@ -98,6 +122,9 @@ def test_network_operators_reject_bad_arguments():
     assert spconv_depthwise3x3(1 << 40, 1 << 41, None, "relu", 2, 1 << 40, 1, 4, 4, 4, check=False) == spconv.E_ARG
     assert spconv_global_avg_pool(1 << 40, 1 << 41, 1, 4, 0, 3, check=False) == spconv.E_SHAPE
     assert spconv_global_avg_pool(None, None, 0, 4, 3, 3, check=False) == spconv.OK
+    assert spconv_linear(1 << 40, 1 << 41, None, "none", 1 << 42, 2, 0, 5, check=False) == spconv.E_SHAPE
+    assert spconv_linear(1 << 40, 1 << 41, None, "none", 1 << 42, 300000, 4, 5, check=False) == spconv.E_SHAPE
+    assert spconv_linear(None, None, None, "none", None, 0, 4, 5, check=False) == spconv.OK
 
 
 def _engine_case(batch, hw, classes, seed):
