@@ -58,6 +58,13 @@ def load_library(path: str):
         ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
         ctypes.c_void_p, ctypes.c_void_p,
     ]
+    lib.spconv_ref_run_blocked.restype = ctypes.c_int
+    lib.spconv_ref_run_blocked.argtypes = [
+        ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+        ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int64,
+        ctypes.c_void_p, ctypes.c_void_p,
+    ]
     lib.spconv_ref_run_f64.restype = ctypes.c_int
     lib.spconv_ref_run_f64.argtypes = [
         ctypes.c_int32, ctypes.c_int32, ctypes.c_int32,
@@ -116,7 +123,7 @@ def _ptr(a):
 
 
 def spconv_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x,
-               storage: str = "f32", with_scale: bool = True, lib=None):
+               storage: str = "f32", with_scale: bool = True, lib=None, block_cols: int = 1):
     """Run the oracle.
 
     ``x`` is [N, Cin, H, W] (or [N, Cin, HW]) float32 for storage "f32" and
@@ -124,6 +131,8 @@ def spconv_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x,
     storage type with the shape [N, Cout, ...] of ``x``, ``y64`` the unrounded
     double values, ``scale`` the error scale (or None).  ``lib`` selects
     another build of the oracle (the tests' planted-mistake builds).
+    ``block_cols`` > 1: blocks of block_rows output x block_cols input
+    channels, values[(t * block_rows + i) * block_cols + j].
     """
     lib = _load() if lib is None else lib
     row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
@@ -145,9 +154,14 @@ def spconv_ref(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, x,
     hw = int(np.prod(spatial)) if len(spatial) else 1
     y64 = np.empty((n, cout, hw), dtype=np.float64)
     scale = np.empty((n, cout, hw), dtype=np.float64) if with_scale else None
-    rc = lib.spconv_ref_run(int(cout), int(cin), int(block_rows), _ptr(row_ptr), _ptr(col_idx),
-                            _ptr(values), _ptr(bias_a), _ACTS[act], _ptr(xbits), f16,
-                            int(n), int(hw), _ptr(y64), _ptr(scale))
+    if block_cols == 1:
+        rc = lib.spconv_ref_run(int(cout), int(cin), int(block_rows), _ptr(row_ptr), _ptr(col_idx),
+                                _ptr(values), _ptr(bias_a), _ACTS[act], _ptr(xbits), f16,
+                                int(n), int(hw), _ptr(y64), _ptr(scale))
+    else:
+        rc = lib.spconv_ref_run_blocked(int(cout), int(cin), int(block_rows), int(block_cols), _ptr(row_ptr),
+                                        _ptr(col_idx), _ptr(values), _ptr(bias_a), _ACTS[act], _ptr(xbits), f16,
+                                        int(n), int(hw), _ptr(y64), _ptr(scale))
     if rc != 0:
         raise ValueError("oracle rejected the input (code %d)" % rc)
     y = y64.astype(np.float16 if storage == "f16" else np.float32)

@@ -79,7 +79,7 @@ static double apply_act(double v, int act)
  * NULL): a per-input-element error scale of x itself, added to the output
  * scale as |W[r, c]| * xs[n, c, p] (used when x is the exact output of an
  * earlier stage that the GPU evaluates in fp32). */
-static int ref_spmm(int32_t cout, int32_t cin, int32_t k,
+static int ref_spmm(int32_t cout, int32_t cin, int32_t k, int32_t kc,
                     const int32_t *row_ptr, const int32_t *col_idx,
                     const float *values, const float *bias, int32_t act,
                     const void *x, int32_t x_kind, const double *xs, int64_t n, int64_t hw,
@@ -88,7 +88,7 @@ static int ref_spmm(int32_t cout, int32_t cin, int32_t k,
     const int32_t rows = cout / k;
     int bad = 0;
     for (int32_t t = 0; t < row_ptr[rows]; ++t)
-        if (col_idx[t] < 0 || col_idx[t] >= cin)
+        if (col_idx[t] < 0 || (int64_t)col_idx[t] + kc > cin)
             bad = 1;
     if (bad)
         return -1;
@@ -113,20 +113,23 @@ static int ref_spmm(int32_t cout, int32_t cin, int32_t k,
                         acc[p] = 0.0;
                         s[p] = 0.0;
                     }
-                    /* stored order: ascending input channel for a valid CSR */
+                    /* stored order: ascending input channel for a valid CSR
+                     * (blocks in order, the kc channels of a block ascending) */
                     for (int32_t t = row_ptr[rb]; t < row_ptr[rb + 1]; ++t) {
-                        const int64_t c = col_idx[t];
-                        const double wv = (double)values[(int64_t)t * k + i];
-                        const int64_t xrow = (img * cin + c) * hw;
-                        for (int64_t p = 0; p < hw; ++p) {
-                            const double xv = x_kind == 2 ? ((const double *)x)[xrow + p]
-                                : x_kind == 1 ? spconv_ref_half_to_double(((const uint16_t *)x)[xrow + p])
-                                : (double)((const float *)x)[xrow + p];
-                            const double prod = wv * xv;
-                            acc[p] += prod;
-                            s[p] += fabs(prod);
-                            if (xs)
-                                s[p] += fabs(wv) * xs[xrow + p];
+                        for (int32_t j = 0; j < kc; ++j) {
+                            const int64_t c = (int64_t)col_idx[t] + j;
+                            const double wv = (double)values[((int64_t)t * k + i) * kc + j];
+                            const int64_t xrow = (img * cin + c) * hw;
+                            for (int64_t p = 0; p < hw; ++p) {
+                                const double xv = x_kind == 2 ? ((const double *)x)[xrow + p]
+                                    : x_kind == 1 ? spconv_ref_half_to_double(((const uint16_t *)x)[xrow + p])
+                                    : (double)((const float *)x)[xrow + p];
+                                const double prod = wv * xv;
+                                acc[p] += prod;
+                                s[p] += fabs(prod);
+                                if (xs)
+                                    s[p] += fabs(wv) * xs[xrow + p];
+                            }
                         }
                     }
                     const double b = bias ? (double)bias[r] : 0.0;
@@ -155,7 +158,24 @@ int spconv_ref_run(int32_t cout, int32_t cin, int32_t k,
                    const void *x, int32_t x_f16, int64_t n, int64_t hw,
                    double *y, double *scale)
 {
-    return ref_spmm(cout, cin, k, row_ptr, col_idx, values, bias, act, x, x_f16 ? 1 : 0, NULL, n, hw, y,
+    return ref_spmm(cout, cin, k, 1, row_ptr, col_idx, values, bias, act, x, x_f16 ? 1 : 0, NULL, n, hw, y,
+                    scale);
+}
+
+/* The same with blocks of k output channels x kc input channels (Sec. 3.2
+ * names the block shapes, Fig. 5 compares 1x4, 4x1 and 2x2 blocks):
+ * col_idx[t] is the first input channel of block t and
+ * values[(t * k + i) * kc + j] = W[rb * k + i, col_idx[t] + j]; a block
+ * must lie inside [0, cin).  kc = 1 is spconv_ref_run. */
+int spconv_ref_run_blocked(int32_t cout, int32_t cin, int32_t k, int32_t kc,
+                           const int32_t *row_ptr, const int32_t *col_idx,
+                           const float *values, const float *bias, int32_t act,
+                           const void *x, int32_t x_f16, int64_t n, int64_t hw,
+                           double *y, double *scale)
+{
+    if (kc < 1)
+        return -1;
+    return ref_spmm(cout, cin, k, kc, row_ptr, col_idx, values, bias, act, x, x_f16 ? 1 : 0, NULL, n, hw, y,
                     scale);
 }
 
@@ -167,7 +187,7 @@ int spconv_ref_run_f64(int32_t cout, int32_t cin, int32_t k,
                        const double *x, const double *xs, int64_t n, int64_t hw,
                        double *y, double *scale)
 {
-    return ref_spmm(cout, cin, k, row_ptr, col_idx, values, bias, act, x, 2, xs, n, hw, y, scale);
+    return ref_spmm(cout, cin, k, 1, row_ptr, col_idx, values, bias, act, x, 2, xs, n, hw, y, scale);
 }
 
 /*

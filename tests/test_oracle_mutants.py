@@ -16,13 +16,14 @@ import pytest
 
 import oracle
 from synth import make_layer, densify
+from blocks_util import dense_from_blocks, random_blocks
 
 SRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "oracle", "spconv_ref.c")
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
 
 MUTANTS = {
     "sign_of_term": ("acc[p] += prod;", "acc[p] -= prod;"),
-    "block_value_index": ("values[(int64_t)t * k + i]", "values[(int64_t)t * k]"),
+    "block_value_index": ("values[((int64_t)t * k + i) * kc + j]", "values[((int64_t)t * k) * kc + j]"),
     "bias_index": ("(double)bias[r]", "(double)bias[rb]"),
     "x_transposed": ("(img * cin + c) * hw", "(c * n + img) * hw"),
     "dropped_first_term": ("t = row_ptr[rb]; t < row_ptr[rb + 1]", "t = row_ptr[rb] + 1; t < row_ptr[rb + 1]"),
@@ -41,6 +42,10 @@ MUTANTS = {
     "dw_scale_signed": ("spconv_ref_dw3x3", "            s += fabs(prod);", "            s += prod;"),
     "dw_border_taps_kept": ("spconv_ref_dw3x3", "if (ix < 0 || ix >= w)", "if (ix < 0 || ix > w)"),
     "input_scale_dropped": ("s[p] += fabs(wv) * xs[xrow + p];", "s[p] += 0.0;"),
+    # input-channel blocks
+    "input_block_channel": ("const int64_t c = (int64_t)col_idx[t] + j;", "const int64_t c = (int64_t)col_idx[t];"),
+    "input_block_value_order": ("values[((int64_t)t * k + i) * kc + j]", "values[((int64_t)t * k + i) * kc + (kc - 1 - j)]"),
+    "input_block_last_dropped": ("for (int32_t j = 0; j < kc; ++j)", "for (int32_t j = 0; j + 1 < kc; ++j)"),
     # the network-level stages: (function, anchor inside it, replacement)
     "dw64_tap_row_offset": ("spconv_ref_dw3x3_f64", "oy * stride + dy - 1", "oy * stride + dy"),
     "dw64_input_scale_dropped": ("spconv_ref_dw3x3_f64", "s += fabs(kv) * xs[plane + iy * w + ix];", "s += 0.0;"),
@@ -104,6 +109,7 @@ def _battery(lib):
             failed.append("brute-scale:k%d:%s" % (k, storage))
     failed += _dw_battery(lib)
     failed += _net_battery(lib)
+    failed += _block_battery(lib)
     bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
     ref = bits.view(np.float16).astype(np.float64)
     got = np.array([lib.spconv_ref_half_to_double(int(b)) for b in bits])
@@ -145,6 +151,26 @@ def _dw_battery(lib):
             failed.append("fused:s%d" % stride)
         elif not np.allclose(s.reshape(syref.shape), syref, rtol=1e-12, atol=1e-300):
             failed.append("fused-scale:s%d" % stride)
+    return failed
+
+
+def _block_battery(lib):
+    """Input-channel (kc) and 2-D blocks against the dense product."""
+    failed = []
+    rng = np.random.default_rng(21)
+    for kr, kc in ((1, 4), (2, 2), (1, 2), (4, 4)):
+        cout, cin = 8, 16
+        rp, ci, va = random_blocks(cout, cin, kr, kc, 0.5, rng)
+        x = rng.standard_normal((2, cin, 3)).astype(np.float32)
+        b = rng.standard_normal(cout).astype(np.float32)
+        _, y64, s = oracle.spconv_ref(cout, cin, kr, rp, ci, va, b, "none", x, lib=lib, block_cols=kc)
+        wd = dense_from_blocks(cout, cin, kr, kc, rp, ci, va)
+        ref = np.einsum("rc,ncp->nrp", wd, x.astype(np.float64)) + b.astype(np.float64)[None, :, None]
+        sref = np.einsum("rc,ncp->nrp", np.abs(wd), np.abs(x.astype(np.float64)))
+        if not np.allclose(y64, ref, rtol=1e-12, atol=1e-12):
+            failed.append("blocks:%dx%d" % (kr, kc))
+        elif not np.allclose(s, sref, rtol=1e-12, atol=0):
+            failed.append("blocks-scale:%dx%d" % (kr, kc))
     return failed
 
 
