@@ -256,6 +256,31 @@ typedef struct {
                             wavefront is done with it */
 } spconv_options;
 
+/*
+ * As spconv_plan_create_ex, with blocks of block_rows consecutive output
+ * channels x block_cols consecutive input channels (Fig. 5: 1x4, 4x1 and 2x2
+ * blocks train to the same accuracy; Sec. 3.2 names the shapes):
+ *   block_cols  1, 2 or 4 (1 is spconv_plan_create_ex)
+ *   col_idx     first input channel of each block; within a block row the
+ *               blocks ascend and do not overlap (col_idx[t] >= col_idx[t-1] +
+ *               block_cols); every block lies inside [0, cin); alignment to
+ *               block_cols is not required
+ *   values      row_ptr[end] * block_rows * block_cols floats:
+ *               values[(t * block_rows + i) * block_cols + j] =
+ *               W[rb * block_rows + i, col_idx[t] + j]
+ * The planner expands each block into block_cols consecutive single-channel
+ * entries of the 1 x block_rows kernels; the sum for each output stays in
+ * ascending input channel, so the result equals that of the same weight
+ * given unblocked.  spconv_plan_unpack returns the blocks as given.
+ * Errors: as spconv_plan_create_ex; SPCONV_E_ARG (block_cols <= 0),
+ * SPCONV_E_UNSUPPORTED (block_cols not 1, 2 or 4), SPCONV_E_FORMAT (a block
+ * outside [0, cin) or overlapping the previous one).
+ */
+spconv_status spconv_plan_create_blocked(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                         int32_t block_cols, const int32_t *row_ptr, const int32_t *col_idx,
+                                         const float *values, const float *bias, spconv_act act,
+                                         spconv_dtype storage, const spconv_options *opts);
+
 /* Fill *opts with the defaults used by spconv_plan_create. */
 void spconv_options_init(spconv_options *opts);
 
@@ -319,13 +344,14 @@ typedef struct {
     int32_t pipe_sets;     /* bundles a wavefront interleaves (0: direct-load kernel or depthwise stage) */
     int32_t regions;       /* strip parts refilled independently (0: direct-load kernel or depthwise
                               stage) */
-    int64_t nnzb;          /* stored blocks */
+    int64_t nnzb;          /* stored blocks (of block_rows x block_cols weights) */
     int64_t slots;         /* packed (channel, weight) slots including padding */
     int64_t max_wave_cost; /* largest per-wavefront work estimate (slots + epilogue) */
     int64_t sum_wave_cost; /* total of the per-wavefront work estimates */
     int64_t device_bytes;  /* device memory the plan holds */
     int32_t dw_stride;     /* fused depthwise stage: 0 none, else its stride */
     int32_t dw_act;        /* its activation */
+    int32_t block_cols;    /* input channels per block (1 unless created by spconv_plan_create_blocked) */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */

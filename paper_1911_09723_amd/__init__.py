@@ -21,6 +21,7 @@ from .spconv import (  # noqa: F401
     spconv_linear,
     spconv_options_init,
     spconv_plan_create,
+    spconv_plan_create_blocked,
     spconv_plan_create_dense,
     spconv_plan_create_fused,
     spconv_plan_get_info,

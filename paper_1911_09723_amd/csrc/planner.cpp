@@ -76,6 +76,15 @@ Status validate(const Input &in, std::string &err) {
         err = os.str();
         return E_UNSUPPORTED;
     }
+    if (in.block_cols <= 0) {
+        err = "block_cols must be positive";
+        return E_ARG;
+    }
+    if (in.block_cols != 1 && in.block_cols != 2 && in.block_cols != 4) {
+        os << "block_cols = " << in.block_cols << " is not supported (1, 2 or 4)";
+        err = os.str();
+        return E_UNSUPPORTED;
+    }
     if (in.cout <= 0 || in.cin <= 0) {
         os << "cout and cin must be >= 1 (got cout = " << in.cout << ", cin = " << in.cin << ")";
         err = os.str();
@@ -119,27 +128,31 @@ Status validate(const Input &in, std::string &err) {
         err = "col_idx or values is NULL but the matrix has stored entries";
         return E_ARG;
     }
-    if (nnzb * static_cast<int64_t>(in.block_rows) > (int64_t(1) << 30)) {
+    const int32_t kc = in.block_cols;
+    if (nnzb * static_cast<int64_t>(in.block_rows) * kc > (int64_t(1) << 30)) {
         err = "too many stored values (limit 2^30)";
         return E_SHAPE;
     }
     for (int32_t r = 0; r < rows; ++r) {
         for (int32_t t = in.row_ptr[r]; t < in.row_ptr[r + 1]; ++t) {
             const int32_t c = in.col_idx[t];
-            if (c < 0 || c >= in.cin) {
-                os << "col_idx[" << t << "] = " << c << " is outside [0, " << in.cin << ") in block row " << r;
+            if (c < 0 || static_cast<int64_t>(c) + kc > in.cin) {
+                os << "col_idx[" << t << "] = " << c;
+                if (kc > 1)
+                    os << " (a block of " << kc << " input channels)";
+                os << " is outside [0, " << in.cin << ") in block row " << r;
                 err = os.str();
                 return E_FORMAT;
             }
-            if (t > in.row_ptr[r] && c <= in.col_idx[t - 1]) {
-                os << "col_idx not strictly ascending in block row " << r << " at entry " << t << " ("
-                   << in.col_idx[t - 1] << ", " << c << ")";
+            if (t > in.row_ptr[r] && c < in.col_idx[t - 1] + kc) {
+                os << "col_idx not strictly ascending" << (kc > 1 ? " (blocks overlap)" : "") << " in block row "
+                   << r << " at entry " << t << " (" << in.col_idx[t - 1] << ", " << c << ")";
                 err = os.str();
                 return E_FORMAT;
             }
         }
     }
-    for (int64_t i = 0; i < nnzb * in.block_rows; ++i) {
+    for (int64_t i = 0; i < nnzb * in.block_rows * kc; ++i) {
         if (!std::isfinite(in.values[i])) {
             os << "values[" << i << "] is not finite";
             err = os.str();
@@ -496,10 +509,41 @@ Status validate_depthwise(const Input &in, const Options &opt, std::string &err)
     return OK;
 }
 
-Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::string &err) {
-    Status st = validate(in, err);
+// Input-channel blocks as the kernels' entries: block t of a row becomes kc
+// entries (channels col_idx[t] .. + kc - 1, in order), each with the block's
+// k output-channel values of that channel.  The per-row order stays ascending
+// channel, so the result is the same as for the equivalent unblocked weight.
+void expand_input_blocks(const Input &in, std::vector<int32_t> &row_ptr, std::vector<int32_t> &col_idx,
+                         std::vector<float> &values) {
+    const int32_t k = in.block_rows, kc = in.block_cols, rows = in.cout / k;
+    const int64_t nnzb = in.row_ptr[rows];
+    row_ptr.resize(rows + 1);
+    for (int32_t r = 0; r <= rows; ++r)
+        row_ptr[r] = in.row_ptr[r] * kc;
+    col_idx.resize(static_cast<size_t>(nnzb * kc));
+    values.resize(static_cast<size_t>(nnzb * kc * k));
+    for (int64_t t = 0; t < nnzb; ++t)
+        for (int32_t j = 0; j < kc; ++j) {
+            col_idx[t * kc + j] = in.col_idx[t] + j;
+            for (int32_t i = 0; i < k; ++i)
+                values[(t * kc + j) * k + i] = in.values[(t * k + i) * kc + j];
+        }
+}
+
+Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::string &err) {
+    Status st = validate(in_arg, err);
     if (st != OK)
         return st;
+    Input in = in_arg;
+    std::vector<int32_t> xrow_ptr, xcol_idx;
+    std::vector<float> xvalues;
+    if (in.block_cols > 1) {
+        expand_input_blocks(in_arg, xrow_ptr, xcol_idx, xvalues);
+        in.row_ptr = xrow_ptr.data();
+        in.col_idx = xcol_idx.data();
+        in.values = xvalues.data();
+        in.block_cols = 1;
+    }
     if (opt.kernel < 0 || opt.kernel > 2) {
         err = "kernel must be 0 (automatic), 1 (strip) or 2 (direct)";
         return E_ARG;
@@ -534,6 +578,7 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &p, std::strin
     p.k = in.block_rows;
     p.act = in.act;
     p.storage = in.storage;
+    p.kc = in_arg.block_cols;
     st = choose_geometry(in, opt, p, err);
     if (st != OK)
         return st;

@@ -108,6 +108,11 @@ constexpr int32_t kDwParams = 16;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
+    // input channels per block (Fig. 5: 4x1 and 2x2 blocks beside 1x4): block t
+    // covers channels col_idx[t] .. col_idx[t] + block_cols - 1 and holds
+    // values[(t * block_rows + i) * block_cols + j]; the planner expands it into
+    // block_cols consecutive entries of the kernels' 1 x block_rows format
+    int32_t block_cols = 1;
     const int32_t *row_ptr = nullptr;
     const int32_t *col_idx = nullptr;
     const float *values = nullptr;
@@ -138,6 +143,7 @@ struct Options {
 struct PackedPlan {
     // shape and epilogue
     int32_t cout = 0, cin = 0, k = 1, act = 0, storage = 0;
+    int32_t kc = 1;  // input channels per block of the caller's format (the packed streams hold the expansion)
     // launch geometry
     int32_t kernel = KERNEL_STRIP;
     int32_t group_lanes = 4;     // G: lanes per block row

@@ -267,6 +267,16 @@ spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t c
     return create_plan(out, in, opts);
 }
 
+spconv_status spconv_plan_create_blocked(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                         int32_t block_cols, const int32_t *row_ptr, const int32_t *col_idx,
+                                         const float *values, const float *bias, spconv_act act,
+                                         spconv_dtype storage, const spconv_options *opts) {
+    g_err.clear();
+    spconv::Input in = make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage);
+    in.block_cols = block_cols;
+    return create_plan(out, in, opts);
+}
+
 spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
                                  const int32_t *row_ptr, const int32_t *col_idx, const float *values,
                                  const float *bias, spconv_act act, spconv_dtype storage) {
@@ -527,14 +537,34 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->pipe_sets = p.kernel == spconv::KERNEL_STRIP ? p.pipe_sets : 0;
     info->regions = p.kernel == spconv::KERNEL_STRIP ? p.regions : 0;
     info->lds_bytes = p.lds_bytes;
-    info->nnzb = p.nnzb;
+    info->nnzb = p.nnzb / p.kc;
     info->slots = p.slots;
     info->max_wave_cost = p.max_wave_cost;
     info->sum_wave_cost = p.sum_wave_cost;
     info->device_bytes = static_cast<int64_t>(plan->dbytes);
     info->dw_stride = p.dw_stride;
     info->dw_act = p.dw_act;
+    info->block_cols = p.kc;
     return SPCONV_OK;
+}
+
+// The packed streams hold input-channel blocks expanded to single channels
+// (kc consecutive entries per block, in order): gather them back.
+static void reblock(const spconv::PackedPlan &p, const std::vector<int32_t> &rp, const std::vector<int32_t> &ci,
+             const std::vector<float> &va, int32_t *row_ptr, int32_t *col_idx, float *values) {
+    const int32_t k = p.k, kc = p.kc, rows = p.cout / k;
+    if (row_ptr)
+        for (int32_t r = 0; r <= rows; ++r)
+            row_ptr[r] = rp[r] / kc;
+    const int64_t nb = rp[rows] / kc;
+    for (int64_t t = 0; t < nb; ++t) {
+        if (col_idx)
+            col_idx[t] = ci[t * kc];
+        if (values)
+            for (int32_t i = 0; i < k; ++i)
+                for (int32_t j = 0; j < kc; ++j)
+                    values[(t * k + i) * kc + j] = va[(t * kc + j) * k + i];
+    }
 }
 
 spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
@@ -542,7 +572,19 @@ spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *co
     g_err.clear();
     if (!plan)
         return fail(SPCONV_E_ARG, "plan is NULL");
-    spconv::unpack_plan(plan->host, row_ptr, col_idx, values, perm);
+    const spconv::PackedPlan &p = plan->host;
+    if (p.kc == 1) {
+        spconv::unpack_plan(p, row_ptr, col_idx, values, perm);
+        return SPCONV_OK;
+    }
+    try {
+        std::vector<int32_t> rp(p.cout / p.k + 1), ci(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1)));
+        std::vector<float> va(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1) * p.k));
+        spconv::unpack_plan(p, rp.data(), ci.data(), va.data(), perm);
+        reblock(p, rp, ci, va, row_ptr, col_idx, values);
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while unpacking");
+    }
     return SPCONV_OK;
 }
 
@@ -552,9 +594,23 @@ spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr,
     if (!plan)
         return fail(SPCONV_E_ARG, "plan is NULL");
     std::string err;
-    const spconv::Status st = spconv::unpack_interleaved(plan->host, row_ptr, col_idx, values, err);
-    if (st != spconv::OK)
-        return fail(static_cast<spconv_status>(st), err);
+    const spconv::PackedPlan &p = plan->host;
+    if (p.kc == 1) {
+        const spconv::Status st = spconv::unpack_interleaved(p, row_ptr, col_idx, values, err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        return SPCONV_OK;
+    }
+    try {
+        std::vector<int32_t> rp(p.cout / p.k + 1), ci(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1)));
+        std::vector<float> va(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1) * p.k));
+        const spconv::Status st = spconv::unpack_interleaved(p, rp.data(), ci.data(), va.data(), err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        reblock(p, rp, ci, va, row_ptr, col_idx, values);
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while unpacking");
+    }
     return SPCONV_OK;
 }
 

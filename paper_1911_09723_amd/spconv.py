@@ -30,7 +30,7 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
-            "spconv_global_avg_pool", "spconv_linear")
+            "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked")
 
 
 class SpconvError(RuntimeError):
@@ -54,7 +54,8 @@ class spconv_plan_info(ctypes.Structure):
                 ("max_parts", ctypes.c_int32), ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32),
                 ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
-                ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32)]
+                ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32),
+                ("block_cols", ctypes.c_int32)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -98,6 +99,9 @@ def load_library(path: Optional[str] = None):
     lib.spconv_dense_to_bcsr.argtypes = [i32, i32, vp, i32, vp, vp, vp, ctypes.c_int64, ctypes.POINTER(ctypes.c_int64)]
     lib.spconv_plan_create_dense.restype = i32
     lib.spconv_plan_create_dense.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, vp, i32, i32]
+    lib.spconv_plan_create_blocked.restype = i32
+    lib.spconv_plan_create_blocked.argtypes = [ctypes.POINTER(vp), i32, i32, i32, i32, vp, vp, vp, vp, i32, i32,
+                                               ctypes.POINTER(spconv_options)]
     lib.spconv_plan_create_fused.restype = i32
     lib.spconv_plan_create_fused.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
                                              i32, i32, ctypes.POINTER(spconv_options)]
@@ -159,6 +163,27 @@ def spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias=Non
     else:
         status = lib.spconv_plan_create_ex(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
                                            _ptr(ci), _ptr(va), _ptr(bi), a, st, ctypes.byref(options))
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
+
+
+def spconv_plan_create_blocked(cout, cin, block_rows, block_cols, row_ptr, col_idx, values, bias=None, act="none",
+                               storage="f32", options: Optional[spconv_options] = None, check: bool = True):
+    """Create a plan from block-CSR weights with block_rows output x block_cols
+    input channels per block (values[(t * block_rows + i) * block_cols + j])."""
+    lib = load_library()
+    rp = _arr(row_ptr, np.int32)
+    ci = _arr(col_idx, np.int32)
+    va = _arr(values, np.float32)
+    bi = _arr(bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    status = lib.spconv_plan_create_blocked(ctypes.byref(out), int(cout), int(cin), int(block_rows), int(block_cols),
+                                            _ptr(rp), _ptr(ci), _ptr(va), _ptr(bi), a, st,
+                                            ctypes.byref(options) if options is not None else None)
     if not check:
         return status, out.value
     _check(status)
@@ -312,23 +337,25 @@ def spconv_plan_unpack(plan):
     """Return (row_ptr, col_idx, values, perm) rebuilt from the plan's packed host image."""
     info = spconv_plan_get_info(plan)
     rows = info["cout"] // info["block_rows"]
+    per = info["block_rows"] * info["block_cols"]
     rp = np.zeros(rows + 1, np.int32)
     ci = np.zeros(max(info["nnzb"], 1), np.int32)
-    va = np.zeros(max(info["nnzb"] * info["block_rows"], 1), np.float32)
+    va = np.zeros(max(info["nnzb"] * per, 1), np.float32)
     perm = np.zeros(rows, np.int32)
     _check(load_library().spconv_plan_unpack(plan, _ptr(rp), _ptr(ci), _ptr(va), _ptr(perm)))
-    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * info["block_rows"]], perm
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per], perm
 
 
 def spconv_plan_unpack_interleaved(plan):
     """Return (row_ptr, col_idx, values) rebuilt from the pipelined kernel's interleaved streams."""
     info = spconv_plan_get_info(plan)
     rows = info["cout"] // info["block_rows"]
+    per = info["block_rows"] * info["block_cols"]
     rp = np.zeros(rows + 1, np.int32)
     ci = np.zeros(max(info["nnzb"], 1), np.int32)
-    va = np.zeros(max(info["nnzb"] * info["block_rows"], 1), np.float32)
+    va = np.zeros(max(info["nnzb"] * per, 1), np.float32)
     _check(load_library().spconv_plan_unpack_interleaved(plan, _ptr(rp), _ptr(ci), _ptr(va)))
-    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * info["block_rows"]]
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per]
 
 
 class Plan:
@@ -351,6 +378,21 @@ class Plan:
         self = cls.__new__(cls)
         self.handle = spconv_plan_create_dense(dense, block_rows, bias, act, storage)
         self.cout, self.cin, self.storage, self.dw_stride = int(dense.shape[0]), int(dense.shape[1]), storage, 0
+        return self
+
+    @classmethod
+    def blocked(cls, cout, cin, block_rows, block_cols, row_ptr, col_idx, values, bias=None, act="none",
+                storage="f32", **options):
+        """Plan for block_rows x block_cols blocks (output x input channels)."""
+        self = cls.__new__(cls)
+        opts = None
+        if options:
+            opts = spconv_options_init()
+            for k, v in options.items():
+                setattr(opts, k, int(v))
+        self.handle = spconv_plan_create_blocked(cout, cin, block_rows, block_cols, row_ptr, col_idx, values, bias,
+                                                 act, storage, options=opts)
+        self.cout, self.cin, self.storage, self.dw_stride = int(cout), int(cin), storage, 0
         return self
 
     @classmethod

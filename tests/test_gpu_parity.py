@@ -274,3 +274,37 @@ def test_dense_weight_plan_matches_block_csr_plan(k, storage):
         plan.close()
     assert np.array_equal(y.view(np.uint8), gpu_run(layer).view(np.uint8))
     assert_parity(layer, y, what="dense k=%d" % k)
+
+
+@pytest.mark.parametrize("kr,kc,storage", [(1, 4, "f32"), (2, 2, "f32"), (1, 2, "f16"), (4, 4, "f32"),
+                                          (2, 4, "f16"), (1, 4, "f16")])
+@pytest.mark.parametrize("cin,h,w", [(64, 14, 14), (1024, 7, 7), (96, 5, 3)])
+def test_input_channel_blocks_match_oracle(kr, kc, storage, cin, h, w):
+    """Blocks of kr output x kc input channels (4x1, 2x2, ...) against the
+    block oracle, on the strip kernel, the direct-load kernel (cin = 1024) and
+    a ragged H*W."""
+    from paper_1911_09723_amd import Plan
+    from blocks_util import random_blocks
+    import oracle
+    rng = np.random.default_rng(kr * 100 + kc * 10 + cin)
+    cout = 128
+    rp, ci, va = random_blocks(cout, cin, kr, kc, 0.1, rng)
+    va = (va * np.sqrt(2.0 / (0.1 * cin))).astype(np.float32)
+    if storage == "f16":
+        va = va.astype(np.float16).astype(np.float32)
+    b = (rng.standard_normal(cout) * 0.1).astype(np.float32)
+    n = 3
+    x = np.maximum(rng.standard_normal((n, cin, h, w)), 0).astype(np.float16 if storage == "f16" else np.float32)
+    plan = Plan.blocked(cout, cin, kr, kc, rp, ci, va, b, "relu6", storage)
+    try:
+        note("blocks %dx%d %s cin %d %dx%d" % (kr, kc, storage, cin, h, w))
+        yt = plan.run(to_gpu(x))
+        import torch
+        torch.cuda.synchronize()
+        y = yt.cpu().numpy()
+    finally:
+        plan.close()
+    y_ref, _, s = oracle.spconv_ref(cout, cin, kr, rp, ci, va, b, "relu6", x, storage=storage, block_cols=kc)
+    tol = oracle.tolerance(y_ref, s, storage)
+    assert y.shape == y_ref.shape
+    assert np.all(np.abs(y.astype(np.float64) - y_ref.astype(np.float64)) <= tol)
