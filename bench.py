@@ -4,7 +4,8 @@
 Workload: Cin = Cout = 512, 14x14, batch 256, 90% sparse weights, fp32, ReLU
 epilogue -- the 512x512 layer of the sparsity sweep.  The unstructured mask is
 the headline (``value``); the 1x4 output-channel-blocked mask of the same
-sweep point is reported beside it.  Inputs are seeded synthetic tensors with
+sweep point is reported beside it, and so are blocks of 4 input channels
+("4x1 in") and of 2 x 2 channels ("2x2 in").  Inputs are seeded synthetic tensors with
 the paper's layer shapes (no trained weights or images are used).
 
 One step = one spconv_run over the whole batch (bias and activation fused).
@@ -78,14 +79,26 @@ def measured_traffic():
     return t
 
 
-def headline_layers():
-    from synth.configs import TARGET, config_layers, build
+def headline_layers(input_blocks=True):
+    """The headline layer, unstructured and 1x4 (output-channel blocks), and
+    with input-channel blocks of 4 (4x1) and 2 x 2 at the same sparsity, same
+    seed recipe."""
+    from synth import make_layer
+    from synth.configs import TARGET, config_layers, build, layer_seed
     specs = [s for s in config_layers(TARGET["config"]) if s["layer"] == TARGET["layer"]]
     out = {}
     for spec in specs:
         tag = "1x%d" % spec["block_rows"]
         log("bench: generating %s" % spec["name"])
         out[tag] = build(TARGET["config"], spec)
+    if input_blocks:
+        spec = specs[0]
+        for vi, (kr, kc) in enumerate(((1, 4), (2, 2)), start=2):
+            tag = "%dx%d in" % (kc, kr)
+            log("bench: generating %s with %d x %d blocks (output x input channels)" % (spec["name"], kr, kc))
+            out[tag] = make_layer(spec["cin"], spec["cout"], spec["h"], spec["w"], spec["n"], spec["sparsity"],
+                                  block_rows=kr, block_cols=kc, act=spec["act"],
+                                  seed=layer_seed(TARGET["config"], TARGET["layer"], vi))
     return out
 
 
@@ -247,7 +260,7 @@ def profile_run(reps: int):
     from paper_1911_09723_amd import Plan, spconv_run
 
     dev = torch.device("cuda:0")
-    layers = headline_layers()
+    layers = headline_layers(input_blocks=False)
     runs = [(tag, layer, None) for tag, layer in layers.items()]
     runs.append(("dw3x3+1x1", layers["1x1"], fused_layer(layers["1x1"])))
     for tag, layer, dw in runs:

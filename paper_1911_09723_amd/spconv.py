@@ -419,6 +419,9 @@ class Plan:
 
     @classmethod
     def from_layer(cls, layer, **options):
+        if getattr(layer, "block_cols", 1) > 1:
+            return cls.blocked(layer.cout, layer.cin, layer.block_rows, layer.block_cols, layer.row_ptr,
+                               layer.col_idx, layer.values, layer.bias, layer.act, layer.storage, **options)
         return cls(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
                    layer.bias, layer.act, layer.storage, **options)
 

@@ -59,6 +59,7 @@ class Layer:
     values: np.ndarray = field(repr=False)
     bias: np.ndarray = field(repr=False)
     x: Optional[np.ndarray] = field(default=None, repr=False)
+    block_cols: int = 1  # input channels per block (values[(t * block_rows + i) * block_cols + j])
 
     @property
     def hw(self) -> int:
@@ -70,8 +71,8 @@ class Layer:
 
     @property
     def nnz(self) -> int:
-        """Stored weight values (k per block)."""
-        return self.nnzb * self.block_rows
+        """Stored weight values (block_rows x block_cols per block)."""
+        return self.nnzb * self.block_rows * self.block_cols
 
     @property
     def x_dtype(self):
@@ -155,25 +156,31 @@ def make_layer(
     act: str = "relu",
     seed: int = 0,
     with_x: bool = True,
+    block_cols: int = 1,
 ) -> Layer:
-    if cout % block_rows:
-        raise ValueError("cout must be a multiple of block_rows")
+    """One seeded layer (recipe in the module docstring).  block_cols > 1
+    draws the mask over aligned blocks of block_cols input channels (the
+    uniform pattern only); block_cols = 1 gives exactly the draws of the
+    unblocked recipe."""
+    if cout % block_rows or cin % block_cols:
+        raise ValueError("cout must be a multiple of block_rows and cin of block_cols")
     if act not in ACTS or storage not in STORAGES:
         raise ValueError("bad act/storage")
     rng = np.random.Generator(np.random.PCG64(seed))
     rows = cout // block_rows
     density = 1.0 - sparsity
     if pattern == "uniform":
-        row_ptr, col_idx = _uniform_mask(rng, rows, cin, density)
+        row_ptr, col_idx = _uniform_mask(rng, rows, cin // block_cols, density)
+        col_idx = (col_idx * block_cols).astype(np.int32)
     elif pattern == "beta":
-        if block_rows != 1:
+        if block_rows != 1 or block_cols != 1:
             raise ValueError("beta row densities are defined for unstructured masks")
         row_ptr, col_idx = _beta_mask(rng, rows, cin, density)
     else:
         raise ValueError(pattern)
     nnzb = int(row_ptr[-1])
     std_w = np.sqrt(2.0 / (0.1 * cin))
-    values = (rng.standard_normal(nnzb * block_rows) * std_w).astype(np.float32)
+    values = (rng.standard_normal(nnzb * block_rows * block_cols) * std_w).astype(np.float32)
     if storage == "f16":
         values = values.astype(np.float16).astype(np.float32)
     bias = (rng.standard_normal(cout) * 0.1).astype(np.float32)
@@ -183,7 +190,7 @@ def make_layer(
         if storage == "f16":
             x = x.astype(np.float16)
     return Layer(cin, cout, h, w, n, block_rows, sparsity, pattern, storage, act, seed,
-                 row_ptr, col_idx, values, bias, x)
+                 row_ptr, col_idx, values, bias, x, block_cols)
 
 
 def densify(cout: int, cin: int, block_rows: int, row_ptr, col_idx, values) -> np.ndarray:
