@@ -364,6 +364,7 @@ def main():
     ap.add_argument("--profile-run", action="store_true", help="launches for rocprofv3 counter passes")
     ap.add_argument("--reps", type=int, default=5, help="launches per variant in --profile-run")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--no-network", action="store_true", help="skip the MobileNet v1 timing")
     ap.add_argument("--network-run", action="store_true",
                     help="only the MobileNet v1 graph replays (batch 64), for rocprofv3 kernel traces")
     ap.add_argument("--command", action="append", default=[], help="command lines recorded in the summary")
@@ -402,7 +403,7 @@ def main():
     log("bench: %s %s" % (tag, json.dumps(results[tag])))
 
     network = []
-    for batch in (1, 64):
+    for batch in (() if args.no_network else (1, 64)):
         log("bench: MobileNet v1 forward, batch %d, graph replays" % batch)
         network.append(time_network(batch, 50, 5))
         log("bench: network %s" % json.dumps({k: v for k, v in network[-1].items() if k != "layers"}))
