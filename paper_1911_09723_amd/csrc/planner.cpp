@@ -592,10 +592,6 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         p.dw_act = in.dw_act;
         p.pipe_sets = 0;
         p.regions = 0;
-        // every LDS byte left after the strip and the bundle table stages input windows
-        p.stage_off = p.lds_bytes - kCtlBytes;
-        p.lds_bytes = static_cast<int32_t>(kMaxLdsBytes);
-        p.stage_bytes = (p.lds_bytes - kCtlBytes - p.stage_off) & ~15;
         p.dw.assign(static_cast<size_t>(p.strip_rows) * kDwParams, 0.0f);
         for (int32_t c = 0; c < in.cin; ++c) {
             for (int32_t t = 0; t < 9; ++t)
@@ -633,6 +629,22 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     // 3. longest-processing-time-first assignment of bundles to waves
     const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(kMaxWaves, nb);
     p.waves = waves;
+    if (p.dw_stride) {
+        // the LDS left after the strip and the bundle table stages input
+        // windows; a plan with at most 8 wavefronts keeps room for 2 (4: 3)
+        // workgroups per CU, so one's depthwise phase overlaps another's 1x1
+        p.stage_off = p.lds_bytes - kCtlBytes;
+        const int32_t want = std::min<int32_t>(3, std::max<int32_t>(1, kMaxWaves / std::max(p.waves, 1)));
+        for (int32_t o = want; o >= 1; --o) {
+            const int64_t budget = (kMaxLdsBytes / o) & ~int64_t(255);
+            const int64_t stage = (budget - kCtlBytes - p.stage_off) & ~int64_t(15);
+            if (o == 1 || stage >= kMinStageBytes) {
+                p.lds_bytes = static_cast<int32_t>(budget);
+                p.stage_bytes = static_cast<int32_t>(stage);
+                break;
+            }
+        }
+    }
     std::vector<int32_t> order(nb);
     std::iota(order.begin(), order.end(), 0);
     std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return bsteps[a] > bsteps[b]; });

@@ -105,6 +105,8 @@ constexpr int32_t kSelSteps = 16;
 constexpr int32_t kWaveEvents = 2 * kMaxRegions;
 // Floats per channel of a fused depthwise stage's parameters (9 taps, bias, padding to 64 bytes).
 constexpr int32_t kDwParams = 16;
+// Smallest depthwise staging area worth a second workgroup per CU.
+constexpr int64_t kMinStageBytes = 16 * 1024;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
