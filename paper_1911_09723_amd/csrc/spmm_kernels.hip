@@ -255,11 +255,17 @@ struct TileAddr {
     }
 };
 
-// Per-element X offsets of a lane's columns for the direct kernel without
-// 16-byte vectors (H*W not a multiple of the vector width): byte offset of
-// column (vector vb[j], element e) from channel 0 of the tile's first image,
-// kOutOfRange past the last column.  Computed once per tile, so the inner
-// loop reads X with one buffer load per element and no division.
+// X offsets of a lane's columns for the direct kernel without aligned 16-byte
+// vectors (H*W not a multiple of the vector width), computed once per tile
+// so the inner loop needs no division.  Byte offsets count from channel 0 of
+// the tile's first image; kOutOfRange past the last column.
+//   fp32 with H*W >= 4 (`pair`): xe[j][0] = offset of element 0 of vector j,
+//     xe[j][1] = the number k of its elements in that image, xe[j][2] = an
+//     offset whose element e >= k is element e of the vector (the next
+//     image's plane, shifted back by k).  A read is one 16-byte load, plus a
+//     second only where a vector straddles two images; the loads are 4-byte
+//     aligned, and raw buffer loads check bounds per dword.
+//   otherwise: xe[j][e] = offset of element e (one 4- or 2-byte load each).
 template <int G, bool F16, bool ON>
 struct ColOff {
     __device__ __forceinline__ void set(const Args &, const Lane<G, F16> &, int32_t) {}
@@ -268,9 +274,23 @@ template <int G, bool F16>
 struct ColOff<G, F16, true> {
     using GE = Geo<G, F16>;
     int32_t xe[GE::V][GE::QE];
+    __device__ __forceinline__ static bool pair(const Args &a) { return !F16 && a.hw >= GE::QE; }
     __device__ __forceinline__ void set(const Args &a, const Lane<G, F16> &L, int32_t tile) {
         const int32_t col0 = tile * GE::TC;
         const int32_t n0 = col0 / a.hw;
+        if (pair(a)) {
+#pragma unroll
+            for (int j = 0; j < GE::V; ++j) {
+                const int32_t c = col0 + L.vb[j] * GE::QE;
+                const int32_t n = c / a.hw;
+                const int32_t p = c - n * a.hw;
+                const int32_t k = std::min(GE::QE, a.hw - p);
+                xe[j][0] = c < a.m ? ((n - n0) * a.cin * a.hw + p) * GE::E : kOutOfRange;
+                xe[j][1] = k;
+                xe[j][2] = c + k < a.m ? ((n + 1 - n0) * a.cin * a.hw - k) * GE::E : kOutOfRange;
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < GE::V; ++j)
 #pragma unroll
@@ -371,6 +391,20 @@ __device__ __forceinline__ u4 read_x(const Args &a, const Lane<G, F16> &L, const
         if constexpr (VEC) {
             return bload16(ta.rx, ta.xo[j] + ro, 0);
         } else {
+            if constexpr (!F16) {
+                if (co.pair(a)) {
+                    u4 va = bload16(ta.rx, co.xe[j][0] + ro, 0);
+                    if (co.xe[j][1] < GE::QE) {
+                        // the vector straddles two images: its tail from the next plane
+                        const u4 vb = bload16(ta.rx, co.xe[j][2] + ro, 0);
+#pragma unroll
+                        for (int e = 1; e < GE::QE; ++e)
+                            if (e >= co.xe[j][1])
+                                va[e] = vb[e];
+                    }
+                    return va;
+                }
+            }
             // any HW: element by element (past the last column: zero)
             T v[GE::QE];
 #pragma unroll

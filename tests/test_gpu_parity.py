@@ -37,6 +37,9 @@ SMALL = [
     (1500, 48, 6, 6, 2, 0.9, 1, "f32", "relu"),
     (1500, 48, 6, 6, 2, 0.9, 4, "f16", "relu"),
     (1300, 48, 8, 8, 2, 0.9, 1, "f16", "none"),
+    (640, 32, 1, 3, 5, 0.9, 1, "f32", "relu"),      # direct, H*W < 4: element loads
+    (640, 32, 3, 3, 7, 0.9, 2, "f32", "relu6"),     # direct, H*W = 9: paired loads, many straddles
+    (640, 40, 5, 5, 9, 0.9, 4, "f32", "none"),
     # 1x2 output-channel blocks (the paper's 16x2 kernels)
     (24, 40, 7, 7, 3, 0.8, 2, "f32", "relu6"),
     (64, 36, 5, 5, 2, 0.5, 2, "f16", "none"),
