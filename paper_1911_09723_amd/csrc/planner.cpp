@@ -360,6 +360,21 @@ Status choose_geometry(const Input &in, const Options &opt, PackedPlan &p, std::
         p.row_scale = 1;
         p.strip_rows = 0;
         p.lds_bytes = static_cast<int32_t>(table);
+        if (opt.group_lanes == 0 && g != 16) {
+            // the direct kernel waits on X loads from L2: 16 lanes per row (one
+            // vector per lane) need the fewest registers, so more wavefronts
+            // stay resident, and give 4x more bundles to spread
+            g = 16;
+            p.group_lanes = g;
+            p.bundle_rows = 64 / g;
+            p.cols_per_lane = (16 / g) * (16 / e);
+            const int64_t t16 = table_bytes(bundles_of(rows, p.bundle_rows), p.bundle_rows, k) + kCtlBytes;
+            if (t16 > kMaxLdsBytes) {
+                err = "the bundle table of cout = " + std::to_string(in.cout) + " rows does not fit in LDS";
+                return E_UNSUPPORTED;
+            }
+            p.lds_bytes = static_cast<int32_t>(t16);
+        }
     }
     return OK;
 }

@@ -337,10 +337,13 @@ def test_geometry_choice():
     # few rows: wider lane groups keep enough bundles for the wavefronts
     check(info_for(24, 32, "f32"), 0, 16, 64, 24, 32, 1)
     check(info_for(144, 24, "f32"), 0, 16, 64, 144, 24, 1)
-    # inputs too wide for an LDS strip: the direct-load kernel
-    check(info_for(1024, 256, "f32"), 1, 4, 64, 1024, 256, 1)
+    # inputs too wide for an LDS strip: the direct-load kernel, 16 lanes per row
+    check(info_for(1024, 256, "f32"), 1, 16, 64, 1024, 256, 1)
     check(info_for(600, 256, "f32"), 0, 4, 64, 600, 256, 1)
-    check(info_for(640, 256, "f32"), 1, 4, 64, 640, 256, 1)
+    check(info_for(640, 256, "f32"), 1, 16, 64, 640, 256, 1)
+    check(info_for(1152, 192, "f16", 4), 1, 16, 128, 1152, 192, 4)
+    # an explicit lane width still holds on the direct-load kernel
+    assert info_for(1024, 256, "f32", group_lanes=4)["group_lanes"] == 4
     # forced choices
     i = info_for(512, 512, "f32", group_lanes=16, waves=7)
     assert i["group_lanes"] == 16 and i["waves"] == 7
