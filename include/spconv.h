@@ -29,6 +29,13 @@
 #include <stddef.h>
 #include <stdint.h>
 
+/* The library is built with hidden visibility; only these entry points are exported. */
+#if defined(__GNUC__) || defined(__clang__)
+#define SPCONV_API __attribute__((visibility("default")))
+#else
+#define SPCONV_API
+#endif
+
 #ifdef __cplusplus
 extern "C" {
 #endif
@@ -78,7 +85,7 @@ typedef enum { SPCONV_ACT_NONE = 0, SPCONV_ACT_RELU = 1, SPCONV_ACT_RELU6 = 2 } 
  * SPCONV_E_HIP (no usable device, allocation or copy failure).  Nothing is
  * leaked on failure.
  */
-spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+SPCONV_API spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
                                  const int32_t *row_ptr, const int32_t *col_idx,
                                  const float *values, const float *bias, spconv_act act,
                                  spconv_dtype storage);
@@ -109,16 +116,16 @@ spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int32_t cin, in
  * (launch failure).  Faults during
  * execution surface at the caller's next synchronization.
  */
-spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
+SPCONV_API spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
                          void *stream);
 
 /* Free the plan and its device buffers.  NULL is a no-op.  The caller must
  * ensure no queued run still uses the plan. */
-spconv_status spconv_destroy(spconv_plan plan);
+SPCONV_API spconv_status spconv_destroy(spconv_plan plan);
 
 /* Message for the calling thread's most recent failure ("" if none).  The
  * pointer stays valid until the next spconv_* call on the same thread. */
-const char *spconv_last_error(void);
+SPCONV_API const char *spconv_last_error(void);
 
 /* ---------------------------------------------------------------------------
  * Dense weights.  Sec. 3.3: a trained (pruned) model keeps its weights as a
@@ -139,7 +146,7 @@ const char *spconv_last_error(void);
  * Errors: SPCONV_E_ARG (NULL pointer), SPCONV_E_SHAPE (cout or cin < 1,
  * cin > 2^24), SPCONV_E_FORMAT (a non-finite weight).
  */
-spconv_status spconv_detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows);
+SPCONV_API spconv_status spconv_detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows);
 
 /*
  * Convert a dense weight to 1 x block_rows block-CSR (the layout that
@@ -158,7 +165,7 @@ spconv_status spconv_detect_block_rows(int32_t cout, int32_t cin, const float *d
  * col_idx, capacity too small), SPCONV_E_UNSUPPORTED (block_rows not 1, 2 or
  * 4), SPCONV_E_SHAPE, SPCONV_E_FORMAT.
  */
-spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t block_rows,
+SPCONV_API spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t block_rows,
                                    int32_t *row_ptr, int32_t *col_idx, float *values, int64_t capacity,
                                    int64_t *nnzb);
 
@@ -168,7 +175,7 @@ spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense
  * (spconv_dense_to_bcsr) and plans.  Other arguments and errors as for
  * spconv_plan_create.
  */
-spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
+SPCONV_API spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
                                        int32_t block_rows, const float *bias, spconv_act act,
                                        spconv_dtype storage);
 
@@ -194,7 +201,7 @@ spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t c
  * pixels), SPCONV_E_UNSUPPORTED (cin > 8 or cout * (9 cin + 1) > 16384:
  * the weights are held in LDS), SPCONV_E_HIP.
  */
-spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const float *bias, spconv_act act,
+SPCONV_API spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const float *bias, spconv_act act,
                                  int32_t stride, float *y, int32_t n, int32_t h, int32_t w, int32_t cin,
                                  int32_t cout, void *stream);
 
@@ -205,7 +212,7 @@ spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const floa
  *   x [n][c][h][w], weight [c][3][3], bias [c] or NULL, y [n][c][(h-1)/s+1][(w-1)/s+1], stride 1 or 2.
  * Errors: SPCONV_E_ARG, SPCONV_E_SHAPE (too many outputs), SPCONV_E_HIP.
  */
-spconv_status spconv_depthwise3x3(const float *x, const float *weight, const float *bias, spconv_act act,
+SPCONV_API spconv_status spconv_depthwise3x3(const float *x, const float *weight, const float *bias, spconv_act act,
                                   int32_t stride, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
                                   void *stream);
 
@@ -217,7 +224,7 @@ spconv_status spconv_depthwise3x3(const float *x, const float *weight, const flo
  * Errors: SPCONV_E_ARG (NULL pointer with work to do, negative size, bad act,
  * overlap), SPCONV_E_SHAPE (cin == 0 with outputs, n > 262140), SPCONV_E_HIP.
  */
-spconv_status spconv_linear(const float *x, const float *weight, const float *bias, spconv_act act, float *y,
+SPCONV_API spconv_status spconv_linear(const float *x, const float *weight, const float *bias, spconv_act act, float *y,
                             int32_t n, int32_t cin, int32_t cout, void *stream);
 
 /*
@@ -225,7 +232,7 @@ spconv_status spconv_linear(const float *x, const float *weight, const float *bi
  * ascending p in fp32.  x [n][c][h][w], y [n][c].
  * Errors: SPCONV_E_ARG, SPCONV_E_SHAPE (h * w == 0 with n * c > 0), SPCONV_E_HIP.
  */
-spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
+SPCONV_API spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
                                      void *stream);
 
 /* ---------------------------------------------------------------------------
@@ -276,16 +283,16 @@ typedef struct {
  * SPCONV_E_UNSUPPORTED (block_cols not 1, 2 or 4), SPCONV_E_FORMAT (a block
  * outside [0, cin) or overlapping the previous one).
  */
-spconv_status spconv_plan_create_blocked(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+SPCONV_API spconv_status spconv_plan_create_blocked(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
                                          int32_t block_cols, const int32_t *row_ptr, const int32_t *col_idx,
                                          const float *values, const float *bias, spconv_act act,
                                          spconv_dtype storage, const spconv_options *opts);
 
 /* Fill *opts with the defaults used by spconv_plan_create. */
-void spconv_options_init(spconv_options *opts);
+SPCONV_API void spconv_options_init(spconv_options *opts);
 
 /* As spconv_plan_create, with explicit planner options (NULL = defaults). */
-spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+SPCONV_API spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
                                     const int32_t *row_ptr, const int32_t *col_idx,
                                     const float *values, const float *bias, spconv_act act,
                                     spconv_dtype storage, const spconv_options *opts);
@@ -323,7 +330,7 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
  * bias), SPCONV_E_UNSUPPORTED (SPCONV_F16 storage, kernel = 2, pipe_sets or
  * regions set, or a strip of cin channels that does not fit in LDS).
  */
-spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+SPCONV_API spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
                                        const int32_t *row_ptr, const int32_t *col_idx,
                                        const float *values, const float *bias, spconv_act act,
                                        const float *dw_weights, const float *dw_bias, spconv_act dw_act,
@@ -355,7 +362,7 @@ typedef struct {
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */
-spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info);
+SPCONV_API spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info);
 
 /*
  * Reconstruct the plan's weights from its packed host image, in the input's
@@ -363,7 +370,7 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info);
  * may be NULL to skip), and perm[cout/k] (may be NULL): perm[i] = the block
  * row processed i-th.  Host only.  Lets tests check that packing loses nothing.
  */
-spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
+SPCONV_API spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values,
                                  int32_t *perm);
 
 /*
@@ -375,7 +382,7 @@ spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, int32_t *co
  * Host only.  SPCONV_E_FORMAT (message set) when the streams are inconsistent
  * or the plan has none (direct-load kernel, depthwise stage).
  */
-spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
+SPCONV_API spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
                                              float *values);
 
 #ifdef __cplusplus

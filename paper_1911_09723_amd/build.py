@@ -25,7 +25,7 @@ SOURCES = ["planner.cpp", "spconv_api.cpp", "spmm_kernels.hip", "net_kernels.hip
 ARCH = "gfx950"
 
 COMMON = [
-    "-std=c++17", "-O3", "-fPIC", "-Wall",
+    "-std=c++17", "-O3", "-fPIC", "-Wall", "-fvisibility=hidden",
     "-I", INCLUDE, "-I", CSRC,
 ]
 # Packed fp32 instructions stay disabled in every device compile.

@@ -481,7 +481,7 @@ void build_interleaved(PackedPlan &p) {
 
 // The fused depthwise stage's arguments: fp32 storage, the strip kernel,
 // stride 1 or 2, finite taps and biases.
-Status validate_depthwise(const Input &in, const Options &opt, std::string &err) {
+static Status validate_depthwise(const Input &in, const Options &opt, std::string &err) {
     if (in.dw_stride == 0)
         return OK;
     if (in.dw_stride != 1 && in.dw_stride != 2) {
@@ -528,7 +528,7 @@ Status validate_depthwise(const Input &in, const Options &opt, std::string &err)
 // entries (channels col_idx[t] .. + kc - 1, in order), each with the block's
 // k output-channel values of that channel.  The per-row order stays ascending
 // channel, so the result is the same as for the equivalent unblocked weight.
-void expand_input_blocks(const Input &in, std::vector<int32_t> &row_ptr, std::vector<int32_t> &col_idx,
+static void expand_input_blocks(const Input &in, std::vector<int32_t> &row_ptr, std::vector<int32_t> &col_idx,
                          std::vector<float> &values) {
     const int32_t k = in.block_rows, kc = in.block_cols, rows = in.cout / k;
     const int64_t nnzb = in.row_ptr[rows];
