@@ -174,7 +174,7 @@ def spconv_ref_layer(layer, x=None, with_scale: bool = True):
     """Run the oracle on a ``synth.Layer`` (optionally on another input x)."""
     return spconv_ref(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx,
                       layer.values, layer.bias, layer.act, layer.x if x is None else x,
-                      storage=layer.storage, with_scale=with_scale)
+                      storage=layer.storage, with_scale=with_scale, block_cols=getattr(layer, "block_cols", 1))
 
 
 def dw3x3_ref(x, k, bias, act, stride: int, lib=None):

@@ -74,3 +74,35 @@ def test_non_finite_block_value_rejected():
     va[3] = np.nan
     st, h = _create(1, 8, 1, 4, rp, np.array([4], np.int32), va)
     assert st == sp.spconv.E_FORMAT and "values[3]" in sp.spconv_last_error()
+
+
+from hypothesis import given, settings, strategies as st
+
+
+@settings(max_examples=60, deadline=None)
+@given(kr=st.sampled_from([1, 2, 4]), kc=st.sampled_from([1, 2, 4]), rows=st.integers(1, 40),
+       bcols=st.integers(1, 40), density=st.floats(0.0, 1.0), seed=st.integers(0, 2 ** 31 - 1),
+       kernel=st.sampled_from([0, 2]))
+def test_blocked_round_trip_property(kr, kc, rows, bcols, density, seed, kernel):
+    """Any aligned block pattern survives planning and unpacking unchanged."""
+    rng = np.random.default_rng(seed)
+    cout, cin = rows * kr, bcols * kc
+    rp, ci, va = random_blocks(cout, cin, kr, kc, density, rng)
+    h = _create(cout, cin, kr, kc, rp, ci, va, check=True, kernel=kernel)
+    try:
+        rp2, ci2, va2, perm = sp.spconv_plan_unpack(h)
+        assert np.array_equal(rp2, rp) and np.array_equal(ci2, ci) and np.array_equal(va2, va)
+        assert sorted(perm.tolist()) == list(range(rows))
+    finally:
+        sp.spconv_destroy(h)
+
+
+def test_oracle_layer_helper_reads_block_cols():
+    """oracle.spconv_ref_layer on a layer with input-channel blocks applies them."""
+    import oracle
+    from synth import make_layer
+    layer = make_layer(16, 8, 3, 3, 2, 0.5, block_rows=2, block_cols=4, seed=4)
+    _, a, _ = oracle.spconv_ref_layer(layer)
+    _, b, _ = oracle.spconv_ref(8, 16, 2, layer.row_ptr, layer.col_idx, layer.values, layer.bias, layer.act,
+                                layer.x, block_cols=4)
+    assert np.array_equal(a, b)
