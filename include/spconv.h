@@ -235,6 +235,36 @@ SPCONV_API spconv_status spconv_linear(const float *x, const float *weight, cons
 SPCONV_API spconv_status spconv_global_avg_pool(const float *x, float *y, int32_t n, int32_t c, int32_t h, int32_t w,
                                      void *stream);
 
+/*
+ * Dense weights to blocks of block_rows output x block_cols input channels
+ * (Fig. 5: 1x4, 4x1 and 2x2 blocks), aligned (block (b, q) covers rows
+ * b*kr .. b*kr + kr - 1 and channels q*kc .. q*kc + kc - 1); the layout that
+ * spconv_plan_create_blocked takes.
+ *
+ * spconv_detect_blocks: the (kr, kc) in {1, 2, 4} x {1, 2, 4} with the most
+ * weights per block (on a tie the taller, output-channel block) such that
+ * kr divides cout, kc divides cin and every aligned block is all zero or all
+ * nonzero.  Errors as spconv_detect_block_rows.
+ *
+ * spconv_dense_to_bcsr_blocked: as spconv_dense_to_bcsr with block_cols
+ * (1, 2 or 4, dividing cin): a block is stored when any of its weights is
+ * nonzero; col_idx[t] = its first input channel; values has capacity *
+ * block_rows * block_cols entries, values[(t * kr + i) * kc + j].
+ *
+ * spconv_plan_create_dense_blocked: detect (block_rows = block_cols = 0) or
+ * take both, convert, and plan as spconv_plan_create_blocked.
+ */
+SPCONV_API spconv_status spconv_detect_blocks(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows,
+                                              int32_t *block_cols);
+SPCONV_API spconv_status spconv_dense_to_bcsr_blocked(int32_t cout, int32_t cin, const float *dense,
+                                                      int32_t block_rows, int32_t block_cols, int32_t *row_ptr,
+                                                      int32_t *col_idx, float *values, int64_t capacity,
+                                                      int64_t *nnzb);
+SPCONV_API spconv_status spconv_plan_create_dense_blocked(spconv_plan *out, int32_t cout, int32_t cin,
+                                                          const float *dense, int32_t block_rows,
+                                                          int32_t block_cols, const float *bias, spconv_act act,
+                                                          spconv_dtype storage);
+
 /* ---------------------------------------------------------------------------
  * Planner controls and introspection.  These let a caller (and the CPU-only
  * tests) see what the host-side planner decided without running a kernel.

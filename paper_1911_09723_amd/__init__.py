@@ -12,17 +12,20 @@ from .spconv import (  # noqa: F401
     SpconvError,
     load_library,
     spconv_dense_to_bcsr,
+    spconv_dense_to_bcsr_blocked,
     spconv_conv3x3_hwc,
     spconv_depthwise3x3,
     spconv_destroy,
     spconv_global_avg_pool,
     spconv_detect_block_rows,
+    spconv_detect_blocks,
     spconv_last_error,
     spconv_linear,
     spconv_options_init,
     spconv_plan_create,
     spconv_plan_create_blocked,
     spconv_plan_create_dense,
+    spconv_plan_create_dense_blocked,
     spconv_plan_create_fused,
     spconv_plan_get_info,
     spconv_plan_unpack,

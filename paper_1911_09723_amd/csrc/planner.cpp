@@ -227,8 +227,40 @@ Status detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t 
     return OK;
 }
 
-Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t *row_ptr,
-                     int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err) {
+Status detect_blocks(int32_t cout, int32_t cin, const float *dense, int32_t &kr, int32_t &kc, std::string &err) {
+    const Status st = check_dense(cout, cin, dense, err);
+    if (st != OK)
+        return st;
+    // most weights per block first; on a tie, output-channel blocks (their
+    // kernels reuse each X vector for every row of the block)
+    static const int32_t cands[][2] = {{4, 4}, {4, 2}, {2, 4}, {4, 1}, {2, 2}, {1, 4}, {2, 1}, {1, 2}};
+    for (const auto &cd : cands) {
+        const int32_t r = cd[0], q = cd[1];
+        if (cout % r || cin % q)
+            continue;
+        bool uniform = true;
+        for (int32_t rb = 0; uniform && rb < cout / r; ++rb)
+            for (int32_t cb = 0; uniform && cb < cin / q; ++cb) {
+                const bool first = dense[static_cast<int64_t>(rb) * r * cin + static_cast<int64_t>(cb) * q] != 0.0f;
+                for (int32_t i = 0; uniform && i < r; ++i)
+                    for (int32_t j = 0; j < q; ++j)
+                        if ((dense[(static_cast<int64_t>(rb) * r + i) * cin + cb * q + j] != 0.0f) != first) {
+                            uniform = false;
+                            break;
+                        }
+            }
+        if (uniform) {
+            kr = r;
+            kc = q;
+            return OK;
+        }
+    }
+    kr = kc = 1;
+    return OK;
+}
+
+Status dense_to_blocks(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t kc, int32_t *row_ptr,
+                       int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err) {
     nnzb = 0;
     Status st = check_dense(cout, cin, dense, err);
     if (st != OK)
@@ -237,8 +269,16 @@ Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, i
         err = "block_rows = " + std::to_string(k) + " is not supported (1, 2 or 4)";
         return k <= 0 ? E_ARG : E_UNSUPPORTED;
     }
+    if (kc != 1 && kc != 2 && kc != 4) {
+        err = "block_cols = " + std::to_string(kc) + " is not supported (1, 2 or 4)";
+        return kc <= 0 ? E_ARG : E_UNSUPPORTED;
+    }
     if (cout % k) {
         err = "cout = " + std::to_string(cout) + " is not a multiple of block_rows = " + std::to_string(k);
+        return E_SHAPE;
+    }
+    if (cin % kc) {
+        err = "cin = " + std::to_string(cin) + " is not a multiple of block_cols = " + std::to_string(kc);
         return E_SHAPE;
     }
     const bool write = col_idx != nullptr;
@@ -246,18 +286,22 @@ Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, i
         err = "row_ptr and values must be given with col_idx";
         return E_ARG;
     }
-    auto stored = [&](int32_t rb, int32_t c) {
+    auto at = [&](int32_t rb, int32_t i, int32_t cb, int32_t j) {
+        return dense[(static_cast<int64_t>(rb) * k + i) * cin + static_cast<int64_t>(cb) * kc + j];
+    };
+    auto stored = [&](int32_t rb, int32_t cb) {
         for (int32_t i = 0; i < k; ++i)
-            if (dense[(static_cast<int64_t>(rb) * k + i) * cin + c] != 0.0f)
-                return true;
+            for (int32_t j = 0; j < kc; ++j)
+                if (at(rb, i, cb, j) != 0.0f)
+                    return true;
         return false;
     };
     int64_t total = 0;
     for (int32_t rb = 0; rb < cout / k; ++rb)
-        for (int32_t c = 0; c < cin; ++c)
-            total += stored(rb, c) ? 1 : 0;
+        for (int32_t cb = 0; cb < cin / kc; ++cb)
+            total += stored(rb, cb) ? 1 : 0;
     nnzb = total;
-    if (total * k > (int64_t(1) << 30)) {
+    if (total * k * kc > (int64_t(1) << 30)) {
         err = "too many stored values (limit 2^30)";
         return E_SHAPE;
     }
@@ -267,8 +311,8 @@ Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, i
             int32_t acc = 0;
             row_ptr[0] = 0;
             for (int32_t rb = 0; rb < cout / k; ++rb) {
-                for (int32_t c = 0; c < cin; ++c)
-                    acc += stored(rb, c) ? 1 : 0;
+                for (int32_t cb = 0; cb < cin / kc; ++cb)
+                    acc += stored(rb, cb) ? 1 : 0;
                 row_ptr[rb + 1] = acc;
             }
         }
@@ -282,17 +326,23 @@ Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, i
     int32_t t = 0;
     row_ptr[0] = 0;
     for (int32_t rb = 0; rb < cout / k; ++rb) {
-        for (int32_t c = 0; c < cin; ++c) {
-            if (!stored(rb, c))
+        for (int32_t cb = 0; cb < cin / kc; ++cb) {
+            if (!stored(rb, cb))
                 continue;
-            col_idx[t] = c;
+            col_idx[t] = cb * kc;
             for (int32_t i = 0; i < k; ++i)
-                values[static_cast<int64_t>(t) * k + i] = dense[(static_cast<int64_t>(rb) * k + i) * cin + c];
+                for (int32_t j = 0; j < kc; ++j)
+                    values[(static_cast<int64_t>(t) * k + i) * kc + j] = at(rb, i, cb, j);
             ++t;
         }
         row_ptr[rb + 1] = t;
     }
     return OK;
+}
+
+Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t *row_ptr,
+                     int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err) {
+    return dense_to_blocks(cout, cin, dense, k, 1, row_ptr, col_idx, values, capacity, nnzb, err);
 }
 
 namespace {

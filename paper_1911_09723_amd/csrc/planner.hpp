@@ -216,6 +216,16 @@ Status detect_block_rows(int32_t cout, int32_t cin, const float *dense, int32_t 
 Status dense_to_bcsr(int32_t cout, int32_t cin, const float *dense, int32_t k, int32_t *row_ptr,
                      int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err);
 
+// The same for blocks of kr output x kc input channels (Fig. 5: 4x1 and 2x2
+// beside 1x4): the (kr, kc) in {1, 2, 4}^2 with the most weights per block
+// (output blocks first on a tie) for which every aligned block is all zero or
+// all nonzero; and the conversion to that block-CSR (col_idx = first input
+// channel of a block, values[(t * kr + i) * kc + j]).  kc = 1 is
+// dense_to_bcsr.
+Status detect_blocks(int32_t cout, int32_t cin, const float *dense, int32_t &kr, int32_t &kc, std::string &err);
+Status dense_to_blocks(int32_t cout, int32_t cin, const float *dense, int32_t kr, int32_t kc, int32_t *row_ptr,
+                       int32_t *col_idx, float *values, int64_t capacity, int64_t &nnzb, std::string &err);
+
 // Check the block-CSR arrays; on failure return the status and set `err`.
 Status validate(const Input &in, std::string &err);
 

@@ -313,6 +313,74 @@ spconv_status spconv_dense_to_bcsr(int32_t cout, int32_t cin, const float *dense
     return SPCONV_OK;
 }
 
+spconv_status spconv_detect_blocks(int32_t cout, int32_t cin, const float *dense, int32_t *block_rows,
+                                   int32_t *block_cols) {
+    g_err.clear();
+    if (!block_rows || !block_cols)
+        return fail(SPCONV_E_ARG, "block_rows or block_cols is NULL");
+    std::string err;
+    int32_t kr = 1, kc = 1;
+    const spconv::Status st = spconv::detect_blocks(cout, cin, dense, kr, kc, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    *block_rows = kr;
+    *block_cols = kc;
+    return SPCONV_OK;
+}
+
+spconv_status spconv_dense_to_bcsr_blocked(int32_t cout, int32_t cin, const float *dense, int32_t block_rows,
+                                           int32_t block_cols, int32_t *row_ptr, int32_t *col_idx, float *values,
+                                           int64_t capacity, int64_t *nnzb) {
+    g_err.clear();
+    if (!nnzb)
+        return fail(SPCONV_E_ARG, "nnzb is NULL");
+    std::string err;
+    int64_t n = 0;
+    const spconv::Status st = spconv::dense_to_blocks(cout, cin, dense, block_rows, block_cols, row_ptr, col_idx,
+                                                      values, capacity, n, err);
+    *nnzb = n;
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_create_dense_blocked(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
+                                               int32_t block_rows, int32_t block_cols, const float *bias,
+                                               spconv_act act, spconv_dtype storage) {
+    g_err.clear();
+    if (!out)
+        return fail(SPCONV_E_ARG, "out is NULL");
+    *out = nullptr;
+    if ((block_rows == 0) != (block_cols == 0))
+        return fail(SPCONV_E_ARG, "block_rows and block_cols must both be 0 (detect) or both be given");
+    std::string err;
+    int32_t kr = block_rows, kc = block_cols;
+    spconv::Status st = spconv::OK;
+    if (kr == 0)
+        st = spconv::detect_blocks(cout, cin, dense, kr, kc, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    int64_t nnzb = 0;
+    st = spconv::dense_to_blocks(cout, cin, dense, kr, kc, nullptr, nullptr, nullptr, 0, nnzb, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    std::vector<int32_t> row_ptr, col_idx;
+    std::vector<float> values;
+    try {
+        row_ptr.resize(static_cast<size_t>(cout / kr) + 1);
+        col_idx.resize(static_cast<size_t>(std::max<int64_t>(nnzb, 1)));
+        values.resize(static_cast<size_t>(std::max<int64_t>(nnzb, 1) * kr * kc));
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while converting the dense weight");
+    }
+    st = spconv::dense_to_blocks(cout, cin, dense, kr, kc, row_ptr.data(), col_idx.data(), values.data(), nnzb,
+                                 nnzb, err);
+    if (st != spconv::OK)
+        return fail(static_cast<spconv_status>(st), err);
+    return spconv_plan_create_blocked(out, cout, cin, kr, kc, row_ptr.data(), col_idx.data(), values.data(), bias,
+                                      act, storage, nullptr);
+}
+
 spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout, int32_t cin, const float *dense,
                                        int32_t block_rows, const float *bias, spconv_act act,
                                        spconv_dtype storage) {

@@ -30,7 +30,8 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_options_init", "spconv_plan_create_ex", "spconv_plan_get_info", "spconv_plan_unpack",
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
-            "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked")
+            "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked", "spconv_detect_blocks",
+            "spconv_dense_to_bcsr_blocked", "spconv_plan_create_dense_blocked")
 
 
 class SpconvError(RuntimeError):
@@ -102,6 +103,13 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_create_blocked.restype = i32
     lib.spconv_plan_create_blocked.argtypes = [ctypes.POINTER(vp), i32, i32, i32, i32, vp, vp, vp, vp, i32, i32,
                                                ctypes.POINTER(spconv_options)]
+    lib.spconv_detect_blocks.restype = i32
+    lib.spconv_detect_blocks.argtypes = [i32, i32, vp, ctypes.POINTER(i32), ctypes.POINTER(i32)]
+    lib.spconv_dense_to_bcsr_blocked.restype = i32
+    lib.spconv_dense_to_bcsr_blocked.argtypes = [i32, i32, vp, i32, i32, vp, vp, vp, ctypes.c_int64,
+                                                 ctypes.POINTER(ctypes.c_int64)]
+    lib.spconv_plan_create_dense_blocked.restype = i32
+    lib.spconv_plan_create_dense_blocked.argtypes = [ctypes.POINTER(vp), i32, i32, vp, i32, i32, vp, i32, i32]
     lib.spconv_plan_create_fused.restype = i32
     lib.spconv_plan_create_fused.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i32,
                                              i32, i32, ctypes.POINTER(spconv_options)]
@@ -211,6 +219,48 @@ def spconv_dense_to_bcsr(dense, block_rows: int):
     va = np.zeros(max(n.value, 1) * k, np.float32)
     _check(lib.spconv_dense_to_bcsr(cout, cin, _ptr(d), k, _ptr(rp), _ptr(ci), _ptr(va), n.value, ctypes.byref(n)))
     return rp, ci[:n.value], va[:n.value * k]
+
+
+def spconv_detect_blocks(dense):
+    """(block_rows, block_cols) detected in a dense [Cout, Cin] weight."""
+    d = _arr(dense, np.float32)
+    kr, kc = ctypes.c_int32(), ctypes.c_int32()
+    _check(load_library().spconv_detect_blocks(int(d.shape[0]), int(d.shape[1]), _ptr(d), ctypes.byref(kr),
+                                               ctypes.byref(kc)))
+    return kr.value, kc.value
+
+
+def spconv_dense_to_bcsr_blocked(dense, block_rows: int, block_cols: int):
+    """Convert a dense weight to block_rows x block_cols blocks: (row_ptr, col_idx, values)."""
+    lib = load_library()
+    d = _arr(dense, np.float32)
+    cout, cin = int(d.shape[0]), int(d.shape[1])
+    kr, kc = int(block_rows), int(block_cols)
+    n = ctypes.c_int64()
+    _check(lib.spconv_dense_to_bcsr_blocked(cout, cin, _ptr(d), kr, kc, None, None, None, 0, ctypes.byref(n)))
+    rp = np.zeros(cout // kr + 1, np.int32)
+    ci = np.zeros(max(n.value, 1), np.int32)
+    va = np.zeros(max(n.value, 1) * kr * kc, np.float32)
+    _check(lib.spconv_dense_to_bcsr_blocked(cout, cin, _ptr(d), kr, kc, _ptr(rp), _ptr(ci), _ptr(va), n.value,
+                                            ctypes.byref(n)))
+    return rp, ci[:n.value], va[:n.value * kr * kc]
+
+
+def spconv_plan_create_dense_blocked(dense, block_rows: int = 0, block_cols: int = 0, bias=None, act="none",
+                                     storage="f32", check: bool = True):
+    """Plan from a dense weight with 2-D blocks (0, 0 = detect)."""
+    d = _arr(dense, np.float32)
+    bi = _arr(bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    status = load_library().spconv_plan_create_dense_blocked(ctypes.byref(out), int(d.shape[0]), int(d.shape[1]),
+                                                             _ptr(d), int(block_rows), int(block_cols), _ptr(bi), a,
+                                                             st)
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
 
 
 def spconv_plan_create_dense(dense, block_rows: int = 0, bias=None, act="none", storage="f32",

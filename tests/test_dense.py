@@ -125,3 +125,59 @@ def test_converted_weight_plans_like_the_block_csr():
     finally:
         sp.spconv_destroy(h)
     assert k == 2 and np.array_equal(urp, rp) and np.array_equal(uci, ci) and np.array_equal(uva, va)
+
+
+# ---- blocks over input channels (4x1, 2x2, ...) ----
+
+from blocks_util import dense_from_blocks, random_blocks  # noqa: E402
+
+
+@pytest.mark.parametrize("kr,kc", [(1, 4), (2, 2), (4, 4), (1, 2), (4, 1), (2, 4)])
+def test_blocked_detection_and_conversion_round_trip(kr, kc):
+    rng = np.random.default_rng(kr * 10 + kc)
+    cout, cin = 8 * kr, 12 * kc
+    rp, ci, va = random_blocks(cout, cin, kr, kc, 0.4, rng)
+    va[va == 0] = 1.0
+    dense = dense_from_blocks(cout, cin, kr, kc, rp, ci, va).astype(np.float32)
+    got = sp.spconv_detect_blocks(dense)
+    # the detected shape holds at least as many weights and also describes the mask
+    assert got[0] * got[1] >= kr * kc
+    rp2, ci2, va2 = sp.spconv_dense_to_bcsr_blocked(dense, kr, kc)
+    assert np.array_equal(rp2, rp) and np.array_equal(ci2, ci) and np.array_equal(va2, va)
+    rp3, ci3, va3 = sp.spconv_dense_to_bcsr_blocked(dense, *got)
+    assert np.array_equal(dense_from_blocks(cout, cin, got[0], got[1], rp3, ci3, va3), dense)
+    assert np.count_nonzero(va3) == np.count_nonzero(dense)  # the detected blocks store no zero
+
+
+def test_detection_prefers_output_blocks_on_a_tie():
+    """The most weights per block wins; among equals the output-channel block."""
+    dense = np.zeros((8, 8), np.float32)
+    dense[0:4, 0:4] = 1.0  # one 4x4 block: 4x4 wins
+    assert sp.spconv_detect_blocks(dense) == (4, 4)
+    dense = np.zeros((4, 6), np.float32)
+    dense[:, 2] = 1.0  # 4 x 1 column: only output blocks of 4 (cin 6 is not a multiple of 4)
+    assert sp.spconv_detect_blocks(dense) == (4, 1)
+    dense = np.zeros((2, 2), np.float32)
+    dense[0, 0] = 1.0  # no block shape fits
+    assert sp.spconv_detect_blocks(dense) == (1, 1)
+
+
+def test_blocked_conversion_errors():
+    dense = np.ones((4, 6), np.float32)
+    lib = sp.load_library()
+    import ctypes
+    n = ctypes.c_int64()
+    assert lib.spconv_dense_to_bcsr_blocked(4, 6, dense.ctypes.data_as(ctypes.c_void_p), 1, 4, None, None, None, 0,
+                                            ctypes.byref(n)) == sp.E_SHAPE
+    assert lib.spconv_dense_to_bcsr_blocked(4, 6, dense.ctypes.data_as(ctypes.c_void_p), 1, 3, None, None, None, 0,
+                                            ctypes.byref(n)) == sp.E_UNSUPPORTED
+    st, h = sp.spconv_plan_create_dense_blocked(dense, 0, 2, check=False)
+    assert st == sp.E_ARG and h is None
+
+
+def test_tie_between_output_and_input_blocks():
+    """A 4 x 4 mask block is also 4x1, 1x4 and 2x2 blocked: 4x4 wins; a 2 x 2
+    block (2x2 vs nothing larger) reports (2, 2) over (2, 1) and (1, 2)."""
+    dense = np.zeros((4, 4), np.float32)
+    dense[0:2, 2:4] = 3.0
+    assert sp.spconv_detect_blocks(dense) == (2, 2)

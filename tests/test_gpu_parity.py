@@ -311,3 +311,34 @@ def test_input_channel_blocks_match_oracle(kr, kc, storage, cin, h, w):
     tol = oracle.tolerance(y_ref, s, storage)
     assert y.shape == y_ref.shape
     assert np.all(np.abs(y.astype(np.float64) - y_ref.astype(np.float64)) <= tol)
+
+
+def test_dense_weight_with_2x2_blocks_plans_like_the_blocked_arrays():
+    """spconv_plan_create_dense_blocked (detecting 2 x 2) gives the same bits
+    as spconv_plan_create_blocked on the same blocks."""
+    from paper_1911_09723_amd import Plan, spconv
+    from blocks_util import dense_from_blocks, random_blocks
+    import torch
+    rng = np.random.default_rng(5)
+    cin, cout = 128, 96
+    rp, ci, va = random_blocks(cout, cin, 2, 2, 0.1, rng)
+    va[va == 0] = 0.25
+    dense = dense_from_blocks(cout, cin, 2, 2, rp, ci, va).astype(np.float32)
+    assert spconv.spconv_detect_blocks(dense) == (2, 2)
+    b = rng.standard_normal(cout).astype(np.float32)
+    x = np.maximum(rng.standard_normal((2, cin, 9, 9)), 0).astype(np.float32)
+    p1 = Plan.blocked(cout, cin, 2, 2, rp, ci, va, b, "relu")
+    p2 = Plan.__new__(Plan)
+    p2.handle = spconv.spconv_plan_create_dense_blocked(dense, 0, 0, b, "relu")
+    p2.cout, p2.cin, p2.storage, p2.dw_stride = cout, cin, "f32", 0
+    try:
+        note("dense 2x2 blocked plan")
+        xt = to_gpu(x)
+        y1 = p1.run(xt)
+        y2 = p2.run(xt)
+        torch.cuda.synchronize()
+        assert p2.info()["block_cols"] == 2 and p2.info()["block_rows"] == 2
+        assert torch.equal(y1, y2)
+    finally:
+        p1.close()
+        p2.close()
