@@ -134,8 +134,9 @@ def _engine_case(batch, hw, classes, seed):
     return net, x, MobileNetV1Engine(net, batch, hw, hw)
 
 
-@pytest.mark.parametrize("batch,hw,classes", [(2, 224, 1000), (3, 32, 10)])
+@pytest.mark.parametrize("batch,hw,classes", [(2, 224, 1000), (3, 32, 10), (64, 224, 1000)])
 def test_mobilenet_v1_forward_matches_oracle(batch, hw, classes):
+    # batch 64 at 224 x 224 is the configuration bench.py times
     net, x, eng = _engine_case(batch, hw, classes, seed=batch)
     try:
         note("mobilenet v1 batch %d %dx%d (%d launches, %d fused blocks)" % (batch, hw, hw, eng.launches(),
