@@ -73,6 +73,16 @@ def load_library(path: Optional[str] = None):
     p = path or LIBRARY_PATH
     if not os.path.exists(p):
         raise RuntimeError("libspconv.so is not built (%s); run `python -m paper_1911_09723_amd.build`" % p)
+    # PyTorch for ROCm carries its own HIP runtime with the same soname
+    # (libamdhip64.so.7) as the one this library links.  Loaded after
+    # PyTorch, the library binds to PyTorch's runtime and the process has one;
+    # loaded first, PyTorch would bring up a second runtime instance and this
+    # library's calls would find no device.  So PyTorch, when installed, is
+    # imported first.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(p)
     vp, i32 = ctypes.c_void_p, ctypes.c_int32
     lib.spconv_plan_create.restype = i32

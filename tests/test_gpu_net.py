@@ -176,3 +176,25 @@ def test_mobilenet_v1_graph_replays_equal_eager_runs():
         assert not np.array_equal(ys[0], ys[1])
     finally:
         eng.close()
+
+
+def test_library_loaded_before_torch_shares_its_runtime():
+    """A fresh process that loads libspconv before importing torch (the
+    binding imports torch first, so both use one HIP runtime) can plan and
+    run; regression test for a second runtime instance finding no device."""
+    import subprocess
+    import sys
+    import os
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "import paper_1911_09723_amd as P\n"
+            "P.load_library()\n"
+            "import numpy as np, torch\n"
+            "from synth import make_layer\n"
+            "l = make_layer(32, 16, 5, 5, 1, 0.5, seed=1)\n"
+            "p = P.Plan.from_layer(l)\n"
+            "y = p.run(torch.from_numpy(l.x).to('cuda:0'))\n"
+            "torch.cuda.synchronize()\n"
+            "print('ran', tuple(y.shape))\n") % os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    note("library before torch (subprocess)")
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=180)
+    assert out.returncode == 0 and "ran (1, 16, 5, 5)" in out.stdout, out.stdout[-2000:] + out.stderr[-2000:]
