@@ -274,9 +274,11 @@ typedef struct {
     int32_t struct_size; /* sizeof(spconv_options) */
     int32_t reorder;     /* 1 (default): process rows in descending nonzero order; 0: natural order */
     int32_t host_only;   /* 1: plan on the host only, no device memory; spconv_run refuses it */
-    int32_t kernel;      /* 0 = choose automatically; 1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED
-                            when the strip of cin channels does not fit in LDS); 2 = direct-load
-                            kernel */
+    int32_t kernel;      /* 0 = choose automatically (the LDS-strip or direct-load kernel);
+                            1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED when the strip of cin
+                            channels does not fit in LDS); 2 = direct-load kernel; 3 =
+                            register-indexed kernel (SPCONV_E_UNSUPPORTED for fp16 storage or a
+                            depthwise stage) */
     int32_t group_lanes; /* 0 = choose automatically; else 4, 8 or 16 lanes per (block) row: each
                             lane accumulates 16 / group_lanes vectors of 16 bytes of the tile's
                             columns, and a wavefront works on 64 / group_lanes rows at a time

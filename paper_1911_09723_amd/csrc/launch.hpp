@@ -48,7 +48,39 @@ struct DevicePlan {
     const int32_t *sel_ptr = nullptr;
     const int32_t *wave_ev = nullptr;
     const float *dw = nullptr;          // depthwise taps and biases, kDwParams per strip channel
+    // register-indexed kernel (planner.hpp)
+    int32_t use_indexed = 0;
+    int32_t rslots = 0, rgroups = 0, rwaves = 0, rnch = 0;
+    const uint32_t *rrec = nullptr;
+    const int32_t *rslot_batch = nullptr;
+    const int32_t *rslot_chunk = nullptr;
+    const int32_t *rslot_rows = nullptr;
+    const float *rslot_bias = nullptr;
+    const int32_t *rpair_ptr = nullptr;
+    const uint32_t *rpair_ent = nullptr;
+    const float *rrow_bias = nullptr;   // bias of every output channel
+    int32_t *flag = nullptr;            // device word: bit 0 set when a bounded wait of a kernel gave up
 };
+
+// How one launch of the register-indexed kernel covers m columns: `tiles`
+// whole tiles of 64 c columns (times the plan's slot groups), then columns
+// [lcol0, m) as `lpieces` (64-column group, row pair) pieces, `lper` per
+// workgroup; `grid` workgroups; LDS offsets of the counters and the lane
+// column table, and the LDS bytes per workgroup.
+struct IndexedLaunch {
+    int32_t c = 1;
+    int64_t tiles = 0;
+    int32_t lcol0 = 0, lpieces = 0, lper = 0;
+    int32_t grid = 1;
+    int32_t ctl_off = 0, xo_off = 0, lds_bytes = 0;
+};
+
+IndexedLaunch plan_indexed_launch(const DevicePlan &p, int64_t m);
+// Once per plan: allow the indexed kernels their LDS.
+hipError_t prepare_indexed(const DevicePlan &p);
+// One launch of the register-indexed kernel over all m = N * hw columns.
+hipError_t launch_indexed(const DevicePlan &p, const float *x, float *y, int32_t m, int32_t hw, int64_t x_bytes,
+                          int64_t y_bytes, hipStream_t stream);
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when
 // needed and record num_cus and blocks_per_cu.

@@ -609,9 +609,13 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         in.values = xvalues.data();
         in.block_cols = 1;
     }
-    if (opt.kernel < 0 || opt.kernel > 2) {
-        err = "kernel must be 0 (automatic), 1 (strip) or 2 (direct)";
+    if (opt.kernel < 0 || opt.kernel > 3) {
+        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct) or 3 (register-indexed)";
         return E_ARG;
+    }
+    if (opt.kernel == 3 && (in.dw_stride || in.storage != 0)) {
+        err = "the register-indexed kernel runs fp32 plans without a depthwise stage";
+        return E_UNSUPPORTED;
     }
     if (opt.group_lanes != 0 && opt.group_lanes != 4 && opt.group_lanes != 8 && opt.group_lanes != 16) {
         err = "group_lanes must be 0, 4, 8 or 16";
@@ -644,7 +648,10 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     p.act = in.act;
     p.storage = in.storage;
     p.kc = in_arg.block_cols;
-    st = choose_geometry(in, opt, p, err);
+    Options gopt = opt;
+    if (gopt.kernel == 3)
+        gopt.kernel = 0;
+    st = choose_geometry(in, gopt, p, err);
     if (st != OK)
         return st;
     if (in.dw_stride) {
@@ -676,6 +683,10 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     auto len = [&](int32_t r) { return in.row_ptr[r + 1] - in.row_ptr[r]; };
     if (opt.reorder)
         std::stable_sort(p.perm.begin(), p.perm.end(), [&](int32_t a, int32_t b) { return len(a) > len(b); });
+    if (!in.dw_stride && in.storage == 0) {
+        build_indexed(in, p.perm, p);
+        p.use_indexed = opt.kernel == 3;
+    }
 
     // 2. bundles of NB consecutive rows in that order, each a whole number of
     // steps of 4 slots and at least one step long
@@ -923,6 +934,303 @@ Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_id
         for (int32_t i = 0; i < S; ++i)
             if (bset[i] < b1)
                 return bad("a wavefront's stream ends before its bundles do");
+    }
+    int32_t acc = 0;
+    if (row_ptr)
+        row_ptr[0] = 0;
+    for (int32_t r = 0; r < rows; ++r) {
+        if (col_idx)
+            std::copy(cols[r].begin(), cols[r].end(), col_idx + acc);
+        if (values)
+            std::copy(vals[r].begin(), vals[r].end(), values + static_cast<int64_t>(acc) * k);
+        acc += static_cast<int32_t>(cols[r].size());
+        if (row_ptr)
+            row_ptr[r + 1] = acc;
+    }
+    return OK;
+}
+
+}  // namespace spconv
+
+namespace spconv {
+
+// Register-indexed kernel: slots, records, row pairs (planner.hpp).
+void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPlan &p) {
+    const int32_t k = in.block_rows;
+    const int32_t rows = in.cout / k;           // block rows
+    const int32_t cap = kSlotRows / k;          // block rows per slot
+    const int32_t S = (rows + cap - 1) / cap;
+    const int32_t G = (S + kSlotsPerGroup - 1) / kSlotsPerGroup;
+    const int32_t W = (S + G - 1) / G;
+    const int32_t nch = (in.cin + kChunk - 1) / kChunk;
+    const int32_t P = rec_slots(k);
+    auto len = [&](int32_t r) { return in.row_ptr[r + 1] - in.row_ptr[r]; };
+    auto weight = [&](int64_t t, int32_t i) {
+        float v = in.values[t * k + i];
+        if (in.storage == 1)
+            v = half_to_float(float_to_half_rne(v));
+        return v;
+    };
+    p.rslots = S;
+    p.rgroups = G;
+    p.rwaves = W;
+    p.rnch = nch;
+
+    // 1. slots: heaviest block rows first, each to the least loaded slot with room
+    std::vector<std::vector<int32_t>> members(S);
+    std::vector<int64_t> load(S, 0);
+    for (int32_t rb : order) {
+        int32_t best = -1;
+        for (int32_t s = 0; s < S; ++s)
+            if (static_cast<int32_t>(members[s].size()) < cap && (best < 0 || load[s] < load[best]))
+                best = s;
+        members[best].push_back(rb);
+        load[best] += len(rb);
+    }
+    p.rslot_rows.assign(static_cast<size_t>(S) * kSlotRows, -1);
+    p.rslot_bias.assign(static_cast<size_t>(S) * kSlotRows, 0.0f);
+    for (int32_t s = 0; s < S; ++s) {
+        std::sort(members[s].begin(), members[s].end());
+        for (int32_t b = 0; b < static_cast<int32_t>(members[s].size()); ++b)
+            for (int32_t i = 0; i < k; ++i) {
+                const int32_t r = members[s][b] * k + i;
+                p.rslot_rows[static_cast<size_t>(s) * kSlotRows + b * k + i] = r;
+                p.rslot_bias[static_cast<size_t>(s) * kSlotRows + b * k + i] = in.bias ? in.bias[r] : 0.0f;
+            }
+    }
+
+    // 2. records: per slot, per channel ascending, groups of at most P blocks
+    p.rrec.clear();
+    p.rslot_batch.assign(S, 0);
+    p.rslot_chunk.assign(static_cast<size_t>(S) * (nch + 1), 0);
+    const int32_t batch_words = kRecWords * kBatchRecs;
+    for (int32_t s = 0; s < S; ++s) {
+        const int64_t first_batch = static_cast<int64_t>(p.rrec.size()) / batch_words;
+        p.rslot_batch[s] = static_cast<int32_t>(first_batch);
+        // (channel, slot position, stored-block index) of every block of the slot
+        struct Ent {
+            int32_t c, pos;
+            int64_t t;
+        };
+        std::vector<Ent> ents;
+        for (int32_t b = 0; b < static_cast<int32_t>(members[s].size()); ++b) {
+            const int32_t rb = members[s][b];
+            for (int32_t t = in.row_ptr[rb]; t < in.row_ptr[rb + 1]; ++t)
+                ents.push_back({in.col_idx[t], b, t});
+        }
+        std::stable_sort(ents.begin(), ents.end(), [](const Ent &a, const Ent &b) {
+            return a.c != b.c ? a.c < b.c : a.pos < b.pos;
+        });
+        size_t e = 0;
+        for (int32_t q = 0; q < nch; ++q) {
+            const int64_t batch_now = static_cast<int64_t>(p.rrec.size()) / batch_words - first_batch;
+            int64_t nrec = 0;
+            while (e < ents.size() && ents[e].c < (q + 1) * kChunk) {
+                const int32_t c = ents[e].c;
+                size_t e1 = e;
+                while (e1 < ents.size() && ents[e1].c == c)
+                    ++e1;
+                for (size_t g = e; g < e1; g += P) {
+                    const int32_t n = static_cast<int32_t>(std::min<size_t>(P, e1 - g));
+                    uint32_t w[kRecWords] = {0, 0, 0, 0, 0, 0, 0, 0};
+                    w[0] = static_cast<uint32_t>(c % kRing);
+                    for (int32_t j = 0; j < n; ++j) {
+                        const uint32_t row = static_cast<uint32_t>(ents[g + j].pos * k);
+                        w[1 + j] = row;
+                        for (int32_t i = 0; i < k; ++i) {
+                            const float v = weight(ents[g + j].t, i);
+                            std::memcpy(&w[4 + j * k + i], &v, 4);
+                        }
+                    }
+                    if (n > 1)
+                        w[1] |= 1u << 8;
+                    if (n > 2)
+                        w[1] |= 1u << 9;
+                    p.rrec.insert(p.rrec.end(), w, w + kRecWords);
+                    ++nrec;
+                }
+                e = e1;
+            }
+            if (nrec % kBatchRecs)
+                p.rrec.insert(p.rrec.end(), kRecWords, 0u);
+            p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + q] =
+                static_cast<int32_t>(batch_now * 2 + (nrec % 2));
+        }
+        const int64_t total = static_cast<int64_t>(p.rrec.size()) / batch_words - first_batch;
+        p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + nch] = static_cast<int32_t>(total * 2);
+    }
+    p.rrec.insert(p.rrec.end(), static_cast<size_t>(2 * batch_words), 0u);
+
+    // 3. row pairs
+    p.rrow_bias.assign(in.cout, 0.0f);
+    if (in.bias)
+        std::copy(in.bias, in.bias + in.cout, p.rrow_bias.begin());
+    const int32_t npairs = (in.cout + 1) / 2;
+    p.rpair_ptr.assign(npairs + 1, 0);
+    p.rpair_ent.clear();
+    for (int32_t j = 0; j < npairs; ++j) {
+        // the blocks of output channels 2j and 2j + 1 (block row r / k, element r % k)
+        int32_t ra = 2 * j, rbb = 2 * j + 1;
+        std::vector<std::pair<int32_t, int32_t>> lst;  // (channel, which) for stored (row, channel)
+        struct W2 {
+            float a = 0.0f, b = 0.0f;
+            uint32_t mask = 0;
+        };
+        std::vector<int32_t> chans;
+        std::vector<W2> ws;
+        auto add_row = [&](int32_t r, int32_t which) {
+            if (r >= in.cout)
+                return;
+            const int32_t rb = r / k, i = r % k;
+            for (int32_t t = in.row_ptr[rb]; t < in.row_ptr[rb + 1]; ++t)
+                lst.push_back({in.col_idx[t], which});
+            (void)i;
+        };
+        add_row(ra, 0);
+        add_row(rbb, 1);
+        std::sort(lst.begin(), lst.end());
+        for (size_t u = 0; u < lst.size(); ++u) {
+            const int32_t c = lst[u].first;
+            if (chans.empty() || chans.back() != c) {
+                chans.push_back(c);
+                ws.push_back(W2());
+            }
+            const int32_t r = lst[u].second ? rbb : ra;
+            const int32_t rb = r / k, i = r % k;
+            const int32_t *b0 = in.col_idx + in.row_ptr[rb];
+            const int32_t *b1 = in.col_idx + in.row_ptr[rb + 1];
+            const int64_t t = std::lower_bound(b0, b1, c) - in.col_idx;
+            const float v = weight(t, i);
+            if (lst[u].second) {
+                ws.back().b = v;
+                ws.back().mask |= 2u;
+            } else {
+                ws.back().a = v;
+                ws.back().mask |= 1u;
+            }
+        }
+        for (size_t u = 0; u < chans.size(); ++u) {
+            uint32_t w[4];
+            w[0] = static_cast<uint32_t>(chans[u]) | (ws[u].mask << 24);
+            std::memcpy(&w[1], &ws[u].a, 4);
+            std::memcpy(&w[2], &ws[u].b, 4);
+            w[3] = 0;
+            p.rpair_ent.insert(p.rpair_ent.end(), w, w + 4);
+        }
+        p.rpair_ptr[j + 1] = static_cast<int32_t>(p.rpair_ent.size() / 4);
+    }
+}
+
+Status unpack_indexed(const PackedPlan &p, bool from_pairs, int32_t *row_ptr, int32_t *col_idx, float *values,
+                      std::string &err) {
+    if (p.rslots == 0) {
+        err = "the plan has no register-indexed streams";
+        return E_FORMAT;
+    }
+    const int32_t k = p.k;
+    const int32_t rows = p.cout / k;
+    std::vector<std::vector<int32_t>> cols(rows);
+    std::vector<std::vector<float>> vals(rows);
+    auto bad = [&](const std::string &m) {
+        err = m;
+        return E_FORMAT;
+    };
+    auto fl = [](uint32_t u) {
+        float v;
+        std::memcpy(&v, &u, 4);
+        return v;
+    };
+    const int32_t nch = p.rnch;
+    const int32_t P = rec_slots(k);
+    if (!from_pairs) {
+        // (block row, element) -> its column and value lists are filled per block row;
+        // per-row element values are collected block-major
+        std::vector<std::vector<int32_t>> bc(rows);
+        std::vector<std::vector<std::vector<float>>> bv(rows);
+        for (int32_t s = 0; s < p.rslots; ++s) {
+            const int64_t base = static_cast<int64_t>(p.rslot_batch[s]) * kBatchRecs;  // first record
+            const int32_t *ch = p.rslot_chunk.data() + static_cast<size_t>(s) * (nch + 1);
+            int32_t prev_c = -1;
+            for (int32_t q = 0; q < nch; ++q) {
+                const int32_t b0 = ch[q] >> 1, b1 = ch[q + 1] >> 1, odd = ch[q] & 1;
+                const int64_t nrec = static_cast<int64_t>(b1 - b0) * kBatchRecs - (odd ? 1 : 0);
+                if (b1 < b0 || (odd && b1 == b0))
+                    return bad("chunk table out of order");
+                for (int64_t r = 0; r < nrec; ++r) {
+                    const uint32_t *w = p.rrec.data() + (base + static_cast<int64_t>(b0) * kBatchRecs + r) * kRecWords;
+                    const int32_t n = 1 + ((w[1] >> 8) & 1) + ((w[1] >> 9) & 1);
+                    if (n > P)
+                        return bad("record holds more blocks than its kind allows");
+                    // the channel: the ring row plus the chunk's ring base
+                    const int32_t c = (q * kChunk) / kRing * kRing + static_cast<int32_t>(w[0]);
+                    if (w[0] >= static_cast<uint32_t>(kRing) || c < q * kChunk || c >= (q + 1) * kChunk || c >= p.cin)
+                        return bad("record channel outside its chunk");
+                    if (c < prev_c)
+                        return bad("records do not ascend by channel");
+                    prev_c = c;
+                    for (int32_t j = 0; j < n; ++j) {
+                        const uint32_t row = w[1 + j] & 0xffu;
+                        if (row % k || static_cast<int32_t>(row) >= kSlotRows)
+                            return bad("slot row out of range");
+                        const int32_t orow = p.rslot_rows[static_cast<size_t>(s) * kSlotRows + row];
+                        if (orow < 0 || orow % k)
+                            return bad("record names an unused slot row");
+                        const int32_t rb = orow / k;
+                        bc[rb].push_back(c);
+                        std::vector<float> v(k);
+                        for (int32_t i = 0; i < k; ++i)
+                            v[i] = fl(w[4 + j * k + i]);
+                        bv[rb].push_back(v);
+                    }
+                }
+            }
+        }
+        for (int32_t rb = 0; rb < rows; ++rb) {
+            std::vector<size_t> idx(bc[rb].size());
+            std::iota(idx.begin(), idx.end(), 0);
+            std::stable_sort(idx.begin(), idx.end(), [&](size_t a, size_t b) { return bc[rb][a] < bc[rb][b]; });
+            for (size_t u : idx) {
+                cols[rb].push_back(bc[rb][u]);
+                for (int32_t i = 0; i < k; ++i)
+                    vals[rb].push_back(bv[rb][u][i]);
+            }
+        }
+    } else {
+        // per output channel, its (channel, value) list; blocks are rebuilt per block row
+        std::vector<std::vector<std::pair<int32_t, float>>> orow(p.cout);
+        const int32_t npairs = static_cast<int32_t>(p.rpair_ptr.size()) - 1;
+        for (int32_t j = 0; j < npairs; ++j) {
+            int32_t prev = -1;
+            for (int32_t u = p.rpair_ptr[j]; u < p.rpair_ptr[j + 1]; ++u) {
+                const uint32_t *w = p.rpair_ent.data() + static_cast<size_t>(u) * 4;
+                const int32_t c = static_cast<int32_t>(w[0] & 0xffffffu);
+                const uint32_t mask = w[0] >> 24;
+                if (c <= prev || c >= p.cin || mask == 0 || mask > 3)
+                    return bad("pair entries malformed");
+                prev = c;
+                if (mask & 1u)
+                    orow[2 * j].push_back({c, fl(w[1])});
+                if (mask & 2u) {
+                    if (2 * j + 1 >= p.cout)
+                        return bad("pair entry for a row past cout");
+                    orow[2 * j + 1].push_back({c, fl(w[2])});
+                }
+            }
+        }
+        for (int32_t rb = 0; rb < rows; ++rb) {
+            const auto &lead = orow[rb * k];
+            for (int32_t i = 1; i < k; ++i)
+                if (orow[rb * k + i].size() != lead.size())
+                    return bad("rows of one block differ in their channels");
+            for (size_t u = 0; u < lead.size(); ++u) {
+                cols[rb].push_back(lead[u].first);
+                for (int32_t i = 0; i < k; ++i) {
+                    if (orow[rb * k + i][u].first != lead[u].first)
+                        return bad("rows of one block differ in their channels");
+                    vals[rb].push_back(orow[rb * k + i][u].second);
+                }
+            }
+        }
     }
     int32_t acc = 0;
     if (row_ptr)

@@ -82,7 +82,7 @@ namespace spconv {
 
 enum Status { OK = 0, E_ARG = 1, E_FORMAT = 2, E_SHAPE = 3, E_UNSUPPORTED = 4, E_NOMEM = 5, E_HIP = 6 };
 
-enum Kernel { KERNEL_STRIP = 0, KERNEL_DIRECT = 1 };
+enum Kernel { KERNEL_STRIP = 0, KERNEL_DIRECT = 1, KERNEL_INDEXED = 2 };
 
 // Largest LDS footprint of one workgroup on gfx950 (160 KiB per CU).
 constexpr int64_t kMaxLdsBytes = 160 * 1024;
@@ -107,6 +107,49 @@ constexpr int32_t kWaveEvents = 2 * kMaxRegions;
 constexpr int32_t kDwParams = 16;
 // Smallest depthwise staging area worth a second workgroup per CU.
 constexpr int64_t kMinStageBytes = 16 * 1024;
+
+// Register-indexed kernel (KERNEL_INDEXED): rows are grouped into slots of
+// kSlotRows output channels, one slot per wavefront; the wavefront walks its
+// slot's nonzeros by ascending input channel, reads each channel's X values
+// once per record from an LDS ring, and adds them into the accumulator of the
+// record's row, chosen at run time by register-relative addressing.
+//
+//   Slots.  Block rows (1 x k blocks) are assigned to slots of at most
+//   kSlotRows / k block rows, longest processing time first (heaviest rows
+//   first, each to the least loaded slot with room), so every slot carries
+//   about the same number of stored blocks.  Slot row i is output channel
+//   rslot_rows[s * kSlotRows + i] (-1: unused), with bias rslot_bias[...].
+//   A block at slot position b occupies slot rows b*k .. b*k + k - 1.
+//
+//   Records (kRecWords 32-bit words each): the stored blocks of one slot at one
+//   input channel c, at most kRecSlots(k) = 3, 2, 1 blocks for k = 1, 2, 4:
+//     w[0]  c % kRing (the LDS ring row holding channel c)
+//     w[1]  first block's slot row | (more than 1 block) << 8 | (more than 2) << 9
+//     w[2]  second block's slot row (k <= 2), w[3] third (k == 1)
+//     w[4..7]  weights: k == 1: one per block; k == 2: 2 per block; k == 4: the 4
+//   A slot's records ascend by channel.  Channels come in chunks of kChunk;
+//   each chunk's records start on a batch boundary (kBatchRecs records,
+//   kRecWords * kBatchRecs words); an odd chunk is padded with one unused
+//   record.  Slot s's stream starts at batch rslot_batch[s];
+//   rslot_chunk[s * (nch + 1) + q] = (first batch of chunk q) * 2 + (chunk q
+//   has an odd number of records), with q = nch giving the stream's end.  The
+//   record array ends with kBatchRecs * 2 zero records (read ahead, unused).
+//
+//   Row pairs (columns left over after the kernel's whole tiles): pair j is
+//   output channels 2j and 2j + 1; rpair_ptr[j] .. rpair_ptr[j + 1] index its
+//   entries in rpair_ent, 4 words each: channel | (mask << 24) (bit 0: channel
+//   2j has a weight at c, bit 1: 2j + 1 has one), the two weights, 0.  Entries
+//   ascend by channel.
+//
+// Every row still sums its products in ascending input channel from zero,
+// then adds the bias, so results do not depend on the slot assignment.
+constexpr int32_t kSlotRows = 16;
+constexpr int32_t kRecWords = 8;
+constexpr int32_t kBatchRecs = 2;
+constexpr int32_t kRing = 64;
+constexpr int32_t kChunk = 16;
+constexpr int32_t kSlotsPerGroup = 16;
+inline int32_t rec_slots(int32_t k) { return k == 1 ? 3 : k == 2 ? 2 : 1; }
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -135,7 +178,7 @@ struct Input {
 struct Options {
     int32_t reorder = 1;
     int32_t host_only = 0;
-    int32_t kernel = 0;       // 0 automatic, 1 strip, 2 direct
+    int32_t kernel = 0;       // 0 automatic, 1 strip, 2 direct, 3 register-indexed
     int32_t group_lanes = 0;  // 0 automatic, else 4, 8 or 16 lanes per block row
     int32_t waves = 0;        // 0 automatic, else 1 .. 16 wavefronts per workgroup
     int32_t pipe_sets = 0;    // 0 automatic, else 1 or 2 bundles interleaved per wavefront
@@ -180,6 +223,21 @@ struct PackedPlan {
     std::vector<uint32_t> psel;
     std::vector<int32_t> sel_ptr;
     std::vector<int32_t> wave_ev;
+    // register-indexed kernel (planner.hpp, "Register-indexed kernel"); empty
+    // when the plan cannot use it
+    int32_t use_indexed = 0;     // spconv_run launches the register-indexed kernel
+    int32_t rslots = 0;          // slots of kSlotRows output channels
+    int32_t rgroups = 0;         // groups of slots sharing one LDS ring (one workgroup each)
+    int32_t rwaves = 0;          // wavefronts per workgroup = slots per group (the last may have fewer)
+    int32_t rnch = 0;            // chunks of kChunk input channels
+    std::vector<uint32_t> rrec;
+    std::vector<int32_t> rslot_batch;
+    std::vector<int32_t> rslot_chunk;
+    std::vector<int32_t> rslot_rows;
+    std::vector<float> rslot_bias;
+    std::vector<int32_t> rpair_ptr;
+    std::vector<uint32_t> rpair_ent;
+    std::vector<float> rrow_bias;  // bias of every output channel (the row-pair phase)
     std::vector<int32_t> perm;     // block rows in processing order
     std::vector<int32_t> row_nnz;  // stored blocks per block row (host only; for unpacking)
     // statistics
@@ -235,6 +293,18 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &out, std::str
 // Rebuild block-CSR arrays (and the processing order) from a packed plan.
 // Any output pointer may be null.
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm);
+
+// Build the register-indexed kernel's slots, records and row pairs (fields
+// r* of PackedPlan) from 1 x k block-CSR arrays; `order` lists the block rows
+// in processing order.
+void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPlan &p);
+
+// Rebuild block-CSR arrays from the register-indexed records (and separately
+// from the row pairs), checking the stream structure: batch alignment of
+// chunks, ascending channels, ring rows, slot-row ranges.  E_FORMAT with `err`
+// set when inconsistent or absent.
+Status unpack_indexed(const PackedPlan &p, bool from_pairs, int32_t *row_ptr, int32_t *col_idx, float *values,
+                      std::string &err);
 
 // The same from the interleaved streams, walking them as the pipelined kernel
 // does (selector bits, set groups) and checking that every strip read lies

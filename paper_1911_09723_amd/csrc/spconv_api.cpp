@@ -79,7 +79,7 @@ spconv_status upload(spconv_plan_s *pl) {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[12] = {
+    } parts[21] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
@@ -92,6 +92,15 @@ spconv_status upload(spconv_plan_s *pl) {
         {h.sel_ptr.data(), h.sel_ptr.size() * sizeof(int32_t), 0},
         {h.wave_ev.data(), h.wave_ev.size() * sizeof(int32_t), 0},
         {h.dw.data(), h.dw.size() * sizeof(float), 0},
+        {h.rrec.data(), h.rrec.size() * sizeof(uint32_t), 0},
+        {h.rslot_batch.data(), h.rslot_batch.size() * sizeof(int32_t), 0},
+        {h.rslot_chunk.data(), h.rslot_chunk.size() * sizeof(int32_t), 0},
+        {h.rslot_rows.data(), h.rslot_rows.size() * sizeof(int32_t), 0},
+        {h.rslot_bias.data(), h.rslot_bias.size() * sizeof(float), 0},
+        {h.rpair_ptr.data(), h.rpair_ptr.size() * sizeof(int32_t), 0},
+        {h.rpair_ent.data(), h.rpair_ent.size() * sizeof(uint32_t), 0},
+        {h.rrow_bias.data(), h.rrow_bias.size() * sizeof(float), 0},
+        {nullptr, 0, 0},  // the error flag word (zeroed)
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -134,6 +143,15 @@ spconv_status upload(spconv_plan_s *pl) {
     d.sel_ptr = reinterpret_cast<const int32_t *>(base + parts[9].off);
     d.wave_ev = reinterpret_cast<const int32_t *>(base + parts[10].off);
     d.dw = reinterpret_cast<const float *>(base + parts[11].off);
+    d.rrec = reinterpret_cast<const uint32_t *>(base + parts[12].off);
+    d.rslot_batch = reinterpret_cast<const int32_t *>(base + parts[13].off);
+    d.rslot_chunk = reinterpret_cast<const int32_t *>(base + parts[14].off);
+    d.rslot_rows = reinterpret_cast<const int32_t *>(base + parts[15].off);
+    d.rslot_bias = reinterpret_cast<const float *>(base + parts[16].off);
+    d.rpair_ptr = reinterpret_cast<const int32_t *>(base + parts[17].off);
+    d.rpair_ent = reinterpret_cast<const uint32_t *>(base + parts[18].off);
+    d.rrow_bias = reinterpret_cast<const float *>(base + parts[19].off);
+    d.flag = reinterpret_cast<int32_t *>(base + parts[20].off);
     return SPCONV_OK;
 }
 
@@ -163,6 +181,11 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.dw_act = h.dw_act;
     d.stage_off = h.stage_off;
     d.stage_bytes = h.stage_bytes;
+    d.use_indexed = h.use_indexed;
+    d.rslots = h.rslots;
+    d.rgroups = h.rgroups;
+    d.rwaves = h.rwaves;
+    d.rnch = h.rnch;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -214,6 +237,8 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
         spconv_status us = upload(pl);
         if (us == SPCONV_OK) {
             hipError_t pe = spconv::prepare_launch(pl->dev);
+            if (pe == hipSuccess && pl->dev.rslots > 0)
+                pe = spconv::prepare_indexed(pl->dev);
             if (pe != hipSuccess)
                 us = hip_fail("kernel launch set-up", pe);
         }
@@ -459,13 +484,19 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     // the kernels address X and Y relative to the first image of a tile with
     // 32-bit byte offsets: the images one tile's columns touch (at most
     // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
-    const int64_t span = (p.tile_cols - 1) / hw + 2;
+    const int64_t tile_cols = p.use_indexed ? 64 * 6 : p.tile_cols;
+    const int64_t span = (tile_cols - 1) / hw + 2;
     if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,
                     "h * w * channels too large: the images of one tile must span less than 2^31 bytes");
-    he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
-                             xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e), h, w,
-                             static_cast<int32_t>(ow), static_cast<hipStream_t>(stream));
+    if (plan->dev.use_indexed)
+        he = spconv::launch_indexed(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
+                                    static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),
+                                    yel * static_cast<int64_t>(e), static_cast<hipStream_t>(stream));
+    else
+        he = spconv::launch_spmm(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
+                                 xel * static_cast<int64_t>(e), yel * static_cast<int64_t>(e), h, w,
+                                 static_cast<int32_t>(ow), static_cast<hipStream_t>(stream));
     if (he != hipSuccess)
         return hip_fail("kernel launch", he);
     return SPCONV_OK;
