@@ -293,6 +293,8 @@ typedef struct {
     int32_t regions;     /* LDS-strip kernel: 0 = choose automatically; else 1 to 4 parts of the
                             strip, each refilled with the next tile's channels as soon as every
                             wavefront is done with it */
+    int32_t lane_cols;   /* register-indexed kernel: 0 = choose automatically at each run; else
+                            1 to 6 columns per lane (tiles of 64 * lane_cols columns) */
 } spconv_options;
 
 /*

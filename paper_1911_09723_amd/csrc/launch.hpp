@@ -50,7 +50,7 @@ struct DevicePlan {
     const float *dw = nullptr;          // depthwise taps and biases, kDwParams per strip channel
     // register-indexed kernel (planner.hpp)
     int32_t use_indexed = 0;
-    int32_t rslots = 0, rgroups = 0, rwaves = 0, rnch = 0;
+    int32_t rslots = 0, rgroups = 0, rwaves = 0, rnch = 0, rlane_cols = 0;
     const uint32_t *rrec = nullptr;
     const int32_t *rslot_batch = nullptr;
     const int32_t *rslot_chunk = nullptr;
@@ -58,6 +58,7 @@ struct DevicePlan {
     const float *rslot_bias = nullptr;
     const int32_t *rpair_ptr = nullptr;
     const uint32_t *rpair_ent = nullptr;
+    int64_t rpair_ent_words = 0;
     const float *rrow_bias = nullptr;   // bias of every output channel
     int32_t *flag = nullptr;            // device word: bit 0 set when a bounded wait of a kernel gave up
 };
@@ -65,14 +66,15 @@ struct DevicePlan {
 // How one launch of the register-indexed kernel covers m columns: `tiles`
 // whole tiles of 64 c columns (times the plan's slot groups), then columns
 // [lcol0, m) as `lpieces` (64-column group, row pair) pieces, `lper` per
-// workgroup; `grid` workgroups; LDS offsets of the counters and the lane
-// column table, and the LDS bytes per workgroup.
+// workgroup; `grid` workgroups; LDS offsets of the counters, the lane column
+// tables and the copy patterns, and the LDS bytes per workgroup.
 struct IndexedLaunch {
     int32_t c = 1;
     int64_t tiles = 0;
     int32_t lcol0 = 0, lpieces = 0, lper = 0;
     int32_t grid = 1;
-    int32_t ctl_off = 0, xo_off = 0, lds_bytes = 0;
+    int32_t ctl_off = 0, xo_off = 0, pat_off = 0, lds_bytes = 0;
+    int32_t ent_off = 0, epw = 0;  // row pairs: LDS entry areas and entries per wavefront area
 };
 
 IndexedLaunch plan_indexed_launch(const DevicePlan &p, int64_t m);

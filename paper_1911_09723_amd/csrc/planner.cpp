@@ -617,6 +617,10 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         err = "the register-indexed kernel runs fp32 plans without a depthwise stage";
         return E_UNSUPPORTED;
     }
+    if (opt.lane_cols < 0 || opt.lane_cols > 6) {
+        err = "lane_cols must be 0 (automatic) or 1 .. 6";
+        return E_ARG;
+    }
     if (opt.group_lanes != 0 && opt.group_lanes != 4 && opt.group_lanes != 8 && opt.group_lanes != 16) {
         err = "group_lanes must be 0, 4, 8 or 16";
         return E_ARG;
@@ -686,6 +690,7 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     if (!in.dw_stride && in.storage == 0) {
         build_indexed(in, p.perm, p);
         p.use_indexed = opt.kernel == 3;
+        p.rlane_cols = opt.lane_cols;
     }
 
     // 2. bundles of NB consecutive rows in that order, each a whole number of
@@ -1003,7 +1008,9 @@ void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPla
     p.rrec.clear();
     p.rslot_batch.assign(S, 0);
     p.rslot_chunk.assign(static_cast<size_t>(S) * (nch + 1), 0);
+    p.rslot_nrec.assign(static_cast<size_t>(S) * nch, 0);
     const int32_t batch_words = kRecWords * kBatchRecs;
+    const int32_t F = flag_word(k);
     for (int32_t s = 0; s < S; ++s) {
         const int64_t first_batch = static_cast<int64_t>(p.rrec.size()) / batch_words;
         p.rslot_batch[s] = static_cast<int32_t>(first_batch);
@@ -1023,8 +1030,10 @@ void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPla
         });
         size_t e = 0;
         for (int32_t q = 0; q < nch; ++q) {
-            const int64_t batch_now = static_cast<int64_t>(p.rrec.size()) / batch_words - first_batch;
-            int64_t nrec = 0;
+            const size_t chunk_start = p.rrec.size();
+            p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + q] =
+                static_cast<int32_t>(static_cast<int64_t>(chunk_start) / batch_words - first_batch);
+            int32_t nrec = 0;
             while (e < ents.size() && ents[e].c < (q + 1) * kChunk) {
                 const int32_t c = ents[e].c;
                 size_t e1 = e;
@@ -1033,7 +1042,7 @@ void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPla
                 for (size_t g = e; g < e1; g += P) {
                     const int32_t n = static_cast<int32_t>(std::min<size_t>(P, e1 - g));
                     uint32_t w[kRecWords] = {0, 0, 0, 0, 0, 0, 0, 0};
-                    w[0] = static_cast<uint32_t>(c % kRing);
+                    w[0] = static_cast<uint32_t>((c % kRing) * kRingRowBytes);
                     for (int32_t j = 0; j < n; ++j) {
                         const uint32_t row = static_cast<uint32_t>(ents[g + j].pos * k);
                         w[1 + j] = row;
@@ -1051,13 +1060,18 @@ void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPla
                 }
                 e = e1;
             }
-            if (nrec % kBatchRecs)
-                p.rrec.insert(p.rrec.end(), kRecWords, 0u);
-            p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + q] =
-                static_cast<int32_t>(batch_now * 2 + (nrec % 2));
+            p.rslot_nrec[static_cast<size_t>(s) * nch + q] = nrec;
+            // pad to whole batches, at least one: weight-0 records on the chunk's first channel
+            const int32_t padded = std::max<int32_t>(kBatchRecs, (nrec + kBatchRecs - 1) / kBatchRecs * kBatchRecs);
+            for (int32_t r = nrec; r < padded; ++r) {
+                uint32_t w[kRecWords] = {static_cast<uint32_t>(((q * kChunk) % kRing) * kRingRowBytes), 0, 0, 0, 0, 0, 0, 0};
+                p.rrec.insert(p.rrec.end(), w, w + kRecWords);
+            }
+            p.rrec[p.rrec.size() - batch_words + F] |= kLastOfChunk;
         }
+        p.rrec[p.rrec.size() - batch_words + F] |= kLastOfStream;
         const int64_t total = static_cast<int64_t>(p.rrec.size()) / batch_words - first_batch;
-        p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + nch] = static_cast<int32_t>(total * 2);
+        p.rslot_chunk[static_cast<size_t>(s) * (nch + 1) + nch] = static_cast<int32_t>(total);
     }
     p.rrec.insert(p.rrec.end(), static_cast<size_t>(2 * batch_words), 0u);
 
@@ -1150,20 +1164,32 @@ Status unpack_indexed(const PackedPlan &p, bool from_pairs, int32_t *row_ptr, in
         for (int32_t s = 0; s < p.rslots; ++s) {
             const int64_t base = static_cast<int64_t>(p.rslot_batch[s]) * kBatchRecs;  // first record
             const int32_t *ch = p.rslot_chunk.data() + static_cast<size_t>(s) * (nch + 1);
+            const int32_t *nr = p.rslot_nrec.data() + static_cast<size_t>(s) * nch;
+            const int32_t F = flag_word(k);
             int32_t prev_c = -1;
             for (int32_t q = 0; q < nch; ++q) {
-                const int32_t b0 = ch[q] >> 1, b1 = ch[q + 1] >> 1, odd = ch[q] & 1;
-                const int64_t nrec = static_cast<int64_t>(b1 - b0) * kBatchRecs - (odd ? 1 : 0);
-                if (b1 < b0 || (odd && b1 == b0))
+                const int32_t b0 = ch[q], b1 = ch[q + 1];
+                const int64_t nrec = nr[q];
+                if (b1 <= b0 || nrec < 0 || (b1 - b0) != std::max<int64_t>(1, (nrec + kBatchRecs - 1) / kBatchRecs))
                     return bad("chunk table out of order");
+                // flags: only the chunk's last batch ends it, only the stream's last ends the stream
+                for (int32_t bb = b0; bb < b1; ++bb) {
+                    const uint32_t f = p.rrec[(base + static_cast<int64_t>(bb) * kBatchRecs) * kRecWords + F];
+                    const uint32_t want =
+                        (bb == b1 - 1 ? kLastOfChunk : 0u) | (q == nch - 1 && bb == b1 - 1 ? kLastOfStream : 0u);
+                    if ((f & 3u) != want)
+                        return bad("batch flags do not match the chunk table");
+                }
                 for (int64_t r = 0; r < nrec; ++r) {
                     const uint32_t *w = p.rrec.data() + (base + static_cast<int64_t>(b0) * kBatchRecs + r) * kRecWords;
                     const int32_t n = 1 + ((w[1] >> 8) & 1) + ((w[1] >> 9) & 1);
                     if (n > P)
                         return bad("record holds more blocks than its kind allows");
                     // the channel: the ring row plus the chunk's ring base
-                    const int32_t c = (q * kChunk) / kRing * kRing + static_cast<int32_t>(w[0]);
-                    if (w[0] >= static_cast<uint32_t>(kRing) || c < q * kChunk || c >= (q + 1) * kChunk || c >= p.cin)
+                    const int32_t c =
+                        (q * kChunk) / kRing * kRing + static_cast<int32_t>(w[0] / static_cast<uint32_t>(kRingRowBytes));
+                    if (w[0] % kRingRowBytes || w[0] >= static_cast<uint32_t>(kRing * kRingRowBytes) || c < q * kChunk ||
+                        c >= (q + 1) * kChunk || c >= p.cin)
                         return bad("record channel outside its chunk");
                     if (c < prev_c)
                         return bad("records do not ascend by channel");

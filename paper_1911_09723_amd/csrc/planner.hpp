@@ -123,17 +123,22 @@ constexpr int64_t kMinStageBytes = 16 * 1024;
 //
 //   Records (kRecWords 32-bit words each): the stored blocks of one slot at one
 //   input channel c, at most kRecSlots(k) = 3, 2, 1 blocks for k = 1, 2, 4:
-//     w[0]  c % kRing (the LDS ring row holding channel c)
+//     w[0]  (c % kRing) * kRingRowBytes (LDS byte offset of the ring row holding c)
 //     w[1]  first block's slot row | (more than 1 block) << 8 | (more than 2) << 9
 //     w[2]  second block's slot row (k <= 2), w[3] third (k == 1)
 //     w[4..7]  weights: k == 1: one per block; k == 2: 2 per block; k == 4: the 4
 //   A slot's records ascend by channel.  Channels come in chunks of kChunk;
-//   each chunk's records start on a batch boundary (kBatchRecs records,
-//   kRecWords * kBatchRecs words); an odd chunk is padded with one unused
-//   record.  Slot s's stream starts at batch rslot_batch[s];
-//   rslot_chunk[s * (nch + 1) + q] = (first batch of chunk q) * 2 + (chunk q
-//   has an odd number of records), with q = nch giving the stream's end.  The
-//   record array ends with kBatchRecs * 2 zero records (read ahead, unused).
+//   each chunk's records fill whole batches (kBatchRecs records, kRecWords *
+//   kBatchRecs words), padded with records of weight 0, and a chunk without
+//   stored blocks in the slot still gets one batch of such records, so a
+//   wavefront passes every chunk.  The first record of every batch carries
+//   the batch's flags in word flag_word(k) (7 for k == 1, else 3): bit 0 the
+//   batch is its chunk's last, bit 1 it is the stream's last.  Padding records
+//   name the chunk's first channel and slot row 0.  Slot s's stream starts at
+//   batch rslot_batch[s]; chunk q of it starts at batch rslot_chunk[s * (nch +
+//   1) + q] of the stream (q = nch: the stream's length) and holds
+//   rslot_nrec[s * nch + q] stored records.  The record array ends with
+//   kBatchRecs * 2 zero records (read ahead, unused).
 //
 //   Row pairs (columns left over after the kernel's whole tiles): pair j is
 //   output channels 2j and 2j + 1; rpair_ptr[j] .. rpair_ptr[j + 1] index its
@@ -146,10 +151,15 @@ constexpr int64_t kMinStageBytes = 16 * 1024;
 constexpr int32_t kSlotRows = 16;
 constexpr int32_t kRecWords = 8;
 constexpr int32_t kBatchRecs = 2;
-constexpr int32_t kRing = 64;
+constexpr int32_t kRing = 96;        // LDS ring rows (channels) of the register-indexed kernel
+constexpr int32_t kRingRowBytes = 1536;  // one ring row: 6 column slots of 64 fp32
 constexpr int32_t kChunk = 16;
+static_assert(kRing % kChunk == 0, "a chunk never wraps around the ring");
 constexpr int32_t kSlotsPerGroup = 16;
 inline int32_t rec_slots(int32_t k) { return k == 1 ? 3 : k == 2 ? 2 : 1; }
+inline int32_t flag_word(int32_t k) { return k == 1 ? 7 : 3; }
+constexpr uint32_t kLastOfChunk = 1u;
+constexpr uint32_t kLastOfStream = 2u;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -183,6 +193,7 @@ struct Options {
     int32_t waves = 0;        // 0 automatic, else 1 .. 16 wavefronts per workgroup
     int32_t pipe_sets = 0;    // 0 automatic, else 1 or 2 bundles interleaved per wavefront
     int32_t regions = 0;      // 0 automatic, else 1 .. kMaxRegions strip parts
+    int32_t lane_cols = 0;    // register-indexed kernel: 0 automatic, else 1 .. 6 columns per lane
 };
 
 struct PackedPlan {
@@ -230,9 +241,11 @@ struct PackedPlan {
     int32_t rgroups = 0;         // groups of slots sharing one LDS ring (one workgroup each)
     int32_t rwaves = 0;          // wavefronts per workgroup = slots per group (the last may have fewer)
     int32_t rnch = 0;            // chunks of kChunk input channels
+    int32_t rlane_cols = 0;      // columns per lane fixed by the caller (0: chosen per run)
     std::vector<uint32_t> rrec;
     std::vector<int32_t> rslot_batch;
     std::vector<int32_t> rslot_chunk;
+    std::vector<int32_t> rslot_nrec;
     std::vector<int32_t> rslot_rows;
     std::vector<float> rslot_bias;
     std::vector<int32_t> rpair_ptr;

@@ -150,6 +150,7 @@ spconv_status upload(spconv_plan_s *pl) {
     d.rslot_bias = reinterpret_cast<const float *>(base + parts[16].off);
     d.rpair_ptr = reinterpret_cast<const int32_t *>(base + parts[17].off);
     d.rpair_ent = reinterpret_cast<const uint32_t *>(base + parts[18].off);
+    d.rpair_ent_words = static_cast<int64_t>(h.rpair_ent.size());
     d.rrow_bias = reinterpret_cast<const float *>(base + parts[19].off);
     d.flag = reinterpret_cast<int32_t *>(base + parts[20].off);
     return SPCONV_OK;
@@ -186,6 +187,7 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.rgroups = h.rgroups;
     d.rwaves = h.rwaves;
     d.rnch = h.rnch;
+    d.rlane_cols = h.rlane_cols;
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -215,6 +217,7 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
     po.waves = o.waves;
     po.pipe_sets = o.pipe_sets;
     po.regions = o.regions;
+    po.lane_cols = o.lane_cols;
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
     if (!pl)

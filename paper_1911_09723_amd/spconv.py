@@ -44,7 +44,8 @@ class SpconvError(RuntimeError):
 class spconv_options(ctypes.Structure):
     _fields_ = [("struct_size", ctypes.c_int32), ("reorder", ctypes.c_int32), ("host_only", ctypes.c_int32),
                 ("kernel", ctypes.c_int32), ("group_lanes", ctypes.c_int32), ("waves", ctypes.c_int32),
-                ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32)]
+                ("pipe_sets", ctypes.c_int32), ("regions", ctypes.c_int32),
+                ("lane_cols", ctypes.c_int32)]
 
 
 class spconv_plan_info(ctypes.Structure):
