@@ -419,6 +419,40 @@ SPCONV_API spconv_status spconv_plan_unpack(spconv_plan plan, int32_t *row_ptr, 
 SPCONV_API spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
                                              float *values);
 
+/*
+ * The same reconstruction from the register-indexed kernel's streams: with
+ * from_pairs = 0 from the slot records (walking each slot's chunk table,
+ * batch flags and ring offsets as the kernel does), with from_pairs = 1 from
+ * the row-pair entries that cover the columns left after the whole tiles.
+ * row_ptr, col_idx, values as for spconv_plan_unpack (each may be NULL).
+ * Host only.  SPCONV_E_FORMAT (message set) when a stream is inconsistent or
+ * the plan has none (fp16 storage, depthwise stage).
+ */
+SPCONV_API spconv_status spconv_plan_unpack_indexed(spconv_plan plan, int32_t from_pairs, int32_t *row_ptr,
+                                                    int32_t *col_idx, float *values);
+
+/*
+ * The plan's device error word, written by its kernels: bit 0
+ * (SPCONV_FLAG_WAIT_GAVE_UP) is set when a bounded wait inside a kernel on an
+ * on-chip counter (a strip or ring part landing, a share being issued) ran
+ * out; that wavefront went on without the data, so the output of that launch
+ * is not to be trusted.  Waits for all work queued on the plan's device to
+ * finish, then reads the word into *flags; with clear != 0 resets it to zero.
+ * SPCONV_E_ARG for a NULL argument or a host-only plan, SPCONV_E_HIP when a
+ * HIP call fails (message set).
+ */
+#define SPCONV_FLAG_WAIT_GAVE_UP 1
+SPCONV_API spconv_status spconv_plan_check(spconv_plan plan, int32_t *flags, int32_t clear);
+
+/*
+ * Test hook for the error path above: the bound of every such wait in the
+ * plan's later launches, in sleeps of about 64 clocks (default 1 << 22, about
+ * 0.1 s).  0 makes every wait that finds its data missing give up at once;
+ * kernels still run to completion.  SPCONV_E_ARG for a NULL plan or a
+ * negative bound.  Host only.
+ */
+SPCONV_API spconv_status spconv_plan_set_wait_limit(spconv_plan plan, int32_t sleeps);
+
 #ifdef __cplusplus
 }
 #endif

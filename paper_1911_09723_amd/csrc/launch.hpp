@@ -61,6 +61,7 @@ struct DevicePlan {
     int64_t rpair_ent_words = 0;
     const float *rrow_bias = nullptr;   // bias of every output channel
     int32_t *flag = nullptr;            // device word: bit 0 set when a bounded wait of a kernel gave up
+    int32_t spin_limit = 1 << 22;       // bound of those waits, in sleeps
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`

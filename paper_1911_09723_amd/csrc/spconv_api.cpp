@@ -716,4 +716,67 @@ spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr,
     return SPCONV_OK;
 }
 
+spconv_status spconv_plan_unpack_indexed(spconv_plan plan, int32_t from_pairs, int32_t *row_ptr, int32_t *col_idx,
+                                         float *values) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    std::string err;
+    const spconv::PackedPlan &p = plan->host;
+    if (p.kc == 1) {
+        const spconv::Status st = spconv::unpack_indexed(p, from_pairs != 0, row_ptr, col_idx, values, err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        return SPCONV_OK;
+    }
+    try {
+        std::vector<int32_t> rp(p.cout / p.k + 1), ci(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1)));
+        std::vector<float> va(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1) * p.k));
+        const spconv::Status st = spconv::unpack_indexed(p, from_pairs != 0, rp.data(), ci.data(), va.data(), err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        reblock(p, rp, ci, va, row_ptr, col_idx, values);
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while unpacking");
+    }
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_check(spconv_plan plan, int32_t *flags, int32_t clear) {
+    g_err.clear();
+    if (!plan || !flags)
+        return fail(SPCONV_E_ARG, "plan or flags is NULL");
+    if (plan->host_only || !plan->dev.flag)
+        return fail(SPCONV_E_ARG, "a host-only plan has no device error word");
+    int cur = -1;
+    hipError_t e = hipGetDevice(&cur);
+    if (e != hipSuccess)
+        return hip_fail("hipGetDevice", e);
+    if (cur != plan->device && (e = hipSetDevice(plan->device)) != hipSuccess)
+        return hip_fail("hipSetDevice", e);
+    spconv_status st = SPCONV_OK;
+    if ((e = hipDeviceSynchronize()) != hipSuccess) {
+        st = hip_fail("hipDeviceSynchronize", e);
+    } else if ((e = hipMemcpy(flags, plan->dev.flag, sizeof(int32_t), hipMemcpyDeviceToHost)) != hipSuccess) {
+        st = hip_fail("hipMemcpy (error word)", e);
+    } else if (clear) {
+        const int32_t zero = 0;
+        if ((e = hipMemcpy(plan->dev.flag, &zero, sizeof(int32_t), hipMemcpyHostToDevice)) != hipSuccess)
+            st = hip_fail("hipMemcpy (clear error word)", e);
+    }
+    if (cur != plan->device)
+        (void)hipSetDevice(cur);
+    return st;
+}
+
+spconv_status spconv_plan_set_wait_limit(spconv_plan plan, int32_t sleeps) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    if (sleeps < 0)
+        return fail(SPCONV_E_ARG, "the wait bound must be >= 0");
+    plan->dev.spin_limit = sleeps;
+    return SPCONV_OK;
+}
+
 }  // extern "C"

@@ -77,7 +77,6 @@ typedef int i4 __attribute__((ext_vector_type(4)));
 
 constexpr int32_t kOOR = static_cast<int32_t>(0x80000000u);  // an offset past every buffer: loads read 0
 constexpr int64_t kMaxRec = 0x7ffffff0;
-constexpr int32_t kSpinMax = 1 << 22;
 constexpr int32_t kRingChunks = kRing / kChunk;             // 6 chunks in the ring
 static_assert(kRingRowBytes == 6 * 256, "a ring row holds 6 column slots");
 static_assert(kRingChunks == 6, "the stream statement counts ring chunks modulo 6");
@@ -182,6 +181,7 @@ struct IArgs {
     int64_t pair_ent_bytes;
     const float *row_bias;
     int32_t *flag;        // set when a bounded wait gives up
+    int32_t spin;         // bound of those waits, in sleeps
 };
 
 // The launch arguments, read afresh from the kernel-argument segment: the
@@ -217,13 +217,14 @@ __device__ __forceinline__ KArgs &kargs() {
 // was told are clobbered.
 //
 // Scalar registers: s34 chunk q, s35 byte offset of the next record load,
-// s36:37 saved exec, s38 ring chunks copied but not yet published (bit per
-// ring chunk), s39 spin count / temporary, s40 ring chunk of q (q mod 6), s41
+// s36:37 saved exec, s38 ring chunks loaded by this wavefront but not yet
+// published (bit per ring chunk; on entry the set-up's chunks 1 .. 5), s39 spin count / temporary, s40 ring chunk of q (q mod 6), s41
 // round of q (q div 6), s42 - s45 temporaries, s46 / s47 ring chunk and round
 // of q + 1, s48 - s63 / s64 - s79 / s80 - s95 the record buffers (batch b in
 // buffer b % 3; record 0 at +0, record 1 at +8).  LDS counters: free[j] at
 // ctl + 4 j (wavefronts done with ring chunk j, all rounds), fill[j] at ctl +
-// 32 + 4 j (times ring chunk j was filled).
+// 32 + 4 j (set-up wavefronts that published their share of ring chunk j's
+// first round, plus one per later round).
 // Vector: accumulators v[a + 16 k + r], activation sets xa0 / xa1 and xb0 /
 // xb1 (batch b in set b % 2), temporaries t, t + 1.
 // ---------------------------------------------------------------------------
@@ -279,11 +280,12 @@ __device__ __forceinline__ KArgs &kargs() {
     "v_add_u32 v[%[t]+1], s[" #RN "+8], %[vl]\n"                 \
     XL(X0, 0) XL(X1, 1)
 
-// Wait until ring chunk s46 has been filled s47 + 1 times (the chunk of round
-// s47 has landed); a bounded wait that sets the plan's flag on giving up.
-// Indexing off.
+// Wait until ring chunk s46 holds round s47: its fill count reaches nws + s47
+// (the first round is counted once per wavefront that loaded a share of it,
+// each later round once by its copier); a bounded wait that sets the plan's
+// flag on giving up.  Indexing off.
 #define RY_WAITFILL(L)                                             \
-    "s_add_u32 s42, s47, 1\n"                                      \
+    "s_add_u32 s42, s47, %[nws]\n"                                 \
     "s_lshl_b32 s43, s46, 2\n"                                     \
     "s_add_u32 s43, s43, %[ctl]\n"                                 \
     "s_add_u32 s43, s43, 32\n"                                     \
@@ -308,17 +310,6 @@ __device__ __forceinline__ KArgs &kargs() {
     "global_atomic_or v[%[t]], v[%[t]+1], %[flag]\n"               \
     "s_mov_b64 exec, s[36:37]\n"                                   \
     L "ok_%=:\n"
-// Enter chunk q + 1: its ring chunk and round into s46 / s47, then wait for it.
-#define RY_ENTER(L)                                                \
-    "s_add_u32 s46, s40, 1\n"                                      \
-    "s_mov_b32 s47, s41\n"                                         \
-    "s_cmp_eq_u32 s46, 6\n"                                        \
-    "s_cbranch_scc0 " L "nx_%=\n"                                  \
-    "s_mov_b32 s46, 0\n"                                           \
-    "s_add_u32 s47, s47, 1\n"                                      \
-    L "nx_%=:\n"                                                   \
-    RY_WAITFILL(L)
-
 // Count the landing of every ring chunk copied earlier (after the copies'
 // loads are complete), one lane adding to its fill counter.
 #define RY_PUB1(j, L)                                                    \
@@ -339,6 +330,21 @@ __device__ __forceinline__ KArgs &kargs() {
     "s_mov_b64 exec, s[36:37]\n"                                   \
     "s_mov_b32 s38, 0\n"                                           \
     L "_%=:\n"
+
+// Enter chunk q + 1: publish this wavefront's landed loads (the set-up's
+// shares of the first ring are published here at the latest, before any
+// wavefront can need them), put chunk q + 1's ring chunk and round into
+// s46 / s47, then wait for it.
+#define RY_ENTER(L)                                                \
+    RY_PUBLISH(L "p")                                              \
+    "s_add_u32 s46, s40, 1\n"                                      \
+    "s_mov_b32 s47, s41\n"                                         \
+    "s_cmp_eq_u32 s46, 6\n"                                        \
+    "s_cbranch_scc0 " L "nx_%=\n"                                  \
+    "s_mov_b32 s46, 0\n"                                           \
+    "s_add_u32 s47, s47, 1\n"                                      \
+    L "nx_%=:\n"                                                   \
+    RY_WAITFILL(L)
 
 // Chunk q + 6 into ring chunk s40: channels [s42, s43) into the 16 ring rows
 // starting at LDS byte s44; v[t + 1] = 4 * lane.
@@ -550,7 +556,7 @@ __device__ __forceinline__ KArgs &kargs() {
 #define RY_STREAM(REC, F, COLS, XL, ZC, CPW, EACH, EPC, CLOBV)                                     \
     asm volatile(ZC                                                                                     \
                  "s_mov_b32 s34, 0\n"                                                                   \
-                 "s_mov_b32 s38, 0\n"                                                                   \
+                 "s_mov_b32 s38, %[pend]\n"                                                             \
                  "s_load_dwordx16 s[48:63], %[ptr], 0\n"                                                \
                  "s_load_dwordx16 s[64:79], %[ptr], 64\n"                                               \
                  "s_mov_b32 s35, 128\n"                                                                 \
@@ -581,18 +587,20 @@ __device__ __forceinline__ KArgs &kargs() {
                  RY_EPILOGUE(EACH, EPC)                                                                 \
                  :                                                                                      \
                  : [a] "i"(L::A), [xa0] "i"(L::XA0), [xa1] "i"(L::XA1), [xb0] "i"(L::XB0),              \
-                   [xb1] "i"(L::XB1), [t] "i"(L::T), [spin] "i"(kSpinMax), [cbytes] "i"(kChunk * kRingRowBytes), \
+                   [xb1] "i"(L::XB1), [t] "i"(L::T), [cbytes] "i"(kChunk * kRingRowBytes), [spin] "s"(spin),  \
                    [ptr] "s"(ptr), [nch] "s"(nch), [ctl] "s"(ctl), [nw] "s"(nw), [rs] "s"(rs),          \
                    [xo] "s"(xo), [yo] "s"(yo), [pat] "s"(pat), [cin] "s"(cin), [hw4] "s"(hw4),          \
                    [base] "s"(base), [flag] "s"(flag), [rows] "s"(rows), [bias] "s"(bias),              \
-                   [ry] "s"(ry), [v4] "s"(v4), [vl] "v"(vl), [lo] "v"(lo), [hi] "v"(hi)                 \
+                   [ry] "s"(ry), [v4] "s"(v4), [nws] "s"(nws), [pend] "s"(pend), [vl] "v"(vl),          \
+                   [lo] "v"(lo), [hi] "v"(hi)                                                           \
                  : "memory", "m0", "scc", "vcc", CLOBV, IY_CLOBS)
 
 template <int K, int C>
 __device__ __forceinline__ void stream_asm(const uint32_t *ptr, int32_t nch, uint32_t ctl, int32_t nw, i4 rs,
                                            uint32_t xo, uint32_t yo, uint32_t pat, int32_t cin, int32_t hw4,
                                            uint32_t base, int32_t *flag, const int32_t *rows, const float *bias,
-                                           i4 ry, int32_t v4, int32_t vl, float lo, float hi) {
+                                           i4 ry, int32_t v4, int32_t nws, int32_t pend, int32_t spin, int32_t vl,
+                                           float lo, float hi) {
     using L = Lay<C>;
 #define RY_BY_C(REC, F)                                                                                \
     if constexpr (C == 1) {                                                                            \
@@ -673,11 +681,20 @@ __device__ __forceinline__ int32_t copy_pattern(KArgs &a, const TaskPos &t, int 
 }
 
 // Set-up of a task: lane column tables, copy patterns and counters into LDS,
-// the first ring's worth of channels copied by every wavefront.
+// then the first ring's worth of channels copied by every wavefront: its
+// share of chunk 0 first, waited for and published at once, then its shares
+// of chunks 1 .. 5, published later (in the stream at the wavefront's first
+// chunk release, or here by a wavefront without a slot).  Returns the
+// bit set of ring chunks this wavefront still has to publish.
+__device__ __forceinline__ void publish_fill(unsigned char *lds, int32_t ctl_off, int32_t bits, int lane) {
+    if (lane < kRingChunks && ((bits >> lane) & 1))
+        __hip_atomic_fetch_add(reinterpret_cast<int32_t *>(lds + ctl_off) + 8 + lane, 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
 template <int C>
-__device__ __forceinline__ void task_setup(int32_t task, unsigned char *lds, uint32_t lds_base, int wave, int nwaves,
-                                           int lane) {
-    using L = Lay<C>;
+__device__ __forceinline__ int32_t task_setup(int32_t task, unsigned char *lds, uint32_t lds_base, int wave,
+                                              int nwaves, int lane) {
     const auto &a = kargs();
     const TaskPos t = task_pos<C>(a, task, wave);
     const int64_t xbase = static_cast<int64_t>(t.n0) * a.cin * a.hw;
@@ -701,37 +718,49 @@ __device__ __forceinline__ void task_setup(int32_t task, unsigned char *lds, uin
         pat_lds[128 + lane] = copy_pattern<C>(a, t, lane, 2);
         if (lane < kRingChunks) {
             freec[lane] = 0;
-            freec[8 + lane] = lane < a.nch ? 1 : 0;
+            freec[8 + lane] = 0;
         }
     }
     __syncthreads();
-    const int32_t rows0 = imin(kRing, a.cin);
     const int32_t hw4 = a.hw * 4;
-    if (a.v4) {
-        const int32_t p0 = pat_lds[lane], p1 = pat_lds[64 + lane], p2 = pat_lds[128 + lane];
-        const int32_t loads = 3 * ((rows0 + 1) / 2);
+    const int32_t nq = imin(kRingChunks, a.nch);   // chunks of the first ring
+    int32_t bits = 0;
 #pragma unroll 1
-        for (int32_t u = wave; u < loads; u += nwaves) {
-            const int32_t rp = u / 3, j = u - 3 * rp;
-            dma_x4(base + static_cast<uint32_t>(rp * 2 * kRingRowBytes + 1024 * j), j == 0 ? p0 : j == 1 ? p1 : p2,
-                   rs, 2 * rp * hw4);
+    for (int32_t q = 0; q < nq; ++q) {
+        const int32_t c0 = q * kChunk;
+        const int32_t rows = imin(kChunk, a.cin - c0);
+        const uint32_t dst = base + static_cast<uint32_t>(q * kChunk * kRingRowBytes);
+        if (a.v4) {
+            const int32_t p0 = pat_lds[lane], p1 = pat_lds[64 + lane], p2 = pat_lds[128 + lane];
+            const int32_t loads = 3 * ((rows + 1) / 2);
+#pragma unroll 1
+            for (int32_t u = wave; u < loads; u += nwaves) {
+                const int32_t rp = u / 3, j = u - 3 * rp;
+                dma_x4(dst + static_cast<uint32_t>(rp * 2 * kRingRowBytes + 1024 * j), j == 0 ? p0 : j == 1 ? p1 : p2,
+                       rs, (c0 + 2 * rp) * hw4);
+            }
+        } else {
+#pragma unroll 1
+            for (int32_t u = wave; u < rows * C; u += nwaves) {
+                const int32_t r = u / C, k = u - r * C;
+                dma_dword(dst + static_cast<uint32_t>(r * kRingRowBytes + 256 * k), xo_lds[k * 64 + lane], rs,
+                          (c0 + r) * hw4);
+            }
         }
-    } else {
-#pragma unroll 1
-        for (int k = 0; k < C; ++k) {
-            const int32_t xo = xo_lds[k * 64 + lane];
-#pragma unroll 1
-            for (int32_t c = wave; c < rows0; c += nwaves)
-                dma_dword(base + static_cast<uint32_t>(c * kRingRowBytes + 256 * k), xo, rs, c * hw4);
+        if (q == 0) {
+            wait_vm0();
+            publish_fill(lds, a.ctl_off, 1, lane);
+        } else {
+            bits |= 1 << q;
         }
     }
-    wait_vm0();
-    __syncthreads();
+    return bits;
 }
 
 // The wavefront's slot over the task's tile (the stream statement).
 template <int K, int C>
-__device__ __forceinline__ void task_stream(int32_t task, uint32_t lds_base, int wave, int lane) {
+__device__ __forceinline__ void task_stream(int32_t task, uint32_t lds_base, int wave, int lane, int32_t nws,
+                                            int32_t pend) {
     const auto &a = kargs();
     const TaskPos t = task_pos<C>(a, task, wave);
     const int64_t xbase = static_cast<int64_t>(t.n0) * a.cin * a.hw;
@@ -752,7 +781,9 @@ __device__ __forceinline__ void task_stream(int32_t task, uint32_t lds_base, int
                      __builtin_amdgcn_readfirstlane(lds_base + static_cast<uint32_t>(a.pat_off)),
                      __builtin_amdgcn_readfirstlane(a.cin), __builtin_amdgcn_readfirstlane(a.hw * 4),
                      __builtin_amdgcn_readfirstlane(lds_base), uniform_ptr(a.flag), rows, bias, ry,
-                     __builtin_amdgcn_readfirstlane(a.v4), static_cast<int32_t>(lds_base) + 4 * lane, lo, hi);
+                     __builtin_amdgcn_readfirstlane(a.v4), __builtin_amdgcn_readfirstlane(nws),
+                     __builtin_amdgcn_readfirstlane(pend), __builtin_amdgcn_readfirstlane(a.spin),
+                     static_cast<int32_t>(lds_base) + 4 * lane, lo, hi);
 }
 
 // Columns [lcol0, m) by row pairs over 64-column groups (see the file comment).
@@ -852,9 +883,13 @@ __device__ __forceinline__ void indexed_body() {
     // one whole-tile task per workgroup (the grid has a workgroup per task)
     const int32_t task = static_cast<int32_t>(blockIdx.x);
     if (task < kargs().main_tasks) {
-        task_setup<C>(task, lds, lds_base, wave, nwaves, lane);
-        if (wave < task_pos<C>(kargs(), task, wave).nw)
-            task_stream<K, C>(task, lds_base, wave, lane);
+        const int32_t pend = task_setup<C>(task, lds, lds_base, wave, nwaves, lane);
+        if (wave < task_pos<C>(kargs(), task, wave).nw) {
+            task_stream<K, C>(task, lds_base, wave, lane, nwaves, pend);
+        } else {
+            wait_vm0();
+            publish_fill(lds, kargs().ctl_off, pend, lane);
+        }
     }
     if (kargs().lpieces > 0)
         run_pairs(lds, lds_base, wave, nwaves, lane);
@@ -1020,6 +1055,7 @@ hipError_t launch_indexed(const DevicePlan &p, const float *x, float *y, int32_t
     a.pair_ent_bytes = static_cast<int64_t>(p.rpair_ent_words) * 4;
     a.row_bias = p.rrow_bias;
     a.flag = p.flag;
+    a.spin = p.spin_limit;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(L.grid)), dim3(p.rwaves * 64), L.lds_bytes, stream, a);
     return hipGetLastError();
 }

@@ -133,7 +133,17 @@ struct Args {
     int32_t dw_stride, dw_act, in_h, in_w, out_w;
     int32_t stage_off, stage_bytes;  // LDS staging area of its input windows
     const float *dw;
+    int32_t *flag;  // the plan's error word: bit 0 set when a bounded wait gives up
+    int32_t spin;   // bound of every wait on a counter (sleeps)
 };
+
+// Bit 0 of the plan's error word: a bounded wait gave up (the output of that
+// launch is not trusted; spconv_plan_check reports it).  One lane, a vector
+// atomic.
+__device__ __forceinline__ void flag_wait_gave_up(const Args &a, int lane) {
+    if (lane == 0)
+        __hip_atomic_fetch_or(a.flag, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // A workgroup's unit of work: a tile, whole (part < 0) or one of tail_parts
 // parts of its bundles; tile < 0 when none is left.  `round` counts the whole
@@ -944,7 +954,6 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
     using DP = PipeDepth<G, K, F16, M>;
     constexpr int D = DP::D, NR = DP::NR;
     constexpr int LPE = 1 + K;          // vector loads per ring entry
-    constexpr int32_t kSpin = 1 << 22;  // bound of every wait on a counter
 
     extern __shared__ __align__(16) unsigned char lds[];
     const T *__restrict__ x = static_cast<const T *>(xv);
@@ -1015,10 +1024,13 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
             wait_vmcnt<0>();
             publish();
         }
-        for (int32_t n = 0; n < kSpin && lds_load_volatile(&ctl[kMaxRegions + q]) < target; ++n) {
+        int32_t n = 0;
+        for (; n < a.spin && lds_load_volatile(&ctl[kMaxRegions + q]) < target; ++n) {
             service(true);
             __builtin_amdgcn_s_sleep(1);
         }
+        if (n == a.spin && lds_load_volatile(&ctl[kMaxRegions + q]) < target)
+            flag_wait_gave_up(a, lane);
         // strip reads stay after the wait
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
     };
@@ -1156,10 +1168,13 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         }
     }
     // shares not issued yet (a wave without bundles issues all of its shares here)
-    for (int32_t n = 0; n < kSpin && ct < R; ++n) {
+    int32_t n_left = 0;
+    for (; n_left < a.spin && ct < R; ++n_left) {
         service(true);
         __builtin_amdgcn_s_sleep(1);
     }
+    if (ct < R)
+        flag_wait_gave_up(a, lane);
     wait_vmcnt<0>();
     if (pend)
         publish();
@@ -1341,6 +1356,8 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.in_w = p.dw_stride ? in_w : 0;
     a.out_w = p.dw_stride ? out_w : 0;
     a.dw = p.dw;
+    a.flag = p.flag;
+    a.spin = p.spin_limit;
     a.stage_off = p.stage_off;
     a.stage_bytes = p.stage_bytes;
     hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(slots)), dim3(p.waves * 64), p.lds_bytes, stream, x, y,

@@ -31,7 +31,8 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_plan_unpack_interleaved", "spconv_detect_block_rows", "spconv_dense_to_bcsr",
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
             "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked", "spconv_detect_blocks",
-            "spconv_dense_to_bcsr_blocked", "spconv_plan_create_dense_blocked")
+            "spconv_dense_to_bcsr_blocked", "spconv_plan_create_dense_blocked", "spconv_plan_unpack_indexed",
+            "spconv_plan_check", "spconv_plan_set_wait_limit")
 
 
 class SpconvError(RuntimeError):
@@ -105,6 +106,12 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_unpack.argtypes = [vp, vp, vp, vp, vp]
     lib.spconv_plan_unpack_interleaved.restype = i32
     lib.spconv_plan_unpack_interleaved.argtypes = [vp, vp, vp, vp]
+    lib.spconv_plan_unpack_indexed.restype = i32
+    lib.spconv_plan_unpack_indexed.argtypes = [vp, i32, vp, vp, vp]
+    lib.spconv_plan_check.restype = i32
+    lib.spconv_plan_check.argtypes = [vp, ctypes.POINTER(i32), i32]
+    lib.spconv_plan_set_wait_limit.restype = i32
+    lib.spconv_plan_set_wait_limit.argtypes = [vp, i32]
     lib.spconv_detect_block_rows.restype = i32
     lib.spconv_detect_block_rows.argtypes = [i32, i32, vp, ctypes.POINTER(i32)]
     lib.spconv_dense_to_bcsr.restype = i32
@@ -419,6 +426,41 @@ def spconv_plan_unpack_interleaved(plan):
     return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per]
 
 
+def spconv_plan_unpack_indexed(plan, from_pairs=False):
+    """Return (row_ptr, col_idx, values) rebuilt from the register-indexed kernel's
+    slot records (or, with from_pairs, its row-pair entries)."""
+    info = spconv_plan_get_info(plan)
+    rows = info["cout"] // info["block_rows"]
+    per = info["block_rows"] * info["block_cols"]
+    rp = np.zeros(rows + 1, np.int32)
+    ci = np.zeros(max(info["nnzb"], 1), np.int32)
+    va = np.zeros(max(info["nnzb"] * per, 1), np.float32)
+    _check(load_library().spconv_plan_unpack_indexed(plan, int(bool(from_pairs)), _ptr(rp), _ptr(ci), _ptr(va)))
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per]
+
+
+SPCONV_FLAG_WAIT_GAVE_UP = 1
+
+
+def spconv_plan_check(plan, clear: bool = False, check: bool = True):
+    """The plan's device error word (bit 0: a bounded wait in a kernel gave up)
+    after all work on its device finished; optionally reset it."""
+    v = ctypes.c_int32(0)
+    status = load_library().spconv_plan_check(plan, ctypes.byref(v), int(bool(clear)))
+    if check:
+        _check(status)
+        return v.value
+    return status, v.value
+
+
+def spconv_plan_set_wait_limit(plan, sleeps: int, check: bool = True):
+    """Test hook: bound every bounded wait of the plan's later launches (sleeps)."""
+    status = load_library().spconv_plan_set_wait_limit(plan, int(sleeps))
+    if check:
+        _check(status)
+    return status
+
+
 class Plan:
     """Owning wrapper: ``Plan(...).run(x, y)`` with torch tensors [N, C, H, W]."""
 
@@ -485,6 +527,10 @@ class Plan:
                                layer.col_idx, layer.values, layer.bias, layer.act, layer.storage, **options)
         return cls(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
                    layer.bias, layer.act, layer.storage, **options)
+
+    def check(self, clear: bool = False) -> int:
+        """The device error word (0 when every bounded wait of every launch succeeded)."""
+        return spconv_plan_check(self.handle, clear)
 
     def info(self) -> dict:
         return spconv_plan_get_info(self.handle)

@@ -31,7 +31,10 @@ def gpu_run(layer, x=None, **options):
         xt = to_gpu(x)
         yt = plan.run(xt)
         torch.cuda.synchronize()
-        return yt.cpu().numpy()
+        y = yt.cpu().numpy()
+        # every bounded wait inside the kernels succeeded
+        assert plan.check() == 0, "a bounded wait gave up (plan error word set)"
+        return y
     finally:
         plan.close()
 
@@ -65,7 +68,9 @@ def gpu_run_fused(layer, dw_k, dw_b, dw_act, stride, x=None, **options):
     try:
         yt = plan.run(to_gpu(x))
         torch.cuda.synchronize()
-        return yt.cpu().numpy()
+        y = yt.cpu().numpy()
+        assert plan.check() == 0, "a bounded wait gave up (plan error word set)"
+        return y
     finally:
         plan.close()
 

@@ -8,7 +8,7 @@ direct-load kernel, so the two give the same bits on finite inputs.
 Cases cover every column count per lane (lane_cols 1 .. 6) with each block
 height, both ring-copy paths (16-byte copies when every image's column count
 is a multiple of 4, one dword per lane otherwise), channel counts that wrap
-the 64-row ring many times or end in a ragged chunk, tiles that end inside an
+the 96-row ring many times or end in a ragged chunk, tiles that end inside an
 image, the row-pair phase for columns left over after the whole tiles, and
 every fp32 layer of the workloads at full size.
 """
@@ -132,3 +132,29 @@ def test_empty_rows_slots_and_chunks():
     y = gpu_run(layer, kernel=3)
     assert_parity(layer, y, what="empty parts")
     assert np.array_equal(y, gpu_run(layer, kernel=2))
+
+
+@pytest.mark.parametrize("kernel", [0, 3], ids=["strip-pipeline", "indexed"])
+def test_a_wait_that_gives_up_is_reported(kernel):
+    """With the plan's wait bound at 0 every bounded wait that finds its data
+    missing gives up at once (the kernels still finish); the plan's error word
+    reports it.  Cleared and run with the default bound, the word stays 0 and
+    the output matches the oracle."""
+    import torch
+    from paper_1911_09723_amd import Plan, spconv_plan_set_wait_limit, SPCONV_FLAG_WAIT_GAVE_UP
+    layer = make_layer(512, 512, 14, 14, 256, 0.9, act="relu", seed=51)
+    note("indexed forced give-up kernel=%d" % kernel)
+    plan = Plan.from_layer(layer, kernel=kernel)
+    try:
+        x = to_gpu(layer.x)
+        spconv_plan_set_wait_limit(plan.handle, 0)
+        plan.run(x)
+        torch.cuda.synchronize()
+        assert plan.check(clear=True) & SPCONV_FLAG_WAIT_GAVE_UP
+        spconv_plan_set_wait_limit(plan.handle, 1 << 22)
+        y = plan.run(x)
+        torch.cuda.synchronize()
+        assert plan.check() == 0
+        assert_parity(layer, y.cpu().numpy(), what="after a forced give-up")
+    finally:
+        plan.close()
