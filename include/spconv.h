@@ -113,8 +113,10 @@ SPCONV_API spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int3
  * elements beyond 2^62), SPCONV_E_UNSUPPORTED (the images one tile of output
  * columns touches, ((tile columns - 1) / (out_h * out_w) + 2) of them, span
  * 2^31 bytes or more of x or of y), SPCONV_E_HIP
- * (launch failure).  Faults during
- * execution surface at the caller's next synchronization.
+ * (launch failure).  Every check on the arguments runs before any HIP call and
+ * before a host-only plan is refused, so a host-only plan exercises them
+ * without a device.  Faults during execution surface at the caller's next
+ * synchronization.
  */
 SPCONV_API spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, int32_t h, int32_t w,
                          void *stream);
@@ -448,8 +450,9 @@ SPCONV_API spconv_status spconv_plan_check(spconv_plan plan, int32_t *flags, int
  * Test hook for the error path above: the bound of every such wait in the
  * plan's later launches, in sleeps of about 64 clocks (default 1 << 22, about
  * 0.1 s).  0 makes every wait that finds its data missing give up at once;
- * kernels still run to completion.  SPCONV_E_ARG for a NULL plan or a
- * negative bound.  Host only.
+ * kernels still run to completion.  The one setting a plan has that can
+ * change: not to be called while another thread queues runs of the plan.
+ * SPCONV_E_ARG for a NULL plan or a negative bound.  Host only.
  */
 SPCONV_API spconv_status spconv_plan_set_wait_limit(spconv_plan plan, int32_t sleeps);
 

@@ -451,8 +451,9 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
         return fail(SPCONV_E_ARG, "plan is NULL");
     if (n < 0 || h < 0 || w < 0)
         return fail(SPCONV_E_ARG, "n, h and w must be >= 0");
-    if (plan->host_only)
-        return fail(SPCONV_E_ARG, "plan was created with host_only = 1 and has no device data");
+    // every check below up to the host-only refusal is on the arguments alone
+    // (no HIP call), so host-only plans exercise them too
+    const char *host_only_msg = "plan was created with host_only = 1 and has no device data";
     const spconv::PackedPlan &p = plan->host;
     // a depthwise stage maps the h x w input to out_h x out_w (zero padding 1)
     const int32_t s = p.dw_stride ? p.dw_stride : 1;
@@ -461,7 +462,7 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t hw = oh * ow, ihw = static_cast<int64_t>(h) * w;
     const int64_t m = static_cast<int64_t>(n) * hw;
     if (m == 0)
-        return SPCONV_OK;
+        return plan->host_only ? fail(SPCONV_E_ARG, host_only_msg) : SPCONV_OK;
     if (!x || !y)
         return fail(SPCONV_E_ARG, "x or y is NULL");
     if (ihw > INT32_MAX || static_cast<int64_t>(n) * ihw > INT32_MAX)
@@ -474,6 +475,16 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
         return fail(SPCONV_E_ARG, "x and y must be aligned to the element size");
     if (ranges_overlap(x, static_cast<size_t>(xel) * e, y, static_cast<size_t>(yel) * e))
         return fail(SPCONV_E_ARG, "x and y overlap; the operation cannot run in place");
+    // the kernels address X and Y relative to the first image of a tile with
+    // 32-bit byte offsets: the images one tile's columns touch (at most
+    // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
+    const int64_t tile_cols = p.use_indexed ? 64 * 6 : p.tile_cols;
+    const int64_t span = (tile_cols - 1) / hw + 2;
+    if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
+        return fail(SPCONV_E_UNSUPPORTED,
+                    "h * w * channels too large: the images of one tile must span less than 2^31 bytes");
+    if (plan->host_only)
+        return fail(SPCONV_E_ARG, host_only_msg);
     int dev = -1;
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess)
@@ -484,14 +495,6 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    // the kernels address X and Y relative to the first image of a tile with
-    // 32-bit byte offsets: the images one tile's columns touch (at most
-    // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
-    const int64_t tile_cols = p.use_indexed ? 64 * 6 : p.tile_cols;
-    const int64_t span = (tile_cols - 1) / hw + 2;
-    if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
-        return fail(SPCONV_E_UNSUPPORTED,
-                    "h * w * channels too large: the images of one tile must span less than 2^31 bytes");
     if (plan->dev.use_indexed)
         he = spconv::launch_indexed(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
                                     static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),

@@ -382,3 +382,49 @@ def test_f16_weights_rounded_to_nearest_even():
         sp.spconv_destroy(h)
     expect = vals.astype(np.float16).astype(np.float32)
     assert np.array_equal(va.view(np.uint32), expect.view(np.uint32))
+
+
+def test_network_operators_reject_bad_arguments():
+    """Argument checks of the network operators run before any HIP call: the
+    addresses below are never dereferenced (stream 0 keeps the binding off
+    torch's device state, so this runs without a GPU)."""
+    from paper_1911_09723_amd import (spconv, spconv_conv3x3_hwc, spconv_depthwise3x3, spconv_global_avg_pool,
+                                      spconv_linear)
+    kw = dict(stream=0, check=False)
+    assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 3, 1 << 42, 1, 4, 4, 3, 8, **kw) == spconv.E_ARG
+    assert spconv_conv3x3_hwc(1 << 40, 1 << 41, None, "relu", 2, 1 << 42, 1, 4, 4, 9, 8, **kw) == \
+        spconv.E_UNSUPPORTED
+    assert spconv_conv3x3_hwc(None, None, None, "relu", 2, None, 0, 4, 4, 3, 8, **kw) == spconv.OK
+    assert spconv_depthwise3x3(1 << 40, 1 << 41, None, "relu", 2, 1 << 40, 1, 4, 4, 4, **kw) == spconv.E_ARG
+    assert spconv_global_avg_pool(1 << 40, 1 << 41, 1, 4, 0, 3, **kw) == spconv.E_SHAPE
+    assert spconv_global_avg_pool(None, None, 0, 4, 3, 3, **kw) == spconv.OK
+    assert spconv_linear(1 << 40, 1 << 41, None, "none", 1 << 42, 2, 0, 5, **kw) == spconv.E_SHAPE
+    assert spconv_linear(1 << 40, 1 << 41, None, "none", 1 << 42, 300000, 4, 5, **kw) == spconv.E_SHAPE
+    assert spconv_linear(None, None, None, "none", None, 0, 4, 5, **kw) == spconv.OK
+
+
+@pytest.mark.parametrize("kernel", [0, 3])
+@pytest.mark.parametrize("fused", [False, True])
+def test_run_rejects_tiles_whose_images_span_2gib(fused, kernel):
+    """Two 1024 x 1024 images of 300 channels: one tile touches both, 2.5 GB of
+    x, beyond the kernels' 32-bit offsets, so spconv_run refuses the call.  The
+    check runs before any HIP call, so a host-only plan reaches it; images of
+    a quarter the size pass it and only then meet the host-only refusal."""
+    from synth import make_depthwise
+    if fused and kernel == 3:
+        pytest.skip("the register-indexed kernel has no depthwise stage")
+    layer = make_layer(300, 8, 1, 1, 1, 0.5, act="relu", seed=91, with_x=False)
+    o = _host_opts(kernel=kernel)
+    if fused:
+        kw, kb = make_depthwise(300, 92)
+        h = sp.spconv_plan_create_fused(8, 300, 1, layer.row_ptr, layer.col_idx, layer.values, layer.bias, "relu",
+                                        kw, kb, "none", 1, options=o)
+    else:
+        h = _create(layer, options=o)
+    try:
+        st = sp.spconv_run(h, 1 << 44, 1 << 45, 2, 1024, 1024, stream=0, check=False)
+        assert st == sp.spconv.E_UNSUPPORTED and "2^31" in sp.spconv_last_error()
+        st = sp.spconv_run(h, 1 << 44, 1 << 45, 4, 512, 512, stream=0, check=False)
+        assert st == sp.spconv.E_ARG and "host_only" in sp.spconv_last_error()
+    finally:
+        sp.spconv_destroy(h)
