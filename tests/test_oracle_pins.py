@@ -208,3 +208,23 @@ def test_tolerance_formula():
     s = np.array([10.0, 0.0, 5.0])
     assert np.allclose(oracle.tolerance(y, s, "f32"), [1e-4 + 1e-6, 1e-6, 5e-5 + 1e-6])
     assert np.allclose(oracle.tolerance(y, s, "f16"), [2e-3 + 1e-4 + 1e-6, 4e-3 + 1e-6, 5e-5 + 1e-6])
+
+
+FP16_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "fp16_rounding.json")
+
+
+@pytest.mark.parametrize("case", json.load(open(FP16_GOLDEN))["cases"], ids=lambda c: c["name"])
+def test_fp16_output_rounds_once_to_nearest_even(case):
+    """The oracle's fp16 result is the exact sum rounded once to binary16,
+    ties to even: hand-derived bit patterns (tests/golden/fp16_rounding.json)
+    that double rounding through fp32, truncation or ties-away would miss."""
+    vals = np.array([float.fromhex(v) for v in case["values"]], np.float32)
+    xs = np.array([float.fromhex(v) for v in case["x"]], np.float64)
+    assert np.array_equal(xs.astype(np.float16).astype(np.float64), xs), "inputs must be fp16 values"
+    cin = len(vals)
+    x = xs.astype(np.float16).reshape(1, cin, 1, 1)
+    y, y64, _ = oracle.spconv_ref(1, cin, 1, np.array([0, cin], np.int32), np.arange(cin, dtype=np.int32), vals,
+                                  None, "none", x, storage="f16")
+    assert y.dtype == np.float16
+    assert int(y.reshape(-1).view(np.uint16)[0]) == int(case["y_bits"], 16), (
+        case["name"], float(y64.reshape(-1)[0]).hex(), hex(int(y.reshape(-1).view(np.uint16)[0])))
