@@ -9,6 +9,8 @@ sweep point is reported beside it, and so are blocks of 4 input channels
 the paper's layer shapes (no trained weights or images are used).
 
 One step = one spconv_run over the whole batch (bias and activation fused).
+The "1x1 indexed" and "1x4 indexed" variants run the same layers on the
+register-indexed kernel (kernel=3) instead of the automatic choice.
 A third variant runs the same 1x1 behind a fused depthwise 3x3 (stride 1,
 ReLU6): one MobileNet v1 block at 512 channels.  The ``network`` entries time
 a whole synthetic MobileNet v1 forward pass (17 launches replayed as one
@@ -17,6 +19,20 @@ Inputs are resident in HBM before timing starts; three (X, Y) buffer sets,
 616 MB in all, rotate so no step finds its operands in the 256 MB
 last-level cache.  Kernel durations come from HIP events recorded on the
 launch stream around every launch.
+
+The ``configs`` list times every layer of every workload configuration (c0
+.. c4: the small parity layer, MobileNet v1's pointwise layers at batch 1
+and 64, the 512x512 sparsity sweep, the MobileNet v2-like heavy-tail
+layers, and the fp16 layers), each on the automatic kernel and, for fp32,
+on the register-indexed kernel, with kernel time, effective GFLOP/s,
+algorithmic GB/s, bound and roofline fraction (the per-layer view of paper
+Sec. 4.1 / Fig. 4).  ``--config C`` runs only configuration C's sweep (for
+rocprofv3 kernel traces).
+
+The CPU baseline is the oracle, built for this host (gcc -O3 -march=native,
+no floating-point contraction), timed in child processes: the median of 3
+runs on the headline layer with all threads (``value``), and 1-thread runs on
+the headline layer and on c0, each also the median of 3.
 
 Prints one JSON line.  ``--gpus`` above 1 is refused: this build measures one GPU.
 
@@ -48,7 +64,7 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E peak
 FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector peak (packed FMA)
 TRAFFIC_BASE = os.path.join(ROOT, "profiles", "traffic_spmm_pipe_512x512_14x14_b256")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_09723_amd", "csrc", f)
-                  for f in ("spmm_kernels.hip", "planner.cpp", "planner.hpp")]
+                  for f in ("spmm_kernels.hip", "spmm_indexed.hip", "planner.cpp", "planner.hpp")]
 COPY_BYTES = 256 << 20        # calibration copy: 256 MiB read + 256 MiB written
 CALIBRATION_KERNEL = "neg_kernel"  # torch.neg(a, out=b): a plain elementwise copy
 METRIC = "effective GFLOP/s (2*nnz*HW*N) + HBM GB/s % peak, sparse 1x1 conv"
@@ -110,13 +126,13 @@ def fused_layer(layer):
     return kw, kb
 
 
-def time_variant(layer, steps, warmup, sets, dw=None):
+def time_variant(layer, steps, warmup, sets, dw=None, **options):
     import torch
     from paper_1911_09723_amd import Plan, spconv_run
 
     dev = torch.device("cuda:0")
     if dw is None:
-        plan = Plan.from_layer(layer)
+        plan = Plan.from_layer(layer, **options)
     else:
         plan = Plan.fused(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
                           layer.bias, layer.act, dw[0], dw[1], "relu6", 1)
@@ -143,10 +159,13 @@ def time_variant(layer, steps, warmup, sets, dw=None):
     region_ms = t_start.elapsed_time(t_end)
     kern_ms = [a.elapsed_time(b) for a, b in ev]
     info = plan.info()
+    flags = plan.check(clear=True)
     plan.close()
+    if flags:
+        raise RuntimeError("a bounded wait gave up during the timed launches (error word %d)" % flags)
     del xs, ys
     torch.cuda.empty_cache()
-    return dict(region_ms=region_ms, wall_s=wall, kernel_ms=kern_ms, info=info)
+    return dict(region_ms=region_ms, wall_s=wall, kernel_ms=kern_ms, info=info, forced_kernel=options.get("kernel"))
 
 
 def time_network(batch, steps, warmup, graph=True):
@@ -215,33 +234,133 @@ def network_alg_bytes(net, batch, fused_blocks, h=224):
     return float(total * e)
 
 
-def cpu_baseline(layer, budget_s=12.0):
-    """The oracle, as it stands, timed on this host on a bounded sample of the
-    same layer (the first images of the batch, repeated to fill the budget)."""
+def sweep_configs(configs, steps, warmup, indexed=True):
+    """Every layer of the given workload configurations on the automatic
+    kernel and (fp32) on the register-indexed kernel."""
+    from synth import config_layers
+    from synth.configs import build
+
+    out = []
+    for c in configs:
+        for spec in config_layers(c):
+            layer = build(c, spec)
+            entry = {"config": "c%d" % c, "layer": spec["name"], "cin": layer.cin, "cout": layer.cout,
+                     "h": layer.h, "w": layer.w, "batch": layer.n, "sparsity": spec["sparsity"],
+                     "block_rows": layer.block_rows, "pattern": spec["pattern"], "storage": layer.storage}
+            kinds = [("auto", {})]
+            if indexed and layer.storage == "f32":
+                kinds.append(("indexed", {"kernel": 3}))
+            for kind, opts in kinds:
+                r = time_variant(layer, steps, warmup, 2, **opts)
+                sm = summarize(layer, r)
+                entry[kind] = {k: sm[k] for k in ("kernel_us_mean", "kernel_us_min", "gflops_effective",
+                                                   "hbm_gbs_algorithmic", "bound", "roofline_us", "roofline_frac")}
+                entry[kind]["ms"] = round(sm["kernel_us_mean"] / 1e3, 5)
+                entry[kind]["kernel"] = sm["plan"]["kernel_run"]
+                if "device_weight_extra_bytes" in sm:
+                    entry[kind]["device_weight_extra_bytes"] = sm["device_weight_extra_bytes"]
+            entry["alg_bytes"] = layer.alg_bytes()
+            entry["flops"] = layer.flops()
+            out.append(entry)
+            log("bench: %s %s auto %.1f us (%s, frac %.3f)%s" % (
+                entry["config"], spec["name"], entry["auto"]["kernel_us_mean"], entry["auto"]["kernel"],
+                entry["auto"]["roofline_frac"],
+                "  indexed %.1f us" % entry["indexed"]["kernel_us_mean"] if "indexed" in entry else ""))
+            del layer
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def native_oracle(path):
+    """The oracle's C source built for this host: -O3 -march=native, OpenMP,
+    no floating-point contraction (the same arithmetic as the tests' build)."""
+    import subprocess
+    import oracle
+    src = os.path.join(os.path.dirname(oracle.__file__), "spconv_ref.c")
+    cmd = ["gcc", "-O3", "-march=native", "-fopenmp", "-ffp-contract=off", "-fPIC", "-shared", "-o", path, src, "-lm"]
+    subprocess.check_call(cmd)
+    return " ".join(cmd[:6])
+
+
+def cpu_leg(lib_path, budget_s):
+    """Child process of the CPU baseline: time the oracle (the library at
+    lib_path) on the headline layer and on c0, 3 runs each, with the threads
+    OMP_NUM_THREADS gives; print one JSON line."""
     import numpy as np
     import oracle
+    from synth import config_layers
+    from synth.configs import TARGET, build
 
-    oracle.build(force=False)
-    t0 = time.perf_counter()
-    oracle.spconv_ref_layer(layer, x=layer.x[:1], with_scale=False)
-    t1 = max(time.perf_counter() - t0, 1e-6)
-    n_s = int(max(1, min(layer.n, budget_s / t1)))
-    xs = np.ascontiguousarray(layer.x[:n_s])
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        oracle.spconv_ref_layer(layer, x=xs, with_scale=False)
-        reps += 1
-        dt = time.perf_counter() - t0
-        if dt >= 0.8 * budget_s or reps >= 1000:
-            break
+    lib = oracle.load_library(lib_path)
+
+    def run(layer, x):
+        oracle.spconv_ref(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values,
+                          layer.bias, layer.act, x, storage=layer.storage, with_scale=False, lib=lib)
+
+    spec_t = [sp for sp in config_layers(TARGET["config"]) if sp["layer"] == TARGET["layer"]][0]
+    layers = {"target": build(TARGET["config"], spec_t), "c0": build(0, config_layers(0)[0])}
+    out = {"threads": int(lib.spconv_ref_threads())}
+    for name, layer in layers.items():
+        # a warm-up pass sizes the runs: each run is `reps` passes over n_s
+        # images, about budget_s / 3 seconds of work
+        n_w = min(layer.n, 8)
+        run(layer, layer.x[:n_w])
+        t0 = time.perf_counter()
+        run(layer, layer.x[:n_w])
+        t_img = max(time.perf_counter() - t0, 1e-6) / n_w
+        n_s = int(max(1, min(layer.n, budget_s / 3.0 / t_img)))
+        reps = int(max(1, min(1000, budget_s / 3.0 / (t_img * n_s))))
+        xs = np.ascontiguousarray(layer.x[:n_s])
+        runs = []
+        for _ in range(3):
+            t0 = time.perf_counter()
+            for _ in range(reps):
+                run(layer, xs)
+            runs.append(reps * layer.flops(n_s) / (time.perf_counter() - t0) / 1e9)
+        out[name] = {"gflops_runs": [round(v, 3) for v in runs], "gflops_median": round(float(np.median(runs)), 3),
+                     "images": n_s, "of": layer.n, "passes": reps}
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(budget_s=8.0):
+    """The oracle as it stands, built for this host, timed in child processes
+    with all threads and with one (see the module docstring)."""
+    import subprocess
+    import tempfile
+    d = tempfile.mkdtemp(prefix="spconv_oracle_")
+    lib = os.path.join(d, "libspconv_ref_native.so")
+    build_cmd = native_oracle(lib)
+    res = {}
+    for threads in (None, 1):
+        env = dict(os.environ)
+        if threads:
+            env["OMP_NUM_THREADS"] = str(threads)
+        out = subprocess.run([sys.executable, os.path.abspath(__file__), "--cpu-leg", lib, "--cpu-budget",
+                              str(budget_s)], env=env, capture_output=True, text=True, check=True)
+        res[threads or "all"] = json.loads(out.stdout.strip().splitlines()[-1])
+    a, one = res["all"], res[1]
     return {
-        "value": round(layer.flops(n_s) * reps / dt / 1e9, 3),
+        "value": a["target"]["gflops_median"],
         "unit": "GFLOP/s",
-        "cores": oracle.threads(),
+        "cores": a["threads"],
         "kind": "oracle",
-        "sample": "%d pass(es) over %d of %d images of the same layer (fp64 accumulation, OpenMP over "
-                  "images x rows), %.1f s" % (reps, n_s, layer.n, dt),
+        "sample": "median of 3 runs, each %d pass(es) over %d of %d images of the headline layer (fp64 "
+                  "accumulation, OpenMP over images x rows)" % (a["target"]["passes"], a["target"]["images"],
+                                                                a["target"]["of"]),
+        "runs": a["target"]["gflops_runs"],
+        "one_thread": {"target": one["target"], "c0": one["c0"]},
+        "c0_all_threads": a["c0"],
+        "cpu_model": cpu_model(),
+        "build": build_cmd,
     }
 
 
@@ -261,7 +380,7 @@ def summarize(layer, r, dw=False):
     t_hbm = b_alg / (HBM_PEAK_GBS * 1e9)
     t_alu = flops / (FP32_VECTOR_PEAK_TFS * 1e12)
     t_roof = max(t_hbm, t_alu)
-    return {
+    out = {
         "gflops_effective": round(flops / t_step / 1e9, 1),
         "ms_per_step": round(t_step * 1e3, 5),
         "kernel_us_mean": round(t_kern * 1e6, 3),
@@ -277,8 +396,17 @@ def summarize(layer, r, dw=False):
         "lds_strip_read_bytes": r["info"]["slots"] * 256 * -(-layer.n * layer.hw // r["info"]["tile_cols"]),
         "flops": flops,
         "plan": {k: r["info"][k] for k in ("kernel", "group_lanes", "tile_cols", "waves", "lds_bytes", "slots",
-                                           "max_parts")},
+                                           "max_parts", "indexed_min_cols")},
     }
+    # the kernel the runs took: 3 (register-indexed) when forced or chosen for this many columns
+    cols = layer.n * layer.hw
+    imc = r["info"]["indexed_min_cols"]
+    out["plan"]["kernel_run"] = 3 if r.get("forced_kernel") == 3 or (imc > 0 and cols >= imc) else r["info"]["kernel"]
+    if layer.storage == "f16":
+        # fp16 plans round W to fp16 but keep it as fp32 in device memory: the
+        # weights move 4 bytes per value, not the 2 alg_bytes counts
+        out["device_weight_extra_bytes"] = 2.0 * layer.nnz
+    return out
 
 
 def profile_run(reps: int):
@@ -388,7 +516,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--sets", type=int, default=3, help="rotating (X, Y) buffer sets")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds of oracle work")
+    ap.add_argument("--cpu-budget", type=float, default=8.0, help="seconds of oracle work per layer and thread count")
     ap.add_argument("--profile-run", action="store_true", help="launches for rocprofv3 counter passes")
     ap.add_argument("--reps", type=int, default=5, help="launches per variant in --profile-run")
     ap.add_argument("--traffic-summary", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
@@ -397,6 +525,10 @@ def main():
                     help="only the MobileNet v1 graph replays (batch 64), for rocprofv3 kernel traces")
     ap.add_argument("--command", action="append", default=[], help="command lines recorded in the summary")
     ap.add_argument("--out", default=TRAFFIC_BASE, help="output path (without extension) of --traffic-summary")
+    ap.add_argument("--config", type=int, help="only the per-layer sweep of workload configuration C (0 .. 4)")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the per-configuration layer sweep")
+    ap.add_argument("--sweep-steps", type=int, default=20, help="timed launches per layer in the sweep")
+    ap.add_argument("--cpu-leg", metavar="LIB", help=argparse.SUPPRESS)
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (got --gpus %d)" % args.gpus,
@@ -404,6 +536,9 @@ def main():
         sys.exit(2)
     if args.traffic_summary:
         traffic_summary(args.traffic_summary[0], args.traffic_summary[1], args.command, args.out)
+        return
+    if args.cpu_leg:
+        cpu_leg(args.cpu_leg, args.cpu_budget)
         return
 
     import torch
@@ -414,6 +549,9 @@ def main():
         return
     if args.network_run:
         print(json.dumps(time_network(64, args.steps, args.warmup)), flush=True)
+        return
+    if args.config is not None:
+        print(json.dumps(sweep_configs([args.config], args.sweep_steps, 3)), flush=True)
         return
 
     layers = headline_layers()
@@ -429,6 +567,18 @@ def main():
     r = time_variant(layers["1x1"], args.steps, args.warmup, args.sets, dw=fused_layer(layers["1x1"]))
     results[tag] = summarize(layers["1x1"], r, dw=True)
     log("bench: %s %s" % (tag, json.dumps(results[tag])))
+    # the headline layers on the register-indexed kernel
+    for base in ("1x1", "1x4"):
+        tag = base + " indexed"
+        log("bench: timing %s" % tag)
+        r = time_variant(layers[base], args.steps, args.warmup, args.sets, kernel=3)
+        results[tag] = summarize(layers[base], r)
+        log("bench: %s %s" % (tag, json.dumps(results[tag])))
+
+    configs = []
+    if not args.no_sweep:
+        log("bench: per-layer sweep of configurations c0 .. c4 (%d launches each)" % args.sweep_steps)
+        configs = sweep_configs(range(5), args.sweep_steps, 3)
 
     network = []
     for batch in (() if args.no_network else (1, 64)):
@@ -469,12 +619,13 @@ def main():
             "traffic": None if traffic is None else traffic.get("bytes_per_launch"),
         },
         "variants": results,
+        "configs": configs,
         "network": network,
         "device": torch.cuda.get_device_name(0),
     }
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle")
-        line["cpu_baseline"] = cpu_baseline(layer, args.cpu_budget)
+        line["cpu_baseline"] = cpu_baseline(args.cpu_budget)
     print(json.dumps(line), flush=True)
 
 

@@ -276,7 +276,9 @@ typedef struct {
     int32_t struct_size; /* sizeof(spconv_options) */
     int32_t reorder;     /* 1 (default): process rows in descending nonzero order; 0: natural order */
     int32_t host_only;   /* 1: plan on the host only, no device memory; spconv_run refuses it */
-    int32_t kernel;      /* 0 = choose automatically (the LDS-strip or direct-load kernel);
+    int32_t kernel;      /* 0 = choose automatically: the LDS-strip or direct-load kernel, or, for
+                            runs with enough columns on layers where it measured faster, the
+                            register-indexed kernel (spconv_plan_info.indexed_min_cols);
                             1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED when the strip of cin
                             channels does not fit in LDS); 2 = direct-load kernel; 3 =
                             register-indexed kernel (SPCONV_E_UNSUPPORTED for fp16 storage or a
@@ -395,6 +397,10 @@ typedef struct {
     int32_t dw_stride;     /* fused depthwise stage: 0 none, else its stride */
     int32_t dw_act;        /* its activation */
     int32_t block_cols;    /* input channels per block (1 unless created by spconv_plan_create_blocked) */
+    int32_t reserved0;
+    int64_t indexed_min_cols; /* kernel chosen automatically: runs of at least this many output columns
+                                 (N * out_h * out_w) take the register-indexed kernel; 0 = never (and
+                                 for host-only plans, which know no device) */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */

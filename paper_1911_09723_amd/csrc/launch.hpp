@@ -62,6 +62,8 @@ struct DevicePlan {
     const float *rrow_bias = nullptr;   // bias of every output channel
     int32_t *flag = nullptr;            // device word: bit 0 set when a bounded wait of a kernel gave up
     int32_t spin_limit = 1 << 22;       // bound of those waits, in sleeps
+    int64_t indexed_min_cols = 0;       // automatic choice: runs of at least this many columns take the
+                                        // register-indexed kernel (0: never)
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`

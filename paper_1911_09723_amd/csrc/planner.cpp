@@ -691,6 +691,7 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         build_indexed(in, p.perm, p);
         p.use_indexed = opt.kernel == 3;
         p.rlane_cols = opt.lane_cols;
+        p.auto_kernel = opt.kernel == 0;
     }
 
     // 2. bundles of NB consecutive rows in that order, each a whole number of

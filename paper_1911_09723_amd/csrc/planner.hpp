@@ -242,6 +242,7 @@ struct PackedPlan {
     int32_t rwaves = 0;          // wavefronts per workgroup = slots per group (the last may have fewer)
     int32_t rnch = 0;            // chunks of kChunk input channels
     int32_t rlane_cols = 0;      // columns per lane fixed by the caller (0: chosen per run)
+    int32_t auto_kernel = 0;     // the caller left the kernel to the library (options.kernel = 0)
     std::vector<uint32_t> rrec;
     std::vector<int32_t> rslot_batch;
     std::vector<int32_t> rslot_chunk;

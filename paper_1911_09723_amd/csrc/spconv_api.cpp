@@ -156,6 +156,24 @@ spconv_status upload(spconv_plan_s *pl) {
     return SPCONV_OK;
 }
 
+// The automatic kernel choice between the LDS-strip / direct-load kernels and
+// the register-indexed one, from their measured times on MI355X over the
+// workload layers: the register-indexed kernel wins where the direct-load
+// kernel would run (inputs too wide for an LDS strip) and, once a run has at
+// least one whole round of its 384-column tiles, on layers with few input
+// channels or denser weights; elsewhere (small batches, few output channels,
+// 90-95% sparse wide layers) the strip kernels are faster.
+int64_t indexed_min_cols(const spconv::PackedPlan &h, const spconv::DevicePlan &d) {
+    if (!h.auto_kernel || d.rslots == 0 || d.num_cus <= 0)
+        return 0;
+    if (h.kernel == spconv::KERNEL_DIRECT)
+        return 1024;
+    const double density = static_cast<double>(h.nnzb) * h.k / (static_cast<double>(h.cout) * h.cin);
+    if (d.rslots >= 4 && (h.cin <= 64 || density >= 0.15))
+        return int64_t(64) * 6 * ((d.num_cus + d.rgroups - 1) / d.rgroups);
+    return 0;
+}
+
 void fill_device_geometry(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
     spconv::DevicePlan &d = pl->dev;
@@ -242,6 +260,7 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
             hipError_t pe = spconv::prepare_launch(pl->dev);
             if (pe == hipSuccess && pl->dev.rslots > 0)
                 pe = spconv::prepare_indexed(pl->dev);
+            pl->dev.indexed_min_cols = indexed_min_cols(pl->host, pl->dev);
             if (pe != hipSuccess)
                 us = hip_fail("kernel launch set-up", pe);
         }
@@ -478,7 +497,8 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     // the kernels address X and Y relative to the first image of a tile with
     // 32-bit byte offsets: the images one tile's columns touch (at most
     // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
-    const int64_t tile_cols = p.use_indexed ? 64 * 6 : p.tile_cols;
+    const bool indexed = plan->dev.use_indexed || (plan->dev.indexed_min_cols > 0 && m >= plan->dev.indexed_min_cols);
+    const int64_t tile_cols = indexed ? 64 * 6 : p.tile_cols;
     const int64_t span = (tile_cols - 1) / hw + 2;
     if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,
@@ -495,7 +515,7 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    if (plan->dev.use_indexed)
+    if (indexed)
         he = spconv::launch_indexed(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
                                     static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),
                                     yel * static_cast<int64_t>(e), static_cast<hipStream_t>(stream));
@@ -650,6 +670,7 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->dw_stride = p.dw_stride;
     info->dw_act = p.dw_act;
     info->block_cols = p.kc;
+    info->indexed_min_cols = plan->host_only ? 0 : plan->dev.indexed_min_cols;
     return SPCONV_OK;
 }
 

@@ -939,7 +939,12 @@ IndexedLaunch plan_indexed_launch(const DevicePlan &p, int64_t m) {
     IndexedLaunch best;
     const int64_t W = p.rwaves;
     const int64_t G = p.rgroups;
-    const int64_t wg_per_cu = std::max<int64_t>(1, kMaxWaves / W);
+    // the ring holds min(kRing, cin rounded up to a chunk) rows, so a layer
+    // with few input channels leaves LDS for more workgroups per CU
+    const int32_t ring_rows = std::min<int32_t>(kRing, p.rnch * kChunk);
+    const int64_t main_lds_max = static_cast<int64_t>(ring_rows) * kRingRowBytes + 64 + 2 * 256 * 6 + 3 * 256;
+    const int64_t wg_per_cu =
+        std::max<int64_t>(1, std::min<int64_t>(kMaxWaves / W, kMaxLdsBytes / main_lds_max));
     const int64_t grid = static_cast<int64_t>(p.num_cus) * wg_per_cu;
     const int64_t pairs = (p.cout + 1) / 2;
     // row pairs: the strip of cin channel rows (256 bytes each, whole 1 KiB
@@ -966,8 +971,10 @@ IndexedLaunch plan_indexed_launch(const DevicePlan &p, int64_t m) {
                 best.lpieces = 0;
             }
         }
-        // one round of whole tiles, the rest by row pairs
-        if (pairs_fit && grid % G == 0) {
+        // one round of whole tiles, the rest by row pairs (their LDS strip
+        // would leave one workgroup per CU, so only where that is all the
+        // ring leaves anyway)
+        if (pairs_fit && wg_per_cu == 1 && grid % G == 0) {
             const int64_t tiles = std::min<int64_t>(grid / G, m / tc);
             if (tiles >= 1) {
                 const int64_t left = m - tiles * tc;
@@ -990,7 +997,7 @@ IndexedLaunch plan_indexed_launch(const DevicePlan &p, int64_t m) {
     best.lper = best.lpieces ? (best.lpieces + best.grid - 1) / best.grid : 0;
     // LDS: the ring, 64 bytes of counters, the lane x and y column tables
     // (256 C bytes each), three copy patterns.
-    best.ctl_off = kRing * kRingRowBytes;
+    best.ctl_off = ring_rows * kRingRowBytes;
     best.xo_off = best.ctl_off + 64;
     best.pat_off = best.xo_off + 2 * 256 * best.c;
     const int32_t main_lds = best.pat_off + 3 * 256;
