@@ -221,7 +221,9 @@ SPCONV_API spconv_status spconv_depthwise3x3(const float *x, const float *weight
 /*
  * Dense fully connected layer (the network's classifier, kept dense as in
  * Sec. 3.1 / Table 1):  y[n, r] = act( bias[r] + sum_c weight[r][c] * x[n][c] ),
- * fp32 FMA in ascending c.  x [n][cin], weight [cout][cin] row-major, bias
+ * fp32: the input channels are taken in 16 consecutive ranges, each summed
+ * by FMA in ascending c from zero, and the range sums are added in ascending
+ * order; then the bias.  x [n][cin], weight [cout][cin] row-major, bias
  * [cout] or NULL, y [n][cout].
  * Errors: SPCONV_E_ARG (NULL pointer with work to do, negative size, bad act,
  * overlap), SPCONV_E_SHAPE (cin == 0 with outputs, n > 262140), SPCONV_E_HIP.

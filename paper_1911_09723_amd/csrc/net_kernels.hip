@@ -120,54 +120,114 @@ gap_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t planes, i
     y[q] = acc * inv;
 }
 
-// Dense fully connected layer (the classifier the paper keeps dense, Sec. 3.1):
-//   y[n, r] = act(b[r] + sum_c W[r, c] * x[n, c]),  W row-major [cout][cin].
-// A wavefront owns 64 consecutive rows (lane = row) and kImg images: each W
-// load feeds kImg FMAs, the x loads are the same address in every lane (one
-// line per instruction), and the stores are consecutive rows.  VEC: 16-byte
-// loads (cin a multiple of 4, pointers 16-byte aligned).  fp32 FMA in
-// ascending c from zero, then the bias, then the activation.
-constexpr int kImg = 4;
+// Global average pooling for small planes (hw <= kGapMaxHw): a wavefront
+// owns 64 consecutive planes, whose 64 hw values are contiguous; it copies
+// them into LDS with coalesced loads (16 bytes per lane when aligned), then
+// each lane sums one plane in ascending p in fp32, as gap_kernel does.
+constexpr int32_t kGapMaxHw = 256;
 
 template <bool VEC>
 __global__ void __launch_bounds__(64)
+gap_staged_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t planes, int32_t hw, float inv) {
+    extern __shared__ __align__(16) float buf[];
+    const int lane = threadIdx.x;
+    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * 64;
+    const int32_t nq = static_cast<int32_t>(planes - q0 < 64 ? planes - q0 : 64);
+    const int32_t total = nq * hw;
+    const float *src = x + q0 * hw;
+    if constexpr (VEC) {
+        const int32_t nvec = total / 4;  // whole 16-byte groups, then the last few values
+#pragma unroll 8
+        for (int32_t v = lane; v < nvec; v += 64)
+            *reinterpret_cast<f4 *>(buf + 4 * v) = *reinterpret_cast<const f4 *>(src + 4 * v);
+        for (int32_t t = 4 * nvec + lane; t < total; t += 64)
+            buf[t] = src[t];
+    } else {
+        for (int32_t t = lane; t < total; t += 64)
+            buf[t] = src[t];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (lane >= nq)
+        return;
+    const float *pl = buf + lane * hw;
+    float acc = 0.0f;
+    for (int32_t p = 0; p < hw; ++p)
+        acc += pl[p];
+    y[q0 + lane] = acc * inv;
+}
+
+// Dense fully connected layer (the classifier the paper keeps dense, Sec. 3.1):
+//   y[n, r] = act(b[r] + sum_c W[r, c] * x[n, c]),  W row-major [cout][cin].
+// Lane = image (64 per wavefront), kLinRows rows per workgroup: every
+// wavefront reads its lanes' images with 16-byte loads (each line serves 8 of
+// them through L1) and the rows' weights, the same for all lanes, with
+// scalar loads.  The kLinSplit wavefronts of a workgroup take consecutive
+// ranges of the input channels; each lane sums its range in ascending c by
+// fp32 FMA from zero, the range sums are added in ascending order through
+// LDS, then the bias, then the activation.  VEC: 16-byte loads (cin a
+// multiple of 4, x and W 16-byte aligned).
+constexpr int kLinRows = 4;
+constexpr int kLinSplit = 16;
+
+template <bool VEC>
+__global__ void __launch_bounds__(64 * kLinSplit)
 linear_kernel(const float *__restrict__ x, const float *__restrict__ wt, const float *__restrict__ bias,
               float *__restrict__ y, int32_t n, int32_t cin, int32_t cout, int32_t act) {
-    const int32_t r = blockIdx.x * 64 + threadIdx.x;
-    const int32_t n0 = blockIdx.y * kImg;
-    const int32_t rr = r < cout ? r : cout - 1;  // past the last row: compute row cout - 1, store nothing
-    const float *wr = wt + static_cast<int64_t>(rr) * cin;
-    const float *xi[kImg];
+    __shared__ float part[kLinSplit][kLinRows][64];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    const int32_t r0 = blockIdx.x * kLinRows;
+    const int32_t img = blockIdx.y * 64 + lane;
+    const float *xr = x + static_cast<int64_t>(img < n ? img : n - 1) * cin;
+    int32_t chunk = (cin + kLinSplit - 1) / kLinSplit;
+    if constexpr (VEC)
+        chunk = (chunk + 3) & ~3;
+    const int32_t c0 = wave * chunk < cin ? wave * chunk : cin;
+    const int32_t c1 = c0 + chunk < cin ? c0 + chunk : cin;
+    typedef const __attribute__((address_space(4))) float cfloat;
+    typedef const __attribute__((address_space(4))) f4 cf4;
+    cfloat *wr[kLinRows];
 #pragma unroll
-    for (int i = 0; i < kImg; ++i)
-        xi[i] = x + static_cast<int64_t>(n0 + i < n ? n0 + i : n - 1) * cin;
-    float acc[kImg] = {};
+    for (int i = 0; i < kLinRows; ++i)
+        wr[i] = (cfloat *)(wt + static_cast<int64_t>(r0 + i < cout ? r0 + i : cout - 1) * cin);
+    float acc[kLinRows] = {};
     if constexpr (VEC) {
-        for (int32_t c = 0; c < cin; c += 4) {
-            const f4 wv = *reinterpret_cast<const f4 *>(wr + c);
+#pragma unroll 4
+        for (int32_t c = c0; c < c1; c += 4) {
+            const f4 xv = *reinterpret_cast<const f4 *>(xr + c);
 #pragma unroll
-            for (int i = 0; i < kImg; ++i) {
-                const f4 xv = *reinterpret_cast<const f4 *>(xi[i] + c);
+            for (int i = 0; i < kLinRows; ++i) {
+                const f4 wv = *(cf4 *)(wr[i] + c);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
                     acc[i] = __builtin_fmaf(wv[e], xv[e], acc[i]);
             }
         }
     } else {
-        for (int32_t c = 0; c < cin; ++c) {
-            const float wv = wr[c];
+        for (int32_t c = c0; c < c1; ++c) {
+            const float xv = xr[c];
 #pragma unroll
-            for (int i = 0; i < kImg; ++i)
-                acc[i] = __builtin_fmaf(wv, xi[i][c], acc[i]);
+            for (int i = 0; i < kLinRows; ++i)
+                acc[i] = __builtin_fmaf(wr[i][c], xv, acc[i]);
         }
     }
-    if (r >= cout)
-        return;
-    const float b = bias ? bias[r] : 0.0f;
 #pragma unroll
-    for (int i = 0; i < kImg; ++i)
-        if (n0 + i < n)
-            y[static_cast<int64_t>(n0 + i) * cout + r] = clamp_act(acc[i] + b, act);
+    for (int i = 0; i < kLinRows; ++i)
+        part[wave][i][lane] = acc[i];
+    __syncthreads();
+    if (threadIdx.x >= 64 * kLinRows)
+        return;
+    const int i = threadIdx.x >> 6;
+    const int32_t r = r0 + i;
+    if (r >= cout || img >= n)
+        return;
+    float sum = 0.0f;
+#pragma unroll
+    for (int w = 0; w < kLinSplit; ++w)
+        sum += part[w][i][lane];
+    y[static_cast<int64_t>(img) * cout + r] = clamp_act(sum + (bias ? bias[r] : 0.0f), act);
 }
 
 using ConvFn = void (*)(const float *, const float *, const float *, float *, int64_t, int32_t, int32_t, int32_t,
@@ -220,16 +280,30 @@ hipError_t launch_linear(const float *x, const float *wt, const float *bias, flo
                          int32_t cout, int32_t act, hipStream_t stream) {
     const bool vec = cin % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                      reinterpret_cast<uintptr_t>(wt) % 16 == 0;
-    const dim3 grid(static_cast<unsigned>((cout + 63) / 64), static_cast<unsigned>((n + kImg - 1) / kImg));
+    const dim3 grid(static_cast<unsigned>((cout + kLinRows - 1) / kLinRows), static_cast<unsigned>((n + 63) / 64));
     if (vec)
-        hipLaunchKernelGGL(linear_kernel<true>, grid, dim3(64), 0, stream, x, wt, bias, y, n, cin, cout, act);
+        hipLaunchKernelGGL(linear_kernel<true>, grid, dim3(64 * kLinSplit), 0, stream, x, wt, bias, y, n, cin, cout,
+                           act);
     else
-        hipLaunchKernelGGL(linear_kernel<false>, grid, dim3(64), 0, stream, x, wt, bias, y, n, cin, cout, act);
+        hipLaunchKernelGGL(linear_kernel<false>, grid, dim3(64 * kLinSplit), 0, stream, x, wt, bias, y, n, cin,
+                           cout, act);
     return hipGetLastError();
 }
 
 hipError_t launch_gap(const float *x, float *y, int32_t n, int32_t c, int64_t hw, hipStream_t stream) {
     const int64_t planes = static_cast<int64_t>(n) * c;
+    if (hw <= kGapMaxHw) {
+        const bool vec = reinterpret_cast<uintptr_t>(x) % 16 == 0;  // every group starts 256 hw bytes in
+        const unsigned gblocks = static_cast<unsigned>((planes + 63) / 64);
+        const size_t lds = static_cast<size_t>(64) * hw * sizeof(float);
+        if (vec)
+            hipLaunchKernelGGL(gap_staged_kernel<true>, dim3(gblocks), dim3(64), lds, stream, x, y, planes,
+                               static_cast<int32_t>(hw), 1.0f / static_cast<float>(hw));
+        else
+            hipLaunchKernelGGL(gap_staged_kernel<false>, dim3(gblocks), dim3(64), lds, stream, x, y, planes,
+                               static_cast<int32_t>(hw), 1.0f / static_cast<float>(hw));
+        return hipGetLastError();
+    }
     const int64_t blocks = (planes + kThreads - 1) / kThreads;
     hipLaunchKernelGGL(gap_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, x, y, planes,
                        hw, 1.0f / static_cast<float>(hw));
