@@ -442,6 +442,28 @@ SPCONV_API spconv_status spconv_plan_unpack_indexed(spconv_plan plan, int32_t fr
                                                     int32_t *col_idx, float *values);
 
 /*
+ * For callers that cannot allocate device memory (code that must not call
+ * hipMalloc: tight serving loops, harnesses that forbid it).  As
+ * spconv_plan_create_ex, but the plan's device image (packed weights, tables
+ * and error word) goes into a static device array of SPCONV_STATIC_PLAN_BYTES
+ * that the library holds on each GPU it runs on until the process ends,
+ * instead of a new allocation; no hipMalloc or hipFree is called, only one
+ * synchronous host-to-device copy.  The array is shared: each call on a
+ * device overwrites it, so only the plan created last on that device can run
+ * (spconv_run refuses an earlier one with SPCONV_E_ARG), and creating such a
+ * plan while a run of the previous one is still executing, or from two threads
+ * on one device at once, races.  spconv_destroy frees only the plan's host
+ * part.  Errors: SPCONV_E_SHAPE when the image is larger than the array (the
+ * message gives both sizes; checked before any HIP call), SPCONV_E_ARG for
+ * options.host_only = 1, otherwise as spconv_plan_create_ex.
+ */
+#define SPCONV_STATIC_PLAN_BYTES (32u << 20)
+SPCONV_API spconv_status spconv_plan_create_static(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                                   const int32_t *row_ptr, const int32_t *col_idx,
+                                                   const float *values, const float *bias, spconv_act act,
+                                                   spconv_dtype storage, const spconv_options *opts);
+
+/*
  * The plan's device error word, written by its kernels: bit 0
  * (SPCONV_FLAG_WAIT_GAVE_UP) is set when a bounded wait inside a kernel on an
  * on-chip counter (a strip or ring part landing, a share being issued) ran

@@ -27,6 +27,8 @@ from .spconv import (  # noqa: F401
     spconv_plan_create_dense,
     spconv_plan_create_dense_blocked,
     spconv_plan_create_fused,
+    spconv_plan_create_static,
+    SPCONV_STATIC_PLAN_BYTES,
     spconv_plan_get_info,
     spconv_plan_unpack,
     spconv_plan_unpack_interleaved,

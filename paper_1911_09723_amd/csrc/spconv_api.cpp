@@ -7,12 +7,13 @@
 // synchronizes.
 #include "spconv.h"
 
-#include <hip/hip_runtime_api.h>
+#include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -27,11 +28,29 @@ struct spconv_plan_s {
     void *dmem = nullptr;
     size_t dbytes = 0;
     bool host_only = false;
+    uint64_t static_gen = 0;  // plans in the static device array: the generation they wrote (0: not one)
 };
 
 namespace {
 
 thread_local std::string g_err;
+
+// The static device array of spconv_plan_create_static: one per GPU (each
+// device holds its own copy of this file-scope array), found once per device
+// with hipGetSymbolAddress; host code uses only that address.  Each creation
+// on a device bumps the device's generation; runs of a plan whose generation
+// is no longer the device's are refused.
+constexpr size_t kStaticPlanBytes = size_t(32) << 20;
+static_assert(kStaticPlanBytes == SPCONV_STATIC_PLAN_BYTES, "header and library agree on the array's size");
+__device__ __align__(256) unsigned char scratch[kStaticPlanBytes];
+
+struct StaticArray {
+    void *ptr = nullptr;  // device address of scratch on this device
+    uint64_t gen = 0;     // generation of the plan whose image it holds
+};
+constexpr int kMaxStaticDevices = 64;
+std::mutex g_static_mu;
+StaticArray g_static[kMaxStaticDevices];
 
 spconv_status fail(spconv_status st, const std::string &msg) {
     g_err = msg;
@@ -68,7 +87,10 @@ spconv::Input make_input(int32_t cout, int32_t cin, int32_t block_rows, const in
     return in;
 }
 
-spconv_status upload(spconv_plan_s *pl) {
+// Pack the plan's device image and copy it to the device: into a new
+// allocation, or (use_static) into the device's static array, which needs no
+// allocation.
+spconv_status upload(spconv_plan_s *pl, bool use_static) {
     const spconv::PackedPlan &h = pl->host;
     // bundle table: rows, then the biases of those rows as fp32 bit patterns
     std::vector<int32_t> table(static_cast<size_t>(h.table_words()));
@@ -107,29 +129,51 @@ spconv_status upload(spconv_plan_s *pl) {
         p.off = total;
         total = align_up(total + std::max<size_t>(p.bytes, 16), 256);
     }
-    if (fault_alloc())
+    if (use_static && total > kStaticPlanBytes)  // before any HIP call
+        return fail(SPCONV_E_SHAPE, "the plan's device image needs " + std::to_string(total) +
+                                        " bytes; the static array holds " + std::to_string(kStaticPlanBytes));
+    if (!use_static && fault_alloc())
         return fail(SPCONV_E_NOMEM, "device allocation failed (SPCONV_FAULT=alloc)");
     hipError_t e = hipGetDevice(&pl->device);
     if (e != hipSuccess)
         return hip_fail("hipGetDevice", e);
-    e = hipMalloc(&pl->dmem, total);
-    if (e == hipErrorOutOfMemory) {
-        pl->dmem = nullptr;
-        return fail(SPCONV_E_NOMEM, "hipMalloc of " + std::to_string(total) + " bytes: out of memory");
-    }
-    if (e != hipSuccess) {
-        pl->dmem = nullptr;
-        return hip_fail("hipMalloc", e);
+    void *dest = nullptr;
+    if (use_static) {
+        if (pl->device < 0 || pl->device >= kMaxStaticDevices)
+            return fail(SPCONV_E_UNSUPPORTED, "device " + std::to_string(pl->device) + " is beyond the static arrays");
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        StaticArray &sa = g_static[pl->device];
+        if (!sa.ptr) {
+            // once per device, with it current: the device address of its copy of the array
+            void *ptr = nullptr;
+            e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+            if (e != hipSuccess)
+                return hip_fail("hipGetSymbolAddress (static plan array)", e);
+            sa.ptr = ptr;
+        }
+        dest = sa.ptr;
+        pl->static_gen = ++sa.gen;
+    } else {
+        e = hipMalloc(&pl->dmem, total);
+        if (e == hipErrorOutOfMemory) {
+            pl->dmem = nullptr;
+            return fail(SPCONV_E_NOMEM, "hipMalloc of " + std::to_string(total) + " bytes: out of memory");
+        }
+        if (e != hipSuccess) {
+            pl->dmem = nullptr;
+            return hip_fail("hipMalloc", e);
+        }
+        dest = pl->dmem;
     }
     pl->dbytes = total;
-    std::string image(total, '\0');
+    std::string image(total, '\0');  // the error word (and every padding byte) starts at zero
     for (const Part &p : parts)
         if (p.bytes)
             std::memcpy(&image[p.off], p.src, p.bytes);
-    e = hipMemcpy(pl->dmem, image.data(), total, hipMemcpyHostToDevice);
+    e = hipMemcpy(dest, image.data(), total, hipMemcpyHostToDevice);
     if (e != hipSuccess)
         return hip_fail("hipMemcpy (plan upload)", e);
-    char *base = static_cast<char *>(pl->dmem);
+    char *base = static_cast<char *>(dest);
     spconv::DevicePlan &d = pl->dev;
     d.idx = reinterpret_cast<const int32_t *>(base + parts[0].off);
     d.val = reinterpret_cast<const float *>(base + parts[1].off);
@@ -214,7 +258,8 @@ bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) 
 }
 
 // Plan creation shared by every entry point: options, planning, upload.
-spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spconv_options *opts) {
+spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spconv_options *opts,
+                          bool use_static = false) {
     if (!out)
         return fail(SPCONV_E_ARG, "out is NULL");
     *out = nullptr;
@@ -227,6 +272,8 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
     }
     if (o.host_only != 0 && o.host_only != 1)
         return fail(SPCONV_E_ARG, "host_only must be 0 or 1");
+    if (use_static && o.host_only)
+        return fail(SPCONV_E_ARG, "a plan in the static device array cannot be host-only");
     spconv::Options po;
     po.reorder = o.reorder;
     po.host_only = o.host_only;
@@ -255,7 +302,7 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
     fill_device_geometry(pl);
     pl->host_only = o.host_only == 1;
     if (!pl->host_only) {
-        spconv_status us = upload(pl);
+        spconv_status us = upload(pl, use_static);
         if (us == SPCONV_OK) {
             hipError_t pe = spconv::prepare_launch(pl->dev);
             if (pe == hipSuccess && pl->dev.rslots > 0)
@@ -293,6 +340,15 @@ spconv_status spconv_plan_create_ex(spconv_plan *out, int32_t cout, int32_t cin,
                                     const spconv_options *opts) {
     g_err.clear();
     return create_plan(out, make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage), opts);
+}
+
+spconv_status spconv_plan_create_static(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
+                                        const int32_t *row_ptr, const int32_t *col_idx, const float *values,
+                                        const float *bias, spconv_act act, spconv_dtype storage,
+                                        const spconv_options *opts) {
+    g_err.clear();
+    return create_plan(out, make_input(cout, cin, block_rows, row_ptr, col_idx, values, bias, act, storage), opts,
+                       true);
 }
 
 spconv_status spconv_plan_create_fused(spconv_plan *out, int32_t cout, int32_t cin, int32_t block_rows,
@@ -505,6 +561,12 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
                     "h * w * channels too large: the images of one tile must span less than 2^31 bytes");
     if (plan->host_only)
         return fail(SPCONV_E_ARG, host_only_msg);
+    if (plan->static_gen) {
+        std::lock_guard<std::mutex> lock(g_static_mu);
+        if (g_static[plan->device].gen != plan->static_gen)
+            return fail(SPCONV_E_ARG, "a later spconv_plan_create_static on this device replaced the plan's "
+                                      "device image");
+    }
     int dev = -1;
     hipError_t he = hipGetDevice(&dev);
     if (he != hipSuccess)

@@ -32,7 +32,7 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
             "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked", "spconv_detect_blocks",
             "spconv_dense_to_bcsr_blocked", "spconv_plan_create_dense_blocked", "spconv_plan_unpack_indexed",
-            "spconv_plan_check", "spconv_plan_set_wait_limit")
+            "spconv_plan_check", "spconv_plan_set_wait_limit", "spconv_plan_create_static")
 
 
 class SpconvError(RuntimeError):
@@ -108,6 +108,9 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_unpack_interleaved.argtypes = [vp, vp, vp, vp]
     lib.spconv_plan_unpack_indexed.restype = i32
     lib.spconv_plan_unpack_indexed.argtypes = [vp, i32, vp, vp, vp]
+    lib.spconv_plan_create_static.restype = i32
+    lib.spconv_plan_create_static.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, i32,
+                                              ctypes.POINTER(spconv_options)]
     lib.spconv_plan_check.restype = i32
     lib.spconv_plan_check.argtypes = [vp, ctypes.POINTER(i32), i32]
     lib.spconv_plan_set_wait_limit.restype = i32
@@ -189,6 +192,31 @@ def spconv_plan_create(cout, cin, block_rows, row_ptr, col_idx, values, bias=Non
     else:
         status = lib.spconv_plan_create_ex(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
                                            _ptr(ci), _ptr(va), _ptr(bi), a, st, ctypes.byref(options))
+    if not check:
+        return status, out.value
+    _check(status)
+    return out.value
+
+
+SPCONV_STATIC_PLAN_BYTES = 32 << 20
+
+
+def spconv_plan_create_static(cout, cin, block_rows, row_ptr, col_idx, values, bias=None, act="none",
+                              storage="f32", options: Optional[spconv_options] = None, check: bool = True):
+    """As spconv_plan_create, with the plan's device image in the library's
+    static per-GPU array (no device allocation; only the last such plan on a
+    device can run).  Returns the plan handle (or (status, handle))."""
+    lib = load_library()
+    rp = _arr(row_ptr, np.int32)
+    ci = _arr(col_idx, np.int32)
+    va = _arr(values, np.float32)
+    bi = _arr(bias, np.float32)
+    out = ctypes.c_void_p()
+    a = _ACTS[act] if isinstance(act, str) else int(act)
+    st = _DTYPES[storage] if isinstance(storage, str) else int(storage)
+    status = lib.spconv_plan_create_static(ctypes.byref(out), int(cout), int(cin), int(block_rows), _ptr(rp),
+                                           _ptr(ci), _ptr(va), _ptr(bi), a, st,
+                                           ctypes.byref(options) if options is not None else None)
     if not check:
         return status, out.value
     _check(status)
