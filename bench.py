@@ -64,7 +64,7 @@ HBM_PEAK_GBS = 8000.0         # MI355X HBM3E peak
 FP32_VECTOR_PEAK_TFS = 157.3  # MI355X fp32 vector peak (packed FMA)
 TRAFFIC_BASE = os.path.join(ROOT, "profiles", "traffic_spmm_pipe_512x512_14x14_b256")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1911_09723_amd", "csrc", f)
-                  for f in ("spmm_kernels.hip", "spmm_indexed.hip", "planner.cpp", "planner.hpp")]
+                  for f in ("spmm_kernels.hip", "spmm_indexed.hip", "spmm_outer.hip", "planner.cpp", "planner.hpp")]
 COPY_BYTES = 256 << 20        # calibration copy: 256 MiB read + 256 MiB written
 CALIBRATION_KERNEL = "neg_kernel"  # torch.neg(a, out=b): a plain elementwise copy
 METRIC = "effective GFLOP/s (2*nnz*HW*N) + HBM GB/s % peak, sparse 1x1 conv"
@@ -567,11 +567,11 @@ def main():
     r = time_variant(layers["1x1"], args.steps, args.warmup, args.sets, dw=fused_layer(layers["1x1"]))
     results[tag] = summarize(layers["1x1"], r, dw=True)
     log("bench: %s %s" % (tag, json.dumps(results[tag])))
-    # the headline layers on the register-indexed kernel
-    for base in ("1x1", "1x4"):
-        tag = base + " indexed"
+    # the headline layers on the register-indexed kernel, and 1x4 on the outer-product kernel
+    for base, kern, name in (("1x1", 3, "indexed"), ("1x4", 3, "indexed"), ("1x4", 4, "outer")):
+        tag = base + " " + name
         log("bench: timing %s" % tag)
-        r = time_variant(layers[base], args.steps, args.warmup, args.sets, kernel=3)
+        r = time_variant(layers[base], args.steps, args.warmup, args.sets, kernel=kern)
         results[tag] = summarize(layers[base], r)
         log("bench: %s %s" % (tag, json.dumps(results[tag])))
 

@@ -112,7 +112,8 @@ SPCONV_API spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int3
  * other device, host-only plan), SPCONV_E_SHAPE (sizes beyond 2^31 columns or
  * elements beyond 2^62), SPCONV_E_UNSUPPORTED (the images one tile of output
  * columns touches, ((tile columns - 1) / (out_h * out_w) + 2) of them, span
- * 2^31 bytes or more of x or of y), SPCONV_E_HIP
+ * 2^31 bytes or more of x or of y; a plan made with kernel = 4 given h * w
+ * not a multiple of 4 or x, y not 16-byte aligned), SPCONV_E_HIP
  * (launch failure).  Every check on the arguments runs before any HIP call and
  * before a host-only plan is refused, so a host-only plan exercises them
  * without a device.  Faults during execution surface at the caller's next
@@ -280,11 +281,15 @@ typedef struct {
     int32_t host_only;   /* 1: plan on the host only, no device memory; spconv_run refuses it */
     int32_t kernel;      /* 0 = choose automatically: the LDS-strip or direct-load kernel, or, for
                             runs with enough columns on layers where it measured faster, the
-                            register-indexed kernel (spconv_plan_info.indexed_min_cols);
+                            register-indexed kernel (spconv_plan_info.indexed_min_cols) or the
+                            outer-product kernel (spconv_plan_info.outer_min_cols);
                             1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED when the strip of cin
                             channels does not fit in LDS); 2 = direct-load kernel; 3 =
                             register-indexed kernel (SPCONV_E_UNSUPPORTED for fp16 storage or a
-                            depthwise stage) */
+                            depthwise stage); 4 = outer-product kernel on the matrix cores
+                            (1 x 4 blocks, fp32, no depthwise stage, cin <= 632, else
+                            SPCONV_E_UNSUPPORTED; spconv_run then needs h * w a multiple of 4
+                            and 16-byte aligned x and y) */
     int32_t group_lanes; /* 0 = choose automatically; else 4, 8 or 16 lanes per (block) row: each
                             lane accumulates 16 / group_lanes vectors of 16 bytes of the tile's
                             columns, and a wavefront works on 64 / group_lanes rows at a time
@@ -403,6 +408,8 @@ typedef struct {
     int64_t indexed_min_cols; /* kernel chosen automatically: runs of at least this many output columns
                                  (N * out_h * out_w) take the register-indexed kernel; 0 = never (and
                                  for host-only plans, which know no device) */
+    int64_t outer_min_cols;   /* the same for the outer-product kernel, which takes precedence; it
+                                 also needs h * w a multiple of 4 and 16-byte aligned x and y */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */
@@ -440,6 +447,19 @@ SPCONV_API spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_
  */
 SPCONV_API spconv_status spconv_plan_unpack_indexed(spconv_plan plan, int32_t from_pairs, int32_t *row_ptr,
                                                     int32_t *col_idx, float *values);
+
+/*
+ * The same reconstruction from the outer-product kernel's records (Sec. 3.2:
+ * 1 x 4 output-channel blocks; the octs of 8 block rows in lockstep, their
+ * records of (weight, LDS channel offset) per lane slot and step, the zero-row
+ * padding, and the per-tile-parity wave lists, all checked as the kernel
+ * walks them).  row_ptr, col_idx, values as for spconv_plan_unpack (each may
+ * be NULL).  Host only.  SPCONV_E_FORMAT (message set) when the records are
+ * inconsistent or the plan has none (not 1 x 4 blocks, fp16 storage,
+ * depthwise stage, cin above 632).
+ */
+SPCONV_API spconv_status spconv_plan_unpack_outer(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
+                                                  float *values);
 
 /*
  * For callers that cannot allocate device memory (code that must not call

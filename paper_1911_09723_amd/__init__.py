@@ -33,6 +33,7 @@ from .spconv import (  # noqa: F401
     spconv_plan_unpack,
     spconv_plan_unpack_interleaved,
     spconv_plan_unpack_indexed,
+    spconv_plan_unpack_outer,
     spconv_plan_check,
     spconv_plan_set_wait_limit,
     SPCONV_FLAG_WAIT_GAVE_UP,

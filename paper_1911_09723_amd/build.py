@@ -21,7 +21,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OBJDIR = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libspconv.so")
 
-SOURCES = ["planner.cpp", "spconv_api.cpp", "spmm_kernels.hip", "spmm_indexed.hip", "net_kernels.hip"]
+SOURCES = ["planner.cpp", "spconv_api.cpp", "spmm_kernels.hip", "spmm_indexed.hip", "spmm_outer.hip", "net_kernels.hip"]
 ARCH = "gfx950"
 
 COMMON = [

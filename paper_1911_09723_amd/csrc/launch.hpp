@@ -64,6 +64,16 @@ struct DevicePlan {
     int32_t spin_limit = 1 << 22;       // bound of those waits, in sleeps
     int64_t indexed_min_cols = 0;       // automatic choice: runs of at least this many columns take the
                                         // register-indexed kernel (0: never)
+    // outer-product kernel (planner.hpp)
+    int32_t use_outer = 0, oocts = 0, owaves = 0, ozrow = 0;
+    const uint32_t *orec = nullptr;
+    const uint32_t *ooff = nullptr;
+    int32_t ooff_bytes = 0;             // the offset table including its read-ahead quads
+    const int32_t *ooct = nullptr;
+    const int32_t *owave_ptr = nullptr;
+    const int32_t *owave_oct = nullptr;
+    int64_t outer_min_cols = 0;         // automatic choice: runs of at least this many columns (with H*W a
+                                        // multiple of 4 and 16-byte aligned X and Y) take it (0: never)
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`
@@ -86,6 +96,15 @@ hipError_t prepare_indexed(const DevicePlan &p);
 // One launch of the register-indexed kernel over all m = N * hw columns.
 hipError_t launch_indexed(const DevicePlan &p, const float *x, float *y, int32_t m, int32_t hw, int64_t x_bytes,
                           int64_t y_bytes, hipStream_t stream);
+
+// Once per plan: allow the outer-product kernel its LDS.
+hipError_t prepare_outer(const DevicePlan &p);
+// LDS bytes of one outer-product workgroup.
+int32_t outer_lds_bytes(const DevicePlan &p);
+// One launch of the outer-product kernel over all m = N * hw columns; hw must
+// be a multiple of 4 and x, y 16-byte aligned.
+hipError_t launch_outer(const DevicePlan &p, const float *x, float *y, int32_t m, int32_t hw, int64_t x_bytes,
+                        hipStream_t stream);
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when
 // needed and record num_cus and blocks_per_cu.

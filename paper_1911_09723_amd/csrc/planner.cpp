@@ -609,9 +609,14 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         in.values = xvalues.data();
         in.block_cols = 1;
     }
-    if (opt.kernel < 0 || opt.kernel > 3) {
-        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct) or 3 (register-indexed)";
+    if (opt.kernel < 0 || opt.kernel > 4) {
+        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct), 3 (register-indexed) or 4 (outer-product)";
         return E_ARG;
+    }
+    if (opt.kernel == 4 && !outer_supported(in)) {
+        err = "the outer-product kernel runs fp32 plans of 1 x 4 blocks without a depthwise stage and with cin <= " +
+              std::to_string(kOuterMaxCin);
+        return E_UNSUPPORTED;
     }
     if (opt.kernel == 3 && (in.dw_stride || in.storage != 0)) {
         err = "the register-indexed kernel runs fp32 plans without a depthwise stage";
@@ -653,7 +658,7 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     p.storage = in.storage;
     p.kc = in_arg.block_cols;
     Options gopt = opt;
-    if (gopt.kernel == 3)
+    if (gopt.kernel == 3 || gopt.kernel == 4)
         gopt.kernel = 0;
     st = choose_geometry(in, gopt, p, err);
     if (st != OK)
@@ -692,6 +697,10 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         p.use_indexed = opt.kernel == 3;
         p.rlane_cols = opt.lane_cols;
         p.auto_kernel = opt.kernel == 0;
+    }
+    if (outer_supported(in) && (opt.kernel == 0 || opt.kernel == 4)) {
+        build_outer(in, p);
+        p.use_outer = opt.kernel == 4;
     }
 
     // 2. bundles of NB consecutive rows in that order, each a whole number of
@@ -1271,6 +1280,206 @@ Status unpack_indexed(const PackedPlan &p, bool from_pairs, int32_t *row_ptr, in
         if (row_ptr)
             row_ptr[r + 1] = acc;
     }
+    return OK;
+}
+
+}  // namespace spconv
+
+namespace spconv {
+
+// Outer-product kernel: octs, records, wave lists (planner.hpp).
+bool outer_supported(const Input &in) {
+    return in.block_rows == 4 && in.storage == 0 && in.dw_stride == 0 && in.cin >= 1 && in.cin <= kOuterMaxCin;
+}
+
+void build_outer(const Input &in, PackedPlan &p) {
+    const int32_t k = in.block_rows;
+    const int32_t rows = in.cout / k;
+    auto len = [&](int32_t r) { return in.row_ptr[r + 1] - in.row_ptr[r]; };
+    std::vector<int32_t> order(rows);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return len(a) > len(b); });
+    const int32_t O = (rows + kOctRows - 1) / kOctRows;
+    p.oocts = O;
+    p.ozrow = (in.cin + 7) / 8 * 8;
+    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * kOuterRowBytes);
+    p.orec.clear();
+    p.ooff.clear();
+    p.ooct_tab.assign(static_cast<size_t>(O) * kOctWords, 0);
+    std::vector<int64_t> steps(O);
+    int32_t quads = 0;
+    for (int32_t o = 0; o < O; ++o) {
+        int32_t l = 0;
+        for (int32_t g = 0; g < kOctRows && o * kOctRows + g < rows; ++g)
+            l = std::max(l, len(order[o * kOctRows + g]));
+        const int32_t nq = std::max<int32_t>(1, (l + kOuterQuadSteps - 1) / kOuterQuadSteps);
+        steps[o] = int64_t(kOuterQuadSteps) * nq;
+        int32_t *tab = &p.ooct_tab[static_cast<size_t>(o) * kOctWords];
+        tab[0] = quads;
+        tab[1] = nq;
+        quads += nq;
+        for (int32_t g = 0; g < kOctRows; ++g)
+            tab[2 + g] = o * kOctRows + g < rows ? order[o * kOctRows + g] : -1;
+        for (int32_t j = 0; j < nq; ++j) {
+            for (int32_t u = 0; u < kOuterSlots; ++u) {
+                const int32_t g = u / 4, t = u % 4, rb = tab[2 + g];
+                for (int32_t h = 0; h < kOuterQuadSteps; ++h) {
+                    const int32_t s = kOuterQuadSteps * j + h;
+                    uint32_t w = 0;
+                    if (rb >= 0 && s < len(rb)) {
+                        const float v = in.values[(static_cast<int64_t>(in.row_ptr[rb]) + s) * k + t];
+                        std::memcpy(&w, &v, 4);
+                    }
+                    p.orec.push_back(w);
+                }
+            }
+            for (int32_t g = 0; g < kOctRows; ++g) {
+                const int32_t rb = tab[2 + g];
+                for (int32_t h = 0; h < kOuterQuadSteps; ++h) {
+                    const int32_t s = kOuterQuadSteps * j + h;
+                    p.ooff.push_back(rb >= 0 && s < len(rb)
+                                         ? static_cast<uint32_t>(in.col_idx[in.row_ptr[rb] + s] * kOuterRowBytes)
+                                         : zoff);
+                }
+            }
+        }
+    }
+    p.orec.insert(p.orec.end(), static_cast<size_t>(kOuterAhead) * kOuterSlots * 4, 0u);
+    p.ooff.insert(p.ooff.end(), static_cast<size_t>(kOuterAhead) * kOctRows * 4, zoff);
+
+    // wave lists: even tiles, then odd tiles continuing from the even loads
+    const int32_t W = std::min<int32_t>(kMaxWaves, O);
+    p.owaves = W;
+    std::vector<int32_t> by_len(O);
+    std::iota(by_len.begin(), by_len.end(), 0);
+    std::stable_sort(by_len.begin(), by_len.end(), [&](int32_t a, int32_t b) { return steps[a] > steps[b]; });
+    std::vector<int64_t> load(W, 0);
+    std::vector<std::vector<int32_t>> lists(2 * W);
+    for (int32_t q = 0; q < 2; ++q)
+        for (int32_t o : by_len) {
+            int32_t best = 0;
+            for (int32_t w = 1; w < W; ++w)
+                if (load[w] < load[best])
+                    best = w;
+            lists[q * W + best].push_back(o);
+            load[best] += steps[o];
+        }
+    p.owave_ptr.assign(2 * W + 1, 0);
+    p.owave_oct.clear();
+    for (int32_t i = 0; i < 2 * W; ++i) {
+        p.owave_ptr[i] = static_cast<int32_t>(p.owave_oct.size());
+        p.owave_oct.insert(p.owave_oct.end(), lists[i].begin(), lists[i].end());
+    }
+    p.owave_ptr[2 * W] = static_cast<int32_t>(p.owave_oct.size());
+    if (p.rrow_bias.size() != static_cast<size_t>(in.cout)) {
+        p.rrow_bias.assign(in.cout, 0.0f);
+        if (in.bias)
+            std::copy(in.bias, in.bias + in.cout, p.rrow_bias.begin());
+    }
+}
+
+Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, std::string &err) {
+    if (p.oocts == 0) {
+        err = "the plan has no outer-product records";
+        return E_FORMAT;
+    }
+    const int32_t k = 4, rows = p.cout / k, O = p.oocts, W = p.owaves;
+    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * kOuterRowBytes);
+    if (p.ozrow != (p.cin + 7) / 8 * 8 || static_cast<int32_t>(p.ooct_tab.size()) != O * kOctWords ||
+        static_cast<int32_t>(p.owave_ptr.size()) != 2 * W + 1) {
+        err = "outer-product tables have the wrong size";
+        return E_FORMAT;
+    }
+    // every oct exactly once per tile parity
+    for (int32_t q = 0; q < 2; ++q) {
+        std::vector<int32_t> seen(O, 0);
+        for (int32_t i = p.owave_ptr[q * W]; i < p.owave_ptr[q * W + W]; ++i) {
+            const int32_t o = p.owave_oct[i];
+            if (o < 0 || o >= O || seen[o]++) {
+                err = "wave lists do not cover every oct once per tile parity";
+                return E_FORMAT;
+            }
+        }
+        if (std::count(seen.begin(), seen.end(), 1) != O) {
+            err = "wave lists miss an oct";
+            return E_FORMAT;
+        }
+    }
+    struct Blk {
+        int32_t c;
+        float w[4];
+    };
+    std::vector<std::vector<Blk>> got(rows);
+    std::vector<int32_t> owner(rows, 0);
+    int64_t next_quad = 0;
+    for (int32_t o = 0; o < O; ++o) {
+        const int32_t *tab = &p.ooct_tab[static_cast<size_t>(o) * kOctWords];
+        const int64_t q0 = tab[0], nq = tab[1];
+        if (q0 != next_quad || nq < 1 ||
+            (q0 + nq + kOuterAhead) * kOuterSlots * 4 > static_cast<int64_t>(p.orec.size()) ||
+            (q0 + nq + kOuterAhead) * kOctRows * 4 > static_cast<int64_t>(p.ooff.size())) {
+            err = "oct " + std::to_string(o) + ": records out of order or out of range";
+            return E_FORMAT;
+        }
+        next_quad = q0 + nq;
+        for (int32_t g = 0; g < kOctRows; ++g) {
+            const int32_t rb = tab[2 + g];
+            if (rb < -1 || rb >= rows || (rb >= 0 && owner[rb]++)) {
+                err = "oct " + std::to_string(o) + ": bad or repeated block row";
+                return E_FORMAT;
+            }
+            bool padding = rb < 0;
+            int32_t last_c = -1;
+            for (int64_t s = 0; s < kOuterQuadSteps * nq; ++s) {
+                const int64_t j = q0 + s / kOuterQuadSteps, h = s % kOuterQuadSteps;
+                Blk b{};
+                for (int32_t t = 0; t < 4; ++t)
+                    std::memcpy(&b.w[t], &p.orec[static_cast<size_t>((j * kOuterSlots + 4 * g + t) * 4 + h)], 4);
+                const uint32_t off = p.ooff[static_cast<size_t>((j * kOctRows + g) * 4 + h)];
+                if (off == zoff) {
+                    if (b.w[0] != 0.0f || b.w[1] != 0.0f || b.w[2] != 0.0f || b.w[3] != 0.0f) {
+                        err = "oct " + std::to_string(o) + ": padding step with a nonzero weight";
+                        return E_FORMAT;
+                    }
+                    padding = true;
+                    continue;
+                }
+                if (padding || off % kOuterRowBytes || static_cast<int32_t>(off / kOuterRowBytes) >= p.cin ||
+                    static_cast<int32_t>(off / kOuterRowBytes) <= last_c) {
+                    err = "oct " + std::to_string(o) + ": block after padding, bad offset or channels not ascending";
+                    return E_FORMAT;
+                }
+                b.c = static_cast<int32_t>(off / kOuterRowBytes);
+                last_c = b.c;
+                got[rb].push_back(b);
+            }
+        }
+    }
+    if (static_cast<int64_t>(p.orec.size()) != (next_quad + kOuterAhead) * kOuterSlots * 4 ||
+        static_cast<int64_t>(p.ooff.size()) != (next_quad + kOuterAhead) * kOctRows * 4) {
+        err = "record arrays' lengths do not match the octs";
+        return E_FORMAT;
+    }
+    for (int32_t rb = 0; rb < rows; ++rb)
+        if (!owner[rb]) {
+            err = "block row " + std::to_string(rb) + " is in no oct";
+            return E_FORMAT;
+        }
+    int64_t nz = 0;
+    for (int32_t rb = 0; rb < rows; ++rb) {
+        if (row_ptr)
+            row_ptr[rb] = static_cast<int32_t>(nz);
+        for (const Blk &b : got[rb]) {
+            if (col_idx)
+                col_idx[nz] = b.c;
+            if (values)
+                for (int32_t t = 0; t < 4; ++t)
+                    values[nz * 4 + t] = b.w[t];
+            ++nz;
+        }
+    }
+    if (row_ptr)
+        row_ptr[rows] = static_cast<int32_t>(nz);
     return OK;
 }
 

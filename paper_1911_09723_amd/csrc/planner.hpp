@@ -161,6 +161,47 @@ inline int32_t flag_word(int32_t k) { return k == 1 ? 7 : 3; }
 constexpr uint32_t kLastOfChunk = 1u;
 constexpr uint32_t kLastOfStream = 2u;
 
+// Outer-product kernel (KERNEL_OUTER, 1 x 4 blocks, fp32): a stored block
+// times a 4-column X vector is a 4 x 4 outer product, and the matrix cores'
+// fp32 4x4x1 instruction computes 16 of them at once, each from its own block
+// of 4 lanes (register r of lane 4b + t gets A[4b + r] * B[4b + t] + C, one
+// rounding, like a fused multiply-add).
+//
+//   Tiles.  kOuterCols = 32 consecutive output columns; the tile's X rows
+//   (kOuterRowBytes = 128 bytes each: channel c at byte c * 128, then unused
+//   rows up to ozrow = cin rounded up to 8, then one row of zeros) fill one of
+//   two LDS buffers.
+//   Octs.  Block rows sorted by stored blocks (descending, ties by row index)
+//   are taken kOctRows = 8 at a time.  Group g of a wavefront (lanes 8g ..
+//   8g + 7, two lane blocks) works on block row g of its oct; the 8 rows move
+//   in lockstep, one stored block each per step, in ascending channel, for
+//   4 * nquads steps (the longest row rounded up to whole quads of 4 steps,
+//   at least one); a row past its last block reads the zero row with weight 0.
+//   Records, per oct and quad j of steps 4j .. 4j + 3:
+//     orec  per slot u = 4g + t (32 slots), four words: the weight of element
+//           t of block row g's block at each of the 4 steps (fp32 bits, 0 for
+//           padding).  Lanes 8g + t and 8g + 4 + t read slot 4g + t.
+//     ooff  per group g (8), four words: the LDS byte offset of the channel
+//           row each of the 4 steps reads (channel * 128; padding ozrow * 128).
+//   Oct o's quads start at quad ooct_tab[kOctWords * o] of both arrays and run
+//   ooct_tab[.. + 1] quads; words 2 .. 9 hold its block rows (-1: none).  Both
+//   arrays end with kOuterAhead zero quads (read ahead, unused).
+//   Waves.  The octs are dealt to owaves wavefronts twice, longest first to
+//   the least loaded: once for even tiles, then again for odd tiles starting
+//   from the even loads, so each wavefront's two-tile total is balanced.  Wave
+//   w's octs for tiles of parity q are owave_oct[owave_ptr[q * owaves + w] ..
+//   owave_ptr[q * owaves + w + 1]).
+constexpr int32_t kOuterCols = 32;
+constexpr int32_t kOuterRowBytes = 128;
+constexpr int32_t kOctRows = 8;
+constexpr int32_t kOctWords = 16;
+constexpr int32_t kOuterAhead = 4;   // quads of records read ahead
+constexpr int32_t kOuterQuadSteps = 4;
+constexpr int32_t kOuterSlots = 32;
+// Widest input the outer-product kernel takes: two buffers of (ozrow + 1) rows
+// and the control words within one workgroup's LDS.
+constexpr int32_t kOuterMaxCin = 632;
+
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
     // input channels per block (Fig. 5: 4x1 and 2x2 blocks beside 1x4): block t
@@ -188,7 +229,7 @@ struct Input {
 struct Options {
     int32_t reorder = 1;
     int32_t host_only = 0;
-    int32_t kernel = 0;       // 0 automatic, 1 strip, 2 direct, 3 register-indexed
+    int32_t kernel = 0;       // 0 automatic, 1 strip, 2 direct, 3 register-indexed, 4 outer-product
     int32_t group_lanes = 0;  // 0 automatic, else 4, 8 or 16 lanes per block row
     int32_t waves = 0;        // 0 automatic, else 1 .. 16 wavefronts per workgroup
     int32_t pipe_sets = 0;    // 0 automatic, else 1 or 2 bundles interleaved per wavefront
@@ -252,6 +293,17 @@ struct PackedPlan {
     std::vector<int32_t> rpair_ptr;
     std::vector<uint32_t> rpair_ent;
     std::vector<float> rrow_bias;  // bias of every output channel (the row-pair phase)
+    // outer-product kernel (planner.hpp, "Outer-product kernel"); empty when
+    // the plan cannot use it
+    int32_t use_outer = 0;   // spconv_run launches the outer-product kernel
+    int32_t oocts = 0;       // octs of kOctRows block rows
+    int32_t owaves = 0;      // wavefronts per workgroup
+    int32_t ozrow = 0;       // LDS row of zeros (cin rounded up to 8)
+    std::vector<uint32_t> orec;
+    std::vector<uint32_t> ooff;
+    std::vector<int32_t> ooct_tab;
+    std::vector<int32_t> owave_ptr;
+    std::vector<int32_t> owave_oct;
     std::vector<int32_t> perm;     // block rows in processing order
     std::vector<int32_t> row_nnz;  // stored blocks per block row (host only; for unpacking)
     // statistics
@@ -312,6 +364,16 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
 // r* of PackedPlan) from 1 x k block-CSR arrays; `order` lists the block rows
 // in processing order.
 void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPlan &p);
+
+// Whether the outer-product kernel can run this layer (1 x 4 blocks, fp32,
+// no depthwise stage, cin <= kOuterMaxCin).
+bool outer_supported(const Input &in);
+// Build its octs, records and wave lists (fields o* of PackedPlan).
+void build_outer(const Input &in, PackedPlan &p);
+// Rebuild block-CSR arrays from the outer-product records, checking their
+// structure (lockstep padding, ascending channels, offsets, wave lists).
+// E_FORMAT with `err` set when inconsistent or absent.
+Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, std::string &err);
 
 // Rebuild block-CSR arrays from the register-indexed records (and separately
 // from the row pairs), checking the stream structure: batch alignment of

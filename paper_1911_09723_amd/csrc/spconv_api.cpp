@@ -101,7 +101,7 @@ spconv_status upload(spconv_plan_s *pl, bool use_static) {
         const void *src;
         size_t bytes;
         size_t off;
-    } parts[21] = {
+    } parts[26] = {
         {h.idx.data(), h.idx.size() * sizeof(int32_t), 0},
         {h.val.data(), h.val.size() * sizeof(float), 0},
         {h.hdr.data(), h.hdr.size() * sizeof(int32_t), 0},
@@ -123,6 +123,11 @@ spconv_status upload(spconv_plan_s *pl, bool use_static) {
         {h.rpair_ent.data(), h.rpair_ent.size() * sizeof(uint32_t), 0},
         {h.rrow_bias.data(), h.rrow_bias.size() * sizeof(float), 0},
         {nullptr, 0, 0},  // the error flag word (zeroed)
+        {h.orec.data(), h.orec.size() * sizeof(uint32_t), 0},
+        {h.ooct_tab.data(), h.ooct_tab.size() * sizeof(int32_t), 0},
+        {h.owave_ptr.data(), h.owave_ptr.size() * sizeof(int32_t), 0},
+        {h.owave_oct.data(), h.owave_oct.size() * sizeof(int32_t), 0},
+        {h.ooff.data(), h.ooff.size() * sizeof(uint32_t), 0},
     };
     size_t total = 0;
     for (Part &p : parts) {
@@ -197,6 +202,11 @@ spconv_status upload(spconv_plan_s *pl, bool use_static) {
     d.rpair_ent_words = static_cast<int64_t>(h.rpair_ent.size());
     d.rrow_bias = reinterpret_cast<const float *>(base + parts[19].off);
     d.flag = reinterpret_cast<int32_t *>(base + parts[20].off);
+    d.orec = reinterpret_cast<const uint32_t *>(base + parts[21].off);
+    d.ooct = reinterpret_cast<const int32_t *>(base + parts[22].off);
+    d.owave_ptr = reinterpret_cast<const int32_t *>(base + parts[23].off);
+    d.owave_oct = reinterpret_cast<const int32_t *>(base + parts[24].off);
+    d.ooff = reinterpret_cast<const uint32_t *>(base + parts[25].off);
     return SPCONV_OK;
 }
 
@@ -250,6 +260,11 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.rwaves = h.rwaves;
     d.rnch = h.rnch;
     d.rlane_cols = h.rlane_cols;
+    d.use_outer = h.use_outer;
+    d.oocts = h.oocts;
+    d.owaves = h.owaves;
+    d.ozrow = h.ozrow;
+    d.ooff_bytes = static_cast<int32_t>(h.ooff.size() * sizeof(uint32_t));
 }
 
 bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) {
@@ -307,6 +322,8 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
             hipError_t pe = spconv::prepare_launch(pl->dev);
             if (pe == hipSuccess && pl->dev.rslots > 0)
                 pe = spconv::prepare_indexed(pl->dev);
+            if (pe == hipSuccess && pl->dev.oocts > 0)
+                pe = spconv::prepare_outer(pl->dev);
             pl->dev.indexed_min_cols = indexed_min_cols(pl->host, pl->dev);
             if (pe != hipSuccess)
                 us = hip_fail("kernel launch set-up", pe);
@@ -553,8 +570,16 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     // the kernels address X and Y relative to the first image of a tile with
     // 32-bit byte offsets: the images one tile's columns touch (at most
     // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
-    const bool indexed = plan->dev.use_indexed || (plan->dev.indexed_min_cols > 0 && m >= plan->dev.indexed_min_cols);
-    const int64_t tile_cols = indexed ? 64 * 6 : p.tile_cols;
+    // the outer-product kernel reads and writes whole 16-byte vectors of 4 columns
+    const bool outer_fits = hw % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                            reinterpret_cast<uintptr_t>(y) % 16 == 0;
+    if (p.use_outer && !outer_fits)
+        return fail(SPCONV_E_UNSUPPORTED, "the outer-product kernel (kernel = 4) needs h * w (after the depthwise "
+                                          "stage) a multiple of 4 and 16-byte aligned x and y");
+    const bool outer = p.use_outer || (outer_fits && plan->dev.outer_min_cols > 0 && m >= plan->dev.outer_min_cols);
+    const bool indexed = !outer && (plan->dev.use_indexed ||
+                                    (plan->dev.indexed_min_cols > 0 && m >= plan->dev.indexed_min_cols));
+    const int64_t tile_cols = outer ? spconv::kOuterCols : indexed ? 64 * 6 : p.tile_cols;
     const int64_t span = (tile_cols - 1) / hw + 2;
     if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,
@@ -577,7 +602,11 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    if (indexed)
+    if (outer)
+        he = spconv::launch_outer(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
+                                  static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),
+                                  static_cast<hipStream_t>(stream));
+    else if (indexed)
         he = spconv::launch_indexed(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
                                     static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),
                                     yel * static_cast<int64_t>(e), static_cast<hipStream_t>(stream));
@@ -733,6 +762,7 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->dw_act = p.dw_act;
     info->block_cols = p.kc;
     info->indexed_min_cols = plan->host_only ? 0 : plan->dev.indexed_min_cols;
+    info->outer_min_cols = plan->host_only ? 0 : plan->dev.outer_min_cols;
     return SPCONV_OK;
 }
 
@@ -793,6 +823,31 @@ spconv_status spconv_plan_unpack_interleaved(spconv_plan plan, int32_t *row_ptr,
         std::vector<int32_t> rp(p.cout / p.k + 1), ci(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1)));
         std::vector<float> va(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1) * p.k));
         const spconv::Status st = spconv::unpack_interleaved(p, rp.data(), ci.data(), va.data(), err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        reblock(p, rp, ci, va, row_ptr, col_idx, values);
+    } catch (const std::bad_alloc &) {
+        return fail(SPCONV_E_NOMEM, "host allocation failed while unpacking");
+    }
+    return SPCONV_OK;
+}
+
+spconv_status spconv_plan_unpack_outer(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx, float *values) {
+    g_err.clear();
+    if (!plan)
+        return fail(SPCONV_E_ARG, "plan is NULL");
+    std::string err;
+    const spconv::PackedPlan &p = plan->host;
+    if (p.kc == 1) {
+        const spconv::Status st = spconv::unpack_outer(p, row_ptr, col_idx, values, err);
+        if (st != spconv::OK)
+            return fail(static_cast<spconv_status>(st), err);
+        return SPCONV_OK;
+    }
+    try {
+        std::vector<int32_t> rp(p.cout / p.k + 1), ci(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1)));
+        std::vector<float> va(static_cast<size_t>(std::max<int64_t>(p.nnzb, 1) * p.k));
+        const spconv::Status st = spconv::unpack_outer(p, rp.data(), ci.data(), va.data(), err);
         if (st != spconv::OK)
             return fail(static_cast<spconv_status>(st), err);
         reblock(p, rp, ci, va, row_ptr, col_idx, values);

@@ -565,7 +565,7 @@ __device__ __forceinline__ void copy_share(const Args &a, const typename Geo<G, 
         asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                      :
                      : "s"(m0), "v"(voff), "s"(rs)
-                     : "memory");
+                     : "memory", "m0");
     }
 }
 

@@ -32,7 +32,8 @@ EXPORTED = ("spconv_plan_create", "spconv_run", "spconv_destroy", "spconv_last_e
             "spconv_plan_create_dense", "spconv_plan_create_fused", "spconv_conv3x3_hwc", "spconv_depthwise3x3",
             "spconv_global_avg_pool", "spconv_linear", "spconv_plan_create_blocked", "spconv_detect_blocks",
             "spconv_dense_to_bcsr_blocked", "spconv_plan_create_dense_blocked", "spconv_plan_unpack_indexed",
-            "spconv_plan_check", "spconv_plan_set_wait_limit", "spconv_plan_create_static")
+            "spconv_plan_check", "spconv_plan_set_wait_limit", "spconv_plan_create_static",
+            "spconv_plan_unpack_outer")
 
 
 class SpconvError(RuntimeError):
@@ -58,7 +59,8 @@ class spconv_plan_info(ctypes.Structure):
                 ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32),
-                ("block_cols", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("indexed_min_cols", ctypes.c_int64)]
+                ("block_cols", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("indexed_min_cols", ctypes.c_int64),
+                ("outer_min_cols", ctypes.c_int64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -108,6 +110,8 @@ def load_library(path: Optional[str] = None):
     lib.spconv_plan_unpack_interleaved.argtypes = [vp, vp, vp, vp]
     lib.spconv_plan_unpack_indexed.restype = i32
     lib.spconv_plan_unpack_indexed.argtypes = [vp, i32, vp, vp, vp]
+    lib.spconv_plan_unpack_outer.restype = i32
+    lib.spconv_plan_unpack_outer.argtypes = [vp, vp, vp, vp]
     lib.spconv_plan_create_static.restype = i32
     lib.spconv_plan_create_static.argtypes = [ctypes.POINTER(vp), i32, i32, i32, vp, vp, vp, vp, i32, i32,
                                               ctypes.POINTER(spconv_options)]
@@ -464,6 +468,18 @@ def spconv_plan_unpack_indexed(plan, from_pairs=False):
     ci = np.zeros(max(info["nnzb"], 1), np.int32)
     va = np.zeros(max(info["nnzb"] * per, 1), np.float32)
     _check(load_library().spconv_plan_unpack_indexed(plan, int(bool(from_pairs)), _ptr(rp), _ptr(ci), _ptr(va)))
+    return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per]
+
+
+def spconv_plan_unpack_outer(plan):
+    """Return (row_ptr, col_idx, values) rebuilt from the outer-product kernel's records."""
+    info = spconv_plan_get_info(plan)
+    rows = info["cout"] // info["block_rows"]
+    per = info["block_rows"] * info["block_cols"]
+    rp = np.zeros(rows + 1, np.int32)
+    ci = np.zeros(max(info["nnzb"], 1), np.int32)
+    va = np.zeros(max(info["nnzb"] * per, 1), np.float32)
+    _check(load_library().spconv_plan_unpack_outer(plan, _ptr(rp), _ptr(ci), _ptr(va)))
     return rp, ci[:info["nnzb"]], va[:info["nnzb"] * per]
 
 

@@ -137,7 +137,7 @@ def test_null_arrays_with_nonzeros_rejected():
 
 def test_options_validated():
     for kw in (dict(group_lanes=2), dict(group_lanes=12), dict(group_lanes=32), dict(group_lanes=-4),
-               dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=4),
+               dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=5),
                dict(kernel=-1), dict(pipe_sets=3), dict(pipe_sets=-1), dict(regions=5), dict(regions=-1)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw

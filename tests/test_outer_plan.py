@@ -1,0 +1,78 @@
+"""Host-only checks of the outer-product kernel's records (no GPU).
+
+fp32 plans of 1 x 4 blocks with at most 632 input channels are laid out a
+third time for the outer-product kernel: octs of 8 block rows in lockstep,
+per lane slot and step a (weight, LDS channel offset) record, padding steps
+that read the zero row with weight 0, and wave lists per tile parity.
+Walking the records back into block-CSR with the kernel's own bookkeeping
+(spconv_plan_unpack_outer, which also checks the padding, ascending
+channels, offsets and wave lists) must return the input exactly; plans the
+kernel cannot take carry no records, and asking for the kernel there is
+refused.
+"""
+
+import numpy as np
+import pytest
+
+import paper_1911_09723_amd as sp
+from synth import make_layer
+
+E_FORMAT, E_UNSUPPORTED = 2, 4
+
+
+def _host_plan(layer, **kw):
+    o = sp.spconv_options_init()
+    o.host_only = 1
+    for k, v in kw.items():
+        setattr(o, k, v)
+    if getattr(layer, "block_cols", 1) > 1:
+        return sp.spconv_plan_create_blocked(layer.cout, layer.cin, layer.block_rows, layer.block_cols,
+                                             layer.row_ptr, layer.col_idx, layer.values, layer.bias, layer.act,
+                                             layer.storage, options=o)
+    return sp.spconv_plan_create(layer.cout, layer.cin, layer.block_rows, layer.row_ptr, layer.col_idx,
+                                 layer.values, layer.bias, layer.act, layer.storage, options=o)
+
+
+CASES = [
+    # (cin, cout, sparsity, kc)
+    (512, 512, 0.9, 1),       # the 1x4 headline layer: 16 octs, one per wavefront and tile
+    (512, 512, 0.7, 1),
+    (632, 96, 0.9, 1),        # widest input; 3 octs, the last one partial
+    (17, 20, 0.5, 1),         # cin not a multiple of 8, one partial oct of 5 block rows
+    (200, 1024, 0.95, 1),     # 32 octs: two per wavefront per tile
+    (130, 64, 0.0, 1),        # dense
+    (64, 48, 1.0, 1),         # no stored blocks: every step is padding
+    (256, 128, 0.8, 2),       # 4x2 blocks expanded to single channels
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "%d-%d-s%g-kc%d" % c)
+def test_records_unpack_to_the_input(case):
+    cin, cout, s, kc = case
+    layer = make_layer(cin, cout, 1, 1, 1, s, block_rows=4, block_cols=kc, seed=cin + cout, with_x=False)
+    h = _host_plan(layer)
+    try:
+        rp, ci, va = sp.spconv_plan_unpack_outer(h)
+        assert np.array_equal(rp, layer.row_ptr)
+        assert np.array_equal(ci, layer.col_idx)
+        assert np.array_equal(va.view(np.uint32), layer.values.view(np.uint32))
+    finally:
+        sp.spconv_destroy(h)
+
+
+@pytest.mark.parametrize("case", [(512, 512, 0.9, 1, "f32"), (64, 64, 0.8, 2, "f32"), (64, 64, 0.8, 4, "f16"),
+                                  (640, 64, 0.9, 4, "f32")],
+                         ids=["k1", "k2", "f16", "cin640"])
+def test_plans_the_kernel_cannot_take(case):
+    cin, cout, s, k, st = case
+    layer = make_layer(cin, cout, 1, 1, 1, s, block_rows=k, storage=st, seed=5, with_x=False)
+    h = _host_plan(layer)
+    try:
+        with pytest.raises(sp.SpconvError) as e:
+            sp.spconv_plan_unpack_outer(h)
+        assert e.value.args[0].startswith("SPCONV_E_FORMAT")
+    finally:
+        sp.spconv_destroy(h)
+    with pytest.raises(sp.SpconvError) as e:
+        _host_plan(layer, kernel=4)
+    assert e.value.args[0].startswith("SPCONV_E_UNSUPPORTED")
