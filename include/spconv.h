@@ -112,8 +112,7 @@ SPCONV_API spconv_status spconv_plan_create(spconv_plan *out, int32_t cout, int3
  * other device, host-only plan), SPCONV_E_SHAPE (sizes beyond 2^31 columns or
  * elements beyond 2^62), SPCONV_E_UNSUPPORTED (the images one tile of output
  * columns touches, ((tile columns - 1) / (out_h * out_w) + 2) of them, span
- * 2^31 bytes or more of x or of y; a plan made with kernel = 4 given h * w
- * not a multiple of 4 or x, y not 16-byte aligned), SPCONV_E_HIP
+ * 2^31 bytes or more of x or of y), SPCONV_E_HIP
  * (launch failure).  Every check on the arguments runs before any HIP call and
  * before a host-only plan is refused, so a host-only plan exercises them
  * without a device.  Faults during execution surface at the caller's next
@@ -287,9 +286,8 @@ typedef struct {
                             channels does not fit in LDS); 2 = direct-load kernel; 3 =
                             register-indexed kernel (SPCONV_E_UNSUPPORTED for fp16 storage or a
                             depthwise stage); 4 = outer-product kernel on the matrix cores
-                            (1 x 4 blocks, fp32, no depthwise stage, cin <= 632, else
-                            SPCONV_E_UNSUPPORTED; spconv_run then needs h * w a multiple of 4
-                            and 16-byte aligned x and y) */
+                            (1 x 4 blocks, no depthwise stage, cin <= 632, else
+                            SPCONV_E_UNSUPPORTED) */
     int32_t group_lanes; /* 0 = choose automatically; else 4, 8 or 16 lanes per (block) row: each
                             lane accumulates 16 / group_lanes vectors of 16 bytes of the tile's
                             columns, and a wavefront works on 64 / group_lanes rows at a time
@@ -408,8 +406,7 @@ typedef struct {
     int64_t indexed_min_cols; /* kernel chosen automatically: runs of at least this many output columns
                                  (N * out_h * out_w) take the register-indexed kernel; 0 = never (and
                                  for host-only plans, which know no device) */
-    int64_t outer_min_cols;   /* the same for the outer-product kernel, which takes precedence; it
-                                 also needs h * w a multiple of 4 and 16-byte aligned x and y */
+    int64_t outer_min_cols;   /* the same for the outer-product kernel, which takes precedence */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */
@@ -455,8 +452,8 @@ SPCONV_API spconv_status spconv_plan_unpack_indexed(spconv_plan plan, int32_t fr
  * padding, and the per-tile-parity wave lists, all checked as the kernel
  * walks them).  row_ptr, col_idx, values as for spconv_plan_unpack (each may
  * be NULL).  Host only.  SPCONV_E_FORMAT (message set) when the records are
- * inconsistent or the plan has none (not 1 x 4 blocks, fp16 storage,
- * depthwise stage, cin above 632).
+ * inconsistent or the plan has none (not 1 x 4 blocks, depthwise stage,
+ * cin above 632).
  */
 SPCONV_API spconv_status spconv_plan_unpack_outer(spconv_plan plan, int32_t *row_ptr, int32_t *col_idx,
                                                   float *values);

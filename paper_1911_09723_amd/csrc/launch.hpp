@@ -72,8 +72,7 @@ struct DevicePlan {
     const int32_t *ooct = nullptr;
     const int32_t *owave_ptr = nullptr;
     const int32_t *owave_oct = nullptr;
-    int64_t outer_min_cols = 0;         // automatic choice: runs of at least this many columns (with H*W a
-                                        // multiple of 4 and 16-byte aligned X and Y) take it (0: never)
+    int64_t outer_min_cols = 0;         // automatic choice: runs of at least this many columns take it (0: never)
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`
@@ -101,10 +100,11 @@ hipError_t launch_indexed(const DevicePlan &p, const float *x, float *y, int32_t
 hipError_t prepare_outer(const DevicePlan &p);
 // LDS bytes of one outer-product workgroup.
 int32_t outer_lds_bytes(const DevicePlan &p);
-// One launch of the outer-product kernel over all m = N * hw columns; hw must
-// be a multiple of 4 and x, y 16-byte aligned.
-hipError_t launch_outer(const DevicePlan &p, const float *x, float *y, int32_t m, int32_t hw, int64_t x_bytes,
-                        hipStream_t stream);
+// One launch of the outer-product kernel over all m = N * hw columns (fp32 or
+// fp16 x and y as the plan's storage).  `vec` != 0 promises hw a multiple of
+// 4 and 16-byte aligned x and y (whole 4-column vectors per image).
+hipError_t launch_outer(const DevicePlan &p, const void *x, void *y, int32_t m, int32_t hw, int32_t vec,
+                        int64_t x_bytes, hipStream_t stream);
 
 // Once per plan, on its device: raise the kernel's dynamic-LDS limit when
 // needed and record num_cus and blocks_per_cu.

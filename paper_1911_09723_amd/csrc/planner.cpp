@@ -614,7 +614,7 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         return E_ARG;
     }
     if (opt.kernel == 4 && !outer_supported(in)) {
-        err = "the outer-product kernel runs fp32 plans of 1 x 4 blocks without a depthwise stage and with cin <= " +
+        err = "the outer-product kernel runs plans of 1 x 4 blocks without a depthwise stage and with cin <= " +
               std::to_string(kOuterMaxCin);
         return E_UNSUPPORTED;
     }
@@ -696,8 +696,8 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         build_indexed(in, p.perm, p);
         p.use_indexed = opt.kernel == 3;
         p.rlane_cols = opt.lane_cols;
-        p.auto_kernel = opt.kernel == 0;
     }
+    p.auto_kernel = opt.kernel == 0;
     if (outer_supported(in) && (opt.kernel == 0 || opt.kernel == 4)) {
         build_outer(in, p);
         p.use_outer = opt.kernel == 4;
@@ -1289,7 +1289,7 @@ namespace spconv {
 
 // Outer-product kernel: octs, records, wave lists (planner.hpp).
 bool outer_supported(const Input &in) {
-    return in.block_rows == 4 && in.storage == 0 && in.dw_stride == 0 && in.cin >= 1 && in.cin <= kOuterMaxCin;
+    return in.block_rows == 4 && in.dw_stride == 0 && in.cin >= 1 && in.cin <= kOuterMaxCin;
 }
 
 void build_outer(const Input &in, PackedPlan &p) {
@@ -1327,7 +1327,9 @@ void build_outer(const Input &in, PackedPlan &p) {
                     const int32_t s = kOuterQuadSteps * j + h;
                     uint32_t w = 0;
                     if (rb >= 0 && s < len(rb)) {
-                        const float v = in.values[(static_cast<int64_t>(in.row_ptr[rb]) + s) * k + t];
+                        float v = in.values[(static_cast<int64_t>(in.row_ptr[rb]) + s) * k + t];
+                        if (in.storage == 1)
+                            v = half_to_float(float_to_half_rne(v));
                         std::memcpy(&w, &v, 4);
                     }
                     p.orec.push_back(w);

@@ -161,7 +161,7 @@ inline int32_t flag_word(int32_t k) { return k == 1 ? 7 : 3; }
 constexpr uint32_t kLastOfChunk = 1u;
 constexpr uint32_t kLastOfStream = 2u;
 
-// Outer-product kernel (KERNEL_OUTER, 1 x 4 blocks, fp32): a stored block
+// Outer-product kernel (1 x 4 blocks, fp32 or fp16 storage): a stored block
 // times a 4-column X vector is a 4 x 4 outer product, and the matrix cores'
 // fp32 4x4x1 instruction computes 16 of them at once, each from its own block
 // of 4 lanes (register r of lane 4b + t gets A[4b + r] * B[4b + t] + C, one
@@ -179,8 +179,9 @@ constexpr uint32_t kLastOfStream = 2u;
 //   at least one); a row past its last block reads the zero row with weight 0.
 //   Records, per oct and quad j of steps 4j .. 4j + 3:
 //     orec  per slot u = 4g + t (32 slots), four words: the weight of element
-//           t of block row g's block at each of the 4 steps (fp32 bits, 0 for
-//           padding).  Lanes 8g + t and 8g + 4 + t read slot 4g + t.
+//           t of block row g's block at each of the 4 steps (fp32 bits of the
+//           weight, rounded to fp16 first for fp16 storage; 0 for padding).
+//           Lanes 8g + t and 8g + 4 + t read slot 4g + t.
 //     ooff  per group g (8), four words: the LDS byte offset of the channel
 //           row each of the 4 steps reads (channel * 128; padding ozrow * 128).
 //   Oct o's quads start at quad ooct_tab[kOctWords * o] of both arrays and run
@@ -365,8 +366,8 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
 // in processing order.
 void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPlan &p);
 
-// Whether the outer-product kernel can run this layer (1 x 4 blocks, fp32,
-// no depthwise stage, cin <= kOuterMaxCin).
+// Whether the outer-product kernel can run this layer (1 x 4 blocks, no
+// depthwise stage, cin <= kOuterMaxCin).
 bool outer_supported(const Input &in);
 // Build its octs, records and wave lists (fields o* of PackedPlan).
 void build_outer(const Input &in, PackedPlan &p);

@@ -228,6 +228,22 @@ int64_t indexed_min_cols(const spconv::PackedPlan &h, const spconv::DevicePlan &
     return 0;
 }
 
+// The automatic choice of the outer-product kernel (1 x 4 blocks), from its
+// measured times on MI355X over the workload layers: it wins once a run has
+// at least one round of its 32-column tiles over the compute units and the
+// octs average at least two quads (8 steps); with shorter rows (few input
+// channels) its per-tile costs dominate and the other kernels are faster.
+int64_t outer_min_cols(const spconv::PackedPlan &h, const spconv::DevicePlan &d) {
+    if (!h.auto_kernel || d.oocts == 0 || d.num_cus <= 0)
+        return 0;
+    int64_t quads = 0;
+    for (int32_t o = 0; o < h.oocts; ++o)
+        quads += h.ooct_tab[static_cast<size_t>(o) * spconv::kOctWords + 1];
+    if (quads < 2 * static_cast<int64_t>(h.oocts))
+        return 0;
+    return int64_t(spconv::kOuterCols) * d.num_cus;
+}
+
 void fill_device_geometry(spconv_plan_s *pl) {
     const spconv::PackedPlan &h = pl->host;
     spconv::DevicePlan &d = pl->dev;
@@ -325,6 +341,7 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
             if (pe == hipSuccess && pl->dev.oocts > 0)
                 pe = spconv::prepare_outer(pl->dev);
             pl->dev.indexed_min_cols = indexed_min_cols(pl->host, pl->dev);
+            pl->dev.outer_min_cols = outer_min_cols(pl->host, pl->dev);
             if (pe != hipSuccess)
                 us = hip_fail("kernel launch set-up", pe);
         }
@@ -570,13 +587,7 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     // the kernels address X and Y relative to the first image of a tile with
     // 32-bit byte offsets: the images one tile's columns touch (at most
     // (tile_cols - 1) / hw + 2 of them) must span less than 2^31 bytes of each
-    // the outer-product kernel reads and writes whole 16-byte vectors of 4 columns
-    const bool outer_fits = hw % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
-                            reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    if (p.use_outer && !outer_fits)
-        return fail(SPCONV_E_UNSUPPORTED, "the outer-product kernel (kernel = 4) needs h * w (after the depthwise "
-                                          "stage) a multiple of 4 and 16-byte aligned x and y");
-    const bool outer = p.use_outer || (outer_fits && plan->dev.outer_min_cols > 0 && m >= plan->dev.outer_min_cols);
+    const bool outer = p.use_outer || (plan->dev.outer_min_cols > 0 && m >= plan->dev.outer_min_cols);
     const bool indexed = !outer && (plan->dev.use_indexed ||
                                     (plan->dev.indexed_min_cols > 0 && m >= plan->dev.indexed_min_cols));
     const int64_t tile_cols = outer ? spconv::kOuterCols : indexed ? 64 * 6 : p.tile_cols;
@@ -603,9 +614,10 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
     if (outer)
-        he = spconv::launch_outer(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
-                                  static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),
-                                  static_cast<hipStream_t>(stream));
+        he = spconv::launch_outer(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw),
+                                  hw % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
+                                      reinterpret_cast<uintptr_t>(y) % 16 == 0,
+                                  xel * static_cast<int64_t>(e), static_cast<hipStream_t>(stream));
     else if (indexed)
         he = spconv::launch_indexed(plan->dev, static_cast<const float *>(x), static_cast<float *>(y),
                                     static_cast<int32_t>(m), static_cast<int32_t>(hw), xel * static_cast<int64_t>(e),

@@ -22,10 +22,15 @@
 // offset table (global memory when it does not fit).
 //
 // Refills.  The last wavefront to leave a buffer publishes the tile it takes
-// next; each wavefront copies its share of that tile (16-byte global-to-LDS
-// loads) at its next check and counts it as landed at the check after
-// (Refill below).  A wavefront starts a tile once every share of it has been
-// counted: a bounded wait that sets the plan's error word if it gives up.
+// next; each wavefront copies its share of that tile at its next check and
+// counts it as landed at the check after (Refill below).  fp32 input with
+// H*W a multiple of 4 is copied by 16-byte global-to-LDS loads; fp16 input
+// (converted to fp32 on the way) and H*W not a multiple of 4 (4-column
+// vectors that straddle two images, read element by element) go through
+// registers, kStageMax instructions per phase.  A wavefront starts a tile
+// once every share of it has been counted: a bounded wait that sets the
+// plan's error word if it gives up.  fp16 output is rounded once, to nearest
+// even, after the bias and the activation.
 
 #include <hip/hip_runtime.h>
 
@@ -38,10 +43,12 @@ namespace {
 
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef int i4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u2 __attribute__((ext_vector_type(2)));
 
 struct OArgs {
-    const float *x;
-    float *y;
+    const void *x;
+    void *y;
     const float *bias;  // every output channel
     const f4 *rec;      // weights, 16 bytes per (quad, slot)
     const i4 *off;      // channel-row offsets, 16 bytes per (quad, group)
@@ -54,24 +61,31 @@ struct OArgs {
     int32_t spin;   // bound of every wait (sleeps)
     int32_t cin, cout, hw, m, act;
     int32_t ntiles, grid, nx;  // tiles, workgroups, XCD groups of the tile map (grid % nx == 0)
+    int32_t rounds, rem;       // whole rounds of the grid, tiles left after them
+    int32_t parts;             // workgroups sharing each of those tiles (grid / rem when at least 2, else 1)
+    int32_t noct;
     int32_t waves, ozrow, buf_bytes;
     int32_t ctl_off;  // LDS byte address of the control words
     int64_t x_bytes;
 };
 
-// LDS control words after the two buffers, per buffer: wavefronts done with
-// it, copy shares of it landed (one per wavefront per tile), and the tile
-// sequence number it is free to take next (set by the last wavefront out).
+// LDS control words after the buffers (and the offset table), per buffer:
+// wavefronts done with it, copy shares of it landed (one per wavefront per
+// tile), and the tile sequence number it is free to take next (set by the
+// last wavefront out).
 constexpr int kCtlRel = 0, kCtlFill = 2, kCtlFree = 4, kCtlWords = 6;
+// Copy instructions a wavefront holds in registers per phase (staged copies):
+// 4 with one load per lane each, 2 with 4 element loads each.
+template <bool VEC>
+constexpr int stage_max() { return VEC ? 4 : 2; }
+constexpr int32_t kOutOfRange = static_cast<int32_t>(0x80000000u);
+constexpr int64_t kMaxRecords = 0x7ffffff0;
 
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
     static_assert(N >= 0 && N < 64, "vmcnt takes 6 bits");
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0f70);
 }
-
-constexpr int32_t kOutOfRange = static_cast<int32_t>(0x80000000u);
-constexpr int64_t kMaxRecords = 0x7ffffff0;
 
 __device__ __forceinline__ i4 rsrc_words(const void *p, int64_t bytes) {
     const uint64_t v = reinterpret_cast<uint64_t>(p);
@@ -83,6 +97,12 @@ __device__ __forceinline__ i4 rsrc_words(const void *p, int64_t bytes) {
     return r;
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void *p, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0),
+                                             static_cast<int>(bytes < kMaxRecords ? bytes : kMaxRecords),
+                                             0x00020000);
+}
+
 // Workgroup wg's position in the tile map: XCD x (= wg % nx) takes the
 // neighbouring tiles x * (grid / nx) .. of every round, so the 128-byte lines
 // two neighbouring tiles share meet in one L2.
@@ -90,99 +110,239 @@ __device__ __forceinline__ int32_t tile_slot(const OArgs &a, int32_t wg) {
     return (wg % a.nx) * (a.grid / a.nx) + wg / a.nx;
 }
 
-// Copy instructions [i0, i1) step `di` of tile `tile` into the LDS buffer at
-// byte `buf`: instruction i moves channel rows 8i .. 8i + 7 (lane l: row
-// 8i + l / 8, vector l % 8), 1 KB, to buf + 1024 i.  Columns past m and
-// channels past cin read zeros.
-__device__ __forceinline__ void copy_tile(const OArgs &a, int32_t tile, uint32_t buf, int i0, int i1, int di,
-                                          int lane) {
-    const int32_t col0 = tile * kOuterCols;
-    const int32_t n0 = col0 / a.hw;
-    const int64_t xbase = static_cast<int64_t>(n0) * a.cin * a.hw;
-    const i4 rs = rsrc_words(a.x + xbase, a.x_bytes - xbase * 4);
-    const int32_t cc = col0 + (lane & 7) * 4;
-    const int32_t n = cc / a.hw;
-    const int32_t p = cc - n * a.hw;
-    const int32_t crow = lane >> 3;
-    const bool ok = cc < a.m;
-    const int32_t lo = ((n - n0) * a.cin * a.hw + crow * a.hw + p) * 4;
-    const int32_t step = 8 * a.hw * 4;
-    for (int i = i0; i < i1; i += di) {
-        const int32_t voff = ok && 8 * i + crow < a.cin ? lo + i * step : kOutOfRange;
-        const uint32_t m0 = __builtin_amdgcn_readfirstlane(buf + 1024 * i);
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
-                     :
-                     : "s"(m0), "v"(voff), "s"(rs)
-                     : "memory", "m0");
-    }
+// Tile of workgroup position `slot` at its k-th tile: one per whole round,
+// then, of the tiles left, the one its group of `parts` neighbouring
+// positions (one XCD) shares, each position taking every parts-th oct.
+__device__ __forceinline__ int32_t tile_of(const OArgs &a, int32_t slot, int32_t k) {
+    return k < a.rounds ? k * a.grid + slot : a.rounds * a.grid + slot / a.parts;
 }
+
+__device__ __forceinline__ int32_t tiles_of(const OArgs &a, int32_t slot) {
+    return a.rounds + (a.rem > 0 && slot / a.parts < a.rem ? 1 : 0);
+}
+
+// The 4 columns of lane vector (lane % 8) of a tile, counted from channel 0
+// of the tile's first image n0 (the images one tile touches span less than
+// 2^31 bytes): X byte offsets (kOutOfRange past the last column) and Y
+// element offsets from ybase (-1 past it).  With VEC the 4 columns lie in one
+// image and only element 0 is kept.
+template <bool F16, bool VEC>
+struct Cols {
+    static constexpr int NE = VEC ? 1 : 4;
+    int32_t n0;
+    int64_t ybase;
+    int32_t xo[NE];
+    int32_t yo[NE];
+    __device__ __forceinline__ void set(const OArgs &a, int32_t tile, int lane) {
+        constexpr int E = F16 ? 2 : 4;
+        const int32_t col0 = tile * kOuterCols;
+        n0 = col0 / a.hw;
+        ybase = static_cast<int64_t>(n0) * a.cout * a.hw;
+#pragma unroll
+        for (int e = 0; e < NE; ++e) {
+            const int32_t c = col0 + (lane & 7) * 4 + e;
+            const int32_t n = c / a.hw;
+            const int32_t p = c - n * a.hw;
+            xo[e] = c < a.m ? ((n - n0) * a.cin * a.hw + p) * E : kOutOfRange;
+            yo[e] = c < a.m ? (n - n0) * a.cout * a.hw + p : -1;
+        }
+    }
+};
 
 __device__ __forceinline__ int32_t lds_load_acquire(const int32_t *p) {
     return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
-// A wavefront's part in refilling the two buffers.  When a buffer's last
-// wavefront leaves it, it publishes the tile sequence number the buffer takes
-// next; every wavefront, at its next check, copies its share of that tile
-// (instructions wave, wave + waves, ...) and, at the check after that, counts
-// the share as landed.  Checks run every kOuterAhead pairs inside an oct (the
-// record loads issued in between guarantee that older copies have completed:
-// loads complete in order), at the end of each tile and while waiting.
-struct Refill {
-    int32_t issued[2];  // sequence number of the last tile whose share this wave copied, per buffer
-    int32_t pend;       // buffers with copied shares not yet counted (bit b)
-
-    __device__ __forceinline__ void count(int32_t *ctl, int lane) {
-        if (lane == 0) {
-            if (pend & 1)
-                __hip_atomic_fetch_add(&ctl[kCtlFill + 0], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-            if (pend & 2)
-                __hip_atomic_fetch_add(&ctl[kCtlFill + 1], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-        }
-        pend = 0;
-    }
-    // Copy this wave's share of any tile a buffer was freed for.
-    __device__ __forceinline__ void issue(const OArgs &a, int32_t *ctl, int32_t slot, int wave, int lane) {
-        for (int b = 0; b < 2; ++b) {
-            const int32_t g = __builtin_amdgcn_readfirstlane(lds_load_acquire(&ctl[kCtlFree + b]));
-            if (g > issued[b]) {
-                copy_tile(a, g * a.grid + slot, b * a.buf_bytes, wave, a.ozrow / 8, a.waves, lane);
-                issued[b] = g;
-                pend |= 1 << b;
-            }
-        }
-    }
-    // Inside an oct: at least N loads were issued since the last check.
-    template <int N>
-    __device__ __forceinline__ void check(const OArgs &a, int32_t *ctl, int32_t slot, int wave, int lane) {
-        if (pend) {
-            wait_vmcnt<N>();
-            count(ctl, lane);
-        }
-        issue(a, ctl, slot, wave, lane);
-    }
-    // Anywhere: wait for this wave's copies, count them, issue new shares.
-    __device__ __forceinline__ void flush(const OArgs &a, int32_t *ctl, int32_t slot, int wave, int lane) {
-        if (pend) {
-            wait_vmcnt<0>();
-            count(ctl, lane);
-        }
-        issue(a, ctl, slot, wave, lane);
-    }
-};
-
 __device__ __forceinline__ f4 lds_vec(const unsigned char *lds, uint32_t byte) {
     return *reinterpret_cast<const f4 *>(lds + byte);
 }
+
+// A wavefront's part in filling the two buffers.  Copy instruction i of a
+// tile moves channel rows 8i .. 8i + 7 (lane l: row 8i + l / 8, the 4 columns
+// of vector l % 8) to LDS bytes buf + 1024 i + 16 l, as fp32; channels past
+// cin and columns past m give zeros.  A wavefront's share of a tile is
+// instructions wave, wave + waves, ...; it starts the share when it sees the
+// buffer freed for that tile, and once its last copy has landed adds one to
+// the buffer's fill count.  One share (or one phase of a staged share) is in
+// flight at a time.  Checks inside an oct come after at least N newer loads,
+// and loads complete in order, so a wait for vmcnt <= N finds the copies done.
+template <bool DMA, bool F16, bool VEC>
+struct Refill {
+    int32_t issued0, issued1;  // sequence number of the last tile whose share this wave started, per buffer
+    int32_t sb;         // buffer of the copy in flight, -1 for none
+    int32_t sk;         // its tile sequence number
+    int32_t sfirst;     // first share instruction of the phase in flight (staged)
+    int32_t sn;         // instructions in it (staged)
+    static constexpr int kStageMax = stage_max<VEC>();
+    uint32_t st[kStageMax][4];
+
+    __device__ __forceinline__ void start(const OArgs &a, int32_t slot, int wave, int lane, int b, int32_t k,
+                                          int32_t first) {
+        sb = b;
+        sk = k;
+        sfirst = first;
+        const int ninstr = a.ozrow / 8;
+        Cols<F16, VEC> cols;
+        cols.set(a, tile_of(a, slot, k), lane);
+        constexpr int E = F16 ? 2 : 4;
+        const int64_t xbase = static_cast<int64_t>(cols.n0) * a.cin * a.hw;
+        const int32_t crow = lane >> 3;
+        const int32_t step = 8 * a.hw * E;
+        if constexpr (DMA) {
+            const i4 rs = rsrc_words(static_cast<const float *>(a.x) + xbase, a.x_bytes - xbase * 4);
+            const int32_t lo = cols.xo[0] == kOutOfRange ? kOutOfRange : cols.xo[0] + crow * a.hw * 4;
+            const uint32_t buf = b * a.buf_bytes;
+            for (int i = wave; i < ninstr; i += a.waves) {
+                const int32_t voff = lo != kOutOfRange && 8 * i + crow < a.cin ? lo + i * step : kOutOfRange;
+                const uint32_t m0 = __builtin_amdgcn_readfirstlane(buf + 1024 * i);
+                asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                             :
+                             : "s"(m0), "v"(voff), "s"(rs)
+                             : "memory", "m0");
+            }
+        } else {
+            const auto rs = make_rsrc(static_cast<const unsigned char *>(a.x) + xbase * E, a.x_bytes - xbase * E);
+            sn = 0;
+#pragma unroll
+            for (int s = 0; s < kStageMax; ++s) {
+                const int i = wave + (first + s) * a.waves;
+                if (i < ninstr) {
+                    const bool row_ok = 8 * i + crow < a.cin;
+                    const int32_t ro = (8 * i + crow) * a.hw * E;
+                    if constexpr (VEC) {
+                        const int32_t o = row_ok && cols.xo[0] != kOutOfRange ? cols.xo[0] + ro : kOutOfRange;
+                        if constexpr (F16) {
+                            const auto v = __builtin_amdgcn_raw_buffer_load_b64(rs, o, 0, 0);
+                            st[s][0] = v[0];
+                            st[s][1] = v[1];
+                        } else {
+                            const auto v = __builtin_amdgcn_raw_buffer_load_b128(rs, o, 0, 0);
+                            st[s][0] = v[0];
+                            st[s][1] = v[1];
+                            st[s][2] = v[2];
+                            st[s][3] = v[3];
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int32_t o = row_ok && cols.xo[e] != kOutOfRange ? cols.xo[e] + ro : kOutOfRange;
+                            if constexpr (F16)
+                                st[s][e] = __builtin_amdgcn_raw_buffer_load_b16(rs, o, 0, 0);
+                            else
+                                st[s][e] = __builtin_amdgcn_raw_buffer_load_b32(rs, o, 0, 0);
+                        }
+                    }
+                    sn = s + 1;
+                }
+            }
+        }
+    }
+    // The copy in flight has completed: write a staged phase to LDS, then start
+    // the share's next phase or count the share as landed.
+    __device__ __forceinline__ void advance(const OArgs &a, unsigned char *lds, int32_t *ctl, int32_t slot,
+                                            int wave, int lane) {
+        if constexpr (!DMA) {
+            const uint32_t buf = sb * a.buf_bytes;
+#pragma unroll
+            for (int s = 0; s < kStageMax; ++s) {
+                if (s < sn) {
+                    const int i = wave + (sfirst + s) * a.waves;
+                    f4 v;
+                    if constexpr (F16) {
+                        uint32_t h[4];
+                        if constexpr (VEC) {
+                            h[0] = st[s][0] & 0xffff;
+                            h[1] = st[s][0] >> 16;
+                            h[2] = st[s][1] & 0xffff;
+                            h[3] = st[s][1] >> 16;
+                        } else {
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                h[e] = st[s][e];
+                        }
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            v[e] = static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(h[e])));
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            v[e] = __uint_as_float(st[s][e]);
+                    }
+                    *reinterpret_cast<f4 *>(lds + buf + 1024 * i + 16 * lane) = v;
+                }
+            }
+            if (wave + (sfirst + sn) * a.waves < a.ozrow / 8) {
+                start(a, slot, wave, lane, sb, sk, sfirst + sn);
+                return;
+            }
+            __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the LDS writes are done
+        }
+        if (lane == 0)
+            __hip_atomic_fetch_add(&ctl[kCtlFill + sb], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+        sb = -1;
+    }
+    // Start this wave's share of a tile a buffer was freed for, if any (one at a time).
+    __device__ __forceinline__ void try_start(const OArgs &a, int32_t *ctl, int32_t slot, int wave, int lane) {
+        if (sb >= 0)
+            return;
+        const int32_t g0 = __builtin_amdgcn_readfirstlane(lds_load_acquire(&ctl[kCtlFree + 0]));
+        if (g0 > issued0) {
+            issued0 = g0;
+            start(a, slot, wave, lane, 0, g0, 0);
+            return;
+        }
+        const int32_t g1 = __builtin_amdgcn_readfirstlane(lds_load_acquire(&ctl[kCtlFree + 1]));
+        if (g1 > issued1) {
+            issued1 = g1;
+            start(a, slot, wave, lane, 1, g1, 0);
+        }
+    }
+    // Inside an oct, at least N loads after the copy in flight was issued.
+    template <int N>
+    __device__ __forceinline__ void check(const OArgs &a, unsigned char *lds, int32_t *ctl, int32_t slot, int wave,
+                                          int lane) {
+        if (sb >= 0) {
+            wait_vmcnt<N>();
+            advance(a, lds, ctl, slot, wave, lane);
+        }
+        try_start(a, ctl, slot, wave, lane);
+    }
+    // Before tile k in buffer bw: finish the copy in flight, and this wave's
+    // whole share of tile k once the buffer is free for it; then start
+    // whatever else is free.
+    __device__ __forceinline__ void flush(const OArgs &a, unsigned char *lds, int32_t *ctl, int32_t slot, int wave,
+                                          int lane, int bw, int32_t k) {
+        for (;;) {
+            if (sb >= 0) {
+                wait_vmcnt<0>();
+                advance(a, lds, ctl, slot, wave, lane);
+                continue;
+            }
+            if ((bw ? issued1 : issued0) < k) {
+                const int32_t g = __builtin_amdgcn_readfirstlane(lds_load_acquire(&ctl[kCtlFree + bw]));
+                if (g >= k) {
+                    if (bw)
+                        issued1 = g;
+                    else
+                        issued0 = g;
+                    start(a, slot, wave, lane, bw, g, 0);
+                    continue;
+                }
+            }
+            break;
+        }
+        try_start(a, ctl, slot, wave, lane);
+    }
+};
 
 // One oct on the tile in the buffer at byte `buf`: lockstep steps, then bias,
 // activation and 16-byte stores of the lane's 4 rows x 4 columns.  OFF_LDS:
 // the channel-row offsets come from the workgroup's LDS copy of the table,
 // else from global memory.
-template <bool OFF_LDS>
-__device__ __forceinline__ void run_oct(const OArgs &a, const unsigned char *lds, int32_t o, uint32_t buf,
-                                        float *ylane, bool col_ok, float lo, float hi, int lane, int32_t *ctl,
-                                        Refill &rf, int32_t slot, int wave) {
+template <bool OFF_LDS, bool DMA, bool F16, bool VEC>
+__device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int32_t o, uint32_t buf,
+                                        const Cols<F16, VEC> &cols, float lo, float hi, int lane, int32_t *ctl,
+                                        Refill<DMA, F16, VEC> &rf, int32_t slot, int wave) {
     const int32_t *tab = a.oct + o * kOctWords;
     const int32_t q0 = __builtin_amdgcn_readfirstlane(tab[0]);
     const int32_t nq = __builtin_amdgcn_readfirstlane(tab[1]);
@@ -244,7 +404,7 @@ __device__ __forceinline__ void run_oct(const OArgs &a, const unsigned char *lds
         }
         wp += kOuterAhead * kOuterSlots;
         // loads since the last check: kOuterAhead weight loads (and as many offset loads)
-        rf.template check<OFF_LDS ? kOuterAhead : 2 * kOuterAhead>(a, ctl, slot, wave, lane);
+        rf.template check<OFF_LDS ? kOuterAhead : 2 * kOuterAhead>(a, lds, ctl, slot, wave, lane);
     }
 #pragma unroll
     for (int i = 0; i < kOuterAhead - 1; ++i) {
@@ -254,9 +414,8 @@ __device__ __forceinline__ void run_oct(const OArgs &a, const unsigned char *lds
             oq = nx;
         }
     }
-    if (rb >= 0 && col_ok) {
+    if (rb >= 0) {
         const f4 bz = *reinterpret_cast<const f4 *>(a.bias + 4 * rb);
-        float *yr = ylane + static_cast<int64_t>(4 * rb) * a.hw;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
             f4 v;
@@ -264,33 +423,56 @@ __device__ __forceinline__ void run_oct(const OArgs &a, const unsigned char *lds
             v.y = fminf(fmaxf(acc1[r] + bz[r], lo), hi);
             v.z = fminf(fmaxf(acc2[r] + bz[r], lo), hi);
             v.w = fminf(fmaxf(acc3[r] + bz[r], lo), hi);
-            *reinterpret_cast<f4 *>(yr + static_cast<int64_t>(r) * a.hw) = v;
+            const int32_t ro = (4 * rb + r) * a.hw;
+            if constexpr (VEC) {
+                if (cols.yo[0] >= 0) {
+                    if constexpr (F16) {
+                        u2 h;
+                        h.x = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.x)) |
+                              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.y))) << 16;
+                        h.y = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.z)) |
+                              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.w))) << 16;
+                        *reinterpret_cast<u2 *>(static_cast<_Float16 *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = h;
+                    } else {
+                        *reinterpret_cast<f4 *>(static_cast<float *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = v;
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    if (cols.yo[e] >= 0) {
+                        if constexpr (F16)
+                            static_cast<_Float16 *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = static_cast<_Float16>(v[e]);
+                        else
+                            static_cast<float *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = v[e];
+                    }
+            }
         }
     }
 }
 
-template <bool OFF_LDS>
+template <bool OFF_LDS, bool F16, bool VEC>
 __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
+    constexpr bool DMA = !F16 && VEC;
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int32_t slot = tile_slot(a, blockIdx.x);
-    const int32_t nt = slot < a.ntiles ? (a.ntiles - slot + a.grid - 1) / a.grid : 0;
+    const int32_t nt = tiles_of(a, slot);
     if (nt == 0)
         return;
     int32_t *ctl = reinterpret_cast<int32_t *>(lds + a.ctl_off);
-    const int ninstr = a.ozrow / 8;
-    // zero rows of both buffers, control words, the first two tiles: tile 0
-    // behind a barrier, tile 1 counted by each wavefront's share
+    // zero rows of both buffers; control words: buffer 0 free for tile 0,
+    // buffer 1 for tile 1; the offset table
     if (threadIdx.x < 16) {
         const int b = threadIdx.x >> 3;
         *reinterpret_cast<f4 *>(lds + b * a.buf_bytes + a.ozrow * kOuterRowBytes + (threadIdx.x & 7) * 16) =
             f4{0.f, 0.f, 0.f, 0.f};
     }
-    if (threadIdx.x < kCtlWords)  // tile 0 is complete at the barrier below: count its shares
-        ctl[threadIdx.x] = threadIdx.x == kCtlFill ? a.waves : 0;
+    if (threadIdx.x < kCtlWords)
+        ctl[threadIdx.x] = threadIdx.x == kCtlFree ? 0 : threadIdx.x == kCtlFree + 1 ? (nt > 1 ? 1 : -1) : 0;
     if constexpr (OFF_LDS) {
-        // the offset table, 1 KB per instruction (reads past its end give zeros)
+        // 1 KB per instruction (reads past the table's end give zeros)
         const i4 rs = rsrc_words(a.off, a.off_bytes);
         for (int i = wave; i < (a.off_bytes + 1023) / 1024; i += a.waves) {
             const uint32_t m0 = __builtin_amdgcn_readfirstlane(a.off_lds + 1024 * i);
@@ -299,45 +481,28 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
                          : "s"(m0), "v"(1024 * i + lane * 16), "s"(rs)
                          : "memory", "m0");
         }
-    }
-    copy_tile(a, slot, 0, wave, ninstr, a.waves, lane);
-    Refill rf;
-    rf.issued[0] = 0;
-    rf.issued[1] = 0;
-    rf.pend = 0;
-    if (nt > 1) {
-        copy_tile(a, slot + a.grid, a.buf_bytes, wave, ninstr, a.waves, lane);
-        rf.issued[1] = 1;
-        rf.pend = 2;
-        // this wavefront's tile-0 copies are the older ones: wait until at most
-        // its tile-1 copies (or fewer) are in flight
-        const int mine = (ninstr - wave + a.waves - 1) / a.waves;
-        if (mine >= 8)
-            wait_vmcnt<8>();
-        else if (mine >= 4)
-            wait_vmcnt<4>();
-        else if (mine >= 2)
-            wait_vmcnt<2>();
-        else
-            wait_vmcnt<0>();
-    } else {
         wait_vmcnt<0>();
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): zero rows and control words written
     __syncthreads();
 
+    Refill<DMA, F16, VEC> rf;
+    rf.issued0 = -1;
+    rf.issued1 = -1;
+    rf.sb = -1;
+    rf.try_start(a, ctl, slot, wave, lane);
     const float lo = a.act == 0 ? -__builtin_huge_valf() : 0.0f;
     const float hi = a.act == 2 ? 6.0f : __builtin_huge_valf();
     for (int32_t k = 0; k < nt; ++k) {
         const int b = k & 1;
         const uint32_t buf = b * a.buf_bytes;
-        if (k >= 1) {
-            // every wavefront's share of tile k's copy landed (this wave's own
-            // share may still be owed: flush issues and counts it)
+        {
+            // every wavefront's share of tile k landed (this wave's own share
+            // may still be owed: flush copies and counts it)
             const int32_t target = a.waves * (k / 2 + 1);
             int32_t spins = 0;
             for (;;) {
-                rf.flush(a, ctl, slot, wave, lane);
+                rf.flush(a, lds, ctl, slot, wave, lane, b, k);
                 if (lds_load_acquire(&ctl[kCtlFill + b]) >= target)
                     break;
                 __builtin_amdgcn_s_sleep(1);
@@ -348,17 +513,20 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
                 }
             }
         }
-        const int32_t tile = k * a.grid + slot;
-        const int32_t cc = tile * kOuterCols + (lane & 7) * 4;
-        const bool col_ok = cc < a.m;
-        const int32_t n = cc / a.hw;
-        float *ylane = a.y + (static_cast<int64_t>(n) * a.cout * a.hw + (cc - n * a.hw));
-        const int q = k & 1;
-        const int32_t e0 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave]);
-        const int32_t e1 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave + 1]);
-        for (int32_t e = e0; e < e1; ++e)
-            run_oct<OFF_LDS>(a, lds, __builtin_amdgcn_readfirstlane(a.wave_oct[e]), buf, ylane, col_ok, lo, hi,
-                             lane, ctl, rf, slot, wave);
+        Cols<F16, VEC> cols;
+        cols.set(a, tile_of(a, slot, k), lane);
+        if (k < a.rounds || a.parts == 1) {
+            const int q = k & 1;
+            const int32_t e0 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave]);
+            const int32_t e1 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave + 1]);
+            for (int32_t e = e0; e < e1; ++e)
+                run_oct<OFF_LDS>(a, lds, __builtin_amdgcn_readfirstlane(a.wave_oct[e]), buf, cols, lo, hi, lane, ctl,
+                                 rf, slot, wave);
+        } else {
+            // a shared last tile: this position's octs, one per wavefront in turn
+            for (int32_t o = slot % a.parts + a.parts * wave; o < a.noct; o += a.parts * a.waves)
+                run_oct<OFF_LDS>(a, lds, o, buf, cols, lo, hi, lane, ctl, rf, slot, wave);
+        }
         if (k + 2 < nt) {
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's reads of the buffer are done
             int32_t old = 0;
@@ -368,10 +536,10 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
             if (old == a.waves * (k / 2 + 1) - 1 && lane == 0)  // the last one out frees the buffer for tile k + 2
                 __hip_atomic_store(&ctl[kCtlFree + b], k + 2, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
         }
-        rf.issue(a, ctl, slot, wave, lane);
+        rf.try_start(a, ctl, slot, wave, lane);
     }
-    // every copy this wave issued was counted before the tile that needed it;
-    // nothing is left in flight but stores
+    // every share this wave started was counted before the tile that needed
+    // it; nothing is left in flight but stores
 }
 
 // LDS layout: two tile buffers, the offset table when it fits, the control words.
@@ -394,14 +562,24 @@ OuterLds outer_lds(const DevicePlan &p) {
     return l;
 }
 
+typedef void (*OKernel)(OArgs);
+
+template <bool OFF_LDS>
+OKernel pick_outer(bool f16, bool vec) {
+    if (f16)
+        return vec ? outer_kernel<OFF_LDS, true, true> : outer_kernel<OFF_LDS, true, false>;
+    return vec ? outer_kernel<OFF_LDS, false, true> : outer_kernel<OFF_LDS, false, false>;
+}
+
 }  // namespace
 
 hipError_t prepare_outer(const DevicePlan &p) {
     (void)p;
-    for (const void *k : {reinterpret_cast<const void *>(outer_kernel<true>),
-                          reinterpret_cast<const void *>(outer_kernel<false>)}) {
-        const hipError_t e =
-            hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(kMaxLdsBytes));
+    for (int v = 0; v < 8; ++v) {
+        const OKernel k = (v & 4) ? pick_outer<true>(v & 1, v & 2) : pick_outer<false>(v & 1, v & 2);
+        const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                 static_cast<int>(kMaxLdsBytes));
         if (e != hipSuccess)
             return e;
     }
@@ -410,8 +588,8 @@ hipError_t prepare_outer(const DevicePlan &p) {
 
 int32_t outer_lds_bytes(const DevicePlan &p) { return outer_lds(p).total; }
 
-hipError_t launch_outer(const DevicePlan &p, const float *x, float *y, int32_t m, int32_t hw, int64_t x_bytes,
-                        hipStream_t stream) {
+hipError_t launch_outer(const DevicePlan &p, const void *x, void *y, int32_t m, int32_t hw, int32_t vec,
+                        int64_t x_bytes, hipStream_t stream) {
     const OuterLds l = outer_lds(p);
     OArgs a;
     a.x = x;
@@ -435,15 +613,26 @@ hipError_t launch_outer(const DevicePlan &p, const float *x, float *y, int32_t m
     const int32_t cus = p.num_cus > 0 ? p.num_cus : 256;
     a.grid = a.ntiles < cus ? a.ntiles : cus;
     a.nx = a.grid % 8 == 0 ? 8 : 1;
+    a.rounds = a.ntiles / a.grid;
+    a.rem = a.ntiles % a.grid;
+    a.noct = p.oocts;
+    // share each left-over tile among as many workgroups as the grid holds
+    // for it, at most one per oct
+    a.parts = 1;
+    if (a.rem > 0)
+        for (int32_t q = a.grid / a.rem; q >= 2; --q)
+            if (q <= p.oocts) {
+                a.parts = q;
+                break;
+            }
     a.waves = p.owaves;
     a.ozrow = p.ozrow;
     a.buf_bytes = l.buf_bytes;
     a.ctl_off = l.ctl_off;
     a.x_bytes = x_bytes;
-    if (l.off_lds >= 0)
-        hipLaunchKernelGGL(outer_kernel<true>, dim3(a.grid), dim3(64 * a.waves), l.total, stream, a);
-    else
-        hipLaunchKernelGGL(outer_kernel<false>, dim3(a.grid), dim3(64 * a.waves), l.total, stream, a);
+    const bool f16 = p.storage == 1;
+    const OKernel k = l.off_lds >= 0 ? pick_outer<true>(f16, vec != 0) : pick_outer<false>(f16, vec != 0);
+    hipLaunchKernelGGL(k, dim3(a.grid), dim3(64 * a.waves), l.total, stream, a);
     return hipGetLastError();
 }
 

@@ -1,7 +1,8 @@
 """GPU parity of the outer-product kernel (kernel=4, 1 x 4 blocks) against the oracle.
 
 Every case calls through the C ABI and compares element by element with the
-oracle to |y_gpu - y_ref| <= 1e-5 * sum|w*x| + 1e-6.  The matrix instruction
+oracle to its tolerance (fp32: |y_gpu - y_ref| <= 1e-5 * sum|w*x| + 1e-6;
+fp16 storage: the fp16 bound).  The matrix instruction
 rounds each product-and-add once, like a fused multiply-add, and every row
 still sums in ascending input channel from zero, so the results also equal
 the direct-load kernel's bit for bit.
@@ -78,11 +79,47 @@ def test_outer_headline_layer(n):
     assert np.array_equal(y, gpu_run(layer, kernel=2))
 
 
-def test_outer_refuses_ragged_images():
-    """kernel = 4 needs h * w a multiple of 4 (whole 16-byte vectors per image)."""
-    import paper_1911_09723_amd as sp
-    layer = make_layer(64, 64, 7, 7, 2, 0.8, block_rows=4, seed=9)
-    note("outer ragged refusal")
-    with pytest.raises(sp.SpconvError) as e:
-        gpu_run(layer, kernel=4)
-    assert "SPCONV_E_UNSUPPORTED" in str(e.value)
+# (cin, cout, h, w, n, sparsity, act, storage): H*W not a multiple of 4 (4-column
+# vectors straddle images, copied and stored element by element) and fp16
+# storage (converted to fp32 on the way into LDS, rounded once on the way out)
+STAGED = [
+    (64, 64, 7, 7, 3, 0.8, "relu", "f32"),
+    (130, 96, 5, 5, 17, 0.9, "none", "f32"),
+    (40, 240, 28, 28, 2, 0.9, "relu6", "f16"),
+    (112, 672, 14, 14, 3, 0.9, "relu6", "f16"),
+    (320, 1280, 7, 7, 5, 0.9, "relu6", "f16"),
+    (24, 36, 3, 3, 7, 0.7, "none", "f16"),
+]
+
+
+@pytest.mark.parametrize("spec", STAGED, ids=lambda s: "%d-%d-%dx%d-n%d-s%g-%s-%s" % s)
+def test_outer_ragged_and_fp16(spec):
+    cin, cout, h, w, n, s, act, st = spec
+    layer = make_layer(cin, cout, h, w, n, s, block_rows=4, act=act, storage=st,
+                       seed=zlib.crc32(repr(spec).encode()) % 1000)
+    note("outer staged %s" % (spec,))
+    y = gpu_run(layer, kernel=4)
+    assert_parity(layer, y, what=str(spec))
+    assert np.array_equal(y, gpu_run(layer, kernel=2)), "not bitwise equal to the direct-load kernel"
+
+
+def test_outer_unaligned_pointers_take_the_staged_copy():
+    """x and y 4 bytes off a 16-byte boundary: element copies and stores."""
+    import torch
+    from paper_1911_09723_amd import Plan
+    from gpu_util import to_gpu, device
+    layer = make_layer(64, 64, 8, 8, 3, 0.8, block_rows=4, act="relu", seed=42)
+    note("outer unaligned")
+    ref = gpu_run(layer, kernel=4)
+    plan = Plan.from_layer(layer, kernel=4)
+    try:
+        flat = to_gpu(np.concatenate([np.zeros(1, layer.x.dtype), layer.x.ravel()]))
+        x = flat[1:].view(layer.x.shape)
+        ybuf = torch.empty(1 + ref.size, dtype=flat.dtype, device=device())
+        y = ybuf[1:].view(ref.shape)
+        plan.run(x, y)
+        torch.cuda.synchronize()
+        assert plan.check() == 0
+        assert np.array_equal(y.cpu().numpy(), ref)
+    finally:
+        plan.close()

@@ -1,6 +1,6 @@
 """Host-only checks of the outer-product kernel's records (no GPU).
 
-fp32 plans of 1 x 4 blocks with at most 632 input channels are laid out a
+Plans of 1 x 4 blocks with at most 632 input channels are laid out a
 third time for the outer-product kernel: octs of 8 block rows in lockstep,
 per lane slot and step a (weight, LDS channel offset) record, padding steps
 that read the zero row with weight 0, and wave lists per tile parity.
@@ -45,6 +45,8 @@ CASES = [
     (256, 128, 0.8, 2),       # 4x2 blocks expanded to single channels
 ]
 
+F16_CASES = [(320, 1280, 0.9), (40, 240, 0.9)]
+
 
 @pytest.mark.parametrize("case", CASES, ids=lambda c: "%d-%d-s%g-kc%d" % c)
 def test_records_unpack_to_the_input(case):
@@ -60,9 +62,24 @@ def test_records_unpack_to_the_input(case):
         sp.spconv_destroy(h)
 
 
-@pytest.mark.parametrize("case", [(512, 512, 0.9, 1, "f32"), (64, 64, 0.8, 2, "f32"), (64, 64, 0.8, 4, "f16"),
-                                  (640, 64, 0.9, 4, "f32")],
-                         ids=["k1", "k2", "f16", "cin640"])
+@pytest.mark.parametrize("case", F16_CASES, ids=lambda c: "%d-%d-s%g" % c)
+def test_fp16_records_hold_the_rounded_weights(case):
+    """fp16 storage: the records carry each weight rounded once to fp16."""
+    cin, cout, s = case
+    layer = make_layer(cin, cout, 1, 1, 1, s, block_rows=4, storage="f16", seed=cin, with_x=False)
+    h = _host_plan(layer)
+    try:
+        rp, ci, va = sp.spconv_plan_unpack_outer(h)
+        assert np.array_equal(rp, layer.row_ptr)
+        assert np.array_equal(ci, layer.col_idx)
+        want = layer.values.astype(np.float16).astype(np.float32)
+        assert np.array_equal(va.view(np.uint32), want.view(np.uint32))
+    finally:
+        sp.spconv_destroy(h)
+
+
+@pytest.mark.parametrize("case", [(512, 512, 0.9, 1, "f32"), (64, 64, 0.8, 2, "f32"), (640, 64, 0.9, 4, "f32")],
+                         ids=["k1", "k2", "cin640"])
 def test_plans_the_kernel_cannot_take(case):
     cin, cout, s, k, st = case
     layer = make_layer(cin, cout, 1, 1, 1, s, block_rows=k, storage=st, seed=5, with_x=False)
