@@ -236,7 +236,8 @@ def network_alg_bytes(net, batch, fused_blocks, h=224):
 
 def sweep_configs(configs, steps, warmup, indexed=True):
     """Every layer of the given workload configurations on the automatic
-    kernel and (fp32) on the register-indexed kernel."""
+    kernel, on the register-indexed kernel (fp32) and on the outer-product
+    kernel (1x4 blocks)."""
     from synth import config_layers
     from synth.configs import build
 
@@ -250,6 +251,8 @@ def sweep_configs(configs, steps, warmup, indexed=True):
             kinds = [("auto", {})]
             if indexed and layer.storage == "f32":
                 kinds.append(("indexed", {"kernel": 3}))
+            if indexed and layer.block_rows == 4 and layer.cin <= 632:
+                kinds.append(("outer", {"kernel": 4}))
             for kind, opts in kinds:
                 r = time_variant(layer, steps, warmup, 2, **opts)
                 sm = summarize(layer, r)
@@ -262,10 +265,11 @@ def sweep_configs(configs, steps, warmup, indexed=True):
             entry["alg_bytes"] = layer.alg_bytes()
             entry["flops"] = layer.flops()
             out.append(entry)
-            log("bench: %s %s auto %.1f us (%s, frac %.3f)%s" % (
+            log("bench: %s %s auto %.1f us (%s, frac %.3f)%s%s" % (
                 entry["config"], spec["name"], entry["auto"]["kernel_us_mean"], entry["auto"]["kernel"],
                 entry["auto"]["roofline_frac"],
-                "  indexed %.1f us" % entry["indexed"]["kernel_us_mean"] if "indexed" in entry else ""))
+                "  indexed %.1f us" % entry["indexed"]["kernel_us_mean"] if "indexed" in entry else "",
+                "  outer %.1f us" % entry["outer"]["kernel_us_mean"] if "outer" in entry else ""))
             del layer
     return out
 
@@ -398,10 +402,21 @@ def summarize(layer, r, dw=False):
         "plan": {k: r["info"][k] for k in ("kernel", "group_lanes", "tile_cols", "waves", "lds_bytes", "slots",
                                            "max_parts", "indexed_min_cols")},
     }
-    # the kernel the runs took: 3 (register-indexed) when forced or chosen for this many columns
+    # the kernel the runs took, as spconv_run chooses it: outer-product, then
+    # register-indexed (forced, or automatic for this many columns), else the
+    # plan's LDS-strip or direct-load kernel
     cols = layer.n * layer.hw
     imc = r["info"]["indexed_min_cols"]
-    out["plan"]["kernel_run"] = 3 if r.get("forced_kernel") == 3 or (imc > 0 and cols >= imc) else r["info"]["kernel"]
+    omc = r["info"]["outer_min_cols"]
+    forced = r.get("forced_kernel")
+    if forced == 4 or (forced in (None, 0) and omc > 0 and cols >= omc):
+        run = "outer"
+    elif forced == 3 or (forced in (None, 0) and imc > 0 and cols >= imc):
+        run = "indexed"
+    else:
+        run = "direct" if r["info"]["kernel"] == 1 else "strip"
+    out["plan"]["kernel_run"] = run
+    out["plan"]["outer_min_cols"] = omc
     if layer.storage == "f16":
         # fp16 plans round W to fp16 but keep it as fp32 in device memory: the
         # weights move 4 bytes per value, not the 2 alg_bytes counts
