@@ -65,7 +65,7 @@ struct DevicePlan {
     int64_t indexed_min_cols = 0;       // automatic choice: runs of at least this many columns take the
                                         // register-indexed kernel (0: never)
     // outer-product kernel (planner.hpp)
-    int32_t use_outer = 0, oocts = 0, owaves = 0, ozrow = 0;
+    int32_t use_outer = 0, omode = 0, otw = 32, oocts = 0, owaves = 0, ozrow = 0;
     const uint32_t *orec = nullptr;
     const uint32_t *ooff = nullptr;
     int32_t ooff_bytes = 0;             // the offset table including its read-ahead quads

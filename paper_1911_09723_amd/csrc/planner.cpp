@@ -610,12 +610,12 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         in.block_cols = 1;
     }
     if (opt.kernel < 0 || opt.kernel > 4) {
-        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct), 3 (register-indexed) or 4 (outer-product)";
+        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct), 3 (register-indexed) or 4 (lockstep)";
         return E_ARG;
     }
     if (opt.kernel == 4 && !outer_supported(in)) {
-        err = "the outer-product kernel runs plans of 1 x 4 blocks without a depthwise stage and with cin <= " +
-              std::to_string(kOuterMaxCin);
+        err = "the lockstep kernel runs plans without a depthwise stage of 1 x 4 blocks with cin <= " +
+              std::to_string(kOuterMaxCin32) + " or unstructured with cin <= " + std::to_string(kOuterMaxCin16);
         return E_UNSUPPORTED;
     }
     if (opt.kernel == 3 && (in.dw_stride || in.storage != 0)) {
@@ -1287,9 +1287,12 @@ Status unpack_indexed(const PackedPlan &p, bool from_pairs, int32_t *row_ptr, in
 
 namespace spconv {
 
-// Outer-product kernel: octs, records, wave lists (planner.hpp).
+// Lockstep kernel: group sets, records, wave lists (planner.hpp).
 bool outer_supported(const Input &in) {
-    return in.block_rows == 4 && in.dw_stride == 0 && in.cin >= 1 && in.cin <= kOuterMaxCin;
+    if (in.dw_stride != 0 || in.cin < 1)
+        return false;
+    return (in.block_rows == 4 && in.cin <= kOuterMaxCin32) ||
+           (in.block_rows == 1 && in.storage == 0 && in.cin <= kOuterMaxCin16);
 }
 
 void build_outer(const Input &in, PackedPlan &p) {
@@ -1299,10 +1302,18 @@ void build_outer(const Input &in, PackedPlan &p) {
     std::vector<int32_t> order(rows);
     std::iota(order.begin(), order.end(), 0);
     std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return len(a) > len(b); });
-    const int32_t O = (rows + kOctRows - 1) / kOctRows;
+    p.omode = k == 4 ? 0 : 1;
+    p.otw = p.omode == 0 || in.cin <= kOuterMaxCin32 ? 32 : 16;
+    p.ogroups = 256 / p.otw;
+    const int32_t G = p.ogroups;
+    const int32_t row_bytes = 4 * p.otw;
+    const int32_t per_copy = 1024 / row_bytes;  // rows one 1 KB copy instruction moves
+    const int32_t kw = k == 4 ? 4 : 1;          // weight slots per group
+    const int32_t slots = G * kw;
+    const int32_t O = (rows + G - 1) / G;
     p.oocts = O;
-    p.ozrow = (in.cin + 7) / 8 * 8;
-    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * kOuterRowBytes);
+    p.ozrow = (in.cin + per_copy - 1) / per_copy * per_copy;
+    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * row_bytes);
     p.orec.clear();
     p.ooff.clear();
     p.ooct_tab.assign(static_cast<size_t>(O) * kOctWords, 0);
@@ -1310,19 +1321,19 @@ void build_outer(const Input &in, PackedPlan &p) {
     int32_t quads = 0;
     for (int32_t o = 0; o < O; ++o) {
         int32_t l = 0;
-        for (int32_t g = 0; g < kOctRows && o * kOctRows + g < rows; ++g)
-            l = std::max(l, len(order[o * kOctRows + g]));
+        for (int32_t g = 0; g < G && o * G + g < rows; ++g)
+            l = std::max(l, len(order[o * G + g]));
         const int32_t nq = std::max<int32_t>(1, (l + kOuterQuadSteps - 1) / kOuterQuadSteps);
         steps[o] = int64_t(kOuterQuadSteps) * nq;
         int32_t *tab = &p.ooct_tab[static_cast<size_t>(o) * kOctWords];
         tab[0] = quads;
         tab[1] = nq;
         quads += nq;
-        for (int32_t g = 0; g < kOctRows; ++g)
-            tab[2 + g] = o * kOctRows + g < rows ? order[o * kOctRows + g] : -1;
+        for (int32_t g = 0; g < G; ++g)
+            tab[2 + g] = o * G + g < rows ? order[o * G + g] : -1;
         for (int32_t j = 0; j < nq; ++j) {
-            for (int32_t u = 0; u < kOuterSlots; ++u) {
-                const int32_t g = u / 4, t = u % 4, rb = tab[2 + g];
+            for (int32_t u = 0; u < slots; ++u) {
+                const int32_t g = u / kw, t = u % kw, rb = tab[2 + g];
                 for (int32_t h = 0; h < kOuterQuadSteps; ++h) {
                     const int32_t s = kOuterQuadSteps * j + h;
                     uint32_t w = 0;
@@ -1335,19 +1346,19 @@ void build_outer(const Input &in, PackedPlan &p) {
                     p.orec.push_back(w);
                 }
             }
-            for (int32_t g = 0; g < kOctRows; ++g) {
+            for (int32_t g = 0; g < G; ++g) {
                 const int32_t rb = tab[2 + g];
                 for (int32_t h = 0; h < kOuterQuadSteps; ++h) {
                     const int32_t s = kOuterQuadSteps * j + h;
                     p.ooff.push_back(rb >= 0 && s < len(rb)
-                                         ? static_cast<uint32_t>(in.col_idx[in.row_ptr[rb] + s] * kOuterRowBytes)
+                                         ? static_cast<uint32_t>(in.col_idx[in.row_ptr[rb] + s] * row_bytes)
                                          : zoff);
                 }
             }
         }
     }
-    p.orec.insert(p.orec.end(), static_cast<size_t>(kOuterAhead) * kOuterSlots * 4, 0u);
-    p.ooff.insert(p.ooff.end(), static_cast<size_t>(kOuterAhead) * kOctRows * 4, zoff);
+    p.orec.insert(p.orec.end(), static_cast<size_t>(kOuterAhead) * slots * 4, 0u);
+    p.ooff.insert(p.ooff.end(), static_cast<size_t>(kOuterAhead) * G * 4, zoff);
 
     // wave lists: even tiles, then odd tiles continuing from the even loads
     const int32_t W = std::min<int32_t>(kMaxWaves, O);
@@ -1382,28 +1393,32 @@ void build_outer(const Input &in, PackedPlan &p) {
 
 Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, std::string &err) {
     if (p.oocts == 0) {
-        err = "the plan has no outer-product records";
+        err = "the plan has no lockstep-kernel records";
         return E_FORMAT;
     }
-    const int32_t k = 4, rows = p.cout / k, O = p.oocts, W = p.owaves;
-    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * kOuterRowBytes);
-    if (p.ozrow != (p.cin + 7) / 8 * 8 || static_cast<int32_t>(p.ooct_tab.size()) != O * kOctWords ||
+    const int32_t k = p.k, rows = p.cout / k, O = p.oocts, W = p.owaves, G = p.ogroups;
+    const int32_t kw = k == 4 ? 4 : 1, slots = G * kw;
+    const int32_t row_bytes = 4 * p.otw, per_copy = 1024 / row_bytes;
+    const uint32_t zoff = static_cast<uint32_t>(p.ozrow * row_bytes);
+    if ((k != 1 && k != 4) || (p.omode != (k == 4 ? 0 : 1)) || (p.otw != 32 && p.otw != 16) ||
+        G != 256 / p.otw || G + 2 > kOctWords || p.ozrow != (p.cin + per_copy - 1) / per_copy * per_copy ||
+        static_cast<int32_t>(p.ooct_tab.size()) != O * kOctWords ||
         static_cast<int32_t>(p.owave_ptr.size()) != 2 * W + 1) {
-        err = "outer-product tables have the wrong size";
+        err = "lockstep-kernel geometry or tables are inconsistent";
         return E_FORMAT;
     }
-    // every oct exactly once per tile parity
+    // every set exactly once per tile parity
     for (int32_t q = 0; q < 2; ++q) {
         std::vector<int32_t> seen(O, 0);
         for (int32_t i = p.owave_ptr[q * W]; i < p.owave_ptr[q * W + W]; ++i) {
             const int32_t o = p.owave_oct[i];
             if (o < 0 || o >= O || seen[o]++) {
-                err = "wave lists do not cover every oct once per tile parity";
+                err = "wave lists do not cover every set once per tile parity";
                 return E_FORMAT;
             }
         }
         if (std::count(seen.begin(), seen.end(), 1) != O) {
-            err = "wave lists miss an oct";
+            err = "wave lists miss a set";
             return E_FORMAT;
         }
     }
@@ -1418,16 +1433,16 @@ Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, flo
         const int32_t *tab = &p.ooct_tab[static_cast<size_t>(o) * kOctWords];
         const int64_t q0 = tab[0], nq = tab[1];
         if (q0 != next_quad || nq < 1 ||
-            (q0 + nq + kOuterAhead) * kOuterSlots * 4 > static_cast<int64_t>(p.orec.size()) ||
-            (q0 + nq + kOuterAhead) * kOctRows * 4 > static_cast<int64_t>(p.ooff.size())) {
-            err = "oct " + std::to_string(o) + ": records out of order or out of range";
+            (q0 + nq + kOuterAhead) * slots * 4 > static_cast<int64_t>(p.orec.size()) ||
+            (q0 + nq + kOuterAhead) * G * 4 > static_cast<int64_t>(p.ooff.size())) {
+            err = "set " + std::to_string(o) + ": records out of order or out of range";
             return E_FORMAT;
         }
         next_quad = q0 + nq;
-        for (int32_t g = 0; g < kOctRows; ++g) {
+        for (int32_t g = 0; g < G; ++g) {
             const int32_t rb = tab[2 + g];
             if (rb < -1 || rb >= rows || (rb >= 0 && owner[rb]++)) {
-                err = "oct " + std::to_string(o) + ": bad or repeated block row";
+                err = "set " + std::to_string(o) + ": bad or repeated block row";
                 return E_FORMAT;
             }
             bool padding = rb < 0;
@@ -1435,36 +1450,37 @@ Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, flo
             for (int64_t s = 0; s < kOuterQuadSteps * nq; ++s) {
                 const int64_t j = q0 + s / kOuterQuadSteps, h = s % kOuterQuadSteps;
                 Blk b{};
-                for (int32_t t = 0; t < 4; ++t)
-                    std::memcpy(&b.w[t], &p.orec[static_cast<size_t>((j * kOuterSlots + 4 * g + t) * 4 + h)], 4);
-                const uint32_t off = p.ooff[static_cast<size_t>((j * kOctRows + g) * 4 + h)];
+                for (int32_t t = 0; t < kw; ++t)
+                    std::memcpy(&b.w[t], &p.orec[static_cast<size_t>((j * slots + kw * g + t) * 4 + h)], 4);
+                const uint32_t off = p.ooff[static_cast<size_t>((j * G + g) * 4 + h)];
                 if (off == zoff) {
-                    if (b.w[0] != 0.0f || b.w[1] != 0.0f || b.w[2] != 0.0f || b.w[3] != 0.0f) {
-                        err = "oct " + std::to_string(o) + ": padding step with a nonzero weight";
-                        return E_FORMAT;
-                    }
+                    for (int32_t t = 0; t < kw; ++t)
+                        if (b.w[t] != 0.0f) {
+                            err = "set " + std::to_string(o) + ": padding step with a nonzero weight";
+                            return E_FORMAT;
+                        }
                     padding = true;
                     continue;
                 }
-                if (padding || off % kOuterRowBytes || static_cast<int32_t>(off / kOuterRowBytes) >= p.cin ||
-                    static_cast<int32_t>(off / kOuterRowBytes) <= last_c) {
-                    err = "oct " + std::to_string(o) + ": block after padding, bad offset or channels not ascending";
+                if (padding || off % row_bytes || static_cast<int32_t>(off / row_bytes) >= p.cin ||
+                    static_cast<int32_t>(off / row_bytes) <= last_c) {
+                    err = "set " + std::to_string(o) + ": block after padding, bad offset or channels not ascending";
                     return E_FORMAT;
                 }
-                b.c = static_cast<int32_t>(off / kOuterRowBytes);
+                b.c = static_cast<int32_t>(off / row_bytes);
                 last_c = b.c;
                 got[rb].push_back(b);
             }
         }
     }
-    if (static_cast<int64_t>(p.orec.size()) != (next_quad + kOuterAhead) * kOuterSlots * 4 ||
-        static_cast<int64_t>(p.ooff.size()) != (next_quad + kOuterAhead) * kOctRows * 4) {
-        err = "record arrays' lengths do not match the octs";
+    if (static_cast<int64_t>(p.orec.size()) != (next_quad + kOuterAhead) * slots * 4 ||
+        static_cast<int64_t>(p.ooff.size()) != (next_quad + kOuterAhead) * G * 4) {
+        err = "record arrays' lengths do not match the sets";
         return E_FORMAT;
     }
     for (int32_t rb = 0; rb < rows; ++rb)
         if (!owner[rb]) {
-            err = "block row " + std::to_string(rb) + " is in no oct";
+            err = "block row " + std::to_string(rb) + " is in no set";
             return E_FORMAT;
         }
     int64_t nz = 0;
@@ -1475,8 +1491,8 @@ Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, flo
             if (col_idx)
                 col_idx[nz] = b.c;
             if (values)
-                for (int32_t t = 0; t < 4; ++t)
-                    values[nz * 4 + t] = b.w[t];
+                for (int32_t t = 0; t < kw; ++t)
+                    values[nz * kw + t] = b.w[t];
             ++nz;
         }
     }

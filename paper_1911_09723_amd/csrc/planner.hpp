@@ -161,47 +161,53 @@ inline int32_t flag_word(int32_t k) { return k == 1 ? 7 : 3; }
 constexpr uint32_t kLastOfChunk = 1u;
 constexpr uint32_t kLastOfStream = 2u;
 
-// Outer-product kernel (1 x 4 blocks, fp32 or fp16 storage): a stored block
-// times a 4-column X vector is a 4 x 4 outer product, and the matrix cores'
-// fp32 4x4x1 instruction computes 16 of them at once, each from its own block
-// of 4 lanes (register r of lane 4b + t gets A[4b + r] * B[4b + t] + C, one
-// rounding, like a fused multiply-add).
+// Lockstep kernel (kernel = 4): a wavefront steps the block rows of one
+// "group set" in lockstep, one stored block each per step, over a tile of
+// output columns whose X rows sit in one of two LDS buffers.  Two modes:
+//   matrix (1 x 4 blocks): a stored block times a 4-column X vector is a
+//     4 x 4 outer product, and the matrix cores' fp32 4x4x1 instruction
+//     computes 16 of them at once, each from its own block of 4 lanes
+//     (register r of lane 4b + t gets A[4b + r] * B[4b + t] + C, one
+//     rounding, like a fused multiply-add);
+//   vector (unstructured, 1 x 1): each lane adds weight * X for its row and 4
+//     columns with fused multiply-adds.
 //
-//   Tiles.  kOuterCols = 32 consecutive output columns; the tile's X rows
-//   (kOuterRowBytes = 128 bytes each: channel c at byte c * 128, then unused
-//   rows up to ozrow = cin rounded up to 8, then one row of zeros) fill one of
-//   two LDS buffers.
-//   Octs.  Block rows sorted by stored blocks (descending, ties by row index)
-//   are taken kOctRows = 8 at a time.  Group g of a wavefront (lanes 8g ..
-//   8g + 7, two lane blocks) works on block row g of its oct; the 8 rows move
-//   in lockstep, one stored block each per step, in ascending channel, for
-//   4 * nquads steps (the longest row rounded up to whole quads of 4 steps,
-//   at least one); a row past its last block reads the zero row with weight 0.
-//   Records, per oct and quad j of steps 4j .. 4j + 3:
-//     orec  per slot u = 4g + t (32 slots), four words: the weight of element
-//           t of block row g's block at each of the 4 steps (fp32 bits of the
-//           weight, rounded to fp16 first for fp16 storage; 0 for padding).
-//           Lanes 8g + t and 8g + 4 + t read slot 4g + t.
-//     ooff  per group g (8), four words: the LDS byte offset of the channel
-//           row each of the 4 steps reads (channel * 128; padding ozrow * 128).
-//   Oct o's quads start at quad ooct_tab[kOctWords * o] of both arrays and run
-//   ooct_tab[.. + 1] quads; words 2 .. 9 hold its block rows (-1: none).  Both
-//   arrays end with kOuterAhead zero quads (read ahead, unused).
-//   Waves.  The octs are dealt to owaves wavefronts twice, longest first to
+//   Tiles.  otw = 32 consecutive output columns (16 in vector mode when cin
+//   exceeds kOuterMaxCin32); the tile's X rows (4 * otw bytes each: channel c
+//   at byte 4 * otw * c, then unused rows up to ozrow = cin rounded up to the
+//   rows one 1 KB copy moves, then one row of zeros) fill one of two LDS
+//   buffers.  A lane covers 4 columns, so a lane group of otw / 4 lanes
+//   covers the tile and a wavefront has ogroups = 256 / otw groups.
+//   Group sets.  Block rows sorted by stored blocks (descending, ties by row
+//   index) are taken ogroups at a time; group g works on block row g of its
+//   set, all in lockstep, in ascending channel, for 4 * nquads steps (the
+//   longest row rounded up to whole quads of 4 steps, at least one); a row
+//   past its last block reads the zero row with weight 0.
+//   Records, per set and quad j of steps 4j .. 4j + 3:
+//     orec  per weight slot u (matrix: u = 4g + t, 32 slots, element t of
+//           group g's block; vector: u = g), four words: the slot's weight at
+//           each of the 4 steps (fp32 bits, rounded to fp16 first for fp16
+//           storage; 0 for padding).  Matrix lanes 8g + t and 8g + 4 + t read
+//           slot 4g + t; vector lanes of group g read slot g.
+//     ooff  per group g, four words: the LDS byte offset of the channel row
+//           each of the 4 steps reads (channel * 4 * otw; padding
+//           ozrow * 4 * otw).
+//   Set o's quads start at quad ooct_tab[kOctWords * o] of both arrays and run
+//   ooct_tab[.. + 1] quads; words 2 .. 2 + ogroups - 1 hold its block rows
+//   (-1: none).  Both arrays end with kOuterAhead zero quads (read ahead).
+//   Waves.  The sets are dealt to owaves wavefronts twice, longest first to
 //   the least loaded: once for even tiles, then again for odd tiles starting
 //   from the even loads, so each wavefront's two-tile total is balanced.  Wave
-//   w's octs for tiles of parity q are owave_oct[owave_ptr[q * owaves + w] ..
+//   w's sets for tiles of parity q are owave_oct[owave_ptr[q * owaves + w] ..
 //   owave_ptr[q * owaves + w + 1]).
-constexpr int32_t kOuterCols = 32;
-constexpr int32_t kOuterRowBytes = 128;
-constexpr int32_t kOctRows = 8;
-constexpr int32_t kOctWords = 16;
+constexpr int32_t kOuterCols = 32;   // the widest tile
+constexpr int32_t kOctWords = 32;
 constexpr int32_t kOuterAhead = 4;   // quads of records read ahead
 constexpr int32_t kOuterQuadSteps = 4;
-constexpr int32_t kOuterSlots = 32;
-// Widest input the outer-product kernel takes: two buffers of (ozrow + 1) rows
-// and the control words within one workgroup's LDS.
-constexpr int32_t kOuterMaxCin = 632;
+// Widest input with two buffers of 32-column tiles (and their control words)
+// in one workgroup's LDS; with 16-column tiles (vector mode only).
+constexpr int32_t kOuterMaxCin32 = 632;
+constexpr int32_t kOuterMaxCin16 = 1264;
 
 struct Input {
     int32_t cout = 0, cin = 0, block_rows = 1;
@@ -296,10 +302,13 @@ struct PackedPlan {
     std::vector<float> rrow_bias;  // bias of every output channel (the row-pair phase)
     // outer-product kernel (planner.hpp, "Outer-product kernel"); empty when
     // the plan cannot use it
-    int32_t use_outer = 0;   // spconv_run launches the outer-product kernel
-    int32_t oocts = 0;       // octs of kOctRows block rows
+    int32_t use_outer = 0;   // spconv_run launches the lockstep kernel
+    int32_t omode = 0;       // 0 matrix (1 x 4 blocks), 1 vector (unstructured)
+    int32_t otw = 32;        // tile columns
+    int32_t ogroups = 8;     // lane groups (block rows of a set) per wavefront
+    int32_t oocts = 0;       // group sets
     int32_t owaves = 0;      // wavefronts per workgroup
-    int32_t ozrow = 0;       // LDS row of zeros (cin rounded up to 8)
+    int32_t ozrow = 0;       // LDS row of zeros
     std::vector<uint32_t> orec;
     std::vector<uint32_t> ooff;
     std::vector<int32_t> ooct_tab;
@@ -366,12 +375,13 @@ void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float 
 // in processing order.
 void build_indexed(const Input &in, const std::vector<int32_t> &order, PackedPlan &p);
 
-// Whether the outer-product kernel can run this layer (1 x 4 blocks, no
-// depthwise stage, cin <= kOuterMaxCin).
+// Whether the lockstep kernel can run this layer: 1 x 4 blocks (matrix
+// mode) with cin <= kOuterMaxCin32, or unstructured fp32 (vector mode) with
+// cin <= kOuterMaxCin16; no depthwise stage.
 bool outer_supported(const Input &in);
-// Build its octs, records and wave lists (fields o* of PackedPlan).
+// Build its group sets, records and wave lists (fields o* of PackedPlan).
 void build_outer(const Input &in, PackedPlan &p);
-// Rebuild block-CSR arrays from the outer-product records, checking their
+// Rebuild block-CSR arrays from the lockstep kernel's records, checking their
 // structure (lockstep padding, ascending channels, offsets, wave lists).
 // E_FORMAT with `err` set when inconsistent or absent.
 Status unpack_outer(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, std::string &err);

@@ -228,20 +228,22 @@ int64_t indexed_min_cols(const spconv::PackedPlan &h, const spconv::DevicePlan &
     return 0;
 }
 
-// The automatic choice of the outer-product kernel (1 x 4 blocks), from its
-// measured times on MI355X over the workload layers: it wins once a run has
-// at least one round of its 32-column tiles over the compute units and the
-// octs average at least two quads (8 steps); with shorter rows (few input
-// channels) its per-tile costs dominate and the other kernels are faster.
+// The automatic choice of the lockstep kernel, from its measured times on
+// MI355X over the workload layers.  Matrix mode (1 x 4 blocks): it wins at
+// every batch measured (runs with fewer tiles than compute units share each
+// tile among workgroups by set) when the sets average at least two quads (8
+// steps); with shorter rows (few input channels) its per-tile costs
+// dominate.  Vector mode (unstructured): it wins only on inputs too wide for
+// an LDS strip (where the others read X from L2 per nonzero).
 int64_t outer_min_cols(const spconv::PackedPlan &h, const spconv::DevicePlan &d) {
     if (!h.auto_kernel || d.oocts == 0 || d.num_cus <= 0)
         return 0;
+    if (h.omode == 1)
+        return h.kernel == spconv::KERNEL_DIRECT ? 1 : 0;
     int64_t quads = 0;
     for (int32_t o = 0; o < h.oocts; ++o)
         quads += h.ooct_tab[static_cast<size_t>(o) * spconv::kOctWords + 1];
-    if (quads < 2 * static_cast<int64_t>(h.oocts))
-        return 0;
-    return int64_t(spconv::kOuterCols) * d.num_cus;
+    return quads >= 2 * static_cast<int64_t>(h.oocts) ? 1 : 0;
 }
 
 void fill_device_geometry(spconv_plan_s *pl) {
@@ -277,6 +279,8 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.rnch = h.rnch;
     d.rlane_cols = h.rlane_cols;
     d.use_outer = h.use_outer;
+    d.omode = h.omode;
+    d.otw = h.otw;
     d.oocts = h.oocts;
     d.owaves = h.owaves;
     d.ozrow = h.ozrow;
@@ -590,7 +594,7 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const bool outer = p.use_outer || (plan->dev.outer_min_cols > 0 && m >= plan->dev.outer_min_cols);
     const bool indexed = !outer && (plan->dev.use_indexed ||
                                     (plan->dev.indexed_min_cols > 0 && m >= plan->dev.indexed_min_cols));
-    const int64_t tile_cols = outer ? spconv::kOuterCols : indexed ? 64 * 6 : p.tile_cols;
+    const int64_t tile_cols = outer ? p.otw : indexed ? 64 * 6 : p.tile_cols;
     const int64_t span = (tile_cols - 1) / hw + 2;
     if (span * std::max(ihw * p.cin, hw * p.cout) * static_cast<int64_t>(e) >= (int64_t(1) << 31) - 16)
         return fail(SPCONV_E_UNSUPPORTED,

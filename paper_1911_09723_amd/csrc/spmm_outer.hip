@@ -34,6 +34,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "launch.hpp"
@@ -78,6 +79,19 @@ constexpr int kCtlRel = 0, kCtlFill = 2, kCtlFree = 4, kCtlWords = 6;
 // 4 with one load per lane each, 2 with 4 element loads each.
 template <bool VEC>
 constexpr int stage_max() { return VEC ? 4 : 2; }
+
+// Geometry of a mode (0 matrix, 1 vector) and tile width TW: lanes per group
+// (4 columns each), groups per wavefront, bytes per LDS row, rows per 1 KB
+// copy instruction, weight slots per group and per quad.
+template <int MODE, int TW>
+struct LGeo {
+    static constexpr int LPG = TW / 4;
+    static constexpr int G = 64 / LPG;
+    static constexpr int RB = TW * 4;
+    static constexpr int RPI = 1024 / RB;
+    static constexpr int KW = MODE == 0 ? 4 : 1;
+    static constexpr int SLOTS = G * KW;
+};
 constexpr int32_t kOutOfRange = static_cast<int32_t>(0x80000000u);
 constexpr int64_t kMaxRecords = 0x7ffffff0;
 
@@ -121,12 +135,12 @@ __device__ __forceinline__ int32_t tiles_of(const OArgs &a, int32_t slot) {
     return a.rounds + (a.rem > 0 && slot / a.parts < a.rem ? 1 : 0);
 }
 
-// The 4 columns of lane vector (lane % 8) of a tile, counted from channel 0
+// The 4 columns of lane vector (lane % (TW / 4)) of a tile, counted from channel 0
 // of the tile's first image n0 (the images one tile touches span less than
 // 2^31 bytes): X byte offsets (kOutOfRange past the last column) and Y
 // element offsets from ybase (-1 past it).  With VEC the 4 columns lie in one
 // image and only element 0 is kept.
-template <bool F16, bool VEC>
+template <int TW, bool F16, bool VEC>
 struct Cols {
     static constexpr int NE = VEC ? 1 : 4;
     int32_t n0;
@@ -135,12 +149,12 @@ struct Cols {
     int32_t yo[NE];
     __device__ __forceinline__ void set(const OArgs &a, int32_t tile, int lane) {
         constexpr int E = F16 ? 2 : 4;
-        const int32_t col0 = tile * kOuterCols;
+        const int32_t col0 = tile * TW;
         n0 = col0 / a.hw;
         ybase = static_cast<int64_t>(n0) * a.cout * a.hw;
 #pragma unroll
         for (int e = 0; e < NE; ++e) {
-            const int32_t c = col0 + (lane & 7) * 4 + e;
+            const int32_t c = col0 + (lane % (TW / 4)) * 4 + e;
             const int32_t n = c / a.hw;
             const int32_t p = c - n * a.hw;
             xo[e] = c < a.m ? ((n - n0) * a.cin * a.hw + p) * E : kOutOfRange;
@@ -166,8 +180,9 @@ __device__ __forceinline__ f4 lds_vec(const unsigned char *lds, uint32_t byte) {
 // the buffer's fill count.  One share (or one phase of a staged share) is in
 // flight at a time.  Checks inside an oct come after at least N newer loads,
 // and loads complete in order, so a wait for vmcnt <= N finds the copies done.
-template <bool DMA, bool F16, bool VEC>
+template <int TW, bool DMA, bool F16, bool VEC>
 struct Refill {
+    using GE = LGeo<1, TW>;  // copy geometry (the same in both modes)
     int32_t issued0, issued1;  // sequence number of the last tile whose share this wave started, per buffer
     int32_t sb;         // buffer of the copy in flight, -1 for none
     int32_t sk;         // its tile sequence number
@@ -181,19 +196,19 @@ struct Refill {
         sb = b;
         sk = k;
         sfirst = first;
-        const int ninstr = a.ozrow / 8;
-        Cols<F16, VEC> cols;
+        const int ninstr = a.ozrow / GE::RPI;
+        Cols<TW, F16, VEC> cols;
         cols.set(a, tile_of(a, slot, k), lane);
         constexpr int E = F16 ? 2 : 4;
         const int64_t xbase = static_cast<int64_t>(cols.n0) * a.cin * a.hw;
-        const int32_t crow = lane >> 3;
-        const int32_t step = 8 * a.hw * E;
+        const int32_t crow = lane / GE::LPG;
+        const int32_t step = GE::RPI * a.hw * E;
         if constexpr (DMA) {
             const i4 rs = rsrc_words(static_cast<const float *>(a.x) + xbase, a.x_bytes - xbase * 4);
             const int32_t lo = cols.xo[0] == kOutOfRange ? kOutOfRange : cols.xo[0] + crow * a.hw * 4;
             const uint32_t buf = b * a.buf_bytes;
             for (int i = wave; i < ninstr; i += a.waves) {
-                const int32_t voff = lo != kOutOfRange && 8 * i + crow < a.cin ? lo + i * step : kOutOfRange;
+                const int32_t voff = lo != kOutOfRange && GE::RPI * i + crow < a.cin ? lo + i * step : kOutOfRange;
                 const uint32_t m0 = __builtin_amdgcn_readfirstlane(buf + 1024 * i);
                 asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                              :
@@ -207,8 +222,8 @@ struct Refill {
             for (int s = 0; s < kStageMax; ++s) {
                 const int i = wave + (first + s) * a.waves;
                 if (i < ninstr) {
-                    const bool row_ok = 8 * i + crow < a.cin;
-                    const int32_t ro = (8 * i + crow) * a.hw * E;
+                    const bool row_ok = GE::RPI * i + crow < a.cin;
+                    const int32_t ro = (GE::RPI * i + crow) * a.hw * E;
                     if constexpr (VEC) {
                         const int32_t o = row_ok && cols.xo[0] != kOutOfRange ? cols.xo[0] + ro : kOutOfRange;
                         if constexpr (F16) {
@@ -271,7 +286,7 @@ struct Refill {
                     *reinterpret_cast<f4 *>(lds + buf + 1024 * i + 16 * lane) = v;
                 }
             }
-            if (wave + (sfirst + sn) * a.waves < a.ozrow / 8) {
+            if (wave + (sfirst + sn) * a.waves < a.ozrow / GE::RPI) {
                 start(a, slot, wave, lane, sb, sk, sfirst + sn);
                 return;
             }
@@ -335,45 +350,57 @@ struct Refill {
     }
 };
 
-// One oct on the tile in the buffer at byte `buf`: lockstep steps, then bias,
-// activation and 16-byte stores of the lane's 4 rows x 4 columns.  OFF_LDS:
-// the channel-row offsets come from the workgroup's LDS copy of the table,
-// else from global memory.
-template <bool OFF_LDS, bool DMA, bool F16, bool VEC>
+// One group set on the tile in the buffer at byte `buf`: lockstep steps,
+// then bias, activation and stores of the lane's rows (matrix: 4, vector: 1)
+// and 4 columns.  OFF_LDS: the channel-row offsets come from the
+// workgroup's LDS copy of the table, else from global memory.
+template <int MODE, int TW, bool OFF_LDS, bool DMA, bool F16, bool VEC>
 __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int32_t o, uint32_t buf,
-                                        const Cols<F16, VEC> &cols, float lo, float hi, int lane, int32_t *ctl,
-                                        Refill<DMA, F16, VEC> &rf, int32_t slot, int wave) {
+                                        const Cols<TW, F16, VEC> &cols, float lo, float hi, int lane, int32_t *ctl,
+                                        Refill<TW, DMA, F16, VEC> &rf, int32_t slot, int wave) {
+    using GE = LGeo<MODE, TW>;
     const int32_t *tab = a.oct + o * kOctWords;
     const int32_t q0 = __builtin_amdgcn_readfirstlane(tab[0]);
     const int32_t nq = __builtin_amdgcn_readfirstlane(tab[1]);
-    const int g = lane >> 3;
+    const int g = lane / GE::LPG;
     const int32_t rb = tab[2 + g];
-    const f4 *wp = a.rec + (static_cast<int64_t>(q0) * kOuterSlots + g * 4 + (lane & 3));
-    const int64_t og = static_cast<int64_t>(q0) * kOctRows + g;  // (quad, group) index of the offsets
+    const int wslot = MODE == 0 ? g * 4 + (lane & 3) : g;
+    const f4 *wp = a.rec + (static_cast<int64_t>(q0) * GE::SLOTS + wslot);
+    const int64_t og = static_cast<int64_t>(q0) * GE::G + g;  // (quad, group) index of the offsets
     auto offs = [&](int32_t j) -> i4 {
         if constexpr (OFF_LDS)
-            return *reinterpret_cast<const i4 *>(lds + a.off_lds + (og + int64_t(j) * kOctRows) * 16);
+            return *reinterpret_cast<const i4 *>(lds + a.off_lds + (og + int64_t(j) * GE::G) * 16);
         else
-            return a.off[og + int64_t(j) * kOctRows];
+            return a.off[og + int64_t(j) * GE::G];
     };
-    const uint32_t xl = buf + (lane & 7) * 16;
+    const uint32_t xl = buf + (lane % GE::LPG) * 16;
     f4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = acc0, acc2 = acc0, acc3 = acc0;
     auto mma = [&](float w, const f4 x) {
-        acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.x, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.y, acc1, 0, 0, 0);
-        acc2 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.z, acc2, 0, 0, 0);
-        acc3 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.w, acc3, 0, 0, 0);
+        if constexpr (MODE == 0) {
+            acc0 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.x, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.y, acc1, 0, 0, 0);
+            acc2 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.z, acc2, 0, 0, 0);
+            acc3 = __builtin_amdgcn_mfma_f32_4x4x1f32(w, x.w, acc3, 0, 0, 0);
+        } else {
+            // fused multiply-adds kept in program order (volatile): otherwise
+            // the compiler sinks them below the refill checks and holds every
+            // X vector of several quads in registers
+            asm volatile("v_fmac_f32 %0, %4, %5\n\tv_fmac_f32 %1, %4, %6\n\tv_fmac_f32 %2, %4, %7\n\t"
+                         "v_fmac_f32 %3, %4, %8"
+                         : "+v"(acc0.x), "+v"(acc0.y), "+v"(acc0.z), "+v"(acc0.w)
+                         : "v"(w), "v"(x.x), "v"(x.y), "v"(x.z), "v"(x.w));
+        }
     };
     auto xrow = [&](int32_t off) { return lds_vec(lds, xl + static_cast<uint32_t>(off)); };
     // Software pipeline: weights kOuterAhead quads ahead in registers (the
     // arrays are padded for it), the next quad's offsets one quad ahead, and
-    // each step's X vector read before the previous step's matrix
-    // instructions (two register sets, alternating by step).
+    // each step's X vector read before the previous step's arithmetic (two
+    // register sets, alternating by step).
     f4 wq[kOuterAhead];
 #pragma unroll
     for (int i = 0; i < kOuterAhead; ++i)
-        wq[i] = wp[i * kOuterSlots];
-    wp += kOuterAhead * kOuterSlots;
+        wq[i] = wp[i * GE::SLOTS];
+    wp += kOuterAhead * GE::SLOTS;
     i4 oq = offs(0);
     f4 xs[2];
     xs[0] = xrow(oq.x);
@@ -398,11 +425,11 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
         for (int i = 0; i < kOuterAhead; ++i) {
             const i4 nx = offs(j + i + 1);
             quad(wq[i], nx);
-            wq[i] = wp[i * kOuterSlots];  // after its last use: no copy of the old weights
+            wq[i] = wp[i * GE::SLOTS];  // after its last use: no copy of the old weights
             oq = nx;
             __builtin_amdgcn_sched_barrier(0);
         }
-        wp += kOuterAhead * kOuterSlots;
+        wp += kOuterAhead * GE::SLOTS;
         // loads since the last check: kOuterAhead weight loads (and as many offset loads)
         rf.template check<OFF_LDS ? kOuterAhead : 2 * kOuterAhead>(a, lds, ctl, slot, wave, lane);
     }
@@ -414,45 +441,63 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
             oq = nx;
         }
     }
-    if (rb >= 0) {
-        const f4 bz = *reinterpret_cast<const f4 *>(a.bias + 4 * rb);
+    if (rb < 0)
+        return;
+    constexpr int NR = MODE == 0 ? 4 : 1;  // rows of this lane
+    float bz[NR];
+    if constexpr (MODE == 0) {
+        const f4 b4 = *reinterpret_cast<const f4 *>(a.bias + 4 * rb);
+        bz[0] = b4.x;
+        bz[1] = b4.y;
+        bz[2] = b4.z;
+        bz[3] = b4.w;
+    } else {
+        bz[0] = a.bias[rb];
+    }
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            f4 v;
+    for (int r = 0; r < NR; ++r) {
+        f4 v;
+        if constexpr (MODE == 0) {
             v.x = fminf(fmaxf(acc0[r] + bz[r], lo), hi);
             v.y = fminf(fmaxf(acc1[r] + bz[r], lo), hi);
             v.z = fminf(fmaxf(acc2[r] + bz[r], lo), hi);
             v.w = fminf(fmaxf(acc3[r] + bz[r], lo), hi);
-            const int32_t ro = (4 * rb + r) * a.hw;
-            if constexpr (VEC) {
-                if (cols.yo[0] >= 0) {
-                    if constexpr (F16) {
-                        u2 h;
-                        h.x = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.x)) |
-                              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.y))) << 16;
-                        h.y = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.z)) |
-                              static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.w))) << 16;
-                        *reinterpret_cast<u2 *>(static_cast<_Float16 *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = h;
-                    } else {
-                        *reinterpret_cast<f4 *>(static_cast<float *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = v;
-                    }
+        } else {
+            v.x = fminf(fmaxf(acc0.x + bz[0], lo), hi);
+            v.y = fminf(fmaxf(acc0.y + bz[0], lo), hi);
+            v.z = fminf(fmaxf(acc0.z + bz[0], lo), hi);
+            v.w = fminf(fmaxf(acc0.w + bz[0], lo), hi);
+        }
+        const int32_t ro = (NR * rb + r) * a.hw;
+        if constexpr (VEC) {
+            if (cols.yo[0] >= 0) {
+                if constexpr (F16) {
+                    u2 h;
+                    h.x = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.x)) |
+                          static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.y))) << 16;
+                    h.y = __builtin_bit_cast(uint16_t, static_cast<_Float16>(v.z)) |
+                          static_cast<uint32_t>(__builtin_bit_cast(uint16_t, static_cast<_Float16>(v.w))) << 16;
+                    *reinterpret_cast<u2 *>(static_cast<_Float16 *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = h;
+                } else {
+                    *reinterpret_cast<f4 *>(static_cast<float *>(a.y) + cols.ybase + (cols.yo[0] + ro)) = v;
                 }
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    if (cols.yo[e] >= 0) {
-                        if constexpr (F16)
-                            static_cast<_Float16 *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = static_cast<_Float16>(v[e]);
-                        else
-                            static_cast<float *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = v[e];
-                    }
             }
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                if (cols.yo[e] >= 0) {
+                    if constexpr (F16)
+                        static_cast<_Float16 *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = static_cast<_Float16>(v[e]);
+                    else
+                        static_cast<float *>(a.y)[cols.ybase + (cols.yo[e] + ro)] = v[e];
+                }
         }
     }
 }
 
-template <bool OFF_LDS, bool F16, bool VEC>
+template <int MODE, int TW, bool OFF_LDS, bool F16, bool VEC>
 __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
+    using GE = LGeo<MODE, TW>;
     constexpr bool DMA = !F16 && VEC;
     extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
     const int lane = threadIdx.x & 63;
@@ -464,9 +509,9 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
     int32_t *ctl = reinterpret_cast<int32_t *>(lds + a.ctl_off);
     // zero rows of both buffers; control words: buffer 0 free for tile 0,
     // buffer 1 for tile 1; the offset table
-    if (threadIdx.x < 16) {
-        const int b = threadIdx.x >> 3;
-        *reinterpret_cast<f4 *>(lds + b * a.buf_bytes + a.ozrow * kOuterRowBytes + (threadIdx.x & 7) * 16) =
+    if (threadIdx.x < 2 * GE::LPG) {
+        const int b = threadIdx.x / GE::LPG;
+        *reinterpret_cast<f4 *>(lds + b * a.buf_bytes + a.ozrow * GE::RB + (threadIdx.x % GE::LPG) * 16) =
             f4{0.f, 0.f, 0.f, 0.f};
     }
     if (threadIdx.x < kCtlWords)
@@ -486,7 +531,7 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
     __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): zero rows and control words written
     __syncthreads();
 
-    Refill<DMA, F16, VEC> rf;
+    Refill<TW, DMA, F16, VEC> rf;
     rf.issued0 = -1;
     rf.issued1 = -1;
     rf.sb = -1;
@@ -513,19 +558,19 @@ __global__ void __launch_bounds__(1024) outer_kernel(OArgs a) {
                 }
             }
         }
-        Cols<F16, VEC> cols;
+        Cols<TW, F16, VEC> cols;
         cols.set(a, tile_of(a, slot, k), lane);
         if (k < a.rounds || a.parts == 1) {
             const int q = k & 1;
             const int32_t e0 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave]);
             const int32_t e1 = __builtin_amdgcn_readfirstlane(a.wave_ptr[q * a.waves + wave + 1]);
             for (int32_t e = e0; e < e1; ++e)
-                run_oct<OFF_LDS>(a, lds, __builtin_amdgcn_readfirstlane(a.wave_oct[e]), buf, cols, lo, hi, lane, ctl,
-                                 rf, slot, wave);
+                run_oct<MODE, TW, OFF_LDS>(a, lds, __builtin_amdgcn_readfirstlane(a.wave_oct[e]), buf, cols, lo, hi,
+                                           lane, ctl, rf, slot, wave);
         } else {
             // a shared last tile: this position's octs, one per wavefront in turn
             for (int32_t o = slot % a.parts + a.parts * wave; o < a.noct; o += a.parts * a.waves)
-                run_oct<OFF_LDS>(a, lds, o, buf, cols, lo, hi, lane, ctl, rf, slot, wave);
+                run_oct<MODE, TW, OFF_LDS>(a, lds, o, buf, cols, lo, hi, lane, ctl, rf, slot, wave);
         }
         if (k + 2 < nt) {
             __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's reads of the buffer are done
@@ -549,7 +594,7 @@ struct OuterLds {
 
 OuterLds outer_lds(const DevicePlan &p) {
     OuterLds l;
-    l.buf_bytes = (p.ozrow + 1) * kOuterRowBytes;
+    l.buf_bytes = (p.ozrow + 1) * 4 * p.otw;
     const int32_t table = (p.ooff_bytes + 1023) / 1024 * 1024;
     if (2 * l.buf_bytes + table + kCtlWords * 4 <= kMaxLdsBytes) {
         l.off_lds = 2 * l.buf_bytes;
@@ -564,19 +609,30 @@ OuterLds outer_lds(const DevicePlan &p) {
 
 typedef void (*OKernel)(OArgs);
 
-template <bool OFF_LDS>
-OKernel pick_outer(bool f16, bool vec) {
-    if (f16)
-        return vec ? outer_kernel<OFF_LDS, true, true> : outer_kernel<OFF_LDS, true, false>;
-    return vec ? outer_kernel<OFF_LDS, false, true> : outer_kernel<OFF_LDS, false, false>;
+template <int MODE, int TW, bool OFF_LDS>
+OKernel pick3(bool f16, bool vec) {
+    if constexpr (MODE == 0) {
+        if (f16)
+            return vec ? outer_kernel<MODE, TW, OFF_LDS, true, true> : outer_kernel<MODE, TW, OFF_LDS, true, false>;
+    }
+    return vec ? outer_kernel<MODE, TW, OFF_LDS, false, true> : outer_kernel<MODE, TW, OFF_LDS, false, false>;
+}
+
+// The instantiation for a plan's mode and tile width, the table's place, the
+// storage type and the vector path (fp16 only in matrix mode).
+OKernel pick_outer(int mode, int tw, bool off_lds, bool f16, bool vec) {
+    if (mode == 0)
+        return off_lds ? pick3<0, 32, true>(f16, vec) : pick3<0, 32, false>(f16, vec);
+    if (tw == 32)
+        return off_lds ? pick3<1, 32, true>(f16, vec) : pick3<1, 32, false>(f16, vec);
+    return off_lds ? pick3<1, 16, true>(f16, vec) : pick3<1, 16, false>(f16, vec);
 }
 
 }  // namespace
 
 hipError_t prepare_outer(const DevicePlan &p) {
-    (void)p;
     for (int v = 0; v < 8; ++v) {
-        const OKernel k = (v & 4) ? pick_outer<true>(v & 1, v & 2) : pick_outer<false>(v & 1, v & 2);
+        const OKernel k = pick_outer(p.omode, p.otw, v & 4, (v & 1) && p.omode == 0, v & 2);
         const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void *>(k),
                                                  hipFuncAttributeMaxDynamicSharedMemorySize,
                                                  static_cast<int>(kMaxLdsBytes));
@@ -609,29 +665,32 @@ hipError_t launch_outer(const DevicePlan &p, const void *x, void *y, int32_t m, 
     a.hw = hw;
     a.m = m;
     a.act = p.act;
-    a.ntiles = (m + kOuterCols - 1) / kOuterCols;
+    a.ntiles = (m + p.otw - 1) / p.otw;
     const int32_t cus = p.num_cus > 0 ? p.num_cus : 256;
-    a.grid = a.ntiles < cus ? a.ntiles : cus;
-    a.nx = a.grid % 8 == 0 ? 8 : 1;
-    a.rounds = a.ntiles / a.grid;
-    a.rem = a.ntiles % a.grid;
     a.noct = p.oocts;
-    // share each left-over tile among as many workgroups as the grid holds
-    // for it, at most one per oct
-    a.parts = 1;
-    if (a.rem > 0)
-        for (int32_t q = a.grid / a.rem; q >= 2; --q)
-            if (q <= p.oocts) {
-                a.parts = q;
-                break;
-            }
+    if (a.ntiles >= cus) {
+        // whole rounds of the grid, then each left-over tile shared among as
+        // many workgroups as the grid holds for it, at most one per set
+        a.grid = cus;
+        a.rounds = a.ntiles / a.grid;
+        a.rem = a.ntiles % a.grid;
+        a.parts = 1;
+        if (a.rem > 0)
+            a.parts = std::max(1, std::min(a.grid / a.rem, p.oocts));
+    } else {
+        // fewer tiles than compute units: every tile shared that way
+        a.rounds = 0;
+        a.rem = a.ntiles;
+        a.parts = std::max(1, std::min(cus / a.ntiles, p.oocts));
+        a.grid = a.ntiles * a.parts;
+    }
+    a.nx = a.grid % 8 == 0 ? 8 : 1;
     a.waves = p.owaves;
     a.ozrow = p.ozrow;
     a.buf_bytes = l.buf_bytes;
     a.ctl_off = l.ctl_off;
     a.x_bytes = x_bytes;
-    const bool f16 = p.storage == 1;
-    const OKernel k = l.off_lds >= 0 ? pick_outer<true>(f16, vec != 0) : pick_outer<false>(f16, vec != 0);
+    const OKernel k = pick_outer(p.omode, p.otw, l.off_lds >= 0, p.storage == 1, vec != 0);
     hipLaunchKernelGGL(k, dim3(a.grid), dim3(64 * a.waves), l.total, stream, a);
     return hipGetLastError();
 }

@@ -123,3 +123,36 @@ def test_outer_unaligned_pointers_take_the_staged_copy():
         assert np.array_equal(y.cpu().numpy(), ref)
     finally:
         plan.close()
+
+
+# (cin, cout, h, w, n, sparsity, act): unstructured layers on the vector mode
+# (one fused multiply-add per lane and column per step): 32-column tiles up
+# to 632 input channels, 16-column tiles above; ragged H*W; a partial set
+VECTOR = [
+    (64, 64, 4, 4, 3, 0.8, "relu"),
+    (512, 512, 14, 14, 4, 0.9, "relu"),
+    (96, 40, 7, 7, 9, 0.7, "relu6"),
+    (1024, 1024, 7, 7, 8, 0.9, "relu6"),
+    (960, 160, 7, 7, 6, 0.85, "none"),
+    (1264, 24, 5, 5, 3, 0.9, "relu"),
+    (17, 20, 2, 2, 9, 0.5, "none"),
+]
+
+
+@pytest.mark.parametrize("spec", VECTOR, ids=lambda s: "%d-%d-%dx%d-n%d-s%g-%s" % s)
+def test_vector_mode_matches_oracle_and_direct_kernel(spec):
+    cin, cout, h, w, n, s, act = spec
+    layer = make_layer(cin, cout, h, w, n, s, block_rows=1, act=act, seed=zlib.crc32(repr(spec).encode()) % 1000)
+    note("lockstep vector %s" % (spec,))
+    y = gpu_run(layer, kernel=4)
+    assert_parity(layer, y, what=str(spec))
+    assert np.array_equal(y, gpu_run(layer, kernel=2)), "not bitwise equal to the direct-load kernel"
+
+
+@pytest.mark.parametrize("n", [64, 256])
+def test_vector_mode_headline_layer(n):
+    layer = make_layer(512, 512, 14, 14, n, 0.9, block_rows=1, act="relu", seed=91 + n)
+    note("lockstep vector headline n=%d" % n)
+    y = gpu_run(layer, kernel=4)
+    assert_parity(layer, y, what="n=%d" % n)
+    assert np.array_equal(y, gpu_run(layer, kernel=2))
