@@ -200,8 +200,8 @@ SPCONV_API spconv_status spconv_plan_create_dense(spconv_plan *out, int32_t cout
  *   stride  1 or 2 (the network stem uses 2)
  * Errors: SPCONV_E_ARG (NULL pointer with work to do, negative size, bad
  * stride or act, overlap), SPCONV_E_SHAPE (cin or cout < 1, too many
- * pixels), SPCONV_E_UNSUPPORTED (cin > 8 or cout * (9 cin + 1) > 16384:
- * the weights are held in LDS), SPCONV_E_HIP.
+ * pixels, an image of 2^31 or more elements, n * ceil(ho * wo / 256) of
+ * 2^31 or more), SPCONV_E_UNSUPPORTED (cin > 8), SPCONV_E_HIP.
  */
 SPCONV_API spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const float *bias, spconv_act act,
                                  int32_t stride, float *y, int32_t n, int32_t h, int32_t w, int32_t cin,

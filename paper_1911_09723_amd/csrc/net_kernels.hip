@@ -7,6 +7,7 @@
 // arithmetic, zero padding 1.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "net_kernels.hpp"
@@ -25,27 +26,27 @@ __device__ __forceinline__ float clamp_act(float v, int32_t act) {
 // Dense 3x3 convolution, HWC in, CHW out:
 //   Y[n, o, oy, ox] = act(b[o] + sum_{dy, dx, i} Wt[o][dy][dx][i] * X[n, s*oy + dy - 1, s*ox + dx - 1, i])
 // Thread = one output pixel: it gathers the 9 * CIN inputs of its receptive
-// field once (zeros outside the image) and produces all cout channels, the
-// weights read from LDS (every lane reads the same word: a broadcast).
-// Consecutive threads are consecutive ox, so each channel's stores coalesce.
+// field once (zeros outside the image) and produces all cout channels.  A
+// weight is the same for every lane, so the weights are read through the
+// constant address space: scalar loads into SGPRs that each FMA takes as an
+// operand (an LDS copy costs one LDS read per four FMAs and bounds the
+// kernel).  Workgroup = 256 consecutive pixels of one image (block b covers
+// image b / bpi), so no thread divides 64-bit indices; consecutive threads
+// are consecutive pixels and each channel's stores coalesce.
+using ConstF = const __attribute__((address_space(4))) float;
+
 template <int CIN>
 __global__ void __launch_bounds__(256)
 conv3x3_hwc_kernel(const float *__restrict__ x, const float *__restrict__ wt, const float *__restrict__ bias,
-                   float *__restrict__ y, int64_t pixels, int32_t h, int32_t w, int32_t ho, int32_t wo,
+                   float *__restrict__ y, int32_t bpi, int32_t h, int32_t w, int32_t ho, int32_t wo,
                    int32_t cout, int32_t stride, int32_t act) {
-    extern __shared__ float sw[];  // cout * 9 * CIN weights, then cout biases
-    const int32_t nw = cout * 9 * CIN;
-    for (int32_t i = threadIdx.x; i < nw; i += blockDim.x)
-        sw[i] = wt[i];
-    for (int32_t i = threadIdx.x; i < cout; i += blockDim.x)
-        sw[nw + i] = bias ? bias[i] : 0.0f;
-    __syncthreads();
-    const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (q >= pixels)
+    const int32_t img = blockIdx.x / bpi;
+    const int32_t plane = ho * wo;
+    const int32_t pp = (blockIdx.x - img * bpi) * 256 + threadIdx.x;
+    if (pp >= plane)
         return;
-    const int64_t img = q / (static_cast<int64_t>(ho) * wo);
-    const int32_t pp = static_cast<int32_t>(q - img * ho * wo);
     const int32_t oy = pp / wo, ox = pp - oy * wo;
+    const float *xi = x + static_cast<int64_t>(img) * h * w * CIN;
     float v[9][CIN];
 #pragma unroll
     for (int dy = 0; dy < 3; ++dy) {
@@ -54,56 +55,114 @@ conv3x3_hwc_kernel(const float *__restrict__ x, const float *__restrict__ wt, co
         for (int dx = 0; dx < 3; ++dx) {
             const int32_t ix = ox * stride + dx - 1;
             const bool in = iy >= 0 && iy < h && ix >= 0 && ix < w;
-            const float *px = x + ((img * h + (in ? iy : 0)) * w + (in ? ix : 0)) * CIN;
+            const float *px = xi + ((in ? iy : 0) * w + (in ? ix : 0)) * CIN;
 #pragma unroll
             for (int i = 0; i < CIN; ++i)
                 v[dy * 3 + dx][i] = in ? px[i] : 0.0f;
         }
     }
-    const int64_t plane = static_cast<int64_t>(ho) * wo;
-    float *yo = y + img * cout * plane + pp;
+    float *yo = y + static_cast<int64_t>(img) * cout * plane + pp;
+    ConstF *cw = (ConstF *)wt;
+    ConstF *cb = (ConstF *)bias;
+#pragma unroll 2
     for (int32_t o = 0; o < cout; ++o) {
-        const float *wo9 = sw + o * 9 * CIN;
+        ConstF *wo9 = cw + o * 9 * CIN;
         float acc = 0.0f;
 #pragma unroll
         for (int t = 0; t < 9; ++t)
 #pragma unroll
             for (int i = 0; i < CIN; ++i)
                 acc = __builtin_fmaf(wo9[t * CIN + i], v[t][i], acc);
-        yo[o * plane] = clamp_act(acc + sw[nw + o], act);
+        yo[static_cast<int64_t>(o) * plane] = clamp_act(acc + (cb ? cb[o] : 0.0f), act);
     }
 }
 
-// Depthwise 3x3: thread = one output element (n, c, oy, ox), taps in dy, dx
-// order from zero, then the bias, then the activation.
+// Depthwise 3x3 by columns: lane = one output column ox of one (n, c)
+// plane and a group of D consecutive output rows oy0 .. oy0 + D - 1.  The
+// lane loads the S*D + 3 - S input rows the group needs (3 values each, its
+// columns S*ox - 1 .. S*ox + 1) all at once, so a wavefront waits for
+// memory once, then forms its D outputs in registers.  A wavefront holds
+// 64 / wo whole planes side by side when wo <= 64 (lane l: plane l / wo,
+// column l % wo), else one 64-column part of a plane; its lanes share the
+// row group, so a row in the top or bottom padding is the same for all of
+// them.  Taps in dy, dx order from zero, then the bias, then the activation;
+// a tap in the padding multiplies a zero (+0 added to a sum that started at
+// +0 changes nothing).
+template <int S, int D>
 __global__ void __launch_bounds__(256)
-dw3x3_kernel(const float *__restrict__ x, const float *__restrict__ k, const float *__restrict__ bias,
-             float *__restrict__ y, int64_t total, int32_t c, int32_t h, int32_t w, int32_t ho, int32_t wo,
-             int32_t stride, int32_t act) {
-    const int64_t q = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (q >= total)
+dw3x3_cols_kernel(const float *__restrict__ x, const float *__restrict__ k, const float *__restrict__ bias,
+                  float *__restrict__ y, int64_t planes, int32_t c, int32_t h, int32_t w, int32_t ho, int32_t wo,
+                  int32_t act, int32_t ppw, int32_t wpp, int32_t segs) {
+    const int32_t lane = threadIdx.x & 63;
+    const int32_t gw = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // grid wavefront
+    const int32_t unit = gw / segs;  // plane group (or plane part) of this wavefront
+    const int32_t seg = gw - unit * segs;
+    int64_t plane0;  // first plane of the wavefront
+    int32_t sub, ox;
+    if (wpp == 0) {
+        plane0 = static_cast<int64_t>(unit) * ppw;
+        sub = lane / wo;
+        ox = lane - sub * wo;
+        if (sub >= ppw)
+            return;
+    } else {
+        const int32_t pl = unit / wpp;
+        plane0 = pl;
+        sub = 0;
+        ox = (unit - pl * wpp) * 64 + lane;
+        if (ox >= wo)
+            return;
+    }
+    const int64_t plane = plane0 + sub;
+    if (plane >= planes)
         return;
-    const int64_t plane_o = static_cast<int64_t>(ho) * wo;
-    const int64_t nc = q / plane_o;  // n * c + channel
-    const int32_t ch = static_cast<int32_t>(nc % c);
-    const int32_t pp = static_cast<int32_t>(q - nc * plane_o);
-    const int32_t oy = pp / wo, ox = pp - oy * wo;
-    const float *xc = x + nc * h * static_cast<int64_t>(w);
-    const float *kc = k + ch * 9;
-    float acc = 0.0f;
+    const int32_t ch = (static_cast<int32_t>(plane0 % c) + sub) % c;
+    float kk[9];
 #pragma unroll
-    for (int dy = 0; dy < 3; ++dy) {
-        const int32_t iy = oy * stride + dy - 1;
-        if (iy < 0 || iy >= h)
-            continue;
+    for (int t = 0; t < 9; ++t)
+        kk[t] = k[ch * 9 + t];
+    const float b = bias ? bias[ch] : 0.0f;
+    const float lo = act == 0 ? -__builtin_huge_valf() : 0.0f;
+    const float hi = act == 2 ? 6.0f : __builtin_huge_valf();
+    const float *xp = x + plane * h * w;
+    float *yp = y + plane * ho * wo + ox;
+    // this lane's three input columns; one outside the image reads column
+    // ix1 (always inside) and is replaced by zero, as is a row outside it
+    // (read as row 0).  The rows are loaded raw and masked after they land.
+    const int32_t ix1 = ox * S;
+    const bool lok = ix1 >= 1, rok = ix1 + 1 < w;
+    const int32_t ix0 = lok ? ix1 - 1 : ix1, ix2 = rok ? ix1 + 1 : ix1;
+    const int32_t oy0 = seg * D;
+    constexpr int R = S * D + 3 - S;  // input rows S*oy0 - 1 .. S*(oy0 + D - 1) + 1
+    float win[R][3];
 #pragma unroll
-        for (int dx = 0; dx < 3; ++dx) {
-            const int32_t ix = ox * stride + dx - 1;
-            if (ix >= 0 && ix < w)
-                acc = __builtin_fmaf(kc[dy * 3 + dx], xc[static_cast<int64_t>(iy) * w + ix], acc);
+    for (int i = 0; i < R; ++i) {
+        const int32_t iy = S * oy0 - 1 + i;
+        const float *r = xp + (iy >= 0 && iy < h ? iy : 0) * w;
+        win[i][0] = r[ix0];
+        win[i][1] = r[ix1];
+        win[i][2] = r[ix2];
+    }
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+        const int32_t iy = S * oy0 - 1 + i;
+        const bool in = iy >= 0 && iy < h;  // the same for the whole wavefront
+        win[i][0] = in && lok ? win[i][0] : 0.0f;
+        win[i][1] = in ? win[i][1] : 0.0f;
+        win[i][2] = in && rok ? win[i][2] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < D; ++j) {
+        if (oy0 + j < ho) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+                for (int dx = 0; dx < 3; ++dx)
+                    acc = __builtin_fmaf(kk[dy * 3 + dx], win[S * j + dy][dx], acc);
+            yp[(oy0 + j) * wo] = fminf(fmaxf(acc + b, lo), hi);
         }
     }
-    y[q] = clamp_act(acc + (bias ? bias[ch] : 0.0f), act);
 }
 
 // Global average pooling: thread = one (n, c) plane, summed in ascending
@@ -230,7 +289,7 @@ linear_kernel(const float *__restrict__ x, const float *__restrict__ wt, const f
     y[static_cast<int64_t>(img) * cout + r] = clamp_act(sum + (bias ? bias[r] : 0.0f), act);
 }
 
-using ConvFn = void (*)(const float *, const float *, const float *, float *, int64_t, int32_t, int32_t, int32_t,
+using ConvFn = void (*)(const float *, const float *, const float *, float *, int32_t, int32_t, int32_t, int32_t,
                         int32_t, int32_t, int32_t, int32_t);
 
 ConvFn pick_conv(int32_t cin) {
@@ -248,6 +307,9 @@ ConvFn pick_conv(int32_t cin) {
 }
 
 constexpr int kThreads = 256;
+// output rows per wavefront of the depthwise kernel, stride 1 and 2
+constexpr int kDwRows1 = 8;
+constexpr int kDwRows2 = 4;
 
 }  // namespace
 
@@ -258,21 +320,32 @@ hipError_t launch_conv3x3_hwc(const float *x, const float *wt, const float *bias
     if (!kern)
         return hipErrorInvalidValue;
     const int32_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
-    const int64_t pixels = static_cast<int64_t>(n) * ho * wo;
-    const int64_t blocks = (pixels + kThreads - 1) / kThreads;
-    const size_t lds = static_cast<size_t>(cout) * (9 * cin + 1) * sizeof(float);
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), lds, stream, x, wt, bias, y,
-                       pixels, h, w, ho, wo, cout, stride, act);
+    const int64_t bpi = (static_cast<int64_t>(ho) * wo + kThreads - 1) / kThreads;
+    // per-image offsets are 32-bit, the grid one dimension
+    if (static_cast<int64_t>(h) * w * cin >= INT32_MAX || bpi * n >= INT32_MAX)
+        return hipErrorInvalidValue;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>(bpi * n)), dim3(kThreads), 0, stream, x, wt, bias, y,
+                       static_cast<int32_t>(bpi), h, w, ho, wo, cout, stride, act);
     return hipGetLastError();
 }
 
 hipError_t launch_dw3x3(const float *x, const float *k, const float *bias, float *y, int32_t n, int32_t c,
                         int32_t h, int32_t w, int32_t stride, int32_t act, hipStream_t stream) {
     const int32_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
-    const int64_t total = static_cast<int64_t>(n) * c * ho * wo;
-    const int64_t blocks = (total + kThreads - 1) / kThreads;
-    hipLaunchKernelGGL(dw3x3_kernel, dim3(static_cast<unsigned>(blocks)), dim3(kThreads), 0, stream, x, k, bias,
-                       y, total, c, h, w, ho, wo, stride, act);
+    const int64_t planes = static_cast<int64_t>(n) * c;
+    // wavefront layout: whole planes side by side, or 64-column parts; one
+    // group of output rows each
+    const int32_t ppw = wo <= 64 ? 64 / wo : 0;
+    const int32_t wpp = wo <= 64 ? 0 : (wo + 63) / 64;
+    const int64_t units = wo <= 64 ? (planes + ppw - 1) / ppw : planes * wpp;
+    const int32_t rows = stride == 1 ? kDwRows1 : kDwRows2;
+    const int32_t segs = (ho + rows - 1) / rows;
+    const int64_t waves = units * segs;
+    if (waves >= INT32_MAX - 3 || static_cast<int64_t>(h) * w >= INT32_MAX)
+        return hipErrorInvalidValue;
+    auto kern = stride == 1 ? dw3x3_cols_kernel<1, kDwRows1> : dw3x3_cols_kernel<2, kDwRows2>;
+    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>((waves + 3) / 4)), dim3(kThreads), 0, stream, x, k, bias, y,
+                       planes, c, h, w, ho, wo, act, ppw, wpp, segs);
     return hipGetLastError();
 }
 

@@ -647,9 +647,8 @@ spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const floa
         return fail(SPCONV_E_ARG, "act must be SPCONV_ACT_NONE, _RELU or _RELU6");
     if (cin < 1 || cout < 1)
         return fail(SPCONV_E_SHAPE, "cin and cout must be >= 1");
-    if (cin > 8 || static_cast<int64_t>(cout) * (9 * cin + 1) > 16384)
-        return fail(SPCONV_E_UNSUPPORTED,
-                    "the HWC convolution supports cin <= 8 and cout * (9 cin + 1) <= 16384 (its weights in LDS)");
+    if (cin > 8)
+        return fail(SPCONV_E_UNSUPPORTED, "the HWC convolution supports cin <= 8");
     if (static_cast<int64_t>(n) * h * w == 0)
         return SPCONV_OK;
     if (!x || !weight || !y)
@@ -658,6 +657,9 @@ spconv_status spconv_conv3x3_hwc(const float *x, const float *weight, const floa
     const int64_t xel = static_cast<int64_t>(n) * h * w * cin, yel = static_cast<int64_t>(n) * cout * ho * wo;
     if (static_cast<int64_t>(n) * ho * wo > (int64_t(1) << 38))
         return fail(SPCONV_E_SHAPE, "too many output pixels");
+    if (static_cast<int64_t>(h) * w * cin >= INT32_MAX || static_cast<int64_t>(n) * ((ho * wo + 255) / 256) >= INT32_MAX)
+        return fail(SPCONV_E_SHAPE, "an image must hold fewer than 2^31 elements and n * ceil(ho * wo / 256) "
+                                    "must stay below 2^31");
     if (ranges_overlap(x, static_cast<size_t>(xel) * 4, y, static_cast<size_t>(yel) * 4))
         return fail(SPCONV_E_ARG, "x and y overlap");
     const hipError_t he = spconv::launch_conv3x3_hwc(x, weight, bias, y, n, h, w, cin, cout, stride,

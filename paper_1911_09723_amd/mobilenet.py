@@ -2,12 +2,20 @@
 
 Layer sequence (paper Sec. 3.1, Sec. 3.3 and Table 1): the dense 3x3 stride-2
 convolution reads the HWC image and writes CHW (``spconv_conv3x3_hwc``,
-ReLU6); 13 blocks of depthwise 3x3 -> sparse 1x1 (ReLU6 after each), each one
-fused plan (``spconv_plan_create_fused``) -- a block whose input strip does
-not fit in LDS (the 1024-channel one) runs ``spconv_depthwise3x3`` and then a
-plain plan on the direct-load kernel; global average pooling
-(``spconv_global_avg_pool``); the dense classifier (``spconv_linear``, no
-activation).
+ReLU6); 13 blocks of depthwise 3x3 -> sparse 1x1 (ReLU6 after each), each
+either one fused plan (``spconv_plan_create_fused``) or
+``spconv_depthwise3x3`` followed by a plain plan (whose automatic kernel
+choice applies); global average pooling (``spconv_global_avg_pool``); the
+dense classifier (``spconv_linear``, no activation).
+
+Both forms of a block compute the same fp32 operations in the same order
+(the depthwise taps in dy, dx order from zero, bias, clamp; each 1x1 output
+summed in ascending channel order), so they give the same bits and the
+choice is a matter of speed only.  ``fuse="auto"`` times both forms once on
+the device at construction and keeps the faster; ``"always"`` fuses every
+block that a fused plan supports (a block whose input strip does not fit in
+LDS, the 1024-channel one, is never fused); ``"never"`` runs every block as
+two launches.
 
 Every step is one kernel launch on the caller's (torch's current) stream;
 nothing is allocated after construction.  ``capture`` records the whole
@@ -31,8 +39,10 @@ class MobileNetV1Engine:
     cin/cout/stride/dw_k/dw_b and the pointwise block-CSR arrays in ``pw``,
     fc_w [classes, 1024], fc_b)."""
 
-    def __init__(self, net, batch: int, h: int = 224, w: int = 224):
+    def __init__(self, net, batch: int, h: int = 224, w: int = 224, fuse: str = "auto"):
         import torch
+        if fuse not in ("auto", "always", "never"):
+            raise ValueError("fuse must be 'auto', 'always' or 'never'")
         dev = torch.device("cuda:0")
         f32 = torch.float32
 
@@ -57,22 +67,38 @@ class MobileNetV1Engine:
             pw = blk.pw
             ho, wo = (hh - 1) // blk.stride + 1, (ww - 1) // blk.stride + 1
             out = torch.empty((batch, blk.cout, ho, wo), dtype=f32, device=dev)
-            try:
-                plan = Plan.fused(pw.cout, pw.cin, pw.block_rows, pw.row_ptr, pw.col_idx, pw.values, pw.bias,
-                                  "relu6", blk.dw_k, blk.dw_b, "relu6", blk.stride)
-                self._keep += [plan, out]
-                self._steps.append(self._run_step(plan, cur, out, batch, hh, ww))
-                self.fused_blocks += 1
-                self.layers.append("fused dw3x3 s%d + 1x1 %d->%d @%dx%d" % (blk.stride, blk.cin, blk.cout, hh, ww))
-            except SpconvError as e:
-                if e.status != E_UNSUPPORTED:
-                    raise
+            fused = None
+            if fuse != "never":
+                try:
+                    fused = Plan.fused(pw.cout, pw.cin, pw.block_rows, pw.row_ptr, pw.col_idx, pw.values, pw.bias,
+                                       "relu6", blk.dw_k, blk.dw_b, "relu6", blk.stride)
+                except SpconvError as e:
+                    if e.status != E_UNSUPPORTED:
+                        raise
+            split = None
+            if fused is None or fuse == "auto":
                 k, b = put(blk.dw_k), put(blk.dw_b)
                 mid = torch.empty((batch, blk.cin, ho, wo), dtype=f32, device=dev)
                 plan = Plan(pw.cout, pw.cin, pw.block_rows, pw.row_ptr, pw.col_idx, pw.values, pw.bias, "relu6")
-                self._keep += [k, b, mid, plan, out]
-                self._steps.append(self._dw_step(cur, k, b, blk.stride, mid, batch, blk.cin, hh, ww))
-                self._steps.append(self._run_step(plan, mid, out, batch, ho, wo))
+                split = ([k, b, mid, plan],
+                         [self._dw_step(cur, k, b, blk.stride, mid, batch, blk.cin, hh, ww),
+                          self._run_step(plan, mid, out, batch, ho, wo)])
+            if fused is not None and split is not None:
+                f_step = [self._run_step(fused, cur, out, batch, hh, ww)]
+                if self._time(f_step) <= self._time(split[1]):
+                    split[0][3].close()
+                    split = None
+                else:
+                    fused.close()
+                    fused = None
+            if fused is not None:
+                self._keep += [fused, out]
+                self._steps.append(self._run_step(fused, cur, out, batch, hh, ww))
+                self.fused_blocks += 1
+                self.layers.append("fused dw3x3 s%d + 1x1 %d->%d @%dx%d" % (blk.stride, blk.cin, blk.cout, hh, ww))
+            else:
+                self._keep += split[0] + [out]
+                self._steps += split[1]
                 self.layers.append("dw3x3 s%d %d @%dx%d" % (blk.stride, blk.cin, hh, ww))
                 self.layers.append("1x1 %d->%d @%dx%d" % (blk.cin, blk.cout, ho, wo))
             cur, ch, hh, ww = out, blk.cout, ho, wo
@@ -89,6 +115,24 @@ class MobileNetV1Engine:
         self._steps.append(lambda: spconv_linear(pooled, fc_w, fc_b, "none", logits, batch, ch, classes))
         self.layers.append("dense fc %d->%d" % (ch, self.classes))
         self.graph = None
+
+    @staticmethod
+    def _time(steps, reps: int = 5) -> float:
+        """Median device time of one pass over ``steps`` (after two warm-up
+        passes), in milliseconds."""
+        import torch
+        for _ in range(2):
+            for st in steps:
+                st()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            for st in steps:
+                st()
+            b.record()
+        torch.cuda.synchronize()
+        t = sorted(a.elapsed_time(b) for a, b in ev)
+        return t[len(t) // 2]
 
     @staticmethod
     def _run_step(plan, x, y, n, h, w):

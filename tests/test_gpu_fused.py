@@ -84,6 +84,34 @@ def test_identity_depthwise_is_bitwise_the_plain_plan(k):
     assert np.array_equal(y_f.view(np.uint32), y_p.view(np.uint32))
 
 
+@pytest.mark.parametrize("spec", [(32, 64, 56, 56, 2, 1), (64, 128, 28, 28, 2, 2), (512, 512, 14, 14, 3, 1),
+                                  (512, 1024, 14, 14, 2, 2), (40, 48, 15, 9, 2, 2)],
+                         ids=lambda s: "%d-%d-%dx%d-n%d-s%d" % s)
+def test_fused_equals_standalone_depthwise_then_plain_plan(spec):
+    """The fused plan against its two-launch form (spconv_depthwise3x3 into a
+    buffer, then the plain plan with its automatic kernel choice): equal bit
+    for bit, so a network may take either form."""
+    import torch
+    from paper_1911_09723_amd import Plan, spconv_depthwise3x3
+    from gpu_util import to_gpu
+    cin, cout, h, w, n, stride = spec
+    layer = make_layer(cin, cout, h, w, n, 0.9, act="relu6", seed=cin + h)
+    kw, kb = make_depthwise(cin, cin + 3)
+    note("fused vs two launches %s" % (spec,))
+    y_f = gpu_run_fused(layer, kw, kb, "relu6", stride)
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    mid = torch.empty((n, cin, ho, wo), device="cuda:0")
+    spconv_depthwise3x3(to_gpu(layer.x), to_gpu(kw), to_gpu(kb), "relu6", stride, mid, n, cin, h, w)
+    plan = Plan(cout, cin, layer.block_rows, layer.row_ptr, layer.col_idx, layer.values, layer.bias, "relu6")
+    try:
+        y_s = plan.run(mid)
+        torch.cuda.synchronize()
+        y_s = y_s.cpu().numpy()
+    finally:
+        plan.close()
+    assert np.array_equal(y_f.view(np.uint32), y_s.view(np.uint32))
+
+
 @pytest.mark.parametrize("n", [1, 3, 85])
 def test_fused_shared_tail_tiles(n):
     """Batches whose last tiles are shared by several workgroups (each part

@@ -43,6 +43,7 @@ def _check(y, y_ref, scale, what):
     (1, 13, 11, 8, 24, 2, "relu6", True),
     (2, 5, 7, 4, 64, 1, "none", True),
     (1, 1, 1, 3, 7, 2, "relu", True),
+    (1, 9, 30, 3, 600, 1, "relu", True),   # more weights than the old LDS copy held
 ])
 def test_stem_conv_parity(n, h, w, cin, cout, stride, act, bias):
     import torch
@@ -61,6 +62,12 @@ def test_stem_conv_parity(n, h, w, cin, cout, stride, act, bias):
 
 @pytest.mark.parametrize("n,c,h,w,stride,act", [
     (2, 1024, 7, 7, 1, "relu6"), (1, 64, 112, 112, 2, "relu"), (3, 5, 9, 4, 2, "none"), (1, 3, 1, 1, 1, "relu6"),
+    # staged kernel: a 112 x 112 plane per workgroup, many 3 x 3 planes per
+    # workgroup crossing image boundaries, width 1 (divisor 1), odd planes
+    # with stride 2, the largest plane that fits its LDS (126 x 126), then
+    # one past it (the direct kernel)
+    (4, 32, 112, 112, 1, "relu6"), (3, 333, 3, 3, 1, "relu"), (2, 6, 7, 1, 1, "none"), (3, 17, 15, 13, 2, "relu6"),
+    (2, 3, 126, 126, 1, "relu6"), (1, 3, 127, 127, 2, "relu"),
 ])
 def test_standalone_depthwise_parity(n, c, h, w, stride, act):
     import torch
@@ -112,11 +119,11 @@ def test_linear_parity(n, cin, cout, act, bias, offset):
     _check(_sync_np(y), y64.reshape(n, cout), s.reshape(n, cout), "linear")
 
 
-def _engine_case(batch, hw, classes, seed):
+def _engine_case(batch, hw, classes, seed, fuse="auto"):
     from paper_1911_09723_amd.mobilenet import MobileNetV1Engine
     net = make_mobilenet_v1(seed=seed, classes=classes)
     x = make_image(batch, hw, hw, seed=seed)
-    return net, x, MobileNetV1Engine(net, batch, hw, hw)
+    return net, x, MobileNetV1Engine(net, batch, hw, hw, fuse=fuse)
 
 
 @pytest.mark.parametrize("batch,hw,classes", [(2, 224, 1000), (3, 32, 10), (64, 224, 1000)])
@@ -126,7 +133,8 @@ def test_mobilenet_v1_forward_matches_oracle(batch, hw, classes):
     try:
         note("mobilenet v1 batch %d %dx%d (%d launches, %d fused blocks)" % (batch, hw, hw, eng.launches(),
                                                                              eng.fused_blocks))
-        assert eng.fused_blocks == 12 and eng.launches() == 1 + 12 + 2 + 2
+        # every block is one launch when fused, two when not
+        assert eng.launches() == 1 + 13 + (13 - eng.fused_blocks) + 2
         y = _sync_np(eng.forward(to_gpu(x)))
     finally:
         eng.close()
@@ -137,6 +145,23 @@ def test_mobilenet_v1_forward_matches_oracle(batch, hw, classes):
     print("max |logit error| %.3g, bound %.3g" % (err.max(), bound))
     assert err.max() <= bound
     assert np.array_equal(y.argmax(axis=1), y_ref.argmax(axis=1))
+
+
+def test_mobilenet_v1_fusion_choice_does_not_change_bits():
+    """Every block fused where possible, no block fused, and the timed
+    choice: the same logits bit for bit (both forms of a block run the same
+    fp32 operations in the same order)."""
+    outs = {}
+    for fuse in ("always", "never", "auto"):
+        net, x, eng = _engine_case(4, 96, 10, seed=5, fuse=fuse)
+        try:
+            note("mobilenet v1 fuse=%s (%d fused blocks)" % (fuse, eng.fused_blocks))
+            assert eng.fused_blocks == {"always": 12, "never": 0}.get(fuse, eng.fused_blocks)
+            outs[fuse] = _sync_np(eng.forward(to_gpu(x))).copy()
+        finally:
+            eng.close()
+    for fuse in ("never", "auto"):
+        assert np.array_equal(outs[fuse].view(np.uint32), outs["always"].view(np.uint32)), fuse
 
 
 def test_mobilenet_v1_graph_replays_equal_eager_runs():
