@@ -197,6 +197,7 @@ def time_network(batch, steps, warmup, graph=True):
     launches = eng.launches()
     layers = list(eng.layers)
     fused = eng.fused_blocks
+    fusion_times = list(eng.fusion_times)
     eng.close()
     torch.cuda.empty_cache()
     b_alg = network_alg_bytes(net, batch)
@@ -206,6 +207,7 @@ def time_network(batch, steps, warmup, graph=True):
         "batch": batch, "graph": graph, "launches": launches, "layers": layers,
         "ms_per_batch_mean": round(float(ms.mean()), 4), "ms_per_batch_min": round(float(ms.min()), 4),
         "images_per_s": round(batch / t, 1), "fused_blocks": fused,
+        "fusion_times_ms": fusion_times,
         "alg_bytes": b_alg, "hbm_gbs_algorithmic": round(b_alg / t / 1e9, 1),
         "roofline_frac": round(b_alg / (HBM_PEAK_GBS * 1e9) / t, 4),
     }

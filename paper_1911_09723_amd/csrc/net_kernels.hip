@@ -1,10 +1,10 @@
 // gfx950 kernels for the CHW operators around the sparse 1x1 in a MobileNet
 // (Fast Sparse ConvNets, Sec. 3.1 and Sec. 3.3): the dense 3x3 convolution
-// that reads the HWC image and writes CHW, a standalone depthwise 3x3 (for
-// layers whose strip does not fit the fused strip kernel), global average
-// pooling and the dense classifier.  All three are memory-bound elementwise-style kernels:
-// one thread per output element (per output pixel for the convolution), fp32
-// arithmetic, zero padding 1.
+// that reads the HWC image and writes CHW, a standalone depthwise 3x3, global
+// average pooling and the dense classifier, all fp32 with zero padding 1.
+// They are memory-bound: each keeps its loads and stores coalesced and its
+// per-element instruction count small (weights that are the same for a whole
+// wavefront come through scalar loads).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -77,44 +77,43 @@ conv3x3_hwc_kernel(const float *__restrict__ x, const float *__restrict__ wt, co
     }
 }
 
-// Depthwise 3x3 by columns: lane = one output column ox of one (n, c)
-// plane and a group of D consecutive output rows oy0 .. oy0 + D - 1.  The
-// lane loads the S*D + 3 - S input rows the group needs (3 values each, its
-// columns S*ox - 1 .. S*ox + 1) all at once, so a wavefront waits for
-// memory once, then forms its D outputs in registers.  A wavefront holds
-// 64 / wo whole planes side by side when wo <= 64 (lane l: plane l / wo,
-// column l % wo), else one 64-column part of a plane; its lanes share the
-// row group, so a row in the top or bottom padding is the same for all of
-// them.  Taps in dy, dx order from zero, then the bias, then the activation;
-// a tap in the padding multiplies a zero (+0 added to a sum that started at
-// +0 changes nothing).
+// Depthwise 3x3 by columns, for planes too wide for whole planes per
+// wavefront: lane = one output column ox of one 64-column part of an
+// (n, c) plane, walking down a segment of its output rows in groups of D.
+// The lane holds the input rows of the current group in registers (its
+// columns S*ox - 1 .. S*ox + 1, three loads per row), and the rows of the
+// next group are loaded while the current one is computed; the lanes of a
+// wavefront walk the same rows.  Taps in dy, dx order from zero, then the
+// bias, then the activation; a tap in the padding multiplies a zero (+0
+// added to a sum that started at +0 changes nothing).
+//
+// Addressing is 32-bit through buffer resources over the wavefront's
+// planes: a tap in the padding (a column outside the image, or any row
+// outside it) gets an offset past the resource's size, and the hardware
+// returns zero for it without touching memory.
+using Rsrc = __amdgpu_buffer_rsrc_t;
+__device__ __forceinline__ Rsrc buffer_of(const void *p, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), static_cast<short>(0), static_cast<int>(bytes),
+                                             0x00020000);
+}
+// Offset of a tap outside the image: at least 2^30 bytes, beyond every
+// resource of this kernel (the host keeps a wavefront's planes below 2^30
+// bytes), and two of them added stay below 2^32.
+constexpr uint32_t kDwOut = 0x40000000u;
+
 template <int S, int D>
 __global__ void __launch_bounds__(256)
 dw3x3_cols_kernel(const float *__restrict__ x, const float *__restrict__ k, const float *__restrict__ bias,
                   float *__restrict__ y, int64_t planes, int32_t c, int32_t h, int32_t w, int32_t ho, int32_t wo,
-                  int32_t act, int32_t ppw, int32_t wpp, int32_t segs) {
+                  int32_t act, int32_t wpp, int32_t segs, int32_t seg_rows) {
     const int32_t lane = threadIdx.x & 63;
     const int32_t gw = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // grid wavefront
-    const int32_t unit = gw / segs;  // plane group (or plane part) of this wavefront
+    const int32_t unit = gw / segs;  // plane part of this wavefront
     const int32_t seg = gw - unit * segs;
-    int64_t plane0;  // first plane of the wavefront
-    int32_t sub, ox;
-    if (wpp == 0) {
-        plane0 = static_cast<int64_t>(unit) * ppw;
-        sub = lane / wo;
-        ox = lane - sub * wo;
-        if (sub >= ppw)
-            return;
-    } else {
-        const int32_t pl = unit / wpp;
-        plane0 = pl;
-        sub = 0;
-        ox = (unit - pl * wpp) * 64 + lane;
-        if (ox >= wo)
-            return;
-    }
-    const int64_t plane = plane0 + sub;
-    if (plane >= planes)
+    const int64_t plane0 = unit / wpp;
+    constexpr int32_t nwp = 1, sub = 0;
+    const int32_t ox = static_cast<int32_t>(unit - plane0 * wpp) * 64 + lane;
+    if (ox >= wo)
         return;
     const int32_t ch = (static_cast<int32_t>(plane0 % c) + sub) % c;
     float kk[9];
@@ -124,44 +123,225 @@ dw3x3_cols_kernel(const float *__restrict__ x, const float *__restrict__ k, cons
     const float b = bias ? bias[ch] : 0.0f;
     const float lo = act == 0 ? -__builtin_huge_valf() : 0.0f;
     const float hi = act == 2 ? 6.0f : __builtin_huge_valf();
-    const float *xp = x + plane * h * w;
-    float *yp = y + plane * ho * wo + ox;
-    // this lane's three input columns; one outside the image reads column
-    // ix1 (always inside) and is replaced by zero, as is a row outside it
-    // (read as row 0).  The rows are loaded raw and masked after they land.
+    const int32_t ihw = h * w, ohw = ho * wo;
+    const Rsrc rx = buffer_of(x + plane0 * ihw, static_cast<uint32_t>(nwp * ihw * 4));
+    const Rsrc ry = buffer_of(y + plane0 * ohw, static_cast<uint32_t>(nwp * ohw * 4));
+    // byte offsets of this lane's three input columns in its plane (past
+    // the resource when outside the image) and of its output column
     const int32_t ix1 = ox * S;
-    const bool lok = ix1 >= 1, rok = ix1 + 1 < w;
-    const int32_t ix0 = lok ? ix1 - 1 : ix1, ix2 = rok ? ix1 + 1 : ix1;
-    const int32_t oy0 = seg * D;
-    constexpr int R = S * D + 3 - S;  // input rows S*oy0 - 1 .. S*(oy0 + D - 1) + 1
-    float win[R][3];
+    const bool lok = ix1 >= 1, rok = ix1 + 1 < w;  // columns inside the image
+    const uint32_t cbase = static_cast<uint32_t>(sub * ihw + ix1) * 4;
+    const uint32_t c0 = lok ? cbase - 4 : kDwOut, c1 = cbase, c2 = rok ? cbase + 4 : kDwOut;
+    const uint32_t yo = static_cast<uint32_t>(sub * ohw + ox) * 4;
+    auto load_row = [&](int32_t iy, float *a) __attribute__((always_inline)) {
+        const uint32_t ro = iy >= 0 && iy < h ? static_cast<uint32_t>(iy * w) * 4 : kDwOut;  // uniform
+        a[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rx, c0 + ro, 0, 0));
+        a[1] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rx, c1 + ro, 0, 0));
+        a[2] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rx, c2 + ro, 0, 0));
+    };
+    // The window holds input rows S*oy - 1 .. S*(oy + D - 1) + 1 of group
+    // oy: C rows carried from the last group and NR new ones, loaded while
+    // the last group was computed.
+    constexpr int C = 3 - S;
+    constexpr int NR = S * D;
+    const int32_t oy0 = seg * seg_rows;
+    const int32_t oy1 = oy0 + seg_rows < ho ? oy0 + seg_rows : ho;
+    float win[C + NR][3], nxt[NR][3];
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-        const int32_t iy = S * oy0 - 1 + i;
-        const float *r = xp + (iy >= 0 && iy < h ? iy : 0) * w;
-        win[i][0] = r[ix0];
-        win[i][1] = r[ix1];
-        win[i][2] = r[ix2];
-    }
+    for (int i = 0; i < C; ++i)
+        load_row(S * oy0 - 1 + i, win[i]);
 #pragma unroll
-    for (int i = 0; i < R; ++i) {
-        const int32_t iy = S * oy0 - 1 + i;
-        const bool in = iy >= 0 && iy < h;  // the same for the whole wavefront
-        win[i][0] = in && lok ? win[i][0] : 0.0f;
-        win[i][1] = in ? win[i][1] : 0.0f;
-        win[i][2] = in && rok ? win[i][2] : 0.0f;
-    }
+    for (int i = 0; i < NR; ++i)
+        load_row(S * oy0 - 1 + C + i, nxt[i]);
+    for (int32_t oy = oy0; oy < oy1; oy += D) {
 #pragma unroll
-    for (int j = 0; j < D; ++j) {
-        if (oy0 + j < ho) {
-            float acc = 0.0f;
+        for (int i = 0; i < NR; ++i)
 #pragma unroll
-            for (int dy = 0; dy < 3; ++dy)
+            for (int e = 0; e < 3; ++e)
+                win[C + i][e] = nxt[i][e];
+        if (oy + D < oy1) {
 #pragma unroll
-                for (int dx = 0; dx < 3; ++dx)
-                    acc = __builtin_fmaf(kk[dy * 3 + dx], win[S * j + dy][dx], acc);
-            yp[(oy0 + j) * wo] = fminf(fmaxf(acc + b, lo), hi);
+            for (int i = 0; i < NR; ++i)
+                load_row(S * (oy + D) - 1 + C + i, nxt[i]);
         }
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            if (oy + j < oy1) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+                    for (int dx = 0; dx < 3; ++dx)
+                        acc = __builtin_fmaf(kk[dy * 3 + dx], win[S * j + dy][dx], acc);
+                __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(fminf(fmaxf(acc + b, lo), hi)), ry, yo,
+                                                      static_cast<int32_t>((oy + j) * wo * 4), 0);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < C; ++i)
+#pragma unroll
+            for (int e = 0; e < 3; ++e)
+                win[i][e] = win[NR + i][e];
+    }
+}
+
+// The same depthwise 3x3 with V adjacent output columns per lane and whole
+// planes in every wavefront: lane = lane-column lc of one plane (outputs
+// V*lc .. V*lc + V - 1), which loads its S*V input columns of a row with one
+// or two V-wide loads (the address unit handles a lane per cycle, whatever
+// the width, so wide loads move several times the bytes per cycle) and takes
+// the column left of them (and, for stride 1, the one right of them) from the
+// neighbouring lanes.  Needs w a multiple of S*V and x, y aligned to 4*V
+// bytes; wo / V lane-columns per plane row at most 64.
+template <int S, int V>
+struct DwVec {
+    static constexpr int D = S == 2 && V == 4 ? 2 : 4;  // output rows per group
+    static constexpr int C = 3 - S;                      // rows carried between groups
+    static constexpr int NR = S * D;                     // new rows per group
+    static constexpr int RW = S * V + 3 - S;             // register row: left, S*V loaded, right (stride 1)
+};
+
+template <int V>
+__device__ __forceinline__ void load_vec(Rsrc r, uint32_t off, float *dst) {
+    if constexpr (V == 4) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            dst[e] = __uint_as_float(v[e]);
+    } else if constexpr (V == 2) {
+        const auto v = __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, 0);
+        dst[0] = __uint_as_float(v[0]);
+        dst[1] = __uint_as_float(v[1]);
+    } else {
+        dst[0] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+    }
+}
+
+template <int V>
+__device__ __forceinline__ void store_vec(Rsrc r, uint32_t off, int32_t soff, const float *src) {
+    if constexpr (V == 4) {
+        typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+        const u4v v = {__float_as_uint(src[0]), __float_as_uint(src[1]), __float_as_uint(src[2]),
+                       __float_as_uint(src[3])};
+        __builtin_amdgcn_raw_buffer_store_b128(v, r, off, soff, 0);
+    } else if constexpr (V == 2) {
+        typedef uint32_t u2v __attribute__((ext_vector_type(2)));
+        const u2v v = {__float_as_uint(src[0]), __float_as_uint(src[1])};
+        __builtin_amdgcn_raw_buffer_store_b64(v, r, off, soff, 0);
+    } else {
+        __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(src[0]), r, off, soff, 0);
+    }
+}
+
+template <int S, int V>
+__global__ void __launch_bounds__(256)
+dw3x3_vec_kernel(const float *__restrict__ x, const float *__restrict__ k, const float *__restrict__ bias,
+                 float *__restrict__ y, int64_t planes, int32_t c, int32_t h, int32_t w, int32_t ho, int32_t wo,
+                 int32_t act, int32_t ppw, int32_t segs, int32_t seg_rows) {
+    using G = DwVec<S, V>;
+    constexpr int D = G::D, C = G::C, NR = G::NR, RW = G::RW;
+    const int32_t lane = threadIdx.x & 63;
+    const int32_t gw = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // grid wavefront
+    const int32_t unit = gw / segs;  // plane group of this wavefront
+    const int32_t seg = gw - unit * segs;
+    const int32_t lcols = wo / V;    // lane-columns per plane row
+    const int64_t plane0 = static_cast<int64_t>(unit) * ppw;
+    const int32_t nwp = static_cast<int32_t>(planes - plane0 < ppw ? planes - plane0 : ppw);
+    const int32_t sub = lane / lcols;
+    const int32_t lc = lane - sub * lcols;
+    if (sub >= nwp)
+        return;
+    const int32_t ch = (static_cast<int32_t>(plane0 % c) + sub) % c;
+    // the plane's 9 taps as three 12-byte loads (one address-unit cycle per
+    // lane each, against nine for single words)
+    float kk[9];
+    {
+        const Rsrc rk = buffer_of(k, static_cast<uint32_t>(c * 36));
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+            const auto t = __builtin_amdgcn_raw_buffer_load_b96(rk, ch * 36 + q * 12, 0, 0);
+#pragma unroll
+            for (int e = 0; e < 3; ++e)
+                kk[q * 3 + e] = __uint_as_float(t[e]);
+        }
+    }
+    const float b = bias ? bias[ch] : 0.0f;
+    const float lo = act == 0 ? -__builtin_huge_valf() : 0.0f;
+    const float hi = act == 2 ? 6.0f : __builtin_huge_valf();
+    const int32_t ihw = h * w, ohw = ho * wo;
+    const Rsrc rx = buffer_of(x + plane0 * ihw, static_cast<uint32_t>(nwp * ihw * 4));
+    const Rsrc ry = buffer_of(y + plane0 * ohw, static_cast<uint32_t>(nwp * ohw * 4));
+    const bool lok = lc > 0, rok = lc + 1 < lcols;  // neighbour lane of the same plane
+    const uint32_t xo = static_cast<uint32_t>(sub * ihw + lc * S * V) * 4;
+    // the second load of stride 2 (columns past the first V): past the row's
+    // end only when V = 1 and w is odd, and then a padding tap
+    const uint32_t xo1 = lc * S * V + V < w ? xo + V * 4 : kDwOut;
+    const uint32_t yo = static_cast<uint32_t>(sub * ohw + lc * V) * 4;
+    const int left = ((lane + 63) & 63) << 2, right = ((lane + 1) & 63) << 2;  // lane byte addresses
+    // a row: S*V loaded values at [1 .. S*V]; [0] and (stride 1) [V + 1]
+    // filled in from the neighbours once the loads have landed
+    auto load_row = [&](int32_t iy, float *a) __attribute__((always_inline)) {
+        const uint32_t ro = iy >= 0 && iy < h ? static_cast<uint32_t>(iy * w) * 4 : kDwOut;  // uniform row
+        load_vec<V>(rx, xo + ro, a + 1);
+        if constexpr (S == 2)
+            load_vec<V>(rx, xo1 + ro, a + 1 + V);
+    };
+    auto finish_row = [&](float *a) __attribute__((always_inline)) {
+        const float l = __int_as_float(__builtin_amdgcn_ds_bpermute(left, __float_as_int(a[S * V])));
+        a[0] = lok ? l : 0.0f;
+        if constexpr (S == 1) {
+            const float r = __int_as_float(__builtin_amdgcn_ds_bpermute(right, __float_as_int(a[1])));
+            a[V + 1] = rok ? r : 0.0f;
+        }
+    };
+    const int32_t oy0 = seg * seg_rows;
+    const int32_t oy1 = oy0 + seg_rows < ho ? oy0 + seg_rows : ho;
+    float win[C + NR][RW], nxt[NR][RW];
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+        load_row(S * oy0 - 1 + i, win[i]);
+#pragma unroll
+    for (int i = 0; i < NR; ++i)
+        load_row(S * oy0 - 1 + C + i, nxt[i]);
+#pragma unroll
+    for (int i = 0; i < C; ++i)
+        finish_row(win[i]);
+    for (int32_t oy = oy0; oy < oy1; oy += D) {
+#pragma unroll
+        for (int i = 0; i < NR; ++i) {
+#pragma unroll
+            for (int e = 0; e < RW; ++e)
+                win[C + i][e] = nxt[i][e];
+            finish_row(win[C + i]);
+        }
+        if (oy + D < oy1) {
+#pragma unroll
+            for (int i = 0; i < NR; ++i)
+                load_row(S * (oy + D) - 1 + C + i, nxt[i]);
+        }
+#pragma unroll
+        for (int j = 0; j < D; ++j) {
+            if (oy + j < oy1) {
+                float out[V];
+#pragma unroll
+                for (int v = 0; v < V; ++v) {
+                    // output column V*lc + v reads register columns S*v .. S*v + 2
+                    float acc = 0.0f;
+#pragma unroll
+                    for (int dy = 0; dy < 3; ++dy)
+#pragma unroll
+                        for (int dx = 0; dx < 3; ++dx)
+                            acc = __builtin_fmaf(kk[dy * 3 + dx], win[S * j + dy][S * v + dx], acc);
+                    out[v] = fminf(fmaxf(acc + b, lo), hi);
+                }
+                store_vec<V>(ry, yo, static_cast<int32_t>((oy + j) * wo * 4), out);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < C; ++i)
+#pragma unroll
+            for (int e = 0; e < RW; ++e)
+                win[i][e] = win[NR + i][e];
     }
 }
 
@@ -307,9 +487,9 @@ ConvFn pick_conv(int32_t cin) {
 }
 
 constexpr int kThreads = 256;
-// output rows per wavefront of the depthwise kernel, stride 1 and 2
-constexpr int kDwRows1 = 8;
-constexpr int kDwRows2 = 4;
+// depthwise kernel: output rows per group, wavefronts wanted per launch
+constexpr int kDwRows = 4;
+constexpr int64_t kDwWaves = 8192;
 
 }  // namespace
 
@@ -333,19 +513,49 @@ hipError_t launch_dw3x3(const float *x, const float *k, const float *bias, float
                         int32_t h, int32_t w, int32_t stride, int32_t act, hipStream_t stream) {
     const int32_t ho = (h - 1) / stride + 1, wo = (w - 1) / stride + 1;
     const int64_t planes = static_cast<int64_t>(n) * c;
-    // wavefront layout: whole planes side by side, or 64-column parts; one
-    // group of output rows each
-    const int32_t ppw = wo <= 64 ? 64 / wo : 0;
-    const int32_t wpp = wo <= 64 ? 0 : (wo + 63) / 64;
-    const int64_t units = wo <= 64 ? (planes + ppw - 1) / ppw : planes * wpp;
-    const int32_t rows = stride == 1 ? kDwRows1 : kDwRows2;
-    const int32_t segs = (ho + rows - 1) / rows;
-    const int64_t waves = units * segs;
-    if (waves >= INT32_MAX - 3 || static_cast<int64_t>(h) * w >= INT32_MAX)
+    // (a wavefront's planes stay below 2^30 bytes)
+    const int64_t pbytes = static_cast<int64_t>(h) * w * 4;
+    if (pbytes >= (int64_t{1} << 30))
         return hipErrorInvalidValue;
-    auto kern = stride == 1 ? dw3x3_cols_kernel<1, kDwRows1> : dw3x3_cols_kernel<2, kDwRows2>;
-    hipLaunchKernelGGL(kern, dim3(static_cast<unsigned>((waves + 3) / 4)), dim3(kThreads), 0, stream, x, k, bias, y,
-                       planes, c, h, w, ho, wo, act, ppw, wpp, segs);
+    // widest lane vector the shape and pointers allow, with whole planes in
+    // a wavefront
+    const uintptr_t align = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y);
+    int32_t vw = 1;
+    for (int32_t v : {4, 2}) {
+        if (w % (stride * v) == 0 && align % (4 * v) == 0 && wo / v <= 64) {
+            vw = v;
+            break;
+        }
+    }
+    const int32_t lcols = wo / vw;
+    const bool vec = lcols <= 64;
+    const int32_t ppw =
+        vec ? static_cast<int32_t>(std::min<int64_t>(64 / lcols, ((int64_t{1} << 30) - 1) / pbytes)) : 0;
+    const int32_t wpp = vec ? 0 : (wo + 63) / 64;
+    const int64_t units = vec ? (planes + ppw - 1) / ppw : planes * wpp;
+    // row segments: about two wavefronts per SIMD slot (8 per SIMD of 256
+    // compute units), a whole number of row groups each
+    const int32_t rows = vec && stride == 2 && vw == 4 ? 2 : kDwRows;
+    const int32_t groups = (ho + rows - 1) / rows;
+    const int32_t want = static_cast<int32_t>(std::min<int64_t>(groups, (kDwWaves + units - 1) / units));
+    const int32_t seg_rows = (groups + want - 1) / want * rows;
+    const int32_t segs = (ho + seg_rows - 1) / seg_rows;
+    const int64_t waves = units * segs;
+    if (waves >= INT32_MAX - 3)
+        return hipErrorInvalidValue;
+    const dim3 grid(static_cast<unsigned>((waves + 3) / 4));
+    if (vec) {
+        using Fn = void (*)(const float *, const float *, const float *, float *, int64_t, int32_t, int32_t, int32_t,
+                            int32_t, int32_t, int32_t, int32_t, int32_t, int32_t);
+        Fn kern = stride == 1 ? (vw == 4 ? dw3x3_vec_kernel<1, 4> : vw == 2 ? dw3x3_vec_kernel<1, 2> : dw3x3_vec_kernel<1, 1>)
+                              : (vw == 4 ? dw3x3_vec_kernel<2, 4> : vw == 2 ? dw3x3_vec_kernel<2, 2> : dw3x3_vec_kernel<2, 1>);
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, x, k, bias, y, planes, c, h, w, ho, wo, act, ppw,
+                           segs, seg_rows);
+    } else {
+        auto kern = stride == 1 ? dw3x3_cols_kernel<1, kDwRows> : dw3x3_cols_kernel<2, kDwRows>;
+        hipLaunchKernelGGL(kern, grid, dim3(kThreads), 0, stream, x, k, bias, y, planes, c, h, w, ho, wo, act, wpp,
+                           segs, seg_rows);
+    }
     return hipGetLastError();
 }
 

@@ -54,6 +54,7 @@ class MobileNetV1Engine:
         self._keep = []   # device tensors and plans the launches refer to
         self._steps = []  # closures, one launch each
         self.fused_blocks = 0
+        self.fusion_times = []  # (block, fused ms, two-launch ms) of each timed choice
         c0 = int(net.stem_w.shape[0])
         hs, ws = (h - 1) // 2 + 1, (w - 1) // 2 + 1
         stem_w, stem_b = put(net.stem_w), put(net.stem_b)
@@ -85,7 +86,9 @@ class MobileNetV1Engine:
                           self._run_step(plan, mid, out, batch, ho, wo)])
             if fused is not None and split is not None:
                 f_step = [self._run_step(fused, cur, out, batch, hh, ww)]
-                if self._time(f_step) <= self._time(split[1]):
+                tf, ts = self._time(f_step), self._time(split[1])
+                self.fusion_times.append((len(self.fusion_times), round(tf, 4), round(ts, 4)))
+                if tf <= ts:
                     split[0][3].close()
                     split = None
                 else:

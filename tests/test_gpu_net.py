@@ -68,6 +68,12 @@ def test_stem_conv_parity(n, h, w, cin, cout, stride, act, bias):
     # one past it (the direct kernel)
     (4, 32, 112, 112, 1, "relu6"), (3, 333, 3, 3, 1, "relu"), (2, 6, 7, 1, 1, "none"), (3, 17, 15, 13, 2, "relu6"),
     (2, 3, 126, 126, 1, "relu6"), (1, 3, 127, 127, 2, "relu"),
+    # every lane width and stride: 4 and 2 columns per lane at stride 2
+    # (w a multiple of 8, of 4 only), one column at stride 2 with w even,
+    # the MobileNet planes 56 and 28 at stride 2; planes too wide for whole
+    # planes per wavefront (one column per lane, 64-column parts), both strides
+    (2, 8, 20, 200, 2, "relu6"), (2, 16, 28, 28, 2, "relu"), (3, 16, 14, 14, 2, "relu6"), (2, 16, 56, 56, 2, "none"),
+    (2, 8, 30, 300, 1, "relu6"), (1, 4, 9, 301, 2, "relu"),
 ])
 def test_standalone_depthwise_parity(n, c, h, w, stride, act):
     import torch
@@ -81,6 +87,24 @@ def test_standalone_depthwise_parity(n, c, h, w, stride, act):
     spconv_depthwise3x3(to_gpu(x), to_gpu(k), to_gpu(b), act, stride, y, n, c, h, w)
     d, sd = oracle.dw3x3_ref(x, k, b, act, stride)
     _check(_sync_np(y), d, sd, "depthwise")
+
+
+@pytest.mark.parametrize("stride", [1, 2])
+def test_standalone_depthwise_unaligned_pointers(stride):
+    """x and y one element off a 16-byte boundary: one column per lane."""
+    import torch
+    from paper_1911_09723_amd import spconv_depthwise3x3
+    n, c, h, w = 2, 12, 28, 28
+    rng = np.random.default_rng(9 + stride)
+    x = rng.standard_normal((n, c, h, w)).astype(np.float32)
+    k, b = make_depthwise(c, 3)
+    ho, wo = (h - 1) // stride + 1, (w - 1) // stride + 1
+    xb = to_gpu(np.concatenate([np.zeros(1, np.float32), x.ravel()]))[1:]
+    yb = torch.full((n * c * ho * wo + 1,), float("nan"), device="cuda:0")
+    note("depthwise unaligned stride %d" % stride)
+    spconv_depthwise3x3(xb, to_gpu(k), to_gpu(b), "relu6", stride, yb[1:], n, c, h, w)
+    d, sd = oracle.dw3x3_ref(x, k, b, "relu6", stride)
+    _check(_sync_np(yb[1:]).reshape(n, c, ho, wo), d, sd, "depthwise unaligned")
 
 
 @pytest.mark.parametrize("n,c,h,w", [(64, 1024, 7, 7), (3, 5, 1, 1), (2, 7, 13, 3)])
