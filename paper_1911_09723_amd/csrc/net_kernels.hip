@@ -360,37 +360,45 @@ gap_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t planes, i
 }
 
 // Global average pooling for small planes (hw <= kGapMaxHw): a wavefront
-// owns 64 consecutive planes, whose 64 hw values are contiguous; it copies
-// them into LDS with coalesced loads (16 bytes per lane when aligned), then
-// each lane sums one plane in ascending p in fp32, as gap_kernel does.
+// owns kGapPlanes consecutive planes, whose values are contiguous; it copies
+// them into its own LDS area with coalesced loads (16 bytes per lane when
+// aligned, all of a lane's loads in flight at once), then each of the first
+// kGapPlanes lanes sums one plane in ascending p in fp32, as gap_kernel
+// does.  Four wavefronts per workgroup, 64 planes.
 constexpr int32_t kGapMaxHw = 256;
+constexpr int32_t kGapPlanes = 16;
 
 template <bool VEC>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(256)
 gap_staged_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t planes, int32_t hw, float inv) {
     extern __shared__ __align__(16) float buf[];
-    const int lane = threadIdx.x;
-    const int64_t q0 = static_cast<int64_t>(blockIdx.x) * 64;
-    const int32_t nq = static_cast<int32_t>(planes - q0 < 64 ? planes - q0 : 64);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    float *wb = buf + wave * kGapPlanes * hw;  // 64 hw bytes per wavefront: 16-byte aligned
+    const int64_t q0 = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * kGapPlanes;
+    if (q0 >= planes)
+        return;
+    const int32_t nq = static_cast<int32_t>(planes - q0 < kGapPlanes ? planes - q0 : kGapPlanes);
     const int32_t total = nq * hw;
-    const float *src = x + q0 * hw;
+    const float *src = x + q0 * hw;  // 64 hw bytes per group of planes: 16-byte aligned when x is
     if constexpr (VEC) {
         const int32_t nvec = total / 4;  // whole 16-byte groups, then the last few values
-#pragma unroll 8
+#pragma unroll 4
         for (int32_t v = lane; v < nvec; v += 64)
-            *reinterpret_cast<f4 *>(buf + 4 * v) = *reinterpret_cast<const f4 *>(src + 4 * v);
+            *reinterpret_cast<f4 *>(wb + 4 * v) = *reinterpret_cast<const f4 *>(src + 4 * v);
         for (int32_t t = 4 * nvec + lane; t < total; t += 64)
-            buf[t] = src[t];
+            wb[t] = src[t];
     } else {
+#pragma unroll 4
         for (int32_t t = lane; t < total; t += 64)
-            buf[t] = src[t];
+            wb[t] = src[t];
     }
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     if (lane >= nq)
         return;
-    const float *pl = buf + lane * hw;
+    const float *pl = wb + lane * hw;
     float acc = 0.0f;
     for (int32_t p = 0; p < hw; ++p)
         acc += pl[p];
@@ -576,14 +584,14 @@ hipError_t launch_linear(const float *x, const float *wt, const float *bias, flo
 hipError_t launch_gap(const float *x, float *y, int32_t n, int32_t c, int64_t hw, hipStream_t stream) {
     const int64_t planes = static_cast<int64_t>(n) * c;
     if (hw <= kGapMaxHw) {
-        const bool vec = reinterpret_cast<uintptr_t>(x) % 16 == 0;  // every group starts 256 hw bytes in
-        const unsigned gblocks = static_cast<unsigned>((planes + 63) / 64);
-        const size_t lds = static_cast<size_t>(64) * hw * sizeof(float);
+        const bool vec = reinterpret_cast<uintptr_t>(x) % 16 == 0;  // every group starts 64 hw bytes in
+        const unsigned gblocks = static_cast<unsigned>((planes + 4 * kGapPlanes - 1) / (4 * kGapPlanes));
+        const size_t lds = static_cast<size_t>(4 * kGapPlanes) * hw * sizeof(float);
         if (vec)
-            hipLaunchKernelGGL(gap_staged_kernel<true>, dim3(gblocks), dim3(64), lds, stream, x, y, planes,
+            hipLaunchKernelGGL(gap_staged_kernel<true>, dim3(gblocks), dim3(256), lds, stream, x, y, planes,
                                static_cast<int32_t>(hw), 1.0f / static_cast<float>(hw));
         else
-            hipLaunchKernelGGL(gap_staged_kernel<false>, dim3(gblocks), dim3(64), lds, stream, x, y, planes,
+            hipLaunchKernelGGL(gap_staged_kernel<false>, dim3(gblocks), dim3(256), lds, stream, x, y, planes,
                                static_cast<int32_t>(hw), 1.0f / static_cast<float>(hw));
         return hipGetLastError();
     }

@@ -975,7 +975,7 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
     int32_t *ctl = reinterpret_cast<int32_t *>(lds + a.ctl_off);  // free[kMaxRegions], fill[kMaxRegions]
     if (tid < kMaxRegions) {
         ctl[tid] = 0;
-        ctl[kMaxRegions + tid] = nwaves;  // tile 0 is copied by everyone below
+        ctl[kMaxRegions + tid] = 0;
     }
     const Rsrc rpi = make_rsrc(pidx, static_cast<uint32_t>(a.idx_bytes));
     const Rsrc rpv = make_rsrc(pval, static_cast<uint32_t>(a.val_bytes));
@@ -984,15 +984,14 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
     const int32_t wb0 = wave_ptr[wave], wb1 = wave_ptr[wave + 1];
     const int32_t R = a.whole_tiles / static_cast<int32_t>(gridDim.x);  // whole rounds of every workgroup
 
-    if (R > 0)
-        copy_share<G, F16>(a, x, lds_base, whole_work(a, 0).tile, 0, a.strip_rows, wave, nwaves, lane);
-    wait_vmcnt<0>();
-    __syncthreads();  // table, zero row, counters and tile 0 ready
+    __syncthreads();  // table, zero row and counters ready
 
     // ---- whole rounds ----
     // the next share this wave copies (part cq of tile ct) and the parts whose
-    // shares are in flight
-    int32_t cq = 0, ct = 1;
+    // shares are in flight.  Tile 0 streams in part by part like every other
+    // tile: a wavefront starts on part 0 as soon as all of its shares have
+    // landed, while the later parts are still on their way.
+    int32_t cq = 0, ct = 0;
     uint32_t pend = 0;
     auto publish = [&]() __attribute__((always_inline)) {
         static_for<kMaxRegions>([&](auto qc) __attribute__((always_inline)) {
