@@ -826,7 +826,11 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
             return E_UNSUPPORTED;
         }
         p.pipe_sets = opt.pipe_sets ? opt.pipe_sets : max_sets;
-        p.regions = opt.regions ? std::min(opt.regions, p.strip_rows / 4) : std::min(kMaxRegions, p.strip_rows / 4);
+        // automatic: about one part per kAutoRegionRows channels (measured on
+        // MI355X: a part's refill is a workgroup-wide dependency, and narrow
+        // strips run fastest in one or two parts, 512 channels in three)
+        const int32_t auto_regions = std::max(1, std::min(kMaxRegions, (p.strip_rows + kAutoRegionRows - 1) / kAutoRegionRows));
+        p.regions = std::min(opt.regions ? opt.regions : auto_regions, p.strip_rows / 4);
         p.region_rows = (p.strip_rows / 4 + p.regions - 1) / p.regions * 4;
         p.regions = (p.strip_rows + p.region_rows - 1) / p.region_rows;  // none left empty
         build_interleaved(p);

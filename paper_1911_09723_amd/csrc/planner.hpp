@@ -96,6 +96,7 @@ constexpr int32_t kMaxWaves = 16;
 constexpr int32_t kMaxParts = 64;
 // Most parts of the strip the pipelined kernel refills independently.
 constexpr int32_t kMaxRegions = 4;
+constexpr int32_t kAutoRegionRows = 192;  // channels per strip part of the automatic choice
 // LDS bytes of the strip-refill counters at the end of a workgroup's LDS
 // (per region: wavefronts done with it, copies of it landed).
 constexpr int32_t kCtlBytes = 8 * kMaxRegions;
