@@ -473,6 +473,11 @@ def _read_counter_dir(d, counter):
     return per
 
 
+def _layer_kernel(name):
+    """A kernel of the sparse 1x1 (strip, direct, register-indexed or outer-product)."""
+    return "spmm" in name or "outer_kernel" in name
+
+
 def traffic_summary(fetch_dir, write_dir, commands, out_base):
     """Scale FETCH_SIZE / WRITE_SIZE (KiB per dispatch) by the copy kernel's
     reading and write the per-launch HBM traffic of the headline kernel."""
@@ -486,14 +491,14 @@ def traffic_summary(fetch_dir, write_dir, commands, out_base):
         copy_kib = float(np.median(copy))
         factor = COPY_BYTES / (copy_kib * 1024.0)
         out[counter] = {"copy_kib_per_dispatch": copy_kib, "factor": factor, "kernels": {}}
-        kinds = sorted({k for (k, _) in per if "spmm" in k})
+        kinds = sorted({k for (k, _) in per if _layer_kernel(k)})
         for k in kinds:
             vals = [v for (kk, _), v in per.items() if kk == k]
             out[counter]["kernels"][k] = {"kib_per_dispatch": float(np.median(vals)), "dispatches": len(vals),
                                           "bytes_scaled": float(np.median(vals)) * 1024.0 * factor}
     # the headline kernel: --profile-run launches the unstructured layer first,
     # so its kernel is the spmm kernel of the lowest dispatch id
-    firsts = sorted((d, k) for (k, d) in _read_counter_dir(fetch_dir, "FETCH_SIZE") if "spmm" in k)
+    firsts = sorted((d, k) for (k, d) in _read_counter_dir(fetch_dir, "FETCH_SIZE") if _layer_kernel(k))
     if firsts:
         k = firsts[0][1]
         out["headline_kernel"] = k
@@ -513,7 +518,7 @@ def traffic_summary(fetch_dir, write_dir, commands, out_base):
     lines += ["", "| kernel | counter | KiB/dispatch | scaled MB |", "|---|---|---|---|"]
     for c in ("FETCH_SIZE", "WRITE_SIZE"):
         for k, v in out[c]["kernels"].items():
-            m = re.search(r"spmm_\w+<[^>]*>", k)
+            m = re.search(r"(spmm_\w+|outer_kernel)<[^>]*>", k)
             lines.append("| `%s` | %s | %.0f | %.2f |" % (m.group(0) if m else k, c, v["kib_per_dispatch"],
                                                           v["bytes_scaled"] / 1e6))
     if "bytes_per_launch" in out:
