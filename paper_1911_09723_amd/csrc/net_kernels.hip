@@ -407,74 +407,88 @@ gap_staged_kernel(const float *__restrict__ x, float *__restrict__ y, int64_t pl
 
 // Dense fully connected layer (the classifier the paper keeps dense, Sec. 3.1):
 //   y[n, r] = act(b[r] + sum_c W[r, c] * x[n, c]),  W row-major [cout][cin].
-// Lane = image (64 per wavefront), kLinRows rows per workgroup: every
-// wavefront reads its lanes' images with 16-byte loads (each line serves 8 of
-// them through L1) and the rows' weights, the same for all lanes, with
-// scalar loads.  The kLinSplit wavefronts of a workgroup take consecutive
-// ranges of the input channels; each lane sums its range in ascending c by
-// fp32 FMA from zero, the range sums are added in ascending order through
-// LDS, then the bias, then the activation.  VEC: 16-byte loads (cin a
-// multiple of 4, x and W 16-byte aligned).
-constexpr int kLinRows = 4;
-constexpr int kLinSplit = 16;
+// A dense product, so it runs on the matrix cores: a workgroup owns a tile of
+// 16 images x 16 output rows (enough tiles to spread the classifier of a
+// batch of 64 over the whole GPU), and its kLinWaves wavefronts split the
+// input channels into equal chunks (a multiple of 16 each).  A wavefront
+// accumulates its chunk with fp32 16x16x4 matrix instructions (lane l
+// supplies image or row l % 16 and the k quarter l / 16); within each block
+// of 16 channels, step s takes channels s, 4 + s, 8 + s and 12 + s, so a
+// lane's four steps read 4 consecutive channels of its image and of its row:
+// one 16-byte load each (VEC: cin a multiple of 4, x and W 16-byte aligned;
+// else element loads), all of a batch of blocks issued before its first
+// matrix instruction.  The chunk sums are added in ascending chunk order
+// through LDS, then the bias, then the activation.  Images and rows past the
+// end read the last one and are not stored.
+constexpr int kLinWaves = 8;
+constexpr int kLinBatch = 4;  // blocks of 16 channels loaded together
 
 template <bool VEC>
-__global__ void __launch_bounds__(64 * kLinSplit)
+__global__ void __launch_bounds__(64 * kLinWaves)
 linear_kernel(const float *__restrict__ x, const float *__restrict__ wt, const float *__restrict__ bias,
               float *__restrict__ y, int32_t n, int32_t cin, int32_t cout, int32_t act) {
-    __shared__ float part[kLinSplit][kLinRows][64];
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    __shared__ float part[kLinWaves * 4 * 64];  // each wavefront's 16 x 16 accumulator tile
     const int lane = threadIdx.x & 63;
-    const int32_t r0 = blockIdx.x * kLinRows;
-    const int32_t img = blockIdx.y * 64 + lane;
-    const float *xr = x + static_cast<int64_t>(img < n ? img : n - 1) * cin;
-    int32_t chunk = (cin + kLinSplit - 1) / kLinSplit;
-    if constexpr (VEC)
-        chunk = (chunk + 3) & ~3;
-    const int32_t c0 = wave * chunk < cin ? wave * chunk : cin;
-    const int32_t c1 = c0 + chunk < cin ? c0 + chunk : cin;
-    typedef const __attribute__((address_space(4))) float cfloat;
-    typedef const __attribute__((address_space(4))) f4 cf4;
-    cfloat *wr[kLinRows];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int i = lane & 15, kq = lane >> 4;
+    const int32_t img = min(static_cast<int32_t>(blockIdx.y) * 16 + i, n - 1);
+    const int32_t row = min(static_cast<int32_t>(blockIdx.x) * 16 + i, cout - 1);
+    const float *xr = x + static_cast<int64_t>(img) * cin;
+    const float *wr = wt + static_cast<int64_t>(row) * cin;
+    // this thread's output after the reduction (threads 0 .. 255): register
+    // r = t / 64 of lane l = t % 64 holds image 4 (l / 16) + r and row l % 16
+    // of the tile; its bias is loaded now, off the critical path
+    const int t = threadIdx.x;
+    const int r_out = (t >> 6) & 3, l_out = t & 63;
+    const int32_t oi = static_cast<int32_t>(blockIdx.y) * 16 + 4 * (l_out >> 4) + r_out;
+    const int32_t oj = static_cast<int32_t>(blockIdx.x) * 16 + (l_out & 15);
+    const float bo = bias && t < 256 ? bias[min(oj, cout - 1)] : 0.0f;
+    const int32_t chunk = ((cin + kLinWaves - 1) / kLinWaves + 15) & ~15;
+    const int32_t k_begin = wave * chunk;
+    const int32_t k_end = min(cin, k_begin + chunk);
+    f4 c = {0.f, 0.f, 0.f, 0.f};
+    for (int32_t kbat = k_begin; kbat < k_end; kbat += 16 * kLinBatch) {
+        float av[kLinBatch][4], bv[kLinBatch][4];
 #pragma unroll
-    for (int i = 0; i < kLinRows; ++i)
-        wr[i] = (cfloat *)(wt + static_cast<int64_t>(r0 + i < cout ? r0 + i : cout - 1) * cin);
-    float acc[kLinRows] = {};
-    if constexpr (VEC) {
-#pragma unroll 4
-        for (int32_t c = c0; c < c1; c += 4) {
-            const f4 xv = *reinterpret_cast<const f4 *>(xr + c);
+        for (int q = 0; q < kLinBatch; ++q) {
+            const int32_t kb = kbat + 16 * q + 4 * kq;  // this lane's 4 channels of block q
+            if constexpr (VEC) {
+                // cin and the chunk bounds are multiples of 4: the 4 channels are all in or all out
+                const bool in = kb < k_end;
+                const f4 xa = in ? *reinterpret_cast<const f4 *>(xr + kb) : f4{0.f, 0.f, 0.f, 0.f};
+                const f4 wb = in ? *reinterpret_cast<const f4 *>(wr + kb) : f4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int i = 0; i < kLinRows; ++i) {
-                const f4 wv = *(cf4 *)(wr[i] + c);
+                for (int e = 0; e < 4; ++e) {
+                    av[q][e] = xa[e];
+                    bv[q][e] = wb[e];
+                }
+            } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    acc[i] = __builtin_fmaf(wv[e], xv[e], acc[i]);
+                for (int e = 0; e < 4; ++e) {
+                    const bool in = kb + e < k_end;
+                    av[q][e] = in ? xr[kb + e] : 0.0f;
+                    bv[q][e] = in ? wr[kb + e] : 0.0f;
+                }
             }
         }
-    } else {
-        for (int32_t c = c0; c < c1; ++c) {
-            const float xv = xr[c];
 #pragma unroll
-            for (int i = 0; i < kLinRows; ++i)
-                acc[i] = __builtin_fmaf(wr[i][c], xv, acc[i]);
-        }
+        for (int q = 0; q < kLinBatch; ++q)
+#pragma unroll
+            for (int sstep = 0; sstep < 4; ++sstep)
+                c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[q][sstep], bv[q][sstep], c, 0, 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < kLinRows; ++i)
-        part[wave][i][lane] = acc[i];
+    for (int r = 0; r < 4; ++r)
+        part[(wave * 4 + r) * 64 + lane] = c[r];
     __syncthreads();
-    if (threadIdx.x >= 64 * kLinRows)
-        return;
-    const int i = threadIdx.x >> 6;
-    const int32_t r = r0 + i;
-    if (r >= cout || img >= n)
+    if (t >= 256)
         return;
     float sum = 0.0f;
 #pragma unroll
-    for (int w = 0; w < kLinSplit; ++w)
-        sum += part[w][i][lane];
-    y[static_cast<int64_t>(img) * cout + r] = clamp_act(sum + (bias ? bias[r] : 0.0f), act);
+    for (int w = 0; w < kLinWaves; ++w)
+        sum += part[(w * 4 + r_out) * 64 + l_out];
+    if (oi < n && oj < cout)
+        y[static_cast<int64_t>(oi) * cout + oj] = clamp_act(sum + bo, act);
 }
 
 using ConvFn = void (*)(const float *, const float *, const float *, float *, int32_t, int32_t, int32_t, int32_t,
@@ -571,12 +585,12 @@ hipError_t launch_linear(const float *x, const float *wt, const float *bias, flo
                          int32_t cout, int32_t act, hipStream_t stream) {
     const bool vec = cin % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                      reinterpret_cast<uintptr_t>(wt) % 16 == 0;
-    const dim3 grid(static_cast<unsigned>((cout + kLinRows - 1) / kLinRows), static_cast<unsigned>((n + 63) / 64));
+    const dim3 grid(static_cast<unsigned>((cout + 15) / 16), static_cast<unsigned>((n + 15) / 16));
     if (vec)
-        hipLaunchKernelGGL(linear_kernel<true>, grid, dim3(64 * kLinSplit), 0, stream, x, wt, bias, y, n, cin, cout,
+        hipLaunchKernelGGL(linear_kernel<true>, grid, dim3(64 * kLinWaves), 0, stream, x, wt, bias, y, n, cin, cout,
                            act);
     else
-        hipLaunchKernelGGL(linear_kernel<false>, grid, dim3(64 * kLinSplit), 0, stream, x, wt, bias, y, n, cin,
+        hipLaunchKernelGGL(linear_kernel<false>, grid, dim3(64 * kLinWaves), 0, stream, x, wt, bias, y, n, cin,
                            cout, act);
     return hipGetLastError();
 }

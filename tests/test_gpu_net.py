@@ -123,6 +123,9 @@ def test_global_avg_pool_parity(n, c, h, w):
 @pytest.mark.parametrize("n,cin,cout,act,bias,offset", [
     (64, 1024, 1000, "none", True, 0), (3, 7, 130, "relu6", True, 0), (5, 64, 64, "relu", False, 1),
     (1, 1, 1, "none", True, 0),
+    # several image and row tiles with ragged edges, channel chunks that end
+    # inside a block of 8, a width that leaves most wavefronts without channels
+    (70, 2052, 33, "relu", True, 0), (33, 12, 65, "none", True, 0), (2, 1030, 7, "relu6", False, 1),
 ])
 def test_linear_parity(n, cin, cout, act, bias, offset):
     """Against the oracle's 1x1 over 1 x 1 images with the dense weight as CSR;
