@@ -208,6 +208,20 @@ struct Entry {
     u4 w[K];
 };
 
+// The same from one resource over both streams, the weights `vdelta` bytes
+// after the channel offsets (the plan's device image keeps them in that
+// order): one buffer descriptor fewer in scalar registers.
+template <int G, int K>
+__device__ __forceinline__ Entry<K> load_entry_one(Rsrc r, int32_t vdelta, int q, int32_t s) {
+    constexpr int NB = 64 / G;
+    Entry<K> en;
+    en.off = bload16(r, q * 16, s * NB * 16);
+#pragma unroll
+    for (int kk = 0; kk < K; ++kk)
+        en.w[kk] = bload16(r, vdelta + q * 16 * K + 16 * kk, s * NB * 16 * K);
+    return en;
+}
+
 template <int G, int K>
 __device__ __forceinline__ Entry<K> load_entry(Rsrc ri, Rsrc rv, int q, int32_t s) {
     constexpr int NB = 64 / G;
@@ -977,8 +991,11 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         ctl[tid] = 0;
         ctl[kMaxRegions + tid] = 0;
     }
-    const Rsrc rpi = make_rsrc(pidx, static_cast<uint32_t>(a.idx_bytes));
-    const Rsrc rpv = make_rsrc(pval, static_cast<uint32_t>(a.val_bytes));
+    // the weight stream follows the channel-offset stream in the plan's image
+    // (checked on the host: 0 <= pval - pidx and the end below 2^31)
+    const int32_t vdelta = static_cast<int32_t>(reinterpret_cast<const char *>(pval) -
+                                                reinterpret_cast<const char *>(pidx));
+    const Rsrc rpr = make_rsrc(pidx, static_cast<uint32_t>(vdelta) + static_cast<uint32_t>(a.val_bytes));
     const float lo = a.act == 0 ? -__builtin_huge_valf() : 0.0f;
     const float hi = a.act == 2 ? 6.0f : __builtin_huge_valf();
     const int32_t wb0 = wave_ptr[wave], wb1 = wave_ptr[wave + 1];
@@ -1098,12 +1115,12 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
         Entry<K> cr[NR];
 #pragma unroll
         for (int dd = 0; dd < D; ++dd)
-            cr[dd] = load_entry<G, K>(rpi, rpv, L.q, ws0 + dd % len);
+            cr[dd] = load_entry_one<G, K>(rpr, vdelta, L.q, ws0 + dd % len);
         for (int32_t g0 = 0; g0 < total; g0 += NR) {
             static_for<NR>([&](auto kc) __attribute__((always_inline)) {
                 constexpr int KI = decltype(kc)::value;
                 if (g0 + KI < total) {
-                    cr[(KI + D) % NR] = load_entry<G, K>(rpi, rpv, L.q, ws0 + lpos);
+                    cr[(KI + D) % NR] = load_entry_one<G, K>(rpr, vdelta, L.q, ws0 + lpos);
                     lpos = lpos + 1 == len ? 0 : lpos + 1;
                     if (pos == pre) {
                         if (pos == 0) {
@@ -1343,6 +1360,13 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.busy_waves = p.busy_waves;
     a.idx_bytes = p.idx_bytes;
     a.val_bytes = p.val_bytes;
+    if (p.pidx && p.pval) {
+        // the pipelined kernel reads both interleaved streams through one
+        // resource based at pidx
+        const int64_t vdelta = reinterpret_cast<const char *>(p.pval) - reinterpret_cast<const char *>(p.pidx);
+        if (vdelta < 0 || vdelta + p.val_bytes > INT32_MAX)
+            return hipErrorInvalidValue;
+    }
     a.x_bytes = x_bytes;
     a.y_bytes = y_bytes;
     a.tiles = static_cast<int32_t>(tiles);
