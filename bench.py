@@ -13,12 +13,15 @@ The "1x1 indexed" and "1x4 indexed" variants run the same layers on the
 register-indexed kernel (kernel=3) instead of the automatic choice.
 A third variant runs the same 1x1 behind a fused depthwise 3x3 (stride 1,
 ReLU6): one MobileNet v1 block at 512 channels.  The ``network`` entries time
-a whole synthetic MobileNet v1 forward pass (17 launches replayed as one
-graph) at batch 1 and 64.
+a whole synthetic MobileNet v1 forward pass (one graph replay) at batch 1
+and 64.
 Inputs are resident in HBM before timing starts; three (X, Y) buffer sets,
 616 MB in all, rotate so no step finds its operands in the 256 MB
-last-level cache.  Kernel durations come from HIP events recorded on the
-launch stream around every launch.
+last-level cache.  The kernel's mean duration is one pair of HIP events on
+the launch stream around the timed region of back-to-back launches, divided
+by the launch count; a second pass with an event pair around every launch
+gives the minimum and ``event_pair_us_mean`` (each event pair adds its own
+cost, a few microseconds).
 
 The ``configs`` list times every layer of every workload configuration (c0
 .. c4: the small parity layer, MobileNet v1's pointwise layers at batch 1
@@ -42,7 +45,7 @@ Two more modes produce the HBM-traffic figures of the ``roofline`` object:
   --traffic-summary F W    read the FETCH_SIZE (F) and WRITE_SIZE (W) counter
                            directories of two such runs, scale each counter by
                            what it read for the copy, and write
-                           profiles/traffic_spmm_strip_512_14_b256.{json,md}
+                           profiles/traffic_spmm_pipe_512x512_14x14_b256.{json,md}
 """
 
 from __future__ import annotations
@@ -143,20 +146,28 @@ def time_variant(layer, steps, warmup, sets, dw=None, **options):
     stream = torch.cuda.current_stream()
     for i in range(warmup):
         spconv_run(plan.handle, xs[i % sets], ys[i % sets], n, h, w, stream)
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    # The timed region: `steps` launches back to back between one pair of
+    # HIP events on the launch stream (its mean is the kernel's average
+    # duration plus the launch gaps; an event pair around every launch would
+    # add each event's own cost), then a second pass with an event pair per
+    # launch for the spread (min, and the per-launch mean it reports).
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     t_start.record(stream)
     for i in range(steps):
-        ev[i][0].record(stream)
         spconv_run(plan.handle, xs[i % sets], ys[i % sets], n, h, w, stream)
-        ev[i][1].record(stream)
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     region_ms = t_start.elapsed_time(t_end)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for i in range(steps):
+        ev[i][0].record(stream)
+        spconv_run(plan.handle, xs[i % sets], ys[i % sets], n, h, w, stream)
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
     kern_ms = [a.elapsed_time(b) for a, b in ev]
     info = plan.info()
     flags = plan.check(clear=True)
@@ -372,7 +383,8 @@ def summarize(layer, r, dw=False):
     import numpy as np
     steps = len(r["kernel_ms"])
     t_step = r["region_ms"] / steps / 1e3
-    t_kern = float(np.mean(r["kernel_ms"])) / 1e3
+    t_kern = t_step  # back-to-back launches in the timed region
+    t_launch = float(np.mean(r["kernel_ms"])) / 1e3  # the per-launch event pairs
     flops = layer.flops()
     b_alg = layer.alg_bytes()
     if dw:
@@ -389,6 +401,7 @@ def summarize(layer, r, dw=False):
         "ms_per_step": round(t_step * 1e3, 5),
         "kernel_us_mean": round(t_kern * 1e6, 3),
         "kernel_us_min": round(min(r["kernel_ms"]) * 1e3, 3),
+        "event_pair_us_mean": round(t_launch * 1e6, 3),
         "hbm_gbs_algorithmic": round(b_alg / t_kern / 1e9, 1),
         "roofline_us": round(t_roof * 1e6, 3),
         "roofline_frac": round(t_roof / t_kern, 4),
