@@ -281,13 +281,21 @@ typedef struct {
     int32_t kernel;      /* 0 = choose automatically: the LDS-strip or direct-load kernel, or, for
                             runs with enough columns on layers where it measured faster, the
                             register-indexed kernel (spconv_plan_info.indexed_min_cols) or the
-                            outer-product kernel (spconv_plan_info.outer_min_cols);
+                            outer-product kernel (spconv_plan_info.outer_min_cols); fp32
+                            unstructured inputs of more than 1264 channels take channel-range
+                            passes (5);
                             1 = LDS-strip kernel (SPCONV_E_UNSUPPORTED when the strip of cin
                             channels does not fit in LDS); 2 = direct-load kernel; 3 =
                             register-indexed kernel (SPCONV_E_UNSUPPORTED for fp16 storage or a
                             depthwise stage); 4 = outer-product kernel on the matrix cores
                             (1 x 4 blocks, no depthwise stage, cin <= 632, else
-                            SPCONV_E_UNSUPPORTED) */
+                            SPCONV_E_UNSUPPORTED); 5 = channel-range passes for inputs too wide
+                            for one LDS strip (Sec. 3.2, 4.1): the input channels in ranges of at
+                            most 512, one LDS-strip launch each on the same y, every launch
+                            after the first adding to the partial sums the earlier ones left in
+                            y, the bias and activation applied by the last; each output is still
+                            summed over all channels in ascending order (fp32 unstructured plans
+                            without a depthwise stage, not static, else SPCONV_E_UNSUPPORTED) */
     int32_t group_lanes; /* 0 = choose automatically; else 4, 8 or 16 lanes per (block) row: each
                             lane accumulates 16 / group_lanes vectors of 16 bytes of the tile's
                             columns, and a wavefront works on 64 / group_lanes rows at a time
@@ -407,6 +415,8 @@ typedef struct {
                                  (N * out_h * out_w) take the register-indexed kernel; 0 = never (and
                                  for host-only plans, which know no device) */
     int64_t outer_min_cols;   /* the same for the outer-product kernel, which takes precedence */
+    int64_t channel_passes;   /* kernel option 5: the number of channel-range passes a run launches
+                                 (0 for other plans) */
 } spconv_plan_info;
 
 /* Describe a plan.  Host only; does not touch the device. */

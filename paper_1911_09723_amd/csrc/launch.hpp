@@ -73,6 +73,11 @@ struct DevicePlan {
     const int32_t *owave_ptr = nullptr;
     const int32_t *owave_oct = nullptr;
     int64_t outer_min_cols = 0;         // automatic choice: runs of at least this many columns take it (0: never)
+    // a pass over one channel range of a wider input (spconv_api.cpp): X's
+    // channels per image (0: cin), and whether the pass adds to the partial
+    // sums already in Y (every pass but the first)
+    int32_t xc = 0;
+    int32_t accum = 0;
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`

@@ -610,7 +610,8 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         in.block_cols = 1;
     }
     if (opt.kernel < 0 || opt.kernel > 4) {
-        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct), 3 (register-indexed) or 4 (lockstep)";
+        err = "kernel must be 0 (automatic), 1 (strip), 2 (direct), 3 (register-indexed), 4 (lockstep) or 5 "
+              "(channel-range passes)";
         return E_ARG;
     }
     if (opt.kernel == 4 && !outer_supported(in)) {

@@ -29,11 +29,18 @@ struct spconv_plan_s {
     size_t dbytes = 0;
     bool host_only = false;
     uint64_t static_gen = 0;  // plans in the static device array: the generation they wrote (0: not one)
+    // channel-range passes (kernel option 5): one plan per range of input
+    // channels starting at pass_c0[i], run in order; empty for other plans
+    std::vector<spconv_plan_s *> passes;
+    std::vector<int32_t> pass_c0;
 };
 
 namespace {
 
 thread_local std::string g_err;
+
+constexpr int32_t kKernelPasses = 5;    // kernel option: channel-range passes
+constexpr int32_t kPassChannels = 512;  // most input channels per pass (its LDS strip fits)
 
 // The static device array of spconv_plan_create_static: one per GPU (each
 // device holds its own copy of this file-scope array), found once per device
@@ -293,8 +300,29 @@ bool ranges_overlap(const void *a, size_t abytes, const void *b, size_t bbytes) 
 }
 
 // Plan creation shared by every entry point: options, planning, upload.
+spconv_status create_passes(spconv_plan_s *pl, const spconv::Input &in, const spconv_options &o);
+
+// Free a plan, its passes and its device image without touching the error
+// message (create_plan's failure paths keep theirs); the first HIP error.
+hipError_t free_plan(spconv_plan_s *pl) {
+    hipError_t st = hipSuccess;
+    for (spconv_plan_s *q : pl->passes) {
+        const hipError_t e = free_plan(q);
+        if (st == hipSuccess)
+            st = e;
+    }
+    if (pl->dmem) {
+        const hipError_t e = hipFree(pl->dmem);
+        if (st == hipSuccess)
+            st = e;
+    }
+    delete pl;
+    return st;
+}
+
+// xc, accum: set for the passes of a channel-range plan (see create_passes)
 spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spconv_options *opts,
-                          bool use_static = false) {
+                          bool use_static = false, int32_t xc = 0, int32_t accum = 0) {
     if (!out)
         return fail(SPCONV_E_ARG, "out is NULL");
     *out = nullptr;
@@ -318,6 +346,21 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
     po.pipe_sets = o.pipe_sets;
     po.regions = o.regions;
     po.lane_cols = o.lane_cols;
+    // automatic choice: fp32 unstructured inputs too wide for the lockstep
+    // kernel's strips (measured: passes over the LDS-strip kernel beat the
+    // direct-load kernel there, 124 against 197 us for 1280 -> 320 @ 7x7,
+    // batch 128; below that width the lockstep kernel is faster)
+    const bool auto_passes = o.kernel == 0 && in.cin > spconv::kOuterMaxCin16 && in.block_rows == 1 &&
+                             in.block_cols <= 1 && in.storage == 0 && !in.dw_stride && !use_static && xc == 0;
+    const bool passes = o.kernel == kKernelPasses || auto_passes;
+    if (passes) {
+        if (in.block_rows != 1 || in.block_cols > 1 || in.storage != 0 || in.dw_stride || use_static) {
+            *out = nullptr;
+            return fail(SPCONV_E_UNSUPPORTED, "channel-range passes (kernel 5) run fp32 unstructured plans without "
+                                              "a depthwise stage, not in the static device array");
+        }
+        po.kernel = 0;  // the plan itself: the automatic choice (its image serves unpacking and info)
+    }
 
     spconv_plan_s *pl = new (std::nothrow) spconv_plan_s();
     if (!pl)
@@ -335,6 +378,8 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
         return fail(static_cast<spconv_status>(st), err);
     }
     fill_device_geometry(pl);
+    pl->dev.xc = xc;
+    pl->dev.accum = accum;
     pl->host_only = o.host_only == 1;
     if (!pl->host_only) {
         spconv_status us = upload(pl, use_static);
@@ -350,13 +395,64 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
                 us = hip_fail("kernel launch set-up", pe);
         }
         if (us != SPCONV_OK) {
-            if (pl->dmem)
-                (void)hipFree(pl->dmem);
-            delete pl;
+            (void)free_plan(pl);
+            return us;
+        }
+    }
+    if (passes) {
+        const spconv_status us = create_passes(pl, in, o);
+        if (us != SPCONV_OK) {
+            (void)free_plan(pl);
             return us;
         }
     }
     *out = pl;
+    return SPCONV_OK;
+}
+
+// Kernel option 5: the input channels in ranges of at most kPassChannels
+// (equal sizes, multiples of 4), each a plan of the LDS-strip kernel over its
+// columns of W (shifted to start at 0) that reads X with the full input's
+// image stride.  The passes run in order on the same Y: every pass after the
+// first starts each row's accumulators from Y (the sums over the earlier
+// ranges), so each output is summed over all channels in ascending order from
+// zero, as in the other kernels; only the last adds the bias and applies the
+// activation.  The passes share the plan's error word.
+spconv_status create_passes(spconv_plan_s *pl, const spconv::Input &in, const spconv_options &o) {
+    const int32_t np = (in.cin + kPassChannels - 1) / kPassChannels;
+    const int32_t per = ((in.cin + np - 1) / np + 3) & ~3;
+    for (int32_t c0 = 0; c0 < in.cin; c0 += per) {
+        const int32_t c1 = std::min(in.cin, c0 + per);
+        const bool last = c1 == in.cin;
+        std::vector<int32_t> rp(static_cast<size_t>(in.cout) + 1, 0), ci;
+        std::vector<float> va;
+        for (int32_t r = 0; r < in.cout; ++r) {
+            for (int32_t t = in.row_ptr[r]; t < in.row_ptr[r + 1]; ++t) {
+                if (in.col_idx[t] >= c0 && in.col_idx[t] < c1) {
+                    ci.push_back(in.col_idx[t] - c0);
+                    va.push_back(in.values[t]);
+                }
+            }
+            rp[static_cast<size_t>(r) + 1] = static_cast<int32_t>(ci.size());
+        }
+        spconv::Input sub = in;
+        sub.cin = c1 - c0;
+        sub.row_ptr = rp.data();
+        sub.col_idx = ci.data();
+        sub.values = va.data();
+        sub.bias = last ? in.bias : nullptr;
+        sub.act = last ? in.act : static_cast<int32_t>(SPCONV_ACT_NONE);
+        spconv_options so = o;
+        so.kernel = 1;  // the LDS-strip kernel
+        spconv_plan q = nullptr;
+        const spconv_status st = create_plan(&q, sub, &so, false, in.cin, c0 > 0 ? 1 : 0);
+        if (st != SPCONV_OK)
+            return st;
+        q->dev.flag = pl->dev.flag;
+        q->dev.spin_limit = pl->dev.spin_limit;
+        pl->passes.push_back(q);
+        pl->pass_c0.push_back(c0);
+    }
     return SPCONV_OK;
 }
 
@@ -617,7 +713,16 @@ spconv_status spconv_run(spconv_plan plan, const void *x, void *y, int32_t n, in
     const int64_t qv = 16 / static_cast<int64_t>(e);  // columns in one 16-byte vector
     const int32_t vec = (hw % qv == 0) && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                         reinterpret_cast<uintptr_t>(y) % 16 == 0;
-    if (outer)
+    if (!plan->passes.empty()) {
+        // channel-range passes in order: pass i reads X from its first channel
+        for (size_t i = 0; i < plan->passes.size() && he == hipSuccess; ++i) {
+            const int64_t skip = static_cast<int64_t>(plan->pass_c0[i]) * ihw * static_cast<int64_t>(e);
+            he = spconv::launch_spmm(plan->passes[i]->dev, static_cast<const char *>(x) + skip, y,
+                                     static_cast<int32_t>(m), static_cast<int32_t>(hw), vec,
+                                     xel * static_cast<int64_t>(e) - skip, yel * static_cast<int64_t>(e), h, w,
+                                     static_cast<int32_t>(ow), static_cast<hipStream_t>(stream));
+        }
+    } else if (outer)
         he = spconv::launch_outer(plan->dev, x, y, static_cast<int32_t>(m), static_cast<int32_t>(hw),
                                   hw % 4 == 0 && reinterpret_cast<uintptr_t>(x) % 16 == 0 &&
                                       reinterpret_cast<uintptr_t>(y) % 16 == 0,
@@ -738,14 +843,8 @@ spconv_status spconv_destroy(spconv_plan plan) {
     g_err.clear();
     if (!plan)
         return SPCONV_OK;
-    spconv_status st = SPCONV_OK;
-    if (plan->dmem) {
-        hipError_t e = hipFree(plan->dmem);
-        if (e != hipSuccess)
-            st = hip_fail("hipFree", e);
-    }
-    delete plan;
-    return st;
+    const hipError_t e = free_plan(plan);
+    return e == hipSuccess ? SPCONV_OK : hip_fail("hipFree", e);
 }
 
 const char *spconv_last_error(void) { return g_err.c_str(); }
@@ -781,6 +880,7 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->block_cols = p.kc;
     info->indexed_min_cols = plan->host_only ? 0 : plan->dev.indexed_min_cols;
     info->outer_min_cols = plan->host_only ? 0 : plan->dev.outer_min_cols;
+    info->channel_passes = static_cast<int64_t>(plan->passes.size());
     return SPCONV_OK;
 }
 
@@ -935,6 +1035,8 @@ spconv_status spconv_plan_set_wait_limit(spconv_plan plan, int32_t sleeps) {
     if (sleeps < 0)
         return fail(SPCONV_E_ARG, "the wait bound must be >= 0");
     plan->dev.spin_limit = sleeps;
+    for (spconv_plan_s *q : plan->passes)
+        q->dev.spin_limit = sleeps;
     return SPCONV_OK;
 }
 

@@ -113,6 +113,8 @@ __device__ __forceinline__ void static_for(F &&f) {
 
 struct Args {
     int32_t cin, cout, hw, m, act;
+    int32_t xc;          // channels per image of X (the plan's cin, or more for a channel-range pass)
+    int32_t accum;       // add Y's values (partial sums of earlier channel ranges) before the bias
     int32_t vec;         // 16-byte global loads and stores (see launch_spmm)
     int32_t strip_rows;  // LDS strip channels (a multiple of 4); 0 for the direct kernel
     int32_t regions;     // strip parts refilled independently (pipelined kernel)
@@ -264,7 +266,7 @@ struct TileAddr {
     __device__ __forceinline__ void set(const Args &a, const Lane<G, F16> &L, const T *x, T *y, int32_t tile) {
         col0 = tile * GE::TC;
         n0 = col0 / a.hw;
-        const int64_t xbase = static_cast<int64_t>(n0) * a.cin * a.hw;
+        const int64_t xbase = static_cast<int64_t>(n0) * a.xc * a.hw;
         const int64_t ybase = static_cast<int64_t>(n0) * a.cout * a.hw;
         rx = make_rsrc(x + xbase, static_cast<uint32_t>(std::min<int64_t>(a.x_bytes - xbase * GE::E, kMaxRecords)));
         ry = make_rsrc(y + ybase, static_cast<uint32_t>(std::min<int64_t>(a.y_bytes - ybase * GE::E, kMaxRecords)));
@@ -273,7 +275,7 @@ struct TileAddr {
             const int32_t c = col0 + L.vb[j] * GE::QE;
             const int32_t n = c / a.hw;
             const int32_t p = c - n * a.hw;
-            xo[j] = c < a.m ? ((n - n0) * a.cin * a.hw + p) * GE::E : kOutOfRange;
+            xo[j] = c < a.m ? ((n - n0) * a.xc * a.hw + p) * GE::E : kOutOfRange;
             yo[j] = c < a.m ? ((n - n0) * a.cout * a.hw + p) * GE::E : kOutOfRange;
         }
     }
@@ -309,9 +311,9 @@ struct ColOff<G, F16, true> {
                 const int32_t n = c / a.hw;
                 const int32_t p = c - n * a.hw;
                 const int32_t k = std::min(GE::QE, a.hw - p);
-                xe[j][0] = c < a.m ? ((n - n0) * a.cin * a.hw + p) * GE::E : kOutOfRange;
+                xe[j][0] = c < a.m ? ((n - n0) * a.xc * a.hw + p) * GE::E : kOutOfRange;
                 xe[j][1] = k;
-                xe[j][2] = c + k < a.m ? ((n + 1 - n0) * a.cin * a.hw - k) * GE::E : kOutOfRange;
+                xe[j][2] = c + k < a.m ? ((n + 1 - n0) * a.xc * a.hw - k) * GE::E : kOutOfRange;
             }
             return;
         }
@@ -321,7 +323,7 @@ struct ColOff<G, F16, true> {
             for (int e = 0; e < GE::QE; ++e) {
                 const int32_t c = col0 + L.vb[j] * GE::QE + e;
                 const int32_t n = c / a.hw;
-                xe[j][e] = c < a.m ? ((n - n0) * a.cin * a.hw + (c - n * a.hw)) * GE::E : kOutOfRange;
+                xe[j][e] = c < a.m ? ((n - n0) * a.xc * a.hw + (c - n * a.hw)) * GE::E : kOutOfRange;
             }
     }
 };
@@ -450,7 +452,7 @@ __device__ __forceinline__ u4 read_x(const Args &a, const Lane<G, F16> &L, const
 // records fetched two steps ahead
 // ---------------------------------------------------------------------------
 
-template <int G, int K, bool F16, bool DIRECT, bool VEC>
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
 __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
                                            const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                            const unsigned char *lds, Rsrc ri, Rsrc rv,
@@ -473,13 +475,56 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
     // the bundle in progress: its row and biases (of this lane's group), steps left
     int32_t b = b0, rb = 0, left = 0;
     float bv[K];
+    // Channel-range passes after the first (ACC, fp32): a row's
+    // accumulators start from its values in Y, the sums over the earlier
+    // channels, so each output is still summed in ascending channel order
+    // from zero.  They are loaded one bundle ahead.
+    float pn[K][GE::V][GE::QE];
+    auto load_part = [&](int32_t bb) __attribute__((always_inline)) {
+        const int32_t row = rows_lds[bb * GE::NB + L.q];
+        const int32_t hwe = a.hw * GE::E;
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk)
+#pragma unroll
+            for (int j = 0; j < GE::V; ++j) {
+                if constexpr (VEC) {
+                    const u4 v = row >= 0 ? bload16(ta.ry, ta.yo[j] + (row * K + kk) * hwe, 0) : u4{0u, 0u, 0u, 0u};
+#pragma unroll
+                    for (int e = 0; e < GE::QE; ++e)
+                        pn[kk][j][e] = __uint_as_float(v[e]);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < GE::QE; ++e) {
+                        const int32_t c = ta.col0 + L.vb[j] * GE::QE + e;
+                        const int32_t n = c / a.hw;
+                        pn[kk][j][e] = row >= 0 && c < a.m
+                                           ? static_cast<float>(y[(static_cast<int64_t>(n) * a.cout + row * K + kk) * a.hw +
+                                                                  (c - n * a.hw)])
+                                           : 0.0f;
+                    }
+                }
+            }
+    };
     auto start_bundle = [&]() __attribute__((always_inline)) {
         rb = rows_lds[b * GE::NB + L.q];
 #pragma unroll
         for (int kk = 0; kk < K; ++kk)
             bv[kk] = bias_lds[(b * GE::NB + L.q) * K + kk];
         left = hdr[2 * b + 1];
+        if constexpr (ACC) {
+#pragma unroll
+            for (int kk = 0; kk < K; ++kk)
+#pragma unroll
+                for (int j = 0; j < GE::V; ++j)
+#pragma unroll
+                    for (int e = 0; e < GE::QE; ++e)
+                        acc[kk][j][e] = pn[kk][j][e];
+            if (b + 1 < b1)
+                load_part(b + 1);
+        }
     };
+    if constexpr (ACC)
+        load_part(b0);
     start_bundle();
 
     // A ring of NR entries (step i of the run in entry i % NR), unrolled over
@@ -514,7 +559,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
 
 // A wavefront's share of a work item: all of its bundles (whole tile) or its
 // bundles of rank % tail_parts == part (shared tile), one run each.
-template <int G, int K, bool F16, bool DIRECT, bool VEC>
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
 __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
                                          const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                          const unsigned char *lds, Rsrc ri, Rsrc rv, const int32_t *__restrict__ hdr,
@@ -530,7 +575,9 @@ __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, c
             b0 = bnext;
             b1 = wb1;
         } else {
-            while (bnext < wb1 && rank[bnext] % a.tail_parts != part)
+            // the wavefront's bundles at positions part, part + tail_parts, ...
+            // of its own list: every wavefront of a part gets an equal share
+            while (bnext < wb1 && (bnext - wb0) % a.tail_parts != part)
                 ++bnext;
             if (bnext >= wb1)
                 break;
@@ -538,7 +585,7 @@ __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, c
             b1 = bnext + 1;
         }
         bnext = b1;
-        run_simple<G, K, F16, DIRECT, VEC>(a, L, ta, co, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo, hi);
+        run_simple<G, K, F16, DIRECT, VEC, ACC>(a, L, ta, co, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo, hi);
     }
 }
 
@@ -564,7 +611,7 @@ __device__ __forceinline__ void copy_share(const Args &a, const typename Geo<G, 
     using GE = Geo<G, F16>;
     const int32_t col0 = tile * GE::TC;
     const int32_t n0 = col0 / a.hw;
-    const int64_t xbase = static_cast<int64_t>(n0) * a.cin * a.hw;
+    const int64_t xbase = static_cast<int64_t>(n0) * a.xc * a.hw;
     const i4 rs = rsrc_words(x + xbase, a.x_bytes - xbase * GE::E);
     const int32_t cc = col0 + (lane & 15) * GE::QE;
     const int32_t n = cc / a.hw;
@@ -572,7 +619,7 @@ __device__ __forceinline__ void copy_share(const Args &a, const typename Geo<G, 
     const int32_t crow = lane >> 4;
     const bool ok = cc < a.m;
     const int32_t hwe = a.hw * GE::E;
-    const int32_t lo = ((n - n0) * a.cin * a.hw + crow * a.hw + p) * GE::E;
+    const int32_t lo = ((n - n0) * a.xc * a.hw + crow * a.hw + p) * GE::E;
     for (int i = r0 / 4 + wave; i < r1 / 4; i += nwaves) {
         const int32_t voff = ok && 4 * i + crow < a.cin ? lo + i * 4 * hwe : kOutOfRange;
         const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds_base + 1024 * i);
@@ -611,7 +658,7 @@ __device__ __forceinline__ void load_strip_simple(const Args &a, const TileAddr<
                 v[e] = T(0);
                 if (row < a.cin && c < a.m) {
                     const int32_t n = c / a.hw;
-                    v[e] = x[(static_cast<int64_t>(n) * a.cin + row) * a.hw + (c - n * a.hw)];
+                    v[e] = x[(static_cast<int64_t>(n) * a.xc + row) * a.hw + (c - n * a.hw)];
                 }
             }
             *reinterpret_cast<u4 *>(lds + i * 16) = *reinterpret_cast<const u4 *>(v);
@@ -841,7 +888,7 @@ __device__ __forceinline__ bool dw_strip_staged(const Args &a, const float *__re
 // bundles; workgroup barriers around each strip.
 // ---------------------------------------------------------------------------
 
-template <int G, int K, bool F16, bool DIRECT, bool VEC>
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
 __global__ void __launch_bounds__(1024)
 spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__restrict__ idx,
             const float *__restrict__ val, const int32_t *__restrict__ hdr, const int32_t *__restrict__ table,
@@ -898,8 +945,8 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
             __syncthreads();  // strip ready
         }
         co.set(a, L, wk.tile);
-        run_item<G, K, F16, DIRECT, VEC>(a, L, ta, co, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0, wb1,
-                                         wk.part, lo, hi);
+        run_item<G, K, F16, DIRECT, VEC, ACC>(a, L, ta, co, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0,
+                                              wb1, wk.part, lo, hi);
         const Work nx = next_work(a, wk);
         if constexpr (!DIRECT)
             __syncthreads();  // done with strip(wk)
@@ -1266,6 +1313,19 @@ KernelFn pick_kv(const DevicePlan &p, bool vec) {
     // 1xk blocks keep the simple loop: their records take too many registers
     // for the pipelined kernel's fetch depth
     // (a depthwise stage computes the strip in the simple kernel)
+    // an accumulating channel-range pass (fp32, 1x1 rows) reads Y in the simple kernel
+    if constexpr (K == 1 && !F16) {
+        if (p.accum) {
+            switch (p.group_lanes) {
+            case 4: return vec ? spmm_kernel<4, 1, false, false, true, true> : spmm_kernel<4, 1, false, false, false, true>;
+            case 8: return vec ? spmm_kernel<8, 1, false, false, true, true> : spmm_kernel<8, 1, false, false, false, true>;
+            case 16: return vec ? spmm_kernel<16, 1, false, false, true, true> : spmm_kernel<16, 1, false, false, false, true>;
+            default: return nullptr;
+            }
+        }
+    }
+    if (p.accum)
+        return nullptr;
     if (vec && K == 1 && !p.dw_stride)
         return pick_pipe<K, F16>(p.group_lanes, p.pipe_sets);
     return vec ? pick_g<K, F16, false, true>(p.group_lanes) : pick_g<K, F16, false, false>(p.group_lanes);
@@ -1346,6 +1406,8 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
         rest ? std::max<int64_t>(1, std::min<int64_t>(pow2_floor(slots / nxcd / per_xcd), p.max_parts)) : 1;
     Args a;
     a.cin = p.cin;
+    a.xc = p.xc > 0 ? p.xc : p.cin;
+    a.accum = p.accum;
     a.cout = p.cout;
     a.hw = hw;
     a.m = m;

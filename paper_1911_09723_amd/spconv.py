@@ -60,7 +60,7 @@ class spconv_plan_info(ctypes.Structure):
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32),
                 ("block_cols", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("indexed_min_cols", ctypes.c_int64),
-                ("outer_min_cols", ctypes.c_int64)]
+                ("outer_min_cols", ctypes.c_int64), ("channel_passes", ctypes.c_int64)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}

@@ -137,7 +137,7 @@ def test_null_arrays_with_nonzeros_rejected():
 
 def test_options_validated():
     for kw in (dict(group_lanes=2), dict(group_lanes=12), dict(group_lanes=32), dict(group_lanes=-4),
-               dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=5),
+               dict(waves=17), dict(waves=-1), dict(reorder=2), dict(host_only=3), dict(kernel=6),
                dict(kernel=-1), dict(pipe_sets=3), dict(pipe_sets=-1), dict(regions=5), dict(regions=-1)):
         st, msg = _status(options=_host_opts(**kw))
         assert st == sp.spconv.E_ARG, kw
@@ -431,5 +431,40 @@ def test_run_rejects_tiles_whose_images_span_2gib(fused, kernel):
         assert st == sp.spconv.E_UNSUPPORTED and "2^31" in sp.spconv_last_error()
         st = sp.spconv_run(h, 1 << 44, 1 << 45, 4, 512, 512, stream=0, check=False)
         assert st == sp.spconv.E_ARG and "host_only" in sp.spconv_last_error()
+    finally:
+        sp.spconv_destroy(h)
+
+
+@pytest.mark.parametrize("cin,passes", [(1024, 2), (960, 2), (1280, 3), (512, 1), (100, 1)])
+def test_channel_range_passes_split_wide_inputs(cin, passes):
+    """Kernel option 5: ranges of at most 512 input channels, one pass each."""
+    layer = make_layer(cin, 96, 1, 1, 1, 0.9, seed=cin, with_x=False)
+    h = _create(layer, options=_host_opts(kernel=5))
+    try:
+        info = sp.spconv_plan_get_info(h)
+        rp, ci, va, _ = sp.spconv_plan_unpack(h)
+    finally:
+        sp.spconv_destroy(h)
+    assert info["channel_passes"] == passes
+    assert np.array_equal(rp, layer.row_ptr) and np.array_equal(ci, layer.col_idx)
+    assert np.array_equal(va, layer.values)
+
+
+@pytest.mark.parametrize("kw", [dict(block_rows=4), dict(storage="f16")], ids=["1x4", "f16"])
+def test_channel_range_passes_refused_outside_fp32_unstructured(kw):
+    layer = make_layer(1024, 96, 1, 1, 1, 0.9, seed=7, with_x=False, **kw)
+    st, h = _create(layer, check=False, options=_host_opts(kernel=5))
+    assert st == sp.spconv.E_UNSUPPORTED and not h, st
+    assert "channel-range" in sp.spconv_last_error()
+
+
+@pytest.mark.parametrize("cin,passes", [(1280, 3), (1264, 0), (2048, 4)])
+def test_automatic_choice_takes_passes_beyond_the_lockstep_width(cin, passes):
+    """Kernel option 0: fp32 unstructured inputs wider than 1264 channels run
+    as channel-range passes; narrower ones do not."""
+    layer = make_layer(cin, 64, 1, 1, 1, 0.9, seed=cin, with_x=False)
+    h = _create(layer, options=_host_opts())
+    try:
+        assert sp.spconv_plan_get_info(h)["channel_passes"] == passes
     finally:
         sp.spconv_destroy(h)

@@ -95,7 +95,7 @@ def test_fp16_and_depthwise_plans_have_no_indexed_streams():
 @pytest.mark.parametrize("opts,status", [
     (dict(kernel=3, lane_cols=7), "E_ARG"),
     (dict(kernel=3, lane_cols=-1), "E_ARG"),
-    (dict(kernel=5), "E_ARG"),
+    (dict(kernel=6), "E_ARG"),
 ])
 def test_bad_indexed_options_are_refused(opts, status):
     layer = make_layer(64, 64, 1, 1, 1, 0.8, seed=5, with_x=False)
