@@ -383,12 +383,24 @@ __device__ __forceinline__ void finish_rows(const Args &a, const Lane<G, F16> &L
                 if constexpr (VEC) {
                     bstore16(*reinterpret_cast<const u4 *>(out), ta.ry, ta.yo[j] + ro);
                 } else {
+                    // element stores through the tile's Y resource (32-bit
+                    // offsets from its first image): the vector's first
+                    // column's image and position, then carried forward (one
+                    // division per vector)
+                    const int32_t c0 = ta.col0 + L.vb[j] * GE::QE;
+                    int32_t n = c0 / a.hw;
+                    int32_t pp = c0 - n * a.hw;
 #pragma unroll
                     for (int e = 0; e < GE::QE; ++e) {
-                        const int32_t c = ta.col0 + L.vb[j] * GE::QE + e;
-                        if (c < a.m) {
-                            const int32_t n = c / a.hw;
-                            y[(static_cast<int64_t>(n) * a.cout + rb * K + kk) * a.hw + (c - n * a.hw)] = out[e];
+                        const int32_t off = c0 + e < a.m ? (((n - ta.n0) * a.cout + rb * K + kk) * a.hw + pp) * GE::E
+                                                         : kOutOfRange;
+                        if constexpr (F16)
+                            __builtin_amdgcn_raw_buffer_store_b16(__builtin_bit_cast(uint16_t, out[e]), ta.ry, off, 0, 0);
+                        else
+                            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, out[e]), ta.ry, off, 0, 0);
+                        if (++pp == a.hw) {
+                            pp = 0;
+                            ++n;
                         }
                     }
                 }
@@ -452,14 +464,14 @@ __device__ __forceinline__ u4 read_x(const Args &a, const Lane<G, F16> &L, const
 // records fetched two steps ahead
 // ---------------------------------------------------------------------------
 
-template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false, int D = 2>
 __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
                                            const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                            const unsigned char *lds, Rsrc ri, Rsrc rv,
                                            const int32_t *__restrict__ hdr, const int32_t *rows_lds,
                                            const float *bias_lds, int32_t b0, int32_t b1, float lo, float hi) {
     using GE = Geo<G, F16>;
-    constexpr int D = 2, NR = D + 1;
+    constexpr int NR = D + 1;  // D records fetched ahead
     const int32_t s_first = hdr[2 * b0];
     const int32_t nsteps = hdr[2 * (b1 - 1)] + hdr[2 * (b1 - 1) + 1] - s_first;
 
@@ -493,14 +505,19 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
                     for (int e = 0; e < GE::QE; ++e)
                         pn[kk][j][e] = __uint_as_float(v[e]);
                 } else {
+                    const int32_t c0 = ta.col0 + L.vb[j] * GE::QE;
+                    int32_t n = c0 / a.hw;
+                    int32_t pp = c0 - n * a.hw;
 #pragma unroll
                     for (int e = 0; e < GE::QE; ++e) {
-                        const int32_t c = ta.col0 + L.vb[j] * GE::QE + e;
-                        const int32_t n = c / a.hw;
-                        pn[kk][j][e] = row >= 0 && c < a.m
-                                           ? static_cast<float>(y[(static_cast<int64_t>(n) * a.cout + row * K + kk) * a.hw +
-                                                                  (c - n * a.hw)])
-                                           : 0.0f;
+                        const int32_t off = row >= 0 && c0 + e < a.m
+                                                ? (((n - ta.n0) * a.cout + row * K + kk) * a.hw + pp) * GE::E
+                                                : kOutOfRange;
+                        pn[kk][j][e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(ta.ry, off, 0, 0));
+                        if (++pp == a.hw) {
+                            pp = 0;
+                            ++n;
+                        }
                     }
                 }
             }
@@ -559,7 +576,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
 
 // A wavefront's share of a work item: all of its bundles (whole tile) or its
 // bundles of rank % tail_parts == part (shared tile), one run each.
-template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false, int D = 2>
 __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
                                          const ColOff<G, F16, DIRECT && !VEC> &co, typename Geo<G, F16>::T *y,
                                          const unsigned char *lds, Rsrc ri, Rsrc rv, const int32_t *__restrict__ hdr,
@@ -585,7 +602,8 @@ __device__ __forceinline__ void run_item(const Args &a, const Lane<G, F16> &L, c
             b1 = bnext + 1;
         }
         bnext = b1;
-        run_simple<G, K, F16, DIRECT, VEC, ACC>(a, L, ta, co, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo, hi);
+        run_simple<G, K, F16, DIRECT, VEC, ACC, D>(a, L, ta, co, y, lds, ri, rv, hdr, rows_lds, bias_lds, b0, b1, lo,
+                                                   hi);
     }
 }
 
@@ -647,8 +665,50 @@ __device__ __forceinline__ void load_strip_simple(const Args &a, const TileAddr<
     if constexpr (VEC) {
         copy_share<G, F16>(a, x, lds_base, tile, 0, a.strip_rows, wave, nwaves, lane);
         wait_vmcnt<0>();  // this wave's copies landed
+    } else if (!F16 && a.hw >= GE::QE) {
+        // fp32, any HW of at least 4: thread = one 16-byte vector of the tile
+        // row (nthreads is a multiple of 16), read with one 16-byte load where
+        // its 4 columns lie in one image and a second where they straddle two
+        // (offsets computed once; raw buffer loads check bounds per dword, so
+        // columns past the last read zero); all of a batch of rows' loads are
+        // issued before their LDS writes
+        const int vi = tid & 15;
+        const int32_t c = ta.col0 + vi * GE::QE;
+        int32_t off0 = kOutOfRange, off2 = kOutOfRange, kfirst = GE::QE;
+        if (c < a.m) {
+            const int32_t n = c / a.hw;
+            const int32_t p = c - n * a.hw;
+            kfirst = std::min(GE::QE, a.hw - p);
+            off0 = ((n - ta.n0) * a.xc * a.hw + p) * GE::E;
+            off2 = c + kfirst < a.m ? ((n + 1 - ta.n0) * a.xc * a.hw - kfirst) * GE::E : kOutOfRange;
+        }
+        const int32_t hwe = a.hw * GE::E;
+        const int32_t step = nthreads >> 4;  // rows covered by one pass of the workgroup
+        constexpr int U = 4;
+        for (int32_t r0 = tid >> 4; r0 < a.strip_rows; r0 += U * step) {
+            u4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t row = r0 + u * step;
+                const bool in = row < a.cin;
+                v[u] = bload16(ta.rx, in ? off0 + row * hwe : kOutOfRange, 0);
+                if (kfirst < GE::QE) {
+                    const u4 vb = bload16(ta.rx, in ? off2 + row * hwe : kOutOfRange, 0);
+#pragma unroll
+                    for (int e = 1; e < GE::QE; ++e)
+                        if (e >= kfirst)
+                            v[u][e] = vb[e];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t row = r0 + u * step;
+                if (row < a.strip_rows)
+                    *reinterpret_cast<u4 *>(lds + row * kRowBytes + vi * 16) = v[u];
+            }
+        }
     } else {
-        // any HW: gather element by element
+        // fp16, or HW below 4: gather element by element
         for (int i = tid; i < a.strip_rows * 16; i += nthreads) {
             const int32_t row = i >> 4;
             T v[GE::QE];
@@ -888,7 +948,10 @@ __device__ __forceinline__ bool dw_strip_staged(const Args &a, const float *__re
 // bundles; workgroup barriers around each strip.
 // ---------------------------------------------------------------------------
 
-template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false>
+// DWS: the plan has a depthwise stage (its strip is computed); without one
+// the kernel carries none of that code and its registers, and fetches records
+// further ahead (short runs of shared tiles would otherwise wait on them).
+template <int G, int K, bool F16, bool DIRECT, bool VEC, bool ACC = false, bool DWS = false>
 __global__ void __launch_bounds__(1024)
 spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__restrict__ idx,
             const float *__restrict__ val, const int32_t *__restrict__ hdr, const int32_t *__restrict__ table,
@@ -932,7 +995,7 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
         ta.set(a, L, x, y, wk.tile);
         if constexpr (!DIRECT) {
             bool computed = false;
-            if constexpr (!F16) {
+            if constexpr (!F16 && DWS) {
                 if (a.dw_stride) {
                     if (!dw_strip_staged(a, x, lds, wk.tile, tid, blockDim.x, wave, nwaves, lane))
                         dw_strip(a, x, lds, wk.tile, wave, nwaves, lane);
@@ -945,8 +1008,10 @@ spmm_kernel(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *_
             __syncthreads();  // strip ready
         }
         co.set(a, L, wk.tile);
-        run_item<G, K, F16, DIRECT, VEC, ACC>(a, L, ta, co, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0,
-                                              wb1, wk.part, lo, hi);
+        // records fetched ahead: as deep as the registers allow
+        constexpr int DR = K == 1 && !F16 && !DWS && !DIRECT ? (VEC ? (ACC ? 3 : 4) : (ACC ? 2 : 3)) : 2;
+        run_item<G, K, F16, DIRECT, VEC, ACC, DR>(a, L, ta, co, y, lds, ri, rv, hdr, rank, rows_lds, bias_lds, wb0,
+                                                  wb1, wk.part, lo, hi);
         const Work nx = next_work(a, wk);
         if constexpr (!DIRECT)
             __syncthreads();  // done with strip(wk)
@@ -1266,17 +1331,27 @@ using KernelFn = void (*)(const void *, void *, const int32_t *, const float *, 
                           const int32_t *, const int32_t *, const int32_t *, const float *, const uint32_t *,
                           const int32_t *, const int32_t *, Args);
 
-template <int K, bool F16, bool DIRECT, bool VEC>
-KernelFn pick_g(int g) {
+template <int K, bool F16, bool DIRECT, bool VEC, bool DWS>
+KernelFn pick_g2(int g) {
     switch (g) {
     case 4:
         if constexpr (K * 4 * (16 / (F16 ? 2 : 4)) <= 64)
-            return spmm_kernel<4, K, F16, DIRECT, VEC>;
+            return spmm_kernel<4, K, F16, DIRECT, VEC, false, DWS>;
         return nullptr;
-    case 8: return spmm_kernel<8, K, F16, DIRECT, VEC>;
-    case 16: return spmm_kernel<16, K, F16, DIRECT, VEC>;
+    case 8: return spmm_kernel<8, K, F16, DIRECT, VEC, false, DWS>;
+    case 16: return spmm_kernel<16, K, F16, DIRECT, VEC, false, DWS>;
     default: return nullptr;
     }
+}
+
+// dws: the plan has a depthwise stage (fp32 LDS-strip plans only)
+template <int K, bool F16, bool DIRECT, bool VEC>
+KernelFn pick_g(int g, bool dws = false) {
+    if constexpr (!F16 && !DIRECT) {
+        if (dws)
+            return pick_g2<K, F16, DIRECT, VEC, true>(g);
+    }
+    return pick_g2<K, F16, DIRECT, VEC, false>(g);
 }
 
 // Accumulators of one set of a lane.
@@ -1328,7 +1403,8 @@ KernelFn pick_kv(const DevicePlan &p, bool vec) {
         return nullptr;
     if (vec && K == 1 && !p.dw_stride)
         return pick_pipe<K, F16>(p.group_lanes, p.pipe_sets);
-    return vec ? pick_g<K, F16, false, true>(p.group_lanes) : pick_g<K, F16, false, false>(p.group_lanes);
+    const bool dws = p.dw_stride != 0;
+    return vec ? pick_g<K, F16, false, true>(p.group_lanes, dws) : pick_g<K, F16, false, false>(p.group_lanes, dws);
 }
 
 KernelFn pick(const DevicePlan &p, bool vec) {
