@@ -393,40 +393,45 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
     };
     auto xrow = [&](int32_t off) { return lds_vec(lds, xl + static_cast<uint32_t>(off)); };
     // Software pipeline: weights kOuterAhead quads ahead in registers (the
-    // arrays are padded for it), the next quad's offsets one quad ahead, and
-    // each step's X vector read before the previous step's arithmetic (two
-    // register sets, alternating by step).
+    // arrays are padded for it) and offsets two quads ahead.  Each step's X
+    // vector is read XA steps before its arithmetic, from a ring of four
+    // register sets (one per step of the quad): vector mode reads three steps
+    // ahead, which covers the LDS latency with the fused multiply-adds of the
+    // three steps in between; matrix mode reads one step ahead (its matrix
+    // instructions already cover the latency; a deeper ring only costs
+    // registers there).
+    constexpr int XA = MODE == 1 ? 3 : 1;
     f4 wq[kOuterAhead];
 #pragma unroll
     for (int i = 0; i < kOuterAhead; ++i)
         wq[i] = wp[i * GE::SLOTS];
     wp += kOuterAhead * GE::SLOTS;
     i4 oq = offs(0);
-    f4 xs[2];
-    xs[0] = xrow(oq.x);
-    // one quad: its 4 steps, the first X of the next quad read during the last
+    i4 o1 = offs(1);
+    f4 xs[4];
+#pragma unroll
+    for (int t = 0; t < XA; ++t)
+        xs[t] = xrow(oq[t]);
+    // one quad: its 4 steps; step t reads the X vector of step t + XA (in
+    // the next quad, offsets nx, once t + XA passes 3)
     auto quad = [&](const f4 w, const i4 nx) {
-        xs[1] = xrow(oq.y);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(w.x, xs[0]);
-        xs[0] = xrow(oq.z);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(w.y, xs[1]);
-        xs[1] = xrow(oq.w);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(w.z, xs[0]);
-        xs[0] = xrow(nx.x);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(w.w, xs[1]);
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const int r = t + XA;
+            xs[r % 4] = xrow(r < 4 ? oq[r] : nx[r - 4]);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(w[t], xs[t]);
+        }
     };
     int32_t j = 0;
     for (; j + kOuterAhead <= nq; j += kOuterAhead) {
 #pragma unroll
         for (int i = 0; i < kOuterAhead; ++i) {
-            const i4 nx = offs(j + i + 1);
-            quad(wq[i], nx);
+            const i4 o2 = offs(j + i + 2);
+            quad(wq[i], o1);
             wq[i] = wp[i * GE::SLOTS];  // after its last use: no copy of the old weights
-            oq = nx;
+            oq = o1;
+            o1 = o2;
             __builtin_amdgcn_sched_barrier(0);
         }
         wp += kOuterAhead * GE::SLOTS;
@@ -436,9 +441,10 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
 #pragma unroll
     for (int i = 0; i < kOuterAhead - 1; ++i) {
         if (j + i < nq) {
-            const i4 nx = offs(j + i + 1);
-            quad(wq[i], nx);
-            oq = nx;
+            const i4 o2 = offs(j + i + 2);
+            quad(wq[i], o1);
+            oq = o1;
+            o1 = o2;
         }
     }
     if (rb < 0)
