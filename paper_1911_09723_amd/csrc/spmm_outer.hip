@@ -392,29 +392,31 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
         }
     };
     auto xrow = [&](int32_t off) { return lds_vec(lds, xl + static_cast<uint32_t>(off)); };
-    // Software pipeline: weights kOuterAhead quads ahead in registers (the
-    // arrays are padded for it) and offsets two quads ahead.  Each step's X
-    // vector is read XA steps before its arithmetic, from a ring of four
-    // register sets (one per step of the quad): vector mode reads three steps
-    // ahead, which covers the LDS latency with the fused multiply-adds of the
-    // three steps in between; matrix mode reads one step ahead (its matrix
-    // instructions already cover the latency; a deeper ring only costs
-    // registers there).
+    // Software pipeline: weights and channel-row offsets kOuterAhead quads
+    // ahead in registers (the arrays are padded for it; the offsets of the
+    // widest layers come from global memory, so they need the same lead as
+    // the weights).  Each step's X vector is read XA steps before its
+    // arithmetic, from a ring of four register sets (one per step of the
+    // quad): vector mode reads three steps ahead, which covers the LDS
+    // latency with the fused multiply-adds of the three steps in between;
+    // matrix mode reads one step ahead (its matrix instructions already cover
+    // the latency; a deeper ring only costs registers there).
     constexpr int XA = MODE == 1 ? 3 : 1;
     f4 wq[kOuterAhead];
+    i4 oqs[kOuterAhead];
 #pragma unroll
-    for (int i = 0; i < kOuterAhead; ++i)
+    for (int i = 0; i < kOuterAhead; ++i) {
         wq[i] = wp[i * GE::SLOTS];
+        oqs[i] = offs(i);
+    }
     wp += kOuterAhead * GE::SLOTS;
-    i4 oq = offs(0);
-    i4 o1 = offs(1);
     f4 xs[4];
 #pragma unroll
     for (int t = 0; t < XA; ++t)
-        xs[t] = xrow(oq[t]);
-    // one quad: its 4 steps; step t reads the X vector of step t + XA (in
-    // the next quad, offsets nx, once t + XA passes 3)
-    auto quad = [&](const f4 w, const i4 nx) {
+        xs[t] = xrow(oqs[0][t]);
+    // one quad (offsets oq): its 4 steps; step t reads the X vector of step
+    // t + XA (in the next quad, offsets nx, once t + XA passes 3)
+    auto quad = [&](const f4 w, const i4 oq, const i4 nx) {
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
             const int r = t + XA;
@@ -427,11 +429,10 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
     for (; j + kOuterAhead <= nq; j += kOuterAhead) {
 #pragma unroll
         for (int i = 0; i < kOuterAhead; ++i) {
-            const i4 o2 = offs(j + i + 2);
-            quad(wq[i], o1);
-            wq[i] = wp[i * GE::SLOTS];  // after its last use: no copy of the old weights
-            oq = o1;
-            o1 = o2;
+            quad(wq[i], oqs[i], oqs[(i + 1) % kOuterAhead]);
+            // after their last use: no copies of the old records
+            wq[i] = wp[i * GE::SLOTS];
+            oqs[i] = offs(j + i + kOuterAhead);
             __builtin_amdgcn_sched_barrier(0);
         }
         wp += kOuterAhead * GE::SLOTS;
@@ -439,14 +440,9 @@ __device__ __forceinline__ void run_oct(const OArgs &a, unsigned char *lds, int3
         rf.template check<OFF_LDS ? kOuterAhead : 2 * kOuterAhead>(a, lds, ctl, slot, wave, lane);
     }
 #pragma unroll
-    for (int i = 0; i < kOuterAhead - 1; ++i) {
-        if (j + i < nq) {
-            const i4 o2 = offs(j + i + 2);
-            quad(wq[i], o1);
-            oq = o1;
-            o1 = o2;
-        }
-    }
+    for (int i = 0; i < kOuterAhead - 1; ++i)
+        if (j + i < nq)
+            quad(wq[i], oqs[i], oqs[i + 1]);
     if (rb < 0)
         return;
     constexpr int NR = MODE == 0 ? 4 : 1;  // rows of this lane
