@@ -57,3 +57,40 @@ def test_channel_range_passes_unaligned_pointers():
     finally:
         plan.close()
     assert_parity(layer, y, what="passes unaligned")
+
+
+def test_automatic_choice_runs_passes_beyond_the_lockstep_limit():
+    """1300 input channels: the automatic choice plans three ranges (512, 512,
+    276) and gives the direct-load kernel's bits."""
+    from paper_1911_09723_amd import Plan
+    layer = make_layer(1300, 40, 7, 7, 2, 0.9, act="relu6", seed=13)
+    plan = Plan.from_layer(layer)
+    try:
+        assert plan.info()["channel_passes"] == 3
+    finally:
+        plan.close()
+    note("passes automatic 1300")
+    y0 = gpu_run(layer)
+    assert_parity(layer, y0, what="passes automatic 1300")
+    assert np.array_equal(y0.view(np.uint32), gpu_run(layer, kernel=2).view(np.uint32))
+
+
+def test_rows_empty_in_some_ranges_or_everywhere():
+    """Row r keeps nonzeros only in range r % 3 of the three 512-channel
+    ranges (its partial sum passes through the other two passes untouched),
+    every 7th row has none at all (bias and activation of zero)."""
+    layer = make_layer(1536, 42, 5, 5, 3, 0.9, act="relu", seed=21)
+    rp, ci, va = [0], [], []
+    for r in range(layer.cout):
+        s, e = layer.row_ptr[r], layer.row_ptr[r + 1]
+        keep = [] if r % 7 == 6 else [i for i in range(s, e) if layer.col_idx[i] // 512 == r % 3]
+        ci += [int(layer.col_idx[i]) for i in keep]
+        va += [float(layer.values[i]) for i in keep]
+        rp.append(len(ci))
+    layer.row_ptr = np.array(rp, np.int32)
+    layer.col_idx = np.array(ci, np.int32)
+    layer.values = np.array(va, np.float32)
+    note("passes empty ranges")
+    y5 = gpu_run(layer, kernel=5)
+    assert_parity(layer, y5, what="passes empty ranges")
+    assert np.array_equal(y5.view(np.uint32), gpu_run(layer, kernel=2).view(np.uint32))
