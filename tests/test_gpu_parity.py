@@ -47,6 +47,13 @@ SMALL = [
     (512, 64, 14, 14, 3, 0.9, 2, "f32", "relu"),
     (601, 96, 7, 7, 2, 0.9, 2, "f32", "relu6"),
     (1500, 48, 6, 6, 2, 0.9, 2, "f16", "relu"),
+    # LDS strip, fp32, H*W not a multiple of 4 (16-byte strip reads with a
+    # second read where a vector straddles two images, element stores): every
+    # residue of H*W mod 4, several images per tile, a ragged last tile
+    (48, 40, 2, 3, 37, 0.7, 1, "f32", "relu"),
+    (48, 40, 1, 5, 29, 0.8, 4, "f32", "relu6"),
+    (96, 24, 3, 5, 11, 0.85, 2, "f32", "none"),
+    (72, 33, 7, 7, 5, 0.9, 1, "f32", "relu6"),
 ]
 
 
