@@ -410,7 +410,11 @@ typedef struct {
     int32_t dw_stride;     /* fused depthwise stage: 0 none, else its stride */
     int32_t dw_act;        /* its activation */
     int32_t block_cols;    /* input channels per block (1 unless created by spconv_plan_create_blocked) */
-    int32_t reserved0;
+    int32_t split_rows;    /* LDS-strip and direct-load kernels: rows more than twice the median length
+                              (at least 32 nonzeros) packed as two pieces, their even and their odd
+                              nonzeros, in neighbouring lane groups whose partial sums are added before
+                              the epilogue (unstructured plans; such a row is summed as its two pieces
+                              rather than in one ascending pass) */
     int64_t indexed_min_cols; /* kernel chosen automatically: runs of at least this many output columns
                                  (N * out_h * out_w) take the register-indexed kernel; 0 = never (and
                                  for host-only plans, which know no device) */

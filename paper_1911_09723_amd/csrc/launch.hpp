@@ -78,6 +78,7 @@ struct DevicePlan {
     // sums already in Y (every pass but the first)
     int32_t xc = 0;
     int32_t accum = 0;
+    int32_t splits = 0;  // the plan has split rows (row-table entries kRowPiece)
 };
 
 // How one launch of the register-indexed kernel covers m columns: `tiles`

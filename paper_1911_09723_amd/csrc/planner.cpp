@@ -704,22 +704,96 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
         p.use_outer = opt.kernel == 4;
     }
 
-    // 2. bundles of NB consecutive rows in that order, each a whole number of
-    // steps of 4 slots and at least one step long
+    // 2. bundles of NB consecutive entries in that order, each a whole number
+    // of steps of 4 slots and at least one step long.  An entry is a row or,
+    // for a row more than twice the median length (a heavy tail, which would
+    // otherwise set the pace of its whole bundle and wavefront), one of its
+    // two pieces: its even and its odd nonzeros, in two neighbouring lane
+    // groups of one bundle, so both walk the channels at the same pace; the
+    // second group's partial sums are added into the first's before the
+    // epilogue.  Unstructured plans only, only with the length order, and not
+    // in channel-range passes (each row summed in one ascending pass there).
     p.row_nnz.resize(rows);
     for (int32_t r = 0; r < rows; ++r)
         p.row_nnz[r] = len(r);
-    const int32_t nb = bundles_of(rows, NB);
+    struct Entry {
+        int32_t row;    // -1: an empty lane group
+        int32_t piece;  // -1 the whole row; 0 / 1 its even / odd nonzeros
+    };
+    auto elen = [&](const Entry &u) {
+        return u.row < 0 ? 0 : u.piece < 0 ? len(u.row) : (len(u.row) + 1 - u.piece) / 2;
+    };
+    int32_t split_min = INT32_MAX;
+    if (k == 1 && NB >= 2 && rows > 0 && opt.reorder && opt.split) {
+        std::vector<int32_t> l(p.row_nnz);
+        std::nth_element(l.begin(), l.begin() + rows / 2, l.end());
+        split_min = std::max<int32_t>(kSplitMinNnz, 2 * l[rows / 2] + 1);
+    }
+    std::vector<Entry> ents;
+    auto lay_out = [&](int32_t min_split) {
+        ents.clear();
+        p.split_rows = 0;
+        std::vector<Entry> items;  // whole rows, and split rows as their first piece
+        for (int32_t r : p.perm)
+            items.push_back(Entry{r, len(r) >= min_split ? 0 : -1});
+        std::stable_sort(items.begin(), items.end(), [&](const Entry &a, const Entry &b) { return elen(a) > elen(b); });
+        for (const Entry &u : items) {
+            if (u.piece < 0) {
+                ents.push_back(u);
+                continue;
+            }
+            if (ents.size() % 2)  // the two pieces take groups 2i and 2i + 1 of one bundle (NB is even)
+                ents.push_back(Entry{-1, -1});
+            ents.push_back(Entry{u.row, 0});
+            ents.push_back(Entry{u.row, 1});
+            ++p.split_rows;
+        }
+    };
+    // split only where the longest row alone would take more than 1.5x the
+    // average wavefront's steps of the unsplit layout (a nearly balanced plan
+    // gains less than its extra entries and epilogue exchanges cost)
+    if (split_min < INT32_MAX) {
+        lay_out(INT32_MAX);
+        int64_t steps0 = 0;
+        for (int32_t b = 0; b < bundles_of(rows, NB); ++b) {
+            int32_t l = 0;
+            for (int32_t q = 0; q < NB; ++q) {
+                const size_t at = static_cast<size_t>(b) * NB + q;
+                if (at < ents.size())
+                    l = std::max(l, elen(ents[at]));
+            }
+            steps0 += std::max<int32_t>(1, (l + kStepSlots - 1) / kStepSlots);
+        }
+        const int32_t w0 = opt.waves ? opt.waves : std::min<int32_t>(kMaxWaves, bundles_of(rows, NB));
+        const int32_t longest = (len(p.perm[0]) + kStepSlots - 1) / kStepSlots;
+        if (2 * static_cast<int64_t>(longest) * w0 <= 3 * steps0)
+            split_min = INT32_MAX;
+    }
+    lay_out(split_min);
+    if (p.split_rows) {
+        // the bundle table (kept in LDS) grows with the extra entries: keep
+        // the split only if it still fits
+        const int64_t grow = table_bytes(bundles_of(static_cast<int32_t>(ents.size()), NB), NB, k) -
+                             table_bytes(bundles_of(rows, NB), NB, k);
+        if (p.lds_bytes + grow <= kMaxLdsBytes)
+            p.lds_bytes += static_cast<int32_t>(grow);
+        else
+            lay_out(INT32_MAX);
+    }
+    const int32_t nb = bundles_of(static_cast<int32_t>(ents.size()), NB);
+    ents.resize(static_cast<size_t>(nb) * NB, Entry{-1, -1});
     std::vector<int32_t> bsteps(nb, 0);
     for (int32_t b = 0; b < nb; ++b) {
         int32_t l = 0;
-        for (int32_t q = 0; q < NB && b * NB + q < rows; ++q)
-            l = std::max(l, len(p.perm[b * NB + q]));
+        for (int32_t q = 0; q < NB; ++q)
+            l = std::max(l, elen(ents[static_cast<size_t>(b) * NB + q]));
         bsteps[b] = std::max<int32_t>(1, (l + kStepSlots - 1) / kStepSlots);
     }
 
     // 3. longest-processing-time-first assignment of bundles to waves
-    const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(kMaxWaves, nb);
+    // (as many as the unsplit layout would have: more wavefronts per
+    // workgroup could cost resident workgroups)
+    const int32_t waves = opt.waves ? opt.waves : std::min<int32_t>(kMaxWaves, bundles_of(rows, NB));
     p.waves = waves;
     if (p.dw_stride) {
         // the LDS left after the strip and the bundle table stages input
@@ -784,19 +858,21 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
             p.hdr.push_back(bsteps[b]);
             p.rank.push_back(rank_of[b]);
             for (int32_t q = 0; q < NB; ++q) {
-                const int32_t pos = b * NB + q;
-                const int32_t rb = pos < rows ? p.perm[pos] : -1;
-                p.rows.push_back(rb);
+                const Entry u = ents[static_cast<size_t>(b) * NB + q];
+                const int32_t rb = u.row;
+                p.rows.push_back(u.piece == 1 ? kRowPiece : rb);
                 for (int32_t i = 0; i < k; ++i)
-                    p.bundle_bias.push_back(rb >= 0 && in.bias ? in.bias[rb * k + i] : 0.0f);
+                    p.bundle_bias.push_back(rb >= 0 && u.piece != 1 && in.bias ? in.bias[rb * k + i] : 0.0f);
                 if (rb < 0)
                     continue;
                 const int32_t r0 = in.row_ptr[rb];
-                for (int32_t t = 0; t < len(rb); ++t) {
+                const int32_t n = elen(u);
+                for (int32_t t = 0; t < n; ++t) {
+                    const int32_t s = u.piece < 0 ? t : 2 * t + u.piece;  // the row's nonzero in slot t
                     const int64_t e = ((step + t / kStepSlots) * NB + q) * kStepSlots + t % kStepSlots;
-                    p.idx[e] = in.col_idx[r0 + t] * p.row_scale;
+                    p.idx[e] = in.col_idx[r0 + s] * p.row_scale;
                     for (int32_t i = 0; i < k; ++i) {
-                        float v = in.values[static_cast<int64_t>(r0 + t) * k + i];
+                        float v = in.values[static_cast<int64_t>(r0 + s) * k + i];
                         if (in.storage == 1)
                             v = half_to_float(float_to_half_rne(v));
                         p.val[e * k + i] = v;
@@ -839,24 +915,53 @@ Status build_plan(const Input &in_arg, const Options &opt, PackedPlan &p, std::s
     return OK;
 }
 
+// What lane group q of bundle b holds: a whole row, a piece of a split row
+// (0: its even nonzeros, 1: its odd ones; the second piece's table entry is
+// kRowPiece, after the first), or nothing; and how many real entries.
+GroupRow group_row(const PackedPlan &p, int32_t b, int32_t q) {
+    const int32_t NB = p.bundle_rows;
+    const size_t at = static_cast<size_t>(b) * NB + q;
+    const int32_t rb = p.rows[at];
+    GroupRow gr{rb, -1, 0};
+    if (rb == kRowPiece) {
+        gr.row = q > 0 ? p.rows[at - 1] : -1;
+        gr.piece = 1;
+    } else if (rb >= 0 && q + 1 < NB && p.rows[at + 1] == kRowPiece) {
+        gr.piece = 0;
+    }
+    if (gr.row >= 0 && gr.row < static_cast<int32_t>(p.row_nnz.size())) {
+        const int32_t l = p.row_nnz[gr.row];
+        gr.n = gr.piece < 0 ? l : (l + 1 - gr.piece) / 2;
+    } else {
+        gr.row = -1;
+    }
+    return gr;
+}
+
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm) {
     const int32_t k = p.k;
     const int32_t rows = p.cout / k;
     const int32_t NB = p.bundle_rows;
     std::vector<std::vector<int32_t>> cols(rows);
     std::vector<std::vector<float>> vals(rows);
-    // each row's real entries are the first row_nnz[rb] slots of its sequence
+    for (int32_t r = 0; r < rows; ++r) {
+        cols[r].assign(p.row_nnz[r], -1);
+        vals[r].assign(static_cast<size_t>(p.row_nnz[r]) * k, 0.0f);
+    }
+    // a lane group's real entries are the first ones of its sequence: the
+    // whole row, or the even / odd nonzeros of a split row
     for (int32_t b = 0; b < p.nbundles(); ++b) {
         const int64_t s_first = p.hdr[2 * b];
         for (int32_t q = 0; q < NB; ++q) {
-            const int32_t rb = p.rows[static_cast<size_t>(b) * NB + q];
-            if (rb < 0)
+            const GroupRow gr = group_row(p, b, q);
+            if (gr.row < 0)
                 continue;
-            for (int32_t t = 0; t < p.row_nnz[rb]; ++t) {
+            for (int32_t t = 0; t < gr.n; ++t) {
                 const int64_t e = ((s_first + t / kStepSlots) * NB + q) * kStepSlots + t % kStepSlots;
-                cols[rb].push_back(p.idx[e] / p.row_scale);
+                const int32_t s = gr.piece < 0 ? t : 2 * t + gr.piece;
+                cols[gr.row][s] = p.idx[e] / p.row_scale;
                 for (int32_t i = 0; i < k; ++i)
-                    vals[rb].push_back(p.val[e * k + i]);
+                    vals[gr.row][static_cast<size_t>(s) * k + i] = p.val[e * k + i];
             }
         }
     }
@@ -886,6 +991,10 @@ Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_id
     const int32_t rows = p.cout / k;
     std::vector<std::vector<int32_t>> cols(rows);
     std::vector<std::vector<float>> vals(rows);
+    for (int32_t r = 0; r < rows; ++r) {
+        cols[r].assign(p.row_nnz[r], -1);
+        vals[r].assign(static_cast<size_t>(p.row_nnz[r]) * k, 0.0f);
+    }
     auto bad = [&](const std::string &m) {
         err = m;
         return E_FORMAT;
@@ -921,12 +1030,13 @@ Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_id
                 return bad("selector runs past a wavefront's bundles");
             const int64_t step = ws0 + i;
             for (int32_t q = 0; q < NB; ++q) {
-                const int32_t rb = p.rows[static_cast<size_t>(b) * NB + q];
+                const GroupRow gr = group_row(p, b, q);
+                const int32_t rb = gr.row;
                 for (int32_t u = 0; u < kStepSlots; ++u) {
                     const int64_t e = (step * NB + q) * kStepSlots + u;
                     const int32_t c = p.pidx[e] / p.row_scale;
                     const int32_t t = cnt[set] * kStepSlots + u;
-                    if (rb < 0 || t >= p.row_nnz[rb]) {
+                    if (rb < 0 || t >= gr.n) {
                         if (c != p.strip_rows)
                             return bad("a padding slot reads a strip channel");
                         for (int32_t j = 0; j < k; ++j)
@@ -937,9 +1047,10 @@ Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_id
                     const int32_t r = c / p.region_rows;
                     if (c < 0 || c >= p.strip_rows || i < lo[r] || i > hi[r])
                         return bad("a step reads a strip part outside its need / release events");
-                    cols[rb].push_back(c);
+                    const int32_t sl = gr.piece < 0 ? t : 2 * t + gr.piece;
+                    cols[rb][sl] = c;
                     for (int32_t j = 0; j < k; ++j)
-                        vals[rb].push_back(p.pval[e * k + j]);
+                        vals[rb][static_cast<size_t>(sl) * k + j] = p.pval[e * k + j];
                 }
             }
             ++cnt[set];
@@ -955,6 +1066,9 @@ Status unpack_interleaved(const PackedPlan &p, int32_t *row_ptr, int32_t *col_id
             if (bset[i] < b1)
                 return bad("a wavefront's stream ends before its bundles do");
     }
+    for (int32_t r = 0; r < rows; ++r)
+        if (std::find(cols[r].begin(), cols[r].end(), -1) != cols[r].end())
+            return bad("row " + std::to_string(r) + " has entries no stream holds");
     int32_t acc = 0;
     if (row_ptr)
         row_ptr[0] = 0;

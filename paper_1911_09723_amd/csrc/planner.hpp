@@ -90,6 +90,11 @@ constexpr int64_t kMaxLdsBytes = 160 * 1024;
 constexpr int32_t kRowBytes = 256;
 // Slots per step (one 16-byte record of channels per lane group).
 constexpr int32_t kStepSlots = 4;
+// A bundle's row-table entry for the second piece of a split row (its lane
+// group's partial sums are added into the previous group's before the
+// epilogue); and the shortest row that may be split.
+constexpr int32_t kRowPiece = -2;
+constexpr int32_t kSplitMinNnz = 32;
 // Wavefronts per workgroup (1024 threads).
 constexpr int32_t kMaxWaves = 16;
 // Finest split of a tile over workgroups.
@@ -243,6 +248,15 @@ struct Options {
     int32_t pipe_sets = 0;    // 0 automatic, else 1 or 2 bundles interleaved per wavefront
     int32_t regions = 0;      // 0 automatic, else 1 .. kMaxRegions strip parts
     int32_t lane_cols = 0;    // register-indexed kernel: 0 automatic, else 1 .. 6 columns per lane
+    int32_t split = 1;        // heavy rows may be packed as two pieces (off for channel-range passes,
+                              // whose rows must be summed in one ascending pass)
+};
+
+// One lane group of a bundle as the row table describes it (group_row).
+struct GroupRow {
+    int32_t row;    // the output (block) row, -1 for none
+    int32_t piece;  // -1 the whole row; 0 / 1 the even / odd nonzeros of a split row
+    int32_t n;      // real entries of the group
 };
 
 struct PackedPlan {
@@ -259,6 +273,7 @@ struct PackedPlan {
     int32_t waves = 1;           // wavefronts per workgroup (each owns a list of bundles)
     int32_t strip_rows = 0;      // cin rounded up to a multiple of 4 (strip kernel)
     int32_t busy_waves = 0;      // wavefronts with at least one bundle
+    int32_t split_rows = 0;      // rows packed as two pieces (heavy rows)
     int32_t lds_bytes = 0;       // strip, zero row, bundle table, counters (strip kernel)
     int32_t pipe_sets = 1;       // bundles a wavefront interleaves (strip kernel)
     int32_t regions = 1;         // strip parts refilled independently (strip kernel)
@@ -369,6 +384,7 @@ Status build_plan(const Input &in, const Options &opt, PackedPlan &out, std::str
 
 // Rebuild block-CSR arrays (and the processing order) from a packed plan.
 // Any output pointer may be null.
+GroupRow group_row(const PackedPlan &p, int32_t b, int32_t q);
 void unpack_plan(const PackedPlan &p, int32_t *row_ptr, int32_t *col_idx, float *values, int32_t *perm);
 
 // Build the register-indexed kernel's slots, records and row pairs (fields

@@ -274,6 +274,7 @@ void fill_device_geometry(spconv_plan_s *pl) {
     d.idx_bytes = static_cast<int32_t>(h.idx.size() * sizeof(int32_t));
     d.val_bytes = static_cast<int32_t>(h.val.size() * sizeof(float));
     d.nbundles = h.nbundles();
+    d.splits = h.split_rows > 0 ? 1 : 0;
     d.max_parts = h.max_parts;
     d.dw_stride = h.dw_stride;
     d.dw_act = h.dw_act;
@@ -346,6 +347,7 @@ spconv_status create_plan(spconv_plan *out, const spconv::Input &in, const spcon
     po.pipe_sets = o.pipe_sets;
     po.regions = o.regions;
     po.lane_cols = o.lane_cols;
+    po.split = xc == 0 && accum == 0 ? 1 : 0;  // a pass's rows are summed in one ascending pass
     // automatic choice: fp32 unstructured inputs too wide for the lockstep
     // kernel's strips (measured: passes over the LDS-strip kernel beat the
     // direct-load kernel there, 124 against 197 us for 1280 -> 320 @ 7x7,
@@ -878,6 +880,7 @@ spconv_status spconv_plan_get_info(spconv_plan plan, spconv_plan_info *info) {
     info->dw_stride = p.dw_stride;
     info->dw_act = p.dw_act;
     info->block_cols = p.kc;
+    info->split_rows = p.split_rows;
     info->indexed_min_cols = plan->host_only ? 0 : plan->dev.indexed_min_cols;
     info->outer_min_cols = plan->host_only ? 0 : plan->dev.outer_min_cols;
     info->channel_passes = static_cast<int64_t>(plan->passes.size());

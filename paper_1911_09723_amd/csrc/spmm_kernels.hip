@@ -115,6 +115,7 @@ struct Args {
     int32_t cin, cout, hw, m, act;
     int32_t xc;          // channels per image of X (the plan's cin, or more for a channel-range pass)
     int32_t accum;       // add Y's values (partial sums of earlier channel ranges) before the bias
+    int32_t splits;      // the plan has split rows (row-table entries kRowPiece)
     int32_t vec;         // 16-byte global loads and stores (see launch_spmm)
     int32_t strip_rows;  // LDS strip channels (a multiple of 4); 0 for the direct kernel
     int32_t regions;     // strip parts refilled independently (pipelined kernel)
@@ -361,14 +362,36 @@ __device__ __forceinline__ void fma_slot(float (&acc)[K][16 / G][16 / (F16 ? 2 :
 }
 
 // Bias, activation (a clamp to [lo, hi]), one rounding, store of block row rb;
-// then the accumulators restart from zero.
+// then the accumulators restart from zero.  rb_next is the next lane group's
+// row-table entry: kRowPiece when this group holds the even nonzeros of a
+// split row and the next one its odd nonzeros, whose partial sums are added
+// here first.
 template <int G, int K, bool F16, bool VEC>
 __device__ __forceinline__ void finish_rows(const Args &a, const Lane<G, F16> &L, const TileAddr<G, F16> &ta,
                                             typename Geo<G, F16>::T *y,
                                             float (&acc)[K][16 / G][16 / (F16 ? 2 : 4)], const float (&bv)[K],
-                                            int32_t rb, float lo, float hi) {
+                                            int32_t rb, int32_t rb_next, float lo, float hi) {
     using GE = Geo<G, F16>;
     using T = typename GE::T;
+    if (a.splits) {
+        // Every lane reads its counterpart in the next group (lane + G), whose
+        // vector j - 1 holds this lane's vector j (the per-group rotation of
+        // the vectors).  Only a first piece adds, and it reads a second piece,
+        // which never adds, so no lane reads a value another has changed.
+        const bool add = rb_next == kRowPiece;
+        const int src = ((static_cast<int>(threadIdx.x & 63) + G) & 63) << 2;
+#pragma unroll
+        for (int kk = 0; kk < K; ++kk)
+#pragma unroll
+            for (int j = 0; j < GE::V; ++j)
+#pragma unroll
+                for (int e = 0; e < GE::QE; ++e) {
+                    const float pv = __int_as_float(__builtin_amdgcn_ds_bpermute(
+                        src, __float_as_int(acc[kk][(j + GE::V - 1) % GE::V][e])));
+                    if (add)
+                        acc[kk][j][e] += pv;
+                }
+    }
     if (rb >= 0) {
         const int32_t hwe = a.hw * GE::E;
 #pragma unroll
@@ -485,7 +508,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
                 acc[kk][j][e] = 0.0f;
 
     // the bundle in progress: its row and biases (of this lane's group), steps left
-    int32_t b = b0, rb = 0, left = 0;
+    int32_t b = b0, rb = 0, rbn = -1, left = 0;
     float bv[K];
     // Channel-range passes after the first (ACC, fp32): a row's
     // accumulators start from its values in Y, the sums over the earlier
@@ -524,6 +547,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
     };
     auto start_bundle = [&]() __attribute__((always_inline)) {
         rb = rows_lds[b * GE::NB + L.q];
+        rbn = L.q + 1 < GE::NB ? rows_lds[b * GE::NB + L.q + 1] : -1;
 #pragma unroll
         for (int kk = 0; kk < K; ++kk)
             bv[kk] = bias_lds[(b * GE::NB + L.q) * K + kk];
@@ -565,7 +589,7 @@ __device__ __forceinline__ void run_simple(const Args &a, const Lane<G, F16> &L,
                     fma_slot<G, K, F16, U>(acc, cr[KI], xr);
                 });
                 if (--left == 0) {
-                    finish_rows<G, K, F16, VEC>(a, L, ta, y, acc, bv, rb, lo, hi);
+                    finish_rows<G, K, F16, VEC>(a, L, ta, y, acc, bv, rb, rbn, lo, hi);
                     if (++b < b1)
                         start_bundle();
                 }
@@ -1217,7 +1241,8 @@ spmm_pipe(const void *__restrict__ xv, void *__restrict__ yv, const int32_t *__r
 #pragma unroll
             for (int kk = 0; kk < K; ++kk)
                 bv[kk] = bias_lds[(b * GE::NB + L.q) * K + kk];
-            finish_rows<G, K, F16, true>(a, L, ta, y, acc[S], bv, rows_lds[b * GE::NB + L.q], lo, hi);
+            finish_rows<G, K, F16, true>(a, L, ta, y, acc[S], bv, rows_lds[b * GE::NB + L.q],
+                                         L.q + 1 < GE::NB ? rows_lds[b * GE::NB + L.q + 1] : -1, lo, hi);
             bset[S] = b + M;
         };
 
@@ -1484,6 +1509,7 @@ hipError_t launch_spmm(const DevicePlan &p, const void *x, void *y, int32_t m, i
     a.cin = p.cin;
     a.xc = p.xc > 0 ? p.xc : p.cin;
     a.accum = p.accum;
+    a.splits = p.splits;
     a.cout = p.cout;
     a.hw = hw;
     a.m = m;

@@ -59,7 +59,7 @@ class spconv_plan_info(ctypes.Structure):
                 ("nnzb", ctypes.c_int64), ("slots", ctypes.c_int64),
                 ("max_wave_cost", ctypes.c_int64), ("sum_wave_cost", ctypes.c_int64),
                 ("device_bytes", ctypes.c_int64), ("dw_stride", ctypes.c_int32), ("dw_act", ctypes.c_int32),
-                ("block_cols", ctypes.c_int32), ("reserved0", ctypes.c_int32), ("indexed_min_cols", ctypes.c_int64),
+                ("block_cols", ctypes.c_int32), ("split_rows", ctypes.c_int32), ("indexed_min_cols", ctypes.c_int64),
                 ("outer_min_cols", ctypes.c_int64), ("channel_passes", ctypes.c_int64)]
 
     def as_dict(self):
